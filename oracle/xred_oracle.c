@@ -1,0 +1,323 @@
+/*
+ * xred_oracle.c -- plain, slow, obviously correct CPU oracle for one rank's
+ * reduce step of ReduceScatter / AllReduce.
+ *
+ * TEST INFRASTRUCTURE ONLY.  Nothing in the product library links, includes
+ * or calls this file; only the test suite, the smoke check and the
+ * benchmark's CPU-baseline leg load it.  It shares no code, header, table or
+ * constant with the HIP path.
+ *
+ * What it computes (the per-rank reduce of the FTAR ring, Section 5 "HSDP:
+ * Fault tolerant AllReduce", and the ReduceScatter/AllReduce semantics of
+ * Section 2.2 "Communication libraries"):
+ *
+ *     out[i] = down( fold( up(src[0][i]), up(src[1][i]), ..., up(src[P-1][i]) ) )
+ *
+ * for every element index i independently, where fold is a LEFT fold in
+ * source order 0..P-1 (the paper never states an order; a fixed rank order is
+ * the reading taken), up() converts an input element to the accumulator type
+ * (binary32 for bf16/fp32, uint32 for int32/uint32: the paper names no
+ * accumulator type), and down() converts back with round-to-nearest-even.
+ *
+ * Arithmetic is carried out in binary32 because the definition being checked
+ * is binary32 accumulation; this file is compiled with -ffp-contract=off and
+ * without fast-math so that every float operation is one IEEE binary32
+ * operation with round-to-nearest-even, subnormals preserved.
+ *
+ * Readings of points the paper leaves open (each is repeated in the design
+ * notes):
+ *   - the accumulator starts from up(src[0][i]), never from 0, so a column of
+ *     -0.0 sums to -0.0;
+ *   - MAX/MIN use the total order -inf < ... < -0 < +0 < ... < +inf; any NaN
+ *     operand gives the canonical quiet NaN 0x7FC00000;
+ *   - NaN payloads of SUM/PROD are not specified ("parity unpinned" for NaN
+ *     payloads: tests compare NaN-ness only);
+ *   - down() of a NaN to bf16 keeps the sign and gives the quiet NaN 0x7FC0.
+ *
+ * Step-wise ring mode (the ReduceCopy of the FTAR pipeline, Section 5 FTAR):
+ * acc <- up(in) on INIT, acc <- acc (+) up(in) otherwise, and on FINAL the
+ * result is written as down(...) to dst instead of to acc.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <string.h>
+#include <stddef.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+/* The oracle's own codes; the Python loader maps dtype/op names onto them. */
+enum { XO_F32 = 10, XO_BF16 = 11, XO_I32 = 13, XO_U32 = 14 };
+enum { XO_SUM = 20, XO_PROD = 21, XO_MAX = 22, XO_MIN = 23 };
+enum { XO_INIT = 1u, XO_FINAL = 2u };
+enum { XO_OK = 0, XO_BAD = -1 };
+
+/* ---------------------------------------------------------------- bits --- */
+
+static uint32_t f2u(float f) { uint32_t u; memcpy(&u, &f, 4); return u; }
+static float u2f(uint32_t u) { float f; memcpy(&f, &u, 4); return f; }
+
+static int is_float_type(int dtype) { return dtype == XO_F32 || dtype == XO_BF16; }
+
+static size_t elem_size(int dtype)
+{
+    switch (dtype) {
+    case XO_F32: case XO_I32: case XO_U32: return 4;
+    case XO_BF16: return 2;
+    default: return 0;
+    }
+}
+
+/* ---------------------------------------------------------------- up() --- */
+
+/* bf16 is the top half of a binary32: widening is exact. */
+static float bf16_to_f32(uint16_t h) { return u2f((uint32_t)h << 16); }
+
+static float up_float(const void *base, uint64_t i, int dtype)
+{
+    if (dtype == XO_BF16) {
+        uint16_t h;
+        memcpy(&h, (const char *)base + 2 * i, 2);
+        return bf16_to_f32(h);
+    }
+    float f;
+    memcpy(&f, (const char *)base + 4 * i, 4);
+    return f;
+}
+
+static uint32_t up_int(const void *base, uint64_t i)
+{
+    uint32_t u;
+    memcpy(&u, (const char *)base + 4 * i, 4);
+    return u;
+}
+
+/* -------------------------------------------------------------- down() --- */
+
+/* binary32 -> bf16, round to nearest, ties to even.  The 16 dropped bits
+ * decide: above half rounds the magnitude up, below half truncates, exactly
+ * half rounds up only when the kept part is odd.  A carry out of the kept
+ * mantissa moves into the exponent, which is the correct next representable
+ * value (and gives +-inf past the largest finite bf16). */
+static uint16_t f32_to_bf16(float f)
+{
+    uint32_t b = f2u(f);
+    if (isnan(f))
+        return (uint16_t)(((b >> 16) & 0x8000u) | 0x7FC0u);
+    uint32_t kept = b >> 16;
+    uint32_t dropped = b & 0xFFFFu;
+    if (dropped > 0x8000u || (dropped == 0x8000u && (kept & 1u)))
+        kept += 1u;
+    return (uint16_t)kept;
+}
+
+static void down_float(void *base, uint64_t i, int dtype, float v)
+{
+    if (dtype == XO_BF16) {
+        uint16_t h = f32_to_bf16(v);
+        memcpy((char *)base + 2 * i, &h, 2);
+    } else {
+        memcpy((char *)base + 4 * i, &v, 4);
+    }
+}
+
+static void down_int(void *base, uint64_t i, uint32_t v)
+{
+    memcpy((char *)base + 4 * i, &v, 4);
+}
+
+/* --------------------------------------------------------- the operators -- */
+
+static float canonical_nan(void) { return u2f(0x7FC00000u); }
+
+/* Total-order maximum: NaN anywhere -> canonical NaN; otherwise the larger
+ * value, with +0 counted above -0. */
+static float max_total(float a, float b)
+{
+    if (isnan(a) || isnan(b)) return canonical_nan();
+    if (a > b) return a;
+    if (b > a) return b;
+    /* a == b numerically: only +-0 can differ in bits */
+    return signbit(a) ? b : a;
+}
+
+static float min_total(float a, float b)
+{
+    if (isnan(a) || isnan(b)) return canonical_nan();
+    if (a < b) return a;
+    if (b < a) return b;
+    return signbit(a) ? a : b;
+}
+
+static float op_float(int op, float a, float b)
+{
+    switch (op) {
+    case XO_SUM: return a + b;
+    case XO_PROD: return a * b;
+    case XO_MAX: return max_total(a, b);
+    default: return min_total(a, b);
+    }
+}
+
+/* Integer ops: sum and product wrap modulo 2^32; max/min compare as signed
+ * int32 for XO_I32 and as unsigned for XO_U32. */
+static uint32_t op_int(int op, int dtype, uint32_t a, uint32_t b)
+{
+    switch (op) {
+    case XO_SUM: return a + b;
+    case XO_PROD: return a * b;
+    case XO_MAX:
+        if (dtype == XO_I32) return ((int32_t)a > (int32_t)b) ? a : b;
+        return a > b ? a : b;
+    default:
+        if (dtype == XO_I32) return ((int32_t)a < (int32_t)b) ? a : b;
+        return a < b ? a : b;
+    }
+}
+
+static int valid_dtype(int dtype) { return elem_size(dtype) != 0; }
+static int valid_op(int op) { return op >= XO_SUM && op <= XO_MIN; }
+
+/* ------------------------------------------------------ the definition --- */
+
+/* out[i] = down(fold_op(up(srcs[0][off+i]), ..., up(srcs[P-1][off+i]))) */
+static void reduce_one(const void *const *srcs, int nsrc, uint64_t off, void *dst,
+                       uint64_t i, int dtype, int op)
+{
+    if (is_float_type(dtype)) {
+        float acc = up_float(srcs[0], off + i, dtype);
+        for (int p = 1; p < nsrc; ++p)
+            acc = op_float(op, acc, up_float(srcs[p], off + i, dtype));
+        down_float(dst, i, dtype, acc);
+    } else {
+        uint32_t acc = up_int(srcs[0], off + i);
+        for (int p = 1; p < nsrc; ++p)
+            acc = op_int(op, dtype, acc, up_int(srcs[p], off + i));
+        down_int(dst, i, acc);
+    }
+}
+
+static int reduce_range(const void *const *srcs, int nsrc, uint64_t off, void *dst,
+                        uint64_t count, int dtype, int op, int nthreads)
+{
+    if (nsrc < 1 || !valid_dtype(dtype) || !valid_op(op)) return XO_BAD;
+    if (count == 0) return XO_OK;
+    if (nthreads < 1) nthreads = 1;
+    /* Elements are independent; splitting the index range over threads does
+     * not change any element's fold order. */
+#ifdef _OPENMP
+#pragma omp parallel for num_threads(nthreads) schedule(static)
+#endif
+    for (int64_t i = 0; i < (int64_t)count; ++i)
+        reduce_one(srcs, nsrc, off, dst, (uint64_t)i, dtype, op);
+    return XO_OK;
+}
+
+/* AllReduce's local reduce: the definition over whole buffers. */
+int xo_allreduce_local(const void *const *srcs, int nsrc, void *dst, uint64_t count,
+                       int dtype, int op, int nthreads)
+{
+    return reduce_range(srcs, nsrc, 0, dst, count, dtype, op, nthreads);
+}
+
+/* ReduceScatter's local reduce for rank r: srcs[p] is rank p's full send
+ * buffer of nsrc*recvcount elements; rank r keeps shard r, i.e. the
+ * definition applied to srcs[p][r*recvcount .. (r+1)*recvcount). */
+int xo_reduce_scatter_local(const void *const *srcs, int nsrc, int rank, void *dst,
+                            uint64_t recvcount, int dtype, int op, int nthreads)
+{
+    if (rank < 0 || rank >= nsrc) return XO_BAD;
+    return reduce_range(srcs, nsrc, (uint64_t)rank * recvcount, dst, recvcount, dtype, op,
+                        nthreads);
+}
+
+/* One ReduceCopy step of a ring (FTAR pipeline, Section 5):
+ *   INIT          acc <- up(in)
+ *   (no flag)     acc <- acc (+) up(in)
+ *   FINAL         dst <- down(acc (+) up(in))      (acc is not written)
+ *   INIT|FINAL    dst <- down(up(in))
+ * acc holds binary32 for float dtypes and uint32 for integer dtypes. */
+int xo_reduce_copy_step(const void *in, void *acc, void *dst, uint64_t count, int dtype,
+                        int op, unsigned flags)
+{
+    if (!valid_dtype(dtype) || !valid_op(op)) return XO_BAD;
+    int init = (flags & XO_INIT) != 0, fin = (flags & XO_FINAL) != 0;
+    for (uint64_t i = 0; i < count; ++i) {
+        if (is_float_type(dtype)) {
+            float x = up_float(in, i, dtype);
+            float a = init ? x : op_float(op, up_float(acc, i, XO_F32), x);
+            if (fin) down_float(dst, i, dtype, a);
+            else down_float(acc, i, XO_F32, a);
+        } else {
+            uint32_t x = up_int(in, i);
+            uint32_t a = init ? x : op_int(op, dtype, up_int(acc, i), x);
+            if (fin) down_int(dst, i, a);
+            else down_int(acc, i, a);
+        }
+    }
+    return XO_OK;
+}
+
+/* dst <- down(acc): the closing cast of a step-wise sequence. */
+int xo_acc_cast(const void *acc, void *dst, uint64_t count, int dtype)
+{
+    if (!valid_dtype(dtype)) return XO_BAD;
+    for (uint64_t i = 0; i < count; ++i) {
+        if (is_float_type(dtype)) down_float(dst, i, dtype, up_float(acc, i, XO_F32));
+        else down_int(dst, i, up_int(acc, i));
+    }
+    return XO_OK;
+}
+
+/* Many independent reductions: the definition applied to each item.  Item k
+ * reads item_srcs[item_src_off[k] .. item_src_off[k]+item_nsrc[k]) and
+ * writes item_count[k] elements to item_dst[k]. */
+int xo_batched_reduce(int nitems, const void *const *item_srcs, const uint64_t *item_src_off,
+                      const int *item_nsrc, void *const *item_dst, const uint64_t *item_count,
+                      int dtype, int op, int nthreads)
+{
+    for (int k = 0; k < nitems; ++k) {
+        int rc = reduce_range(item_srcs + item_src_off[k], item_nsrc[k], 0, item_dst[k],
+                              item_count[k], dtype, op, nthreads);
+        if (rc != XO_OK) return rc;
+    }
+    return XO_OK;
+}
+
+/* Bulk conversions, exposed so tests can check down()/up() on their own. */
+void xo_f32_bits_to_bf16(const uint32_t *in, uint16_t *out, uint64_t n)
+{
+    for (uint64_t i = 0; i < n; ++i) out[i] = f32_to_bf16(u2f(in[i]));
+}
+
+void xo_bf16_to_f32_bits(const uint16_t *in, uint32_t *out, uint64_t n)
+{
+    for (uint64_t i = 0; i < n; ++i) out[i] = f2u(bf16_to_f32(in[i]));
+}
+
+/* Returns 0 when the floating-point environment is the one the definition
+ * needs: subnormal results kept (no flush-to-zero), subnormal inputs honoured
+ * (no denormals-are-zero), round-to-nearest. */
+int xo_selfcheck(void)
+{
+    volatile float tiny = u2f(0x00000001u);   /* 2^-149 */
+    volatile float two_tiny = tiny + tiny;   /* 2^-148, needs no FTZ/DAZ */
+    if (f2u(two_tiny) != 0x00000002u) return 1;
+    volatile float one = 1.0f, eps_half = u2f(0x33800000u); /* 2^-24 */
+    volatile float r = one + eps_half;       /* tie: stays 1.0 under RNE */
+    if (f2u(r) != 0x3F800000u) return 2;
+    volatile float r2 = one + u2f(0x33800001u); /* just above the tie: rounds up */
+    if (f2u(r2) != 0x3F800001u) return 3;
+    return 0;
+}
+
+int xo_max_threads(void)
+{
+#ifdef _OPENMP
+    return omp_get_max_threads();
+#else
+    return 1;
+#endif
+}
+
+int xo_version(void) { return 1; }

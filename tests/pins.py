@@ -1,0 +1,334 @@
+"""Checks that pin the CPU oracle to something other than itself.
+
+Each ``pin_*`` function takes an ``oracle.Oracle`` and raises AssertionError
+on a mismatch.  They are run against the real oracle (test_oracle_pins.py)
+and against copies of it with planted mistakes (test_oracle_mutants.py),
+which must each fail at least one pin.
+
+What pins what:
+  - exact rational brute force (tests/brute.py) on tiny random and special
+    inputs, every dtype x op: single-rounding correctness and fold order;
+  - hand-derived IEEE 754 closed forms (tests/golden/);
+  - PyTorch's CPU binary32 -> bf16 conversion over every sign/exponent/
+    high-mantissa pattern with each class of dropped bits;
+  - closed forms at scale: integer-valued inputs make every binary32 partial
+    sum exact, so the result is the int64 sum;
+  - integer sums and products against numpy int64 modulo 2^32;
+  - invariants: all-ones columns sum to P, a -0.0 buffer is the bitwise
+    identity for sum, P=1 is a copy, max/min are permutation invariant,
+    integer sums are permutation invariant, ReduceScatter shards concatenate
+    to the AllReduce, the step-wise sequence equals the fused left fold, a
+    batch equals its items.
+"""
+from __future__ import annotations
+
+import json
+from pathlib import Path
+
+import numpy as np
+
+import brute
+
+GOLDEN = Path(__file__).resolve().parent / "golden"
+NP = {"f32": np.float32, "bf16": np.uint16, "i32": np.int32, "u32": np.uint32}
+DTYPES = ("f32", "bf16", "i32", "u32")
+OPS = ("sum", "prod", "max", "min")
+
+F32_SPECIALS = [
+    0x00000000, 0x80000000, 0x7F800000, 0xFF800000, 0x7F7FFFFF, 0xFF7FFFFF,
+    0x00000001, 0x80000001, 0x007FFFFF, 0x807FFFFF, 0x00800000, 0x80800000,
+    0x3F800000, 0xBF800000, 0x3F800001, 0x33800000, 0x33800001, 0xB3800000,
+    0x4B800000, 0x3F000000, 0x7FC00000, 0x7F800001, 0xFFC00000, 0x00400000,
+]
+BF16_SPECIALS = [
+    0x0000, 0x8000, 0x7F80, 0xFF80, 0x7F7F, 0xFF7F, 0x0001, 0x8001, 0x007F, 0x0080,
+    0x3F80, 0xBF80, 0x3F81, 0x3B80, 0x3B00, 0x4B80, 0x7FC0, 0x7F81, 0xFFC0, 0x3F00,
+]
+
+
+def _bits(a: np.ndarray) -> np.ndarray:
+    return a.view(np.uint32) if a.dtype.itemsize == 4 else a.view(np.uint16)
+
+
+def _is_nan_bits(b: int, dtype: str) -> bool:
+    if dtype == "bf16":
+        return (b & 0x7F80) == 0x7F80 and (b & 0x7F) != 0
+    if dtype == "f32":
+        return brute.is_nan32(b)
+    return False
+
+
+def _same(got: int, exp: int, dtype: str, op: str) -> bool:
+    """Bitwise equality, except that NaN payloads of sum/prod are unpinned."""
+    if dtype in ("f32", "bf16") and op in ("sum", "prod") and _is_nan_bits(exp, dtype):
+        return _is_nan_bits(got, dtype)
+    return got == exp
+
+
+def random_column_values(rng, dtype: str, n: int) -> np.ndarray:
+    """Random bit patterns mixing specials, random bits and nearby magnitudes."""
+    if dtype == "f32":
+        pool = np.array(F32_SPECIALS, np.uint32)
+        rb = rng.integers(0, 2**32, size=n, dtype=np.uint64).astype(np.uint32)
+        near = (rng.standard_normal(n).astype(np.float32)).view(np.uint32)
+        tiny = rng.integers(0, 1 << 24, size=n, dtype=np.uint32)   # subnormal / tiny normal
+        pick = rng.integers(0, 4, size=n)
+        out = np.where(pick == 0, pool[rng.integers(0, pool.size, n)],
+                       np.where(pick == 1, rb, np.where(pick == 2, near, tiny)))
+        return out.astype(np.uint32).view(np.float32)
+    if dtype == "bf16":
+        pool = np.array(BF16_SPECIALS, np.uint16)
+        rb = rng.integers(0, 2**16, size=n, dtype=np.uint32).astype(np.uint16)
+        near = (rng.standard_normal(n).astype(np.float32).view(np.uint32) >> 16).astype(np.uint16)
+        tiny = rng.integers(0, 0x0100, size=n, dtype=np.uint32).astype(np.uint16)
+        pick = rng.integers(0, 4, size=n)
+        return np.where(pick == 0, pool[rng.integers(0, pool.size, n)],
+                        np.where(pick == 1, rb, np.where(pick == 2, near, tiny))).astype(np.uint16)
+    specials = np.array([0, 1, 0xFFFFFFFF, 0x7FFFFFFF, 0x80000000, 2, 0x10000], np.uint32)
+    rb = rng.integers(0, 2**32, size=n, dtype=np.uint64).astype(np.uint32)
+    small = rng.integers(0, 8, size=n, dtype=np.uint32)
+    pick = rng.integers(0, 3, size=n)
+    out = np.where(pick == 0, specials[rng.integers(0, specials.size, n)],
+                   np.where(pick == 1, rb, small)).astype(np.uint32)
+    return out.view(np.int32) if dtype == "i32" else out
+
+
+def pin_bruteforce(orc, seed: int = 7, ncols: int = 48, nsrc_list=(1, 2, 3, 5, 8)) -> None:
+    """Oracle == exact rational brute force, every dtype x op, tiny inputs."""
+    rng = np.random.default_rng(seed)
+    for dtype in DTYPES:
+        for op in OPS:
+            for P in nsrc_list:
+                srcs = [random_column_values(rng, dtype, ncols) for _ in range(P)]
+                got = _bits(orc.allreduce_local(srcs, dtype, op))
+                sb = [_bits(s) for s in srcs]
+                for i in range(ncols):
+                    col = [int(s[i]) for s in sb]
+                    exp = brute.reduce_column(col, dtype, op)
+                    assert _same(int(got[i]), exp, dtype, op), (
+                        f"{dtype} {op} P={P} col={[hex(c) for c in col]} "
+                        f"got={int(got[i]):#x} exp={exp:#x}")
+
+
+def pin_golden_reduce(orc) -> None:
+    """Oracle == hand-derived IEEE 754 closed forms (tests/golden/reduce_cases.json)."""
+    cases = json.loads((GOLDEN / "reduce_cases.json").read_text())
+    for c in cases:
+        dtype, op = c["dtype"], c["op"]
+        srcs = [np.array([int(h, 16)], np.uint16 if dtype == "bf16" else np.uint32)
+                .view(NP[dtype]) for h in c["column"]]
+        got = int(_bits(orc.allreduce_local(srcs, dtype, op))[0])
+        if c["expect"] == "NAN":
+            assert _is_nan_bits(got, dtype), f"{c}: got {got:#x}"
+        else:
+            assert got == int(c["expect"], 16), f"{c}: got {got:#x}"
+
+
+def pin_golden_bf16(orc) -> None:
+    """down() == hand-derived roundTiesToEven cases (tests/golden/bf16_rne_cases.txt)."""
+    ins, exps = [], []
+    for line in (GOLDEN / "bf16_rne_cases.txt").read_text().splitlines():
+        if not line.strip() or line.startswith("#"):
+            continue
+        f, b = line.split()[:2]
+        ins.append(int(f, 16))
+        exps.append(int(b, 16))
+    got = orc.f32_bits_to_bf16(np.array(ins, np.uint32))
+    for x, g, e in zip(ins, got, exps):
+        assert int(g) == e, f"{x:#010x}: got {int(g):#06x} expected {e:#06x}"
+
+
+def pin_bf16_vs_brute(orc, seed: int = 3, n: int = 4000) -> None:
+    """down() == exact rational rounding on random and boundary patterns."""
+    rng = np.random.default_rng(seed)
+    hi = rng.integers(0, 1 << 16, size=n, dtype=np.uint32)
+    lo = np.array([0, 1, 0x7FFF, 0x8000, 0x8001, 0xFFFF], np.uint32)[rng.integers(0, 6, n)]
+    bits = (hi << 16) | lo
+    got = orc.f32_bits_to_bf16(bits)
+    for b, g in zip(bits.tolist(), got.tolist()):
+        e = brute.f32_to_bf16(b)
+        assert g == e, f"{b:#010x}: got {g:#06x} expected {e:#06x}"
+
+
+def pin_bf16_vs_torch(orc, lows=(0, 1, 0x7FFF, 0x8000, 0x8001, 0xFFFF), extra_random=1 << 20,
+                      seed: int = 11) -> None:
+    """down() == PyTorch CPU float32 -> bfloat16 for every high half and each class of
+    dropped bits, plus a random sample; NaNs compared by class only."""
+    import torch
+    hi = np.arange(1 << 16, dtype=np.uint32) << 16
+    parts = [hi | np.uint32(l) for l in lows]
+    if extra_random:
+        parts.append(np.random.default_rng(seed).integers(0, 2**32, size=extra_random,
+                                                          dtype=np.uint64).astype(np.uint32))
+    bits = np.concatenate(parts)
+    got = orc.f32_bits_to_bf16(bits)
+    exp = torch.from_numpy(bits.view(np.float32)).to(torch.bfloat16).view(torch.int16)
+    exp = exp.numpy().view(np.uint16)
+    nan_in = ((bits & 0x7F800000) == 0x7F800000) & ((bits & 0x7FFFFF) != 0)
+    got_nan = ((got & 0x7F80) == 0x7F80) & ((got & 0x7F) != 0)
+    assert np.array_equal(got_nan, nan_in), "NaN class differs"
+    ok = nan_in | (got == exp)
+    if not ok.all():
+        i = int(np.flatnonzero(~ok)[0])
+        raise AssertionError(f"{int(bits[i]):#010x}: got {int(got[i]):#06x} torch {int(exp[i]):#06x}")
+
+
+def pin_up_bf16(orc) -> None:
+    """up() of every bf16 pattern is the exact binary32 whose top half it is."""
+    h = np.arange(1 << 16, dtype=np.uint32).astype(np.uint16)
+    got = orc.bf16_to_f32_bits(h)
+    assert np.array_equal(got, h.astype(np.uint32) << 16)
+
+
+def pin_integer_closed_form(orc, n: int = 1 << 16, P: int = 8, seed: int = 5) -> None:
+    """Integer-valued inputs in [-128,128]: every partial sum is exact in binary32,
+    so the result equals the int64 sum (bf16 output: PyTorch's rounding of it)."""
+    import torch
+    rng = np.random.default_rng(seed)
+    ints = [rng.integers(-128, 129, size=n) for _ in range(P)]
+    exact = np.sum(np.stack(ints), axis=0)
+    srcs32 = [x.astype(np.float32) for x in ints]
+    got32 = orc.allreduce_local(srcs32, "f32", "sum")
+    assert np.array_equal(got32, exact.astype(np.float32)), "f32 integer closed form"
+    srcs16 = [torch.from_numpy(x.astype(np.float32)).to(torch.bfloat16).view(torch.int16)
+              .numpy().view(np.uint16) for x in ints]
+    got16 = orc.allreduce_local(srcs16, "bf16", "sum")
+    exp16 = torch.from_numpy(exact.astype(np.float32)).to(torch.bfloat16).view(torch.int16)
+    assert np.array_equal(got16, exp16.numpy().view(np.uint16)), "bf16 integer closed form"
+    prod_src = [rng.integers(-2, 3, size=n).astype(np.float32) for _ in range(P)]
+    exp_prod = np.prod(np.stack(prod_src).astype(np.int64), axis=0).astype(np.float32)
+    assert np.array_equal(orc.allreduce_local(prod_src, "f32", "prod"), exp_prod)
+
+
+def pin_int_mod32(orc, n: int = 1 << 14, P: int = 32, seed: int = 9) -> None:
+    """int32/uint32 sum and product == numpy int64 arithmetic reduced modulo 2^32;
+    max/min == numpy's signed/unsigned extrema."""
+    rng = np.random.default_rng(seed)
+    raw = [rng.integers(0, 2**32, size=n, dtype=np.uint64) for _ in range(P)]
+    u = [r.astype(np.uint32) for r in raw]
+    i = [x.view(np.int32) for x in u]
+    mask = np.uint64(0xFFFFFFFF)
+    s = np.zeros(n, np.uint64)
+    pr = np.ones(n, np.uint64)
+    for r in raw:
+        s = (s + r) & mask
+        pr = (pr * r) & mask     # exact: both factors < 2^32, product < 2^64
+    for dt, srcs in (("i32", i), ("u32", u)):
+        assert np.array_equal(_bits(orc.allreduce_local(srcs, dt, "sum")), s.astype(np.uint32))
+        assert np.array_equal(_bits(orc.allreduce_local(srcs, dt, "prod")), pr.astype(np.uint32))
+    st = np.stack(i)
+    assert np.array_equal(orc.allreduce_local(i, "i32", "max"), st.max(axis=0))
+    assert np.array_equal(orc.allreduce_local(i, "i32", "min"), st.min(axis=0))
+    ut = np.stack(u)
+    assert np.array_equal(orc.allreduce_local(u, "u32", "max"), ut.max(axis=0))
+    assert np.array_equal(orc.allreduce_local(u, "u32", "min"), ut.min(axis=0))
+
+
+def pin_invariants(orc, n: int = 4099, seed: int = 13) -> None:
+    """All-ones -> P; -0 buffer identity; P=1 copy; permutation invariance of
+    max/min and integer sum."""
+    rng = np.random.default_rng(seed)
+    for P in (1, 2, 7, 64):
+        ones32 = [np.ones(n, np.float32)] * P
+        assert np.all(orc.allreduce_local(ones32, "f32", "sum") == np.float32(P))
+        ones16 = [np.full(n, 0x3F80, np.uint16)] * P
+        got = orc.allreduce_local(ones16, "bf16", "sum")
+        assert np.all(got.astype(np.uint32) << 16 == np.float32(P).view(np.uint32)), P
+    # -0.0 is the bitwise identity for sum (keeps -0 elements as -0)
+    x = random_column_values(rng, "f32", n)
+    x[::5] = np.float32(-0.0)
+    nz = np.full(n, -0.0, np.float32)
+    for srcs in ([x, nz], [nz, x], [x, nz, nz]):
+        got = _bits(orc.allreduce_local(srcs, "f32", "sum"))
+        xb = _bits(x)
+        nan = ((xb & 0x7F800000) == 0x7F800000) & ((xb & 0x7FFFFF) != 0)
+        assert np.array_equal(got[~nan], xb[~nan])
+    # +0.0 is the identity by value, and turns -0 into +0
+    pz = np.zeros(n, np.float32)
+    got = _bits(orc.allreduce_local([x, pz], "f32", "sum"))
+    negz = _bits(x) == 0x80000000
+    assert np.all(got[negz] == 0)
+    # P = 1 is a copy of the source (non-NaN), in every dtype
+    for dt in DTYPES:
+        s = random_column_values(rng, dt, n)
+        sb = _bits(s)
+        for op in OPS:
+            got = _bits(orc.allreduce_local([s], dt, op))
+            if dt in ("f32", "bf16"):
+                nan = np.array([_is_nan_bits(int(v), dt) for v in sb])
+                assert np.array_equal(got[~nan], sb[~nan]), (dt, op)
+            else:
+                assert np.array_equal(got, sb), (dt, op)
+    # max/min over a random permutation of sources: identical bits
+    for dt in ("f32", "bf16", "i32", "u32"):
+        srcs = [random_column_values(rng, dt, n) for _ in range(9)]
+        perm = [srcs[j] for j in rng.permutation(9)]
+        for op in ("max", "min"):
+            a = _bits(orc.allreduce_local(srcs, dt, op))
+            b = _bits(orc.allreduce_local(perm, dt, op))
+            assert np.array_equal(a, b), (dt, op)
+        if dt in ("i32", "u32"):
+            for op in ("sum", "prod"):
+                assert np.array_equal(_bits(orc.allreduce_local(srcs, dt, op)),
+                                      _bits(orc.allreduce_local(perm, dt, op)))
+
+
+def pin_composition(orc, seed: int = 17) -> None:
+    """ReduceScatter shards concatenate to the AllReduce; the step-wise sequence
+    equals the fused left fold; a batch equals its items."""
+    rng = np.random.default_rng(seed)
+    for dt in DTYPES:
+        for op in OPS:
+            P, rc = 5, 37
+            srcs = [random_column_values(rng, dt, P * rc) for _ in range(P)]
+            full = _bits(orc.allreduce_local(srcs, dt, op))
+            for r in range(P):
+                sh = _bits(orc.reduce_scatter_local(srcs, r, dt, op))
+                exp = full[r * rc:(r + 1) * rc]
+                if dt in ("f32", "bf16") and op in ("sum", "prod"):
+                    both_nan = np.array([_is_nan_bits(int(a), dt) and _is_nan_bits(int(b), dt)
+                                         for a, b in zip(sh, exp)], bool)
+                    assert np.array_equal(sh[~both_nan], exp[~both_nan]), (dt, op, r)
+                else:
+                    assert np.array_equal(sh, exp), (dt, op, r)
+            # step-wise: INIT with chunk 0, add chunks 1..P-2, FINAL with chunk P-1;
+            # and INIT + adds + acc_cast; both equal the fused fold over the P chunks
+            chunks = [random_column_values(rng, dt, 53) for _ in range(P)]
+            fused = _bits(orc.allreduce_local(chunks, dt, op))
+            acc = orc.reduce_copy_step(chunks[0], None, dt, op, init=True)
+            for c in chunks[1:-1]:
+                acc = orc.reduce_copy_step(c, acc, dt, op)
+            acc_copy = acc.copy()
+            fin = _bits(orc.reduce_copy_step(chunks[-1], acc, dt, op, final=True))
+            assert np.array_equal(_bits(acc), _bits(acc_copy)), "FINAL must not write acc"
+            acc2 = orc.reduce_copy_step(chunks[-1], acc_copy, dt, op)
+            cast = _bits(orc.acc_cast(acc2, dt))
+            for got in (fin, cast):
+                if dt in ("f32", "bf16") and op in ("sum", "prod"):
+                    mask = np.array([not (_is_nan_bits(int(a), dt) and _is_nan_bits(int(b), dt))
+                                     for a, b in zip(got, fused)], bool)
+                    assert np.array_equal(got[mask], fused[mask]), (dt, op)
+                else:
+                    assert np.array_equal(got, fused), (dt, op)
+            one = _bits(orc.reduce_copy_step(chunks[0], None, dt, op, init=True, final=True))
+            assert np.array_equal(one, _bits(orc.allreduce_local([chunks[0]], dt, op)))
+    # batch == items
+    items = []
+    for k in range(6):
+        P = int(rng.integers(1, 9))
+        n = int(rng.integers(1, 300))
+        items.append([random_column_values(rng, "bf16", n) for _ in range(P)])
+    outs = orc.batched_reduce(items, "bf16", "sum")
+    for srcs, out in zip(items, outs):
+        exp = orc.allreduce_local(srcs, "bf16", "sum")
+        nan = np.array([_is_nan_bits(int(v), "bf16") for v in exp], bool)
+        assert np.array_equal(out[~nan], exp[~nan])
+
+
+def pin_selfcheck(orc) -> None:
+    assert orc.selfcheck() == 0, "floating-point environment"
+
+
+FAST_PINS = [pin_selfcheck, pin_golden_reduce, pin_golden_bf16, pin_bf16_vs_brute,
+             pin_up_bf16, pin_integer_closed_form, pin_int_mod32, pin_invariants,
+             pin_composition, pin_bruteforce]
