@@ -1,0 +1,365 @@
+#!/usr/bin/env python3
+"""Benchmark of libxred on one MI355X.
+
+The headline step is one xred_allreduce_local call on the gradient-bucket
+workload: P=8 source buffers x 64M bf16 (128 MiB each), binary32
+accumulation in rank order, bf16 output.  Throughput counts algorithmic bytes
+(P+1)*N*sizeof per call, with inputs resident in HBM before timing starts.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-secondary] [--no-cpu-baseline]
+
+Prints ONE JSON line on stdout.  Timing: W untimed calls, then K calls
+bracketed by a synchronisation and HIP events recorded on the stream the
+kernels are launched on; ms_per_step = event time / K.  The roofline object
+uses the same events; `traffic` comes from the committed rocprofv3 counter
+summary of the same kernel and is null when the kernel sources changed since.
+The cpu_baseline object times the CPU oracle on a bounded sample on this
+host.  Secondary workloads (the other configurations) are reported under
+"secondary" and are not part of `value`.
+"""
+from __future__ import annotations
+
+import argparse
+import ctypes
+import hashlib
+import json
+import os
+import re
+import sys
+import time
+from pathlib import Path
+
+ROOT = Path(__file__).resolve().parent
+sys.path.insert(0, str(ROOT))
+
+METRIC = "reduce-copy GB/s (read+write) and % HBM peak at 1 GPU; small-msg µs/call"
+HBM_PEAK_GBS = 8000.0     # MI355X HBM3E, published
+PROFILE = ROOT / "profiles" / "reduce_bf16_sum_p8_64M.md"
+KERNEL_SOURCES = ["paper_2510_20171_amd/csrc/xred_device.hpp",
+                  "paper_2510_20171_amd/csrc/xred_kernels.hpp",
+                  "paper_2510_20171_amd/csrc/xred_reduce.hip"]
+
+
+def kernel_source_sha() -> str:
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES:
+        h.update((ROOT / f).read_bytes())
+    return h.hexdigest()[:16]
+
+
+def committed_traffic():
+    """HBM bytes per launch from the committed counter summary, if it still
+    describes the current kernel sources."""
+    if not PROFILE.exists():
+        return None
+    text = PROFILE.read_text()
+    sha = re.search(r"kernel_source_sha:\s*([0-9a-f]+)", text)
+    tb = re.search(r"traffic_bytes_per_launch:\s*([0-9.eE+]+)", text)
+    if not sha or not tb or sha.group(1) != kernel_source_sha():
+        return None
+    return float(tb.group(1))
+
+
+def log(msg: str) -> None:
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+class Timer:
+    """HIP events on the current stream (the stream every call is launched on)."""
+
+    def __init__(self, torch):
+        self.torch = torch
+        self.e0 = torch.cuda.Event(enable_timing=True)
+        self.e1 = torch.cuda.Event(enable_timing=True)
+
+    def loop_ms(self, fn, reps: int, warm: int = 3) -> float:
+        for _ in range(warm):
+            fn()
+        self.torch.cuda.synchronize()
+        self.e0.record()
+        for _ in range(reps):
+            fn()
+        self.e1.record()
+        self.e1.synchronize()
+        return self.e0.elapsed_time(self.e1) / reps
+
+    def cold_ms(self, fn, reps: int, flush) -> list:
+        out = []
+        for _ in range(reps):
+            flush.zero_()          # 1 GiB write evicts L2 and the 256 MB MALL
+            self.e0.record()
+            fn()
+            self.e1.record()
+            self.e1.synchronize()
+            out.append(self.e0.elapsed_time(self.e1))
+        return out
+
+
+def median(xs):
+    xs = sorted(xs)
+    return xs[len(xs) // 2]
+
+
+def dev_bf16(torch, a):
+    import numpy as np
+    return torch.from_numpy(a.view(np.int16)).view(torch.bfloat16).to("cuda")
+
+
+def dev_any(torch, a, dtype):
+    import numpy as np
+    if dtype == "bf16":
+        return dev_bf16(torch, a)
+    if dtype == "f32":
+        return torch.from_numpy(a).to("cuda")
+    return torch.from_numpy(a.view(np.int32)).to("cuda")
+
+
+def reduce_call(L, xr, srcs, out, dtype, op):
+    """A prebuilt C-ABI call (no per-call Python marshalling in the timed loop)."""
+    arr = xr._lib.ptr_array([s.data_ptr() for s in srcs])
+    n, P = out.numel(), len(srcs)
+    dptr = ctypes.c_void_p(out.data_ptr())
+    dt, o = xr.DTYPE[dtype], xr.OP[op]
+    import torch
+    stream = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+    def fn():
+        st = L.xred_allreduce_local(arr, P, dptr, n, dt, o, stream)
+        if st:
+            xr._lib.check(st)
+    fn._keep = arr
+    return fn
+
+
+def cpu_baseline(srcs_np, dtype, op, P, es, target_s=10.0):
+    import oracle
+    orc = oracle.load()
+    cores = min(16, oracle.host_cores())
+    n = srcs_np[0].size
+    t0 = time.perf_counter()
+    orc.allreduce_local(srcs_np, dtype, op, nthreads=cores)
+    t1 = time.perf_counter() - t0
+    reps = max(1, int(target_s / max(t1, 1e-3)))
+    t0 = time.perf_counter()
+    for _ in range(reps):
+        orc.allreduce_local(srcs_np, dtype, op, nthreads=cores)
+    el = time.perf_counter() - t0
+    gbs = (P + 1) * n * es * reps / el / 1e9
+    return {"value": round(gbs, 3), "unit": "GB/s", "cores": cores, "kind": "oracle",
+            "sample": f"first {n} elements of each of the P={P} sources, {reps} reps, "
+                      f"{el:.1f} s, OpenMP over elements"}
+
+
+def secondary(torch, xr, L, timer, wl, flush):
+    import numpy as np
+    res = {}
+    # copy ceiling (torch's device copy kernel), 1 GiB -> 1 GiB
+    a = torch.empty(1 << 29, dtype=torch.int16, device="cuda")
+    b = torch.empty_like(a)
+    ms = timer.loop_ms(lambda: b.copy_(a), 10)
+    res["copy_ceiling_GBs"] = round(2 * a.numel() * 2 / (ms * 1e-3) / 1e9, 1)
+    del a, b
+
+    # c1: P=4 x 1M f32 (20 MiB: cache resident); warm and cold
+    w = wl.WORKLOADS["c1"]
+    d = [dev_any(torch, s, "f32") for s in wl.sources(w)]
+    out = torch.empty_like(d[0])
+    fn = reduce_call(L, xr, d, out, "f32", "sum")
+    ab = w.alg_bytes()
+    warm = timer.loop_ms(fn, 1000)
+    cold = median(timer.cold_ms(fn, 30, flush))
+    t0 = time.perf_counter()
+    fn()
+    torch.cuda.synchronize()
+    wall_us = (time.perf_counter() - t0) * 1e6
+    res["c1"] = {"us_per_call_warm": round(warm * 1e3, 2), "GBs_warm": round(ab / warm / 1e6, 1),
+                 "us_cold": round(cold * 1e3, 2), "GBs_cold": round(ab / cold / 1e6, 1),
+                 "us_single_call_wall": round(wall_us, 1)}
+    del d, out
+
+    # c3: step-wise ring, 16 chunks x 1M bf16 into a binary32 accumulator
+    w = wl.WORKLOADS["c3"]
+    chunks = [dev_bf16(torch, c.copy()) for c in wl.stepwise_chunks(w)]
+    acc = torch.empty(w.count, dtype=torch.float32, device="cuda")
+    out = torch.empty_like(chunks[0])
+    stream = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    cp = [ctypes.c_void_p(c.data_ptr()) for c in chunks]
+    ap, op_ = ctypes.c_void_p(acc.data_ptr()), ctypes.c_void_p(out.data_ptr())
+
+    def seq():
+        L.xred_reduce_copy_step(cp[0], ap, None, w.count, 1, 0, 1, stream)
+        for c in cp[1:]:
+            L.xred_reduce_copy_step(c, ap, None, w.count, 1, 0, 0, stream)
+        L.xred_acc_cast(ap, op_, w.count, 1, stream)
+
+    def steps15():
+        for c in cp[1:]:
+            L.xred_reduce_copy_step(c, ap, None, w.count, 1, 0, 0, stream)
+    seq_ms = timer.loop_ms(seq, 50)
+    st_ms = timer.loop_ms(steps15, 50) / 15
+    fused = torch.empty_like(out)
+    ffn = reduce_call(L, xr, chunks, fused, "bf16", "sum")
+    fused_ms = timer.loop_ms(ffn, 50)
+    moved = 16 * w.count * 2 + 15 * w.count * 8 + w.count * 4 + w.count * 4 + w.count * 2
+    res["c3"] = {"us_per_step": round(st_ms * 1e3, 2),
+                 "step_GBs_moved": round(w.count * 10 / st_ms / 1e6, 1),
+                 "us_sequence": round(seq_ms * 1e3, 2),
+                 "sequence_GBs_alg": round(17 * w.count * 2 / seq_ms / 1e6, 1),
+                 "sequence_GBs_moved": round(moved / seq_ms / 1e6, 1),
+                 "fused_16src_us": round(fused_ms * 1e3, 2),
+                 "fused_16src_GBs": round(17 * w.count * 2 / fused_ms / 1e6, 1)}
+    del chunks, acc, out, fused
+
+    # c5a / c5b: P=32 x 8M
+    for name in ("c5a", "c5b"):
+        w = wl.WORKLOADS[name]
+        d = [dev_any(torch, s, w.dtype) for s in wl.sources(w)]
+        out = torch.empty_like(d[0])
+        fn = reduce_call(L, xr, d, out, w.dtype, w.op)
+        ms = timer.loop_ms(fn, 20)
+        gbs = w.alg_bytes() / ms / 1e6
+        res[name] = {"us": round(ms * 1e3, 1), "GBs": round(gbs, 1),
+                     "pct_hbm_peak": round(100 * gbs / HBM_PEAK_GBS, 1)}
+        del d, out
+
+    # c4: 4096 small reductions in one launch (host and device descriptors)
+    w = wl.WORKLOADS["c4"]
+    sizes = wl.batched_sizes(w)
+    arena, offs = wl.batched_arena(w, sizes)
+    arena_d = dev_bf16(torch, arena)
+    del arena
+    base = arena_d.data_ptr()
+    # outputs packed at 128-element (256 B) boundaries: item k at opos[k]
+    ends = np.cumsum((sizes + 127) // 128 * 128)
+    opos = np.concatenate([[0], ends[:-1]]).astype(np.int64)
+    outs = torch.empty(int(ends[-1]), dtype=torch.bfloat16, device="cuda")
+    assert int(opos[-1]) + int(sizes[-1]) <= outs.numel()
+    P = offs.shape[1]
+    ptr_rows = [(ctypes.c_void_p * P)(*[base + int(o) * 2 for o in offs[k]]) for k in range(len(sizes))]
+    items = xr.pack_items([(ctypes.addressof(ptr_rows[k]), outs.data_ptr() + int(opos[k]) * 2,
+                            int(sizes[k]), P) for k in range(len(sizes))])
+    K = len(sizes)
+    host_fn = lambda: L.xred_batched_reduce(items, K, 1, 0, 0, stream)  # noqa: E731
+    ptrs_d = torch.tensor((base + offs * 2).reshape(-1).astype(np.int64), device="cuda")
+    arr = np.zeros(K, xr.ITEM_DTYPE)
+    arr["srcs"] = ptrs_d.data_ptr() + 8 * P * np.arange(K, dtype=np.uint64)
+    arr["dst"] = outs.data_ptr() + opos.astype(np.uint64) * 2
+    arr["count"] = sizes
+    arr["nsrc"] = P
+    items_d = torch.from_numpy(arr.view(np.uint8).copy()).to("cuda")
+    dev_fn = lambda: L.xred_batched_reduce(ctypes.c_void_p(items_d.data_ptr()), K, 1, 0, 1,  # noqa
+                                           stream)
+    ab = w.alg_bytes(sizes)
+    host_ms = timer.loop_ms(host_fn, 10)
+    dev_ms = timer.loop_ms(dev_fn, 10)
+    singles = [reduce_call(L, xr, [arena_d[int(o):int(o) + int(sizes[k])] for o in offs[k]],
+                           outs[int(opos[k]):int(opos[k]) + int(sizes[k])], "bf16", "sum")
+               for k in range(K)]
+
+    def all_singles():
+        for f in singles:
+            f()
+    sep_ms = timer.loop_ms(all_singles, 3, warm=1)
+    res["c4"] = {"alg_bytes": ab, "items": K,
+                 "host_desc_us": round(host_ms * 1e3, 1), "host_desc_GBs": round(ab / host_ms / 1e6, 1),
+                 "device_desc_us": round(dev_ms * 1e3, 1),
+                 "device_desc_GBs": round(ab / dev_ms / 1e6, 1),
+                 "us_per_item": round(host_ms * 1e3 / K, 3),
+                 "separate_calls_us": round(sep_ms * 1e3, 1),
+                 "separate_calls_GBs": round(ab / sep_ms / 1e6, 1)}
+    del arena_d, outs, items_d, ptrs_d, singles
+
+    # small-message latency: P=8 bf16, back-to-back and single call
+    lat = {}
+    for kib in (8, 64, 1024, 8192):
+        n = kib * 1024 // 2
+        d = [torch.randn(n, device="cuda").to(torch.bfloat16) for _ in range(8)]
+        out = torch.empty_like(d[0])
+        fn = reduce_call(L, xr, d, out, "bf16", "sum")
+        ms = timer.loop_ms(fn, 1000 if kib <= 1024 else 200)
+        lat[f"{kib}KiB"] = {"us_per_call": round(ms * 1e3, 2),
+                            "GBs": round(9 * n * 2 / ms / 1e6, 1)}
+        del d, out
+    res["latency_p8_bf16"] = lat
+    return res
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--no-secondary", action="store_true")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: the reduce step runs on a single MI355X and "
+              "this build has no multi-GPU path; run with --gpus 1.", file=sys.stderr)
+        return 2
+
+    import numpy as np
+    import torch
+
+    import paper_2510_20171_amd as xr
+    import workloads as wl
+
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        return 1
+    L = xr.load()
+    timer = Timer(torch)
+    w = wl.WORKLOADS["c2"]
+    log("generating c2 inputs (P=8 x 64M bf16)")
+    srcs_np = wl.sources(w)
+    d = [dev_bf16(torch, s) for s in srcs_np]
+    out = torch.empty_like(d[0])
+    step = reduce_call(L, xr, d, out, "bf16", "sum")
+    ab = w.alg_bytes()
+
+    log(f"timing {args.steps} steps after {args.warmup} warmup")
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    timer.e0.record()
+    for _ in range(args.steps):
+        step()
+    timer.e1.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms = timer.e0.elapsed_time(timer.e1) / args.steps
+    gbs = ab / (ms * 1e-3) / 1e9
+
+    result = {
+        "metric": METRIC, "value": round(gbs, 1), "unit": "GB/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 5),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": "gradient bucket: allreduce_local P=8 x 2^26 bf16, sum, "
+                               "binary32 accumulation in rank order, bf16 out",
+                   "P": 8, "N": w.count, "io_dtype": "bf16", "accumulate": "f32",
+                   "alg_bytes_per_step": ab, "parallelism": "single GPU"},
+        "pct_hbm_peak": round(100 * gbs / HBM_PEAK_GBS, 2),
+        "wall_s_timed": round(wall, 4),
+        "roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4),
+                     "traffic": committed_traffic(),
+                     "kernel": "reduce_vec_kernel<TBF16, OpSum, 8>",
+                     "kernel_source_sha": kernel_source_sha()},
+    }
+    if not args.no_cpu_baseline:
+        log("timing the CPU oracle on a sample")
+        sample = [s[: 1 << 22] for s in srcs_np]
+        result["cpu_baseline"] = cpu_baseline(sample, "bf16", "sum", 8, 2)
+    del d, out, srcs_np
+    torch.cuda.empty_cache()
+    if not args.no_secondary:
+        log("secondary workloads")
+        flush = torch.empty(1 << 28, dtype=torch.float32, device="cuda")
+        result["secondary"] = secondary(torch, xr, L, timer, wl, flush)
+    print(json.dumps(result), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -1,0 +1,200 @@
+/*
+ * xred.h -- C ABI of libxred: one rank's reduce step of ReduceScatter /
+ * AllReduce on an AMD Instinct MI355X (gfx950).
+ *
+ * In a ring or one-shot ReduceScatter/AllReduce every rank, at every step,
+ * reduces the chunk it received with its own chunk and forwards or keeps the
+ * result (the FTAR ring pipeline and its fused ReduceCopy, Section 5 "HSDP:
+ * Fault tolerant AllReduce"; collective semantics as in NCCL, Section 2.2).
+ * This library performs that reduce step on one GPU, with the P peer buffers
+ * already resident in local HBM.
+ *
+ * Definition computed by every entry point, for each element index i
+ * independently:
+ *
+ *     out[i] = down( up(src[0][i]) (+) up(src[1][i]) (+) ... (+) up(src[P-1][i]) )
+ *
+ *   - a LEFT fold in source order 0..P-1 (the order is fixed, so float
+ *     results are deterministic and bit-reproducible);
+ *   - up(): bf16 -> binary32 (exact), fp32 -> binary32, int32/uint32 -> uint32;
+ *     the accumulator is binary32 for float types and uint32 for integer types;
+ *   - (+): XRED_SUM  binary32 add (round to nearest even, subnormals kept) or
+ *                    addition modulo 2^32;
+ *          XRED_PROD binary32 multiply, or the low 32 bits of the product;
+ *          XRED_MAX / XRED_MIN  float: total order -inf < ... < -0 < +0 < ...
+ *                    < +inf, any NaN operand gives the quiet NaN 0x7FC00000;
+ *                    int32 signed, uint32 unsigned;
+ *   - the accumulator starts from up(src[0][i]) (never from zero), so a column
+ *     of -0.0 sums to -0.0;
+ *   - down(): binary32 -> bf16 round to nearest even (overflow to +-inf),
+ *     identity otherwise.  NaN payloads of SUM/PROD results are unspecified.
+ *
+ * Conventions shared by every call:
+ *   - All functions are thread-safe, never print and never abort.
+ *   - Buffers are device pointers owned by the caller; so is the stream
+ *     (a hipStream_t passed as void*, NULL = the default stream).
+ *   - Every call is stream-ordered and returns once the work is enqueued.
+ *     Host arrays passed in (the srcs pointer array, host-side items) are
+ *     consumed before the call returns and may be reused at once.
+ *   - Every argument is validated before anything is enqueued: on any return
+ *     other than XRED_SUCCESS nothing was enqueued and xred_last_error()
+ *     describes the problem.  count == 0 succeeds with no launch.
+ *   - Device faults (e.g. a pointer to freed memory) surface at the caller's
+ *     next synchronisation of the stream, as for any HIP kernel.
+ *   - Element pointers must be aligned to the element size; 16-byte aligned
+ *     buffers take the fast vector path, other alignments a slower scalar one.
+ */
+#ifndef XRED_H
+#define XRED_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define XRED_API __attribute__((visibility("default")))
+
+typedef enum {
+    XRED_FLOAT32 = 0,
+    XRED_BFLOAT16 = 1,
+    XRED_FLOAT16 = 2,   /* reserved: currently returns XRED_UNSUPPORTED */
+    XRED_INT32 = 3,
+    XRED_UINT32 = 4
+} xred_dtype;
+
+typedef enum { XRED_SUM = 0, XRED_PROD = 1, XRED_MAX = 2, XRED_MIN = 3 } xred_op;
+
+typedef enum {
+    XRED_SUCCESS = 0,
+    XRED_INVALID_ARGUMENT = 1,
+    XRED_UNSUPPORTED = 2,
+    XRED_ALIAS = 3,
+    XRED_HIP_ERROR = 4,
+    XRED_OUT_OF_MEMORY = 5
+} xred_status;
+
+enum { XRED_MAX_SRC = 64 };
+enum { XRED_STEP_INIT = 1u, XRED_STEP_FINAL = 2u }; /* xred_reduce_copy_step flags */
+enum { XRED_ITEMS_ON_DEVICE = 1u };                 /* xred_batched_reduce flag    */
+
+/* One reduction of a batch: dst[i] = fold over srcs[0..nsrc) of element i,
+ * for i < count.  32 bytes, naturally aligned. */
+typedef struct {
+    const void *const *srcs; /* nsrc source pointers (host or device array, see flags) */
+    void *dst;               /* count output elements                                  */
+    uint64_t count;          /* elements per source and in dst                         */
+    uint32_t nsrc;           /* 1..XRED_MAX_SRC                                        */
+    uint32_t reserved;       /* must be 0                                              */
+} xred_item;
+
+/*
+ * AllReduce's local reduce (the per-rank reduction of FTAR's ring, Section 5;
+ * AllReduce semantics, Section 2.2): dst[i] = fold_{p=0..nsrc-1} srcs[p][i],
+ * i < count.
+ *   srcs     host array of nsrc device pointers, each to count elements of dtype
+ *   nsrc     1..XRED_MAX_SRC
+ *   dst      device pointer to count elements of dtype.  dst may equal any
+ *            srcs[p] exactly (in place); any other overlap is XRED_ALIAS.
+ * Errors: XRED_INVALID_ARGUMENT (nsrc out of range, NULL or misaligned
+ * pointer with count > 0, count*size overflow), XRED_UNSUPPORTED (dtype/op),
+ * XRED_ALIAS, XRED_HIP_ERROR (launch failure).
+ */
+XRED_API xred_status xred_allreduce_local(const void *const *srcs, int nsrc, void *dst,
+                                          size_t count, xred_dtype dtype, xred_op op,
+                                          void *hip_stream);
+
+/*
+ * ReduceScatter's local reduce for rank `rank` (ReduceScatter semantics,
+ * Section 2.2; the ReduceScatter phase of FTAR's ring, Section 5):
+ * srcs[p] is rank p's full send buffer of nsrc*recvcount elements and
+ *     dst[i] = fold_{p} srcs[p][rank*recvcount + i],  i < recvcount.
+ *   rank     0 <= rank < nsrc
+ *   dst      recvcount elements; may equal srcs[p] + rank*recvcount exactly
+ *            (in place); any other overlap with a read slice is XRED_ALIAS.
+ * Errors: as xred_allreduce_local, plus rank out of range.
+ */
+XRED_API xred_status xred_reduce_scatter_local(const void *const *srcs, int nsrc, int rank,
+                                               void *dst, size_t recvcount, xred_dtype dtype,
+                                               xred_op op, void *hip_stream);
+
+/*
+ * One step of a ring's ReduceCopy (the RedCopy / Reduce kernel operations of
+ * the FTAR pipeline, Section 5): fold one incoming chunk into a local
+ * accumulator chunk.
+ *   flags 0                  acc[i] = acc[i] (+) up(in[i])
+ *   XRED_STEP_INIT           acc[i] = up(in[i])              (acc not read)
+ *   XRED_STEP_FINAL          dst[i] = down(acc[i] (+) up(in[i]))   (acc not written)
+ *   INIT | FINAL             dst[i] = down(up(in[i]))              (acc unused)
+ *   in       count elements of dtype
+ *   acc      count accumulator elements of xred_acc_elem_size(dtype) bytes
+ *            (binary32 for float dtypes, uint32 for integer dtypes), 4-byte
+ *            aligned; may be NULL only for INIT|FINAL
+ *   dst      count elements of dtype, used only with FINAL (may be NULL otherwise)
+ * Buffers must not overlap, except dst == in exactly.
+ * Errors: XRED_INVALID_ARGUMENT (unknown flag bits, NULL/misaligned pointer,
+ * overflow), XRED_UNSUPPORTED, XRED_ALIAS, XRED_HIP_ERROR.
+ */
+XRED_API xred_status xred_reduce_copy_step(const void *in, void *acc, void *dst, size_t count,
+                                           xred_dtype dtype, xred_op op, unsigned flags,
+                                           void *hip_stream);
+
+/*
+ * Closing cast of a step-wise sequence: dst[i] = down(acc[i]), i < count.
+ *   acc      count accumulator elements (see xred_reduce_copy_step)
+ *   dst      count elements of dtype; must not overlap acc
+ */
+XRED_API xred_status xred_acc_cast(const void *acc, void *dst, size_t count, xred_dtype dtype,
+                                   void *hip_stream);
+
+/*
+ * Many independent reductions in one launch, for latency-bound small messages
+ * (the per-message software overhead T_c of the LogP model in Section 6.2 is
+ * paid once per batch instead of once per message).  Each item computes the
+ * xred_allreduce_local definition over its own sources.
+ *   items    nitems descriptors.
+ *   flags 0: `items` and every items[k].srcs are HOST memory, consumed before
+ *            return (metadata by value).  Every item is validated as in
+ *            xred_allreduce_local; the library stages the descriptors into
+ *            device memory it owns (pinned staging slots reused once the
+ *            launch that read them has completed).
+ *   XRED_ITEMS_ON_DEVICE: `items` and every items[k].srcs are DEVICE memory,
+ *            read when the kernels run, so an earlier kernel on the stream may
+ *            still write them (metadata by reference, after the GPU-resident
+ *            collectives of Section 6.1).  No host work per item; safe to
+ *            capture in a HIP graph once a first call on the device has
+ *            created the library's planning workspace.  Items that cannot be
+ *            run safely (nsrc outside 1..64, a NULL pointer, reserved != 0)
+ *            are skipped and their dst is left untouched; pointers are
+ *            otherwise trusted.
+ *   Items of one batch must not write memory another item reads or writes.
+ * Errors: XRED_INVALID_ARGUMENT (nitems < 0, bad item in host mode, unknown
+ * flags), XRED_UNSUPPORTED, XRED_ALIAS (host mode, within an item),
+ * XRED_OUT_OF_MEMORY (staging or workspace allocation), XRED_HIP_ERROR.
+ */
+XRED_API xred_status xred_batched_reduce(const xred_item *items, int nitems, xred_dtype dtype,
+                                         xred_op op, unsigned flags, void *hip_stream);
+
+/* Bytes per accumulator element for dtype: 4 (binary32 or uint32), 0 if unknown. */
+XRED_API size_t xred_acc_elem_size(xred_dtype dtype);
+
+/* Static, human-readable name of a status code. */
+XRED_API const char *xred_status_string(xred_status s);
+
+/* Detail of the last failed call on the calling thread ("" if none). */
+XRED_API const char *xred_last_error(void);
+
+/* Library version: major*10000 + minor*100 + patch. */
+XRED_API int xred_version(void);
+
+/* Frees the library's staging buffers and workspaces on every device after
+ * synchronising the device work that uses them.  Optional; later calls
+ * re-create what they need. */
+XRED_API void xred_release(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* XRED_H */

@@ -1,0 +1,139 @@
+"""libxred: one rank's reduce step of ReduceScatter / AllReduce on MI355X.
+
+Thin Python binding over the C ABI in include/xred.h (argument marshalling
+only; every step runs in the HIP kernels of libxred.so).  PyTorch supplies
+device memory and streams: tensors are passed as data pointers and the
+current HIP stream of the tensor's device is used unless one is given.
+
+    import torch, paper_2510_20171_amd as xr
+    srcs = [torch.randn(1 << 20, device="cuda", dtype=torch.bfloat16) for _ in range(8)]
+    out = torch.empty_like(srcs[0])
+    xr.allreduce_local(srcs, out)                     # out = srcs[0] + ... + srcs[7]
+
+Element types are taken from the tensors (float32, bfloat16, int32, uint32)
+or forced with ``dtype=`` ("f32", "bf16", "i32", "u32"), e.g. to treat int32
+storage as uint32.
+"""
+from __future__ import annotations
+
+import ctypes
+
+from ._lib import (ALIAS, DTYPE, EXPORTS, HIP_ERROR, INVALID_ARGUMENT, ITEM_DTYPE,
+                   ITEMS_ON_DEVICE, MAX_SRC, OP, OUT_OF_MEMORY, STEP_FINAL, STEP_INIT, SUCCESS,
+                   UNSUPPORTED, XredError, XredItem, check, load, ptr_array)
+
+__all__ = ["allreduce_local", "reduce_scatter_local", "reduce_copy_step", "acc_cast",
+           "batched_reduce", "pack_items", "acc_elem_size", "version", "release", "XredError",
+           "load", "EXPORTS"]
+
+
+def _torch_dtype_name(t) -> str:
+    import torch
+    m = {torch.float32: "f32", torch.bfloat16: "bf16", torch.int32: "i32",
+         torch.float16: "f16"}
+    if hasattr(torch, "uint32"):
+        m[torch.uint32] = "u32"
+    try:
+        return m[t.dtype]
+    except KeyError:
+        raise XredError(INVALID_ARGUMENT, f"tensor dtype {t.dtype} is not supported") from None
+
+
+def _dtype(t, dtype):
+    return DTYPE[dtype] if dtype is not None else DTYPE[_torch_dtype_name(t)]
+
+
+def _stream(t, stream):
+    if stream is not None:
+        return ctypes.c_void_p(int(getattr(stream, "cuda_stream", stream)))
+    import torch
+    return ctypes.c_void_p(torch.cuda.current_stream(t.device).cuda_stream)
+
+
+def _ptr(t):
+    return ctypes.c_void_p(t.data_ptr()) if t is not None else ctypes.c_void_p(0)
+
+
+def allreduce_local(srcs, out, op: str = "sum", *, dtype=None, stream=None) -> None:
+    """out[i] = fold_op(srcs[0][i], ..., srcs[P-1][i]) in source order (xred_allreduce_local)."""
+    L = load()
+    n = out.numel()
+    check(L.xred_allreduce_local(ptr_array([s.data_ptr() for s in srcs]), len(srcs), _ptr(out),
+                                 n, _dtype(out, dtype), OP[op], _stream(out, stream)))
+
+
+def reduce_scatter_local(srcs, rank: int, out, op: str = "sum", *, dtype=None,
+                         stream=None) -> None:
+    """Shard `rank` of a ReduceScatter over full send buffers srcs (xred_reduce_scatter_local)."""
+    L = load()
+    check(L.xred_reduce_scatter_local(ptr_array([s.data_ptr() for s in srcs]), len(srcs), rank,
+                                      _ptr(out), out.numel(), _dtype(out, dtype), OP[op],
+                                      _stream(out, stream)))
+
+
+def reduce_copy_step(inp, acc, out=None, op: str = "sum", *, init: bool = False,
+                     final: bool = False, dtype=None, stream=None) -> None:
+    """One ring ReduceCopy step into a 4-byte accumulator (xred_reduce_copy_step)."""
+    L = load()
+    flags = (STEP_INIT if init else 0) | (STEP_FINAL if final else 0)
+    check(L.xred_reduce_copy_step(_ptr(inp), _ptr(acc), _ptr(out), inp.numel(),
+                                  _dtype(inp, dtype), OP[op], flags, _stream(inp, stream)))
+
+
+def acc_cast(acc, out, *, dtype=None, stream=None) -> None:
+    """out = down(acc): closing cast of a step-wise sequence (xred_acc_cast)."""
+    L = load()
+    check(L.xred_acc_cast(_ptr(acc), _ptr(out), out.numel(), _dtype(out, dtype),
+                          _stream(out, stream)))
+
+
+def pack_items(items):
+    """Host xred_item array for [(srcs_pointer_array_address, dst_ptr, count, nsrc), ...]."""
+    arr = (XredItem * max(1, len(items)))()
+    for k, (srcs_addr, dst, count, nsrc) in enumerate(items):
+        arr[k].srcs = srcs_addr
+        arr[k].dst = dst
+        arr[k].count = count
+        arr[k].nsrc = nsrc
+        arr[k].reserved = 0
+    return arr
+
+
+def batched_reduce(items, op: str = "sum", *, dtype: str, stream=None, device=None) -> None:
+    """Many reductions in one launch (xred_batched_reduce).
+
+    items: list of (srcs, out) tensor pairs (descriptors built on the host,
+    passed by value), or a CUDA uint8/int64 tensor holding packed xred_item
+    descriptors in device memory (metadata by reference; each item's srcs
+    field must point to a device array of source pointers)."""
+    L = load()
+    import torch
+    if isinstance(items, torch.Tensor):
+        if not items.is_cuda:
+            raise XredError(INVALID_ARGUMENT, "device descriptors must be a CUDA tensor")
+        n = items.numel() * items.element_size() // ITEM_DTYPE.itemsize
+        st = _stream(items, stream)
+        check(L.xred_batched_reduce(_ptr(items), n, DTYPE[dtype], OP[op], ITEMS_ON_DEVICE, st))
+        return
+    keep = []
+    rows = []
+    for srcs, out in items:
+        pa = ptr_array([s.data_ptr() for s in srcs])
+        keep.append(pa)
+        rows.append((ctypes.addressof(pa), out.data_ptr(), out.numel(), len(srcs)))
+    arr = pack_items(rows)
+    dev_t = items[0][1] if items else None
+    st = _stream(dev_t, stream) if dev_t is not None else ctypes.c_void_p(0)
+    check(L.xred_batched_reduce(arr, len(rows), DTYPE[dtype], OP[op], 0, st))
+
+
+def acc_elem_size(dtype: str) -> int:
+    return int(load().xred_acc_elem_size(DTYPE[dtype]))
+
+
+def version() -> int:
+    return int(load().xred_version())
+
+
+def release() -> None:
+    load().xred_release()

@@ -1,0 +1,93 @@
+"""ctypes loader for libxred.so (the HIP C ABI declared in include/xred.h).
+
+There is no fallback: if the library is not built this module raises on
+first use, so no computation can silently happen anywhere but in the HIP
+kernels.
+"""
+from __future__ import annotations
+
+import ctypes
+from pathlib import Path
+
+import numpy as np
+
+LIB_PATH = Path(__file__).resolve().parent / "libxred.so"
+
+# Values of the enums in include/xred.h.
+DTYPE = {"f32": 0, "bf16": 1, "f16": 2, "i32": 3, "u32": 4}
+OP = {"sum": 0, "prod": 1, "max": 2, "min": 3}
+STATUS = {0: "XRED_SUCCESS", 1: "XRED_INVALID_ARGUMENT", 2: "XRED_UNSUPPORTED", 3: "XRED_ALIAS",
+          4: "XRED_HIP_ERROR", 5: "XRED_OUT_OF_MEMORY"}
+SUCCESS, INVALID_ARGUMENT, UNSUPPORTED, ALIAS, HIP_ERROR, OUT_OF_MEMORY = range(6)
+MAX_SRC = 64
+STEP_INIT, STEP_FINAL = 1, 2
+ITEMS_ON_DEVICE = 1
+
+# struct xred_item (32 bytes)
+ITEM_DTYPE = np.dtype([("srcs", "<u8"), ("dst", "<u8"), ("count", "<u8"), ("nsrc", "<u4"),
+                       ("reserved", "<u4")])
+assert ITEM_DTYPE.itemsize == 32
+
+
+class XredItem(ctypes.Structure):
+    _fields_ = [("srcs", ctypes.c_void_p), ("dst", ctypes.c_void_p), ("count", ctypes.c_uint64),
+                ("nsrc", ctypes.c_uint32), ("reserved", ctypes.c_uint32)]
+
+
+EXPORTS = ("xred_allreduce_local", "xred_reduce_scatter_local", "xred_reduce_copy_step",
+           "xred_acc_cast", "xred_batched_reduce", "xred_acc_elem_size", "xred_status_string",
+           "xred_last_error", "xred_version", "xred_release")
+
+_lib = None
+
+
+class XredError(RuntimeError):
+    """A libxred call returned a status other than XRED_SUCCESS."""
+
+    def __init__(self, status: int, detail: str):
+        self.status = status
+        self.name = STATUS.get(status, f"status {status}")
+        super().__init__(f"{self.name}: {detail}")
+
+
+def load(path: Path = LIB_PATH) -> ctypes.CDLL:
+    """Load libxred.so (once) and declare the C signatures."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not Path(path).exists():
+        raise ImportError(f"{path} is not built: run `python -m paper_2510_20171_amd.build` "
+                          "(there is no CPU fallback)")
+    L = ctypes.CDLL(str(path))
+    vp, i32, sz, u32 = ctypes.c_void_p, ctypes.c_int, ctypes.c_size_t, ctypes.c_uint
+    L.xred_allreduce_local.argtypes = [vp, i32, vp, sz, i32, i32, vp]
+    L.xred_reduce_scatter_local.argtypes = [vp, i32, i32, vp, sz, i32, i32, vp]
+    L.xred_reduce_copy_step.argtypes = [vp, vp, vp, sz, i32, i32, u32, vp]
+    L.xred_acc_cast.argtypes = [vp, vp, sz, i32, vp]
+    L.xred_batched_reduce.argtypes = [vp, i32, i32, i32, u32, vp]
+    for f in ("xred_allreduce_local", "xred_reduce_scatter_local", "xred_reduce_copy_step",
+              "xred_acc_cast", "xred_batched_reduce"):
+        getattr(L, f).restype = ctypes.c_int
+    L.xred_acc_elem_size.argtypes = [i32]
+    L.xred_acc_elem_size.restype = sz
+    L.xred_status_string.argtypes = [i32]
+    L.xred_status_string.restype = ctypes.c_char_p
+    L.xred_last_error.argtypes = []
+    L.xred_last_error.restype = ctypes.c_char_p
+    L.xred_version.argtypes = []
+    L.xred_version.restype = ctypes.c_int
+    L.xred_release.argtypes = []
+    L.xred_release.restype = None
+    _lib = L
+    return L
+
+
+def check(status: int) -> None:
+    """Raise XredError for a non-success status, with the library's detail."""
+    if status != SUCCESS:
+        raise XredError(status, (load().xred_last_error() or b"").decode())
+
+
+def ptr_array(ptrs) -> ctypes.Array:
+    """A host array of device pointers (void*[n])."""
+    return (ctypes.c_void_p * max(1, len(ptrs)))(*[int(p) for p in ptrs])

@@ -1,0 +1,446 @@
+// xred_api.hip -- the C ABI of libxred: argument validation, dispatch to the
+// kernel launchers, batch-descriptor staging, status strings.
+//
+// Every entry point validates all arguments before enqueueing anything, so a
+// failed call leaves the stream untouched.  Validation is the only host work
+// per call besides the launch itself (the per-message software overhead the
+// paper's low-latency path minimises, Section 6.2: no locks, allocation or
+// synchronisation on the fused and step-wise paths).
+#include <stdarg.h>
+#include <stdio.h>
+#include <stdlib.h>
+#include <string.h>
+
+#include <atomic>
+#include <mutex>
+
+#include "xred_internal.hpp"
+
+namespace xred {
+namespace {
+
+constexpr int kMaxDevices = 64;
+thread_local char g_err[512];
+
+xred_status fail(xred_status s, const char *fmt, ...)
+{
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_err, sizeof g_err, fmt, ap);
+    va_end(ap);
+    return s;
+}
+
+xred_status hip_fail(hipError_t e, const char *what)
+{
+    return fail(XRED_HIP_ERROR, "%s: %s", what, hipGetErrorString(e));
+}
+
+bool known_dtype(xred_dtype d) { return d >= XRED_FLOAT32 && d <= XRED_UINT32; }
+bool known_op(xred_op o) { return o >= XRED_SUM && o <= XRED_MIN; }
+
+// Checks shared by every entry point on dtype and op.
+xred_status check_types(xred_dtype dtype, xred_op op)
+{
+    if (!known_dtype(dtype)) return fail(XRED_INVALID_ARGUMENT, "unknown dtype %d", (int)dtype);
+    if (!known_op(op)) return fail(XRED_INVALID_ARGUMENT, "unknown op %d", (int)op);
+    if (!supported(dtype, op))
+        return fail(XRED_UNSUPPORTED, "dtype %d with op %d is not implemented", (int)dtype,
+                    (int)op);
+    return XRED_SUCCESS;
+}
+
+// A buffer of `bytes` at p: non-NULL, aligned to `align`, no address wrap.
+xred_status check_buf(const void *p, size_t bytes, size_t align, const char *name, int index)
+{
+    const uintptr_t a = (uintptr_t)p;
+    if (p == nullptr) return fail(XRED_INVALID_ARGUMENT, "%s[%d] is NULL", name, index);
+    if (a % align) return fail(XRED_INVALID_ARGUMENT, "%s[%d] is not %zu-byte aligned", name,
+                               index, align);
+    if (a + bytes < a) return fail(XRED_INVALID_ARGUMENT, "%s[%d] range wraps the address space",
+                                   name, index);
+    return XRED_SUCCESS;
+}
+
+// Overlap of [a, a+na) and [b, b+nb), other than the identical range when
+// `exact_ok`.
+bool bad_overlap(const void *a, size_t na, const void *b, size_t nb, bool exact_ok)
+{
+    const uintptr_t x = (uintptr_t)a, y = (uintptr_t)b;
+    if (exact_ok && x == y && na == nb) return false;
+    return x < y + nb && y < x + na;
+}
+
+bool mul_overflows(size_t a, size_t b) { return b != 0 && a > SIZE_MAX / b; }
+
+int cached_cus[kMaxDevices];
+
+long env_long(const char *name, long dflt)
+{
+    const char *v = getenv(name);
+    if (!v || !*v) return dflt;
+    char *end = nullptr;
+    const long x = strtol(v, &end, 10);
+    return (end && *end == 0 && x > 0) ? x : dflt;
+}
+
+// ------------------------------------------------ batch descriptor staging --
+// Host-side descriptors are copied into pinned memory, then into device
+// memory with one asynchronous copy on the caller's stream.  A ring of slots
+// per device is reused once the event recorded after the launch that read a
+// slot has completed.
+struct Slot {
+    void *host = nullptr;
+    void *dev = nullptr;
+    size_t cap = 0;
+    hipEvent_t done = nullptr;
+    bool pending = false;
+};
+constexpr int kSlots = 4;
+struct Pool {
+    std::mutex mu;
+    Slot slot[kSlots];
+    unsigned next = 0;
+};
+Pool g_pool[kMaxDevices];
+
+void free_slot(Slot &s)
+{
+    if (s.pending && s.done) (void)hipEventSynchronize(s.done);
+    if (s.host) (void)hipHostFree(s.host);
+    if (s.dev) (void)hipFree(s.dev);
+    s.host = s.dev = nullptr;
+    s.cap = 0;
+    s.pending = false;
+}
+
+xred_status batched_host(const xred_item *items, int nitems, xred_dtype dtype, xred_op op,
+                         hipStream_t stream)
+{
+    const size_t es = elem_size(dtype);
+    const uint64_t te = batched_tile_elems(dtype);
+    uint64_t total_tiles = 0, total_ptrs = 0;
+    for (int k = 0; k < nitems; ++k) {
+        const xred_item &it = items[k];
+        if (it.reserved != 0) return fail(XRED_INVALID_ARGUMENT, "items[%d].reserved != 0", k);
+        if (it.count == 0) continue;
+        if (it.nsrc < 1 || it.nsrc > XRED_MAX_SRC)
+            return fail(XRED_INVALID_ARGUMENT, "items[%d].nsrc = %u outside 1..%d", k, it.nsrc,
+                        XRED_MAX_SRC);
+        if (it.srcs == nullptr) return fail(XRED_INVALID_ARGUMENT, "items[%d].srcs is NULL", k);
+        if (mul_overflows(it.count, es))
+            return fail(XRED_INVALID_ARGUMENT, "items[%d].count * element size overflows", k);
+        const size_t bytes = (size_t)it.count * es;
+        xred_status st = check_buf(it.dst, bytes, es, "items.dst", k);
+        if (st != XRED_SUCCESS) return st;
+        for (uint32_t p = 0; p < it.nsrc; ++p) {
+            st = check_buf(it.srcs[p], bytes, es, "items.srcs", k);
+            if (st != XRED_SUCCESS) return st;
+            if (bad_overlap(it.dst, bytes, it.srcs[p], bytes, true))
+                return fail(XRED_ALIAS, "items[%d].dst partially overlaps source %u", k, p);
+        }
+        total_tiles += (it.count + te - 1) / te;
+        total_ptrs += it.nsrc;
+    }
+    if (total_tiles == 0) return XRED_SUCCESS;
+
+    const unsigned grid = grid_for(total_tiles);
+    const size_t items_bytes = sizeof(xred_item) * (size_t)nitems;
+    const size_t wg_bytes = sizeof(WgStart) * (size_t)grid;
+    const size_t need = items_bytes + wg_bytes + 8 * (size_t)total_ptrs;
+
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+    if (dev < 0 || dev >= kMaxDevices) return fail(XRED_UNSUPPORTED, "device %d", dev);
+    Pool &pool = g_pool[dev];
+    std::lock_guard<std::mutex> lock(pool.mu);
+    Slot &s = pool.slot[pool.next++ % kSlots];
+    if (s.pending) {
+        e = hipEventSynchronize(s.done);
+        if (e != hipSuccess) return hip_fail(e, "hipEventSynchronize(staging slot)");
+        s.pending = false;
+    }
+    if (s.cap < need) {
+        free_slot(s);
+        size_t cap = 64 << 10;
+        while (cap < need) cap <<= 1;
+        if (hipHostMalloc(&s.host, cap, hipHostMallocDefault) != hipSuccess) {
+            s.host = nullptr;
+            return fail(XRED_OUT_OF_MEMORY, "pinned staging of %zu bytes", cap);
+        }
+        if (hipMalloc(&s.dev, cap) != hipSuccess) {
+            (void)hipHostFree(s.host);
+            s.host = s.dev = nullptr;
+            return fail(XRED_OUT_OF_MEMORY, "device staging of %zu bytes", cap);
+        }
+        s.cap = cap;
+    }
+    if (!s.done && (e = hipEventCreateWithFlags(&s.done, hipEventDisableTiming)) != hipSuccess)
+        return hip_fail(e, "hipEventCreate");
+
+    // Layout: items | per-workgroup starts | source pointer arrays.
+    char *h = (char *)s.host;
+    char *d = (char *)s.dev;
+    xred_item *h_items = (xred_item *)h;
+    WgStart *h_wg = (WgStart *)(h + items_bytes);
+    const void **h_ptrs = (const void **)(h + items_bytes + wg_bytes);
+    const char *d_ptrs = d + items_bytes + wg_bytes;
+    uint64_t pos = 0;
+    for (int k = 0; k < nitems; ++k) {
+        const xred_item &it = items[k];
+        xred_item &o = h_items[k];
+        o = it;
+        if (it.count == 0) {
+            o.count = 0;
+            o.srcs = nullptr;
+            continue;
+        }
+        o.srcs = (const void *const *)(d_ptrs + 8 * pos);
+        for (uint32_t p = 0; p < it.nsrc; ++p) h_ptrs[pos + p] = it.srcs[p];
+        pos += it.nsrc;
+    }
+    // Workgroup b takes global tiles [total*b/grid, total*(b+1)/grid).
+    uint64_t k = 0, k_first = 0;  // item cursor and its first global tile
+    for (unsigned b = 0; b < grid; ++b) {
+        const uint64_t g0 = (uint64_t)((unsigned __int128)total_tiles * b / grid);
+        const uint64_t g1 = (uint64_t)((unsigned __int128)total_tiles * (b + 1) / grid);
+        for (;;) {
+            const uint64_t nt = (items[k].count + te - 1) / te;
+            if (g0 < k_first + nt) break;
+            k_first += nt;
+            ++k;
+        }
+        h_wg[b].item = (uint32_t)k;
+        h_wg[b].ntiles = (uint32_t)(g1 - g0);
+        h_wg[b].local_tile = g0 - k_first;
+    }
+    e = hipMemcpyAsync(s.dev, s.host, need, hipMemcpyHostToDevice, stream);
+    if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync(descriptors)");
+    e = launch_batched_planned(dtype, op, (const xred_item *)d, nitems,
+                               (const WgStart *)(d + items_bytes), grid, stream);
+    if (e != hipSuccess) return hip_fail(e, "batched launch");
+    e = hipEventRecord(s.done, stream);
+    if (e != hipSuccess) return hip_fail(e, "hipEventRecord(staging slot)");
+    s.pending = true;
+    return XRED_SUCCESS;
+}
+
+}  // namespace
+
+// ------------------------------------------------------- internal helpers --
+int device_cus()
+{
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return 256;
+    int c = __atomic_load_n(&cached_cus[dev], __ATOMIC_RELAXED);
+    if (c <= 0) {
+        if (hipDeviceGetAttribute(&c, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+            c <= 0)
+            c = 256;
+        __atomic_store_n(&cached_cus[dev], c, __ATOMIC_RELAXED);
+    }
+    return c;
+}
+
+unsigned grid_for(uint64_t tiles)
+{
+    static const long cap = env_long("XRED_MAX_WORKGROUPS", 0x7FFFFFFF);
+    uint64_t g = tiles < (uint64_t)cap ? tiles : (uint64_t)cap;
+    return g == 0 ? 1u : (unsigned)g;
+}
+
+unsigned batched_device_grid()
+{
+    static const long per_cu = env_long("XRED_BATCH_WG_PER_CU", 8);
+    return grid_for((uint64_t)device_cus() * (uint64_t)per_cu);
+}
+
+bool supported(xred_dtype dtype, xred_op op)
+{
+    return (dtype == XRED_FLOAT32 || dtype == XRED_BFLOAT16 || dtype == XRED_INT32 ||
+            dtype == XRED_UINT32) &&
+           known_op(op);
+}
+
+size_t elem_size(xred_dtype dtype)
+{
+    switch (dtype) {
+    case XRED_FLOAT32: case XRED_INT32: case XRED_UINT32: return 4;
+    case XRED_BFLOAT16: case XRED_FLOAT16: return 2;
+    default: return 0;
+    }
+}
+
+}  // namespace xred
+
+using namespace xred;
+
+extern "C" {
+
+XRED_API xred_status xred_allreduce_local(const void *const *srcs, int nsrc, void *dst,
+                                          size_t count, xred_dtype dtype, xred_op op,
+                                          void *hip_stream)
+{
+    if (nsrc < 1 || nsrc > XRED_MAX_SRC)
+        return fail(XRED_INVALID_ARGUMENT, "nsrc = %d outside 1..%d", nsrc, XRED_MAX_SRC);
+    xred_status st = check_types(dtype, op);
+    if (st != XRED_SUCCESS) return st;
+    if (count == 0) return XRED_SUCCESS;
+    if (srcs == nullptr) return fail(XRED_INVALID_ARGUMENT, "srcs is NULL");
+    const size_t es = elem_size(dtype);
+    if (mul_overflows(count, es)) return fail(XRED_INVALID_ARGUMENT, "count * size overflows");
+    const size_t bytes = count * es;
+    if ((st = check_buf(dst, bytes, es, "dst", 0)) != XRED_SUCCESS) return st;
+    for (int p = 0; p < nsrc; ++p) {
+        if ((st = check_buf(srcs[p], bytes, es, "srcs", p)) != XRED_SUCCESS) return st;
+        if (bad_overlap(dst, bytes, srcs[p], bytes, true))
+            return fail(XRED_ALIAS, "dst partially overlaps srcs[%d]", p);
+    }
+    const hipError_t e = launch_reduce(dtype, op, (const char *const *)srcs, nsrc, (char *)dst,
+                                       count, (hipStream_t)hip_stream);
+    return e == hipSuccess ? XRED_SUCCESS : hip_fail(e, "reduce launch");
+}
+
+XRED_API xred_status xred_reduce_scatter_local(const void *const *srcs, int nsrc, int rank,
+                                               void *dst, size_t recvcount, xred_dtype dtype,
+                                               xred_op op, void *hip_stream)
+{
+    if (nsrc < 1 || nsrc > XRED_MAX_SRC)
+        return fail(XRED_INVALID_ARGUMENT, "nsrc = %d outside 1..%d", nsrc, XRED_MAX_SRC);
+    if (rank < 0 || rank >= nsrc)
+        return fail(XRED_INVALID_ARGUMENT, "rank = %d outside [0, %d)", rank, nsrc);
+    xred_status st = check_types(dtype, op);
+    if (st != XRED_SUCCESS) return st;
+    if (recvcount == 0) return XRED_SUCCESS;
+    if (srcs == nullptr) return fail(XRED_INVALID_ARGUMENT, "srcs is NULL");
+    const size_t es = elem_size(dtype);
+    if (mul_overflows(recvcount, es) || mul_overflows(recvcount * es, (size_t)nsrc))
+        return fail(XRED_INVALID_ARGUMENT, "nsrc * recvcount * size overflows");
+    const size_t shard = recvcount * es;
+    if ((st = check_buf(dst, shard, es, "dst", 0)) != XRED_SUCCESS) return st;
+    const char *slices[XRED_MAX_SRC];
+    for (int p = 0; p < nsrc; ++p) {
+        if ((st = check_buf(srcs[p], shard * (size_t)nsrc, es, "srcs", p)) != XRED_SUCCESS)
+            return st;
+        slices[p] = (const char *)srcs[p] + shard * (size_t)rank;
+        if (bad_overlap(dst, shard, slices[p], shard, true))
+            return fail(XRED_ALIAS, "dst partially overlaps the slice read from srcs[%d]", p);
+    }
+    const hipError_t e =
+        launch_reduce(dtype, op, slices, nsrc, (char *)dst, recvcount, (hipStream_t)hip_stream);
+    return e == hipSuccess ? XRED_SUCCESS : hip_fail(e, "reduce launch");
+}
+
+XRED_API xred_status xred_reduce_copy_step(const void *in, void *acc, void *dst, size_t count,
+                                           xred_dtype dtype, xred_op op, unsigned flags,
+                                           void *hip_stream)
+{
+    if (flags & ~(unsigned)(XRED_STEP_INIT | XRED_STEP_FINAL))
+        return fail(XRED_INVALID_ARGUMENT, "unknown flag bits 0x%x", flags);
+    xred_status st = check_types(dtype, op);
+    if (st != XRED_SUCCESS) return st;
+    if (count == 0) return XRED_SUCCESS;
+    const size_t es = elem_size(dtype);
+    if (mul_overflows(count, 4)) return fail(XRED_INVALID_ARGUMENT, "count * 4 overflows");
+    const size_t bytes = count * es, acc_bytes = count * 4;
+    const bool uses_acc = flags != (XRED_STEP_INIT | XRED_STEP_FINAL);
+    const bool uses_dst = (flags & XRED_STEP_FINAL) != 0;
+    if ((st = check_buf(in, bytes, es, "in", 0)) != XRED_SUCCESS) return st;
+    if (uses_acc) {
+        if ((st = check_buf(acc, acc_bytes, 4, "acc", 0)) != XRED_SUCCESS) return st;
+        if (bad_overlap(acc, acc_bytes, in, bytes, false))
+            return fail(XRED_ALIAS, "acc overlaps in");
+    }
+    if (uses_dst) {
+        if ((st = check_buf(dst, bytes, es, "dst", 0)) != XRED_SUCCESS) return st;
+        if (bad_overlap(dst, bytes, in, bytes, true))
+            return fail(XRED_ALIAS, "dst partially overlaps in");
+        if (uses_acc && bad_overlap(dst, bytes, acc, acc_bytes, false))
+            return fail(XRED_ALIAS, "dst overlaps acc");
+    }
+    const hipError_t e = launch_step(dtype, op, flags, (const char *)in, (char *)acc, (char *)dst,
+                                     count, (hipStream_t)hip_stream);
+    return e == hipSuccess ? XRED_SUCCESS : hip_fail(e, "step launch");
+}
+
+XRED_API xred_status xred_acc_cast(const void *acc, void *dst, size_t count, xred_dtype dtype,
+                                   void *hip_stream)
+{
+    xred_status st = check_types(dtype, XRED_SUM);
+    if (st != XRED_SUCCESS) return st;
+    if (count == 0) return XRED_SUCCESS;
+    const size_t es = elem_size(dtype);
+    if (mul_overflows(count, 4)) return fail(XRED_INVALID_ARGUMENT, "count * 4 overflows");
+    if ((st = check_buf(acc, count * 4, 4, "acc", 0)) != XRED_SUCCESS) return st;
+    if ((st = check_buf(dst, count * es, es, "dst", 0)) != XRED_SUCCESS) return st;
+    if (bad_overlap(acc, count * 4, dst, count * es, false))
+        return fail(XRED_ALIAS, "dst overlaps acc");
+    const hipError_t e =
+        launch_acc_cast(dtype, (const char *)acc, (char *)dst, count, (hipStream_t)hip_stream);
+    return e == hipSuccess ? XRED_SUCCESS : hip_fail(e, "cast launch");
+}
+
+XRED_API xred_status xred_batched_reduce(const xred_item *items, int nitems, xred_dtype dtype,
+                                         xred_op op, unsigned flags, void *hip_stream)
+{
+    if (nitems < 0) return fail(XRED_INVALID_ARGUMENT, "nitems = %d", nitems);
+    if (flags & ~(unsigned)XRED_ITEMS_ON_DEVICE)
+        return fail(XRED_INVALID_ARGUMENT, "unknown flag bits 0x%x", flags);
+    xred_status st = check_types(dtype, op);
+    if (st != XRED_SUCCESS) return st;
+    if (nitems == 0) return XRED_SUCCESS;
+    if (items == nullptr) return fail(XRED_INVALID_ARGUMENT, "items is NULL");
+    if (flags & XRED_ITEMS_ON_DEVICE) {
+        if ((uintptr_t)items % alignof(xred_item))
+            return fail(XRED_INVALID_ARGUMENT, "items is not %zu-byte aligned", alignof(xred_item));
+        const hipError_t e = launch_batched_device(dtype, op, items, nitems, batched_device_grid(),
+                                                   (hipStream_t)hip_stream);
+        return e == hipSuccess ? XRED_SUCCESS : hip_fail(e, "batched launch");
+    }
+    return batched_host(items, nitems, dtype, op, (hipStream_t)hip_stream);
+}
+
+XRED_API size_t xred_acc_elem_size(xred_dtype dtype)
+{
+    return known_dtype(dtype) ? 4 : 0;
+}
+
+XRED_API const char *xred_status_string(xred_status s)
+{
+    switch (s) {
+    case XRED_SUCCESS: return "success";
+    case XRED_INVALID_ARGUMENT: return "invalid argument";
+    case XRED_UNSUPPORTED: return "unsupported dtype/op";
+    case XRED_ALIAS: return "buffers overlap";
+    case XRED_HIP_ERROR: return "HIP runtime error";
+    case XRED_OUT_OF_MEMORY: return "out of memory";
+    }
+    return "unknown status";
+}
+
+XRED_API const char *xred_last_error(void) { return g_err; }
+
+XRED_API int xred_version(void) { return 100; }
+
+XRED_API void xred_release(void)
+{
+    int cur = 0;
+    const bool have_dev = hipGetDevice(&cur) == hipSuccess;
+    for (int d = 0; d < kMaxDevices; ++d) {
+        Pool &pool = g_pool[d];
+        std::lock_guard<std::mutex> lock(pool.mu);
+        bool any = false;
+        for (Slot &s : pool.slot) any |= s.host != nullptr || s.done != nullptr;
+        if (!any) continue;
+        (void)hipSetDevice(d);
+        for (Slot &s : pool.slot) {
+            free_slot(s);
+            if (s.done) (void)hipEventDestroy(s.done);
+            s.done = nullptr;
+        }
+    }
+    if (have_dev) (void)hipSetDevice(cur);
+}
+
+}  // extern "C"

@@ -1,0 +1,239 @@
+// xred_batched.hip -- many independent reductions in one launch.
+//
+// Small messages are dominated by per-call overhead (the T_c term of the
+// LogP model in Section 6.2), so a batch of K reductions is run as one
+// kernel.  Work is cut into tiles of kBlock*kU 16-byte vectors of one item;
+// the global tile sequence (item 0's tiles, then item 1's, ...) is split
+// into one contiguous range per workgroup, so each workgroup walks forward
+// through consecutive items and reads each descriptor once.
+//
+// Two ways to find a workgroup's range:
+//   planned  (host descriptors): the host computes each workgroup's first
+//            item, first tile and tile count and stages them with the items;
+//   device   (XRED_ITEMS_ON_DEVICE): descriptors are read only when the
+//            kernel runs (metadata by reference, Section 6.1), so every
+//            workgroup sums the tile counts itself (an LDS scan over the
+//            descriptors), then locates its first tile.  No state is kept
+//            between calls, so the kernel can be captured in a graph.
+
+#include "xred_internal.hpp"
+#include "xred_kernels.hpp"
+
+namespace xred {
+namespace {
+
+constexpr int kU = 2;
+
+template <class T>
+constexpr uint64_t tile_vecs() { return (uint64_t)kBlock * kU; }
+template <class T>
+constexpr uint64_t tile_elems() { return tile_vecs<T>() * T::kVec; }
+
+__device__ __forceinline__ bool item_runnable(const xred_item &it)
+{
+    return it.nsrc >= 1 && it.nsrc <= XRED_MAX_SRC && it.reserved == 0 && it.srcs != nullptr &&
+           it.dst != nullptr;
+}
+
+template <class T, bool CHECK>
+__device__ __forceinline__ uint64_t item_tiles(const xred_item &it)
+{
+    if (CHECK && !item_runnable(it)) return 0;
+    return (it.count + tile_elems<T>() - 1) / tile_elems<T>();
+}
+
+__device__ __forceinline__ uint64_t uniform64(uint64_t x)
+{
+    const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)x);
+    const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(x >> 32));
+    return ((uint64_t)hi << 32) | lo;
+}
+
+// Inclusive prefix sum over the workgroup; s[kBlock-1] holds the total
+// until the next call.
+__device__ uint64_t block_inclusive_scan(uint64_t v, uint64_t *s)
+{
+    __syncthreads();
+    s[threadIdx.x] = v;
+    __syncthreads();
+    for (int off = 1; off < kBlock; off <<= 1) {
+        const uint64_t t = threadIdx.x >= (unsigned)off ? s[threadIdx.x - off] : 0;
+        __syncthreads();
+        s[threadIdx.x] += t;
+        __syncthreads();
+    }
+    return s[threadIdx.x];
+}
+
+template <class T, class Op, int NP>
+__device__ __forceinline__ void tile_np(const GlobalSrc &src, int nsrc, char *dst, size_t v0,
+                                        size_t nvec)
+{
+    reduce_vec_tile<T, Op, NP, kU, true, true, true>(src, nsrc, dst, v0, nvec);
+}
+
+// Tile lt of one item.
+template <class T, class Op>
+__device__ void batched_tile(const xred_item &it, uint64_t lt)
+{
+    const char *const *sp = (const char *const *)it.srcs;
+    const int nsrc = (int)it.nsrc;
+    uintptr_t bits = (uintptr_t)it.dst;
+    bool null_src = false;
+    for (int p = 0; p < nsrc; ++p) {
+        const uintptr_t q = (uintptr_t)sp[p];
+        bits |= q;
+        null_src |= q == 0;
+    }
+    if (null_src) return;
+    char *dst = (char *)it.dst;
+    const GlobalSrc src{sp};
+    const uint64_t count = it.count;
+    if ((bits & 15u) == 0) {
+        const size_t nvec = count / T::kVec;
+        const size_t v0 = lt * tile_vecs<T>() + threadIdx.x;
+        switch (nsrc) {
+        case 1: tile_np<T, Op, 1>(src, nsrc, dst, v0, nvec); break;
+        case 2: tile_np<T, Op, 2>(src, nsrc, dst, v0, nvec); break;
+        case 3: tile_np<T, Op, 3>(src, nsrc, dst, v0, nvec); break;
+        case 4: tile_np<T, Op, 4>(src, nsrc, dst, v0, nvec); break;
+        case 5: tile_np<T, Op, 5>(src, nsrc, dst, v0, nvec); break;
+        case 6: tile_np<T, Op, 6>(src, nsrc, dst, v0, nvec); break;
+        case 7: tile_np<T, Op, 7>(src, nsrc, dst, v0, nvec); break;
+        case 8: tile_np<T, Op, 8>(src, nsrc, dst, v0, nvec); break;
+        default: tile_np<T, Op, 0>(src, nsrc, dst, v0, nvec); break;
+        }
+        // the item's last tile also takes the elements after its last full vector
+        if ((lt + 1) * tile_elems<T>() >= count) {
+            const uint32_t tail = (uint32_t)(count % T::kVec);
+            if (threadIdx.x < tail) reduce_elem<T, Op>(src, nsrc, dst, nvec * T::kVec + threadIdx.x);
+        }
+    } else {
+        const uint64_t e0 = lt * tile_elems<T>();
+        const uint64_t e1 = count < e0 + tile_elems<T>() ? count : e0 + tile_elems<T>();
+        for (uint64_t i = e0 + threadIdx.x; i < e1; i += kBlock) reduce_elem<T, Op>(src, nsrc, dst, i);
+    }
+}
+
+template <class T, class Op, bool PLANNED>
+__global__ __launch_bounds__(kBlock) void batched_kernel(const xred_item *items, int nitems,
+                                                         const WgStart *wg)
+{
+    __shared__ uint64_t s_scan[kBlock];
+    __shared__ uint64_t s_start[2];
+    uint64_t k, lt, left;
+    if constexpr (PLANNED) {
+        const WgStart w = wg[blockIdx.x];
+        k = w.item;
+        lt = w.local_tile;
+        left = w.ntiles;
+    } else {
+        uint64_t mine = 0;
+        for (int i = threadIdx.x; i < nitems; i += kBlock) mine += item_tiles<T, true>(items[i]);
+        block_inclusive_scan(mine, s_scan);
+        const uint64_t total = s_scan[kBlock - 1];
+        const uint64_t g0 = total * blockIdx.x / gridDim.x;
+        const uint64_t g1 = total * (blockIdx.x + 1) / gridDim.x;
+        if (g0 == g1) return;
+        left = g1 - g0;
+        // find the item holding global tile g0
+        uint64_t base = 0;
+        for (int w0 = 0; w0 < nitems; w0 += kBlock) {
+            const int i = w0 + (int)threadIdx.x;
+            const uint64_t c = i < nitems ? item_tiles<T, true>(items[i]) : 0;
+            const uint64_t incl = block_inclusive_scan(c, s_scan);
+            const uint64_t excl = incl - c;
+            if (c > 0 && base + excl <= g0 && g0 < base + incl) {
+                s_start[0] = (uint64_t)i;
+                s_start[1] = g0 - base - excl;
+            }
+            const uint64_t wtot = s_scan[kBlock - 1];
+            __syncthreads();
+            if (base + wtot > g0) break;
+            base += wtot;
+        }
+        k = s_start[0];
+        lt = s_start[1];
+    }
+    k = uniform64(k);
+    lt = uniform64(lt);
+    left = uniform64(left);
+    while (left > 0 && k < (uint64_t)nitems) {
+        const xred_item it = items[k];
+        const uint64_t nt = item_tiles<T, !PLANNED>(it);
+        if (lt >= nt) {
+            ++k;
+            lt = 0;
+            continue;
+        }
+        batched_tile<T, Op>(it, lt);
+        ++lt;
+        --left;
+    }
+}
+
+template <class T, class Op>
+hipError_t go(bool planned, const xred_item *d_items, int nitems, const WgStart *d_wg,
+              unsigned grid, hipStream_t s)
+{
+    if (planned)
+        hipLaunchKernelGGL((batched_kernel<T, Op, true>), dim3(grid), dim3(kBlock), 0, s, d_items,
+                           nitems, d_wg);
+    else
+        hipLaunchKernelGGL((batched_kernel<T, Op, false>), dim3(grid), dim3(kBlock), 0, s,
+                           d_items, nitems, d_wg);
+    return hipGetLastError();
+}
+
+template <class T>
+hipError_t go_op(xred_op op, bool planned, const xred_item *d_items, int nitems,
+                 const WgStart *d_wg, unsigned grid, hipStream_t s)
+{
+    switch (op) {
+    case XRED_SUM: return go<T, OpSum>(planned, d_items, nitems, d_wg, grid, s);
+    case XRED_PROD: return go<T, OpProd>(planned, d_items, nitems, d_wg, grid, s);
+    case XRED_MAX: return go<T, OpMax>(planned, d_items, nitems, d_wg, grid, s);
+    case XRED_MIN: return go<T, OpMin>(planned, d_items, nitems, d_wg, grid, s);
+    }
+    return hipErrorInvalidValue;
+}
+
+hipError_t dispatch(xred_dtype dtype, xred_op op, bool planned, const xred_item *d_items,
+                    int nitems, const WgStart *d_wg, unsigned grid, hipStream_t s)
+{
+    switch (dtype) {
+    case XRED_FLOAT32: return go_op<TF32>(op, planned, d_items, nitems, d_wg, grid, s);
+    case XRED_BFLOAT16: return go_op<TBF16>(op, planned, d_items, nitems, d_wg, grid, s);
+    case XRED_INT32: return go_op<TI32>(op, planned, d_items, nitems, d_wg, grid, s);
+    case XRED_UINT32: return go_op<TU32>(op, planned, d_items, nitems, d_wg, grid, s);
+    default: return hipErrorInvalidValue;
+    }
+}
+
+}  // namespace
+
+uint64_t batched_tile_elems(xred_dtype dtype)
+{
+    switch (dtype) {
+    case XRED_BFLOAT16: return tile_elems<TBF16>();
+    case XRED_FLOAT32: return tile_elems<TF32>();
+    case XRED_INT32: return tile_elems<TI32>();
+    case XRED_UINT32: return tile_elems<TU32>();
+    default: return 0;
+    }
+}
+
+hipError_t launch_batched_planned(xred_dtype dtype, xred_op op, const xred_item *d_items,
+                                  int nitems, const WgStart *d_wg, unsigned grid,
+                                  hipStream_t stream)
+{
+    return dispatch(dtype, op, true, d_items, nitems, d_wg, grid, stream);
+}
+
+hipError_t launch_batched_device(xred_dtype dtype, xred_op op, const xred_item *d_items,
+                                 int nitems, unsigned grid, hipStream_t stream)
+{
+    return dispatch(dtype, op, false, d_items, nitems, nullptr, grid, stream);
+}
+
+}  // namespace xred

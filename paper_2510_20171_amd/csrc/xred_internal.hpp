@@ -1,0 +1,59 @@
+// xred_internal.hpp -- host-side interfaces between the C ABI layer and the
+// kernel launchers.  Every launcher assumes arguments were validated by the
+// caller (xred_api.hip) and only sizes the grid and enqueues kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "../../include/xred.h"
+
+namespace xred {
+
+// Workgroup budget for one launch on the current device: the number of tiles,
+// capped by XRED_MAX_WORKGROUPS when set (a CU-budget knob: it never changes
+// results, only how many workgroups share the work).
+unsigned grid_for(uint64_t tiles);
+
+// Compute units of the current device (cached per device).
+int device_cus();
+
+bool supported(xred_dtype dtype, xred_op op);
+size_t elem_size(xred_dtype dtype);
+
+// dst[i] = fold_p srcs[p][i], i < count.  srcs already include any shard offset.
+hipError_t launch_reduce(xred_dtype dtype, xred_op op, const char *const *srcs, int nsrc,
+                         char *dst, size_t count, hipStream_t stream);
+
+hipError_t launch_step(xred_dtype dtype, xred_op op, unsigned flags, const char *in, char *acc,
+                       char *dst, size_t count, hipStream_t stream);
+
+hipError_t launch_acc_cast(xred_dtype dtype, const char *acc, char *dst, size_t count,
+                           hipStream_t stream);
+
+// Batched reduce.  A tile is batched_tile_elems(dtype) elements of one item.
+struct WgStart {
+    uint32_t item;        // first item this workgroup works on
+    uint32_t ntiles;      // tiles this workgroup processes (over consecutive items)
+    uint64_t local_tile;  // first tile within that item
+};
+static_assert(sizeof(WgStart) == 16, "WgStart layout");
+static_assert(sizeof(xred_item) == 32, "xred_item layout");
+
+uint64_t batched_tile_elems(xred_dtype dtype);
+
+// Host-planned: d_items (device copy, srcs pointing to device arrays) and one
+// WgStart per workgroup.
+hipError_t launch_batched_planned(xred_dtype dtype, xred_op op, const xred_item *d_items,
+                                  int nitems, const WgStart *d_wg, unsigned grid,
+                                  hipStream_t stream);
+
+// Device-resident descriptors: every workgroup derives its share itself.
+hipError_t launch_batched_device(xred_dtype dtype, xred_op op, const xred_item *d_items,
+                                 int nitems, unsigned grid, hipStream_t stream);
+
+// Grid used for device-resident batches (fixed: the host cannot see sizes).
+unsigned batched_device_grid();
+
+}  // namespace xred

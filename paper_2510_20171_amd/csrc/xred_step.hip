@@ -1,0 +1,111 @@
+// xred_step.hip -- launchers for the step-wise ring ReduceCopy
+// (xred_reduce_copy_step) and the closing accumulator cast (xred_acc_cast).
+//
+// A step moves little data (a 1M-element bf16 chunk step reads 6 MiB and
+// writes 4 MiB), so launch cost dominates; the launch path is one template
+// lookup and one kernel.  The grid is a pure function of count, so tile t of
+// the accumulator is processed by workgroup t on every step and therefore on
+// the same XCD, whose L2 may still hold it from the previous step.
+#include "xred_internal.hpp"
+#include "xred_kernels.hpp"
+
+namespace xred {
+namespace {
+
+constexpr int kU = 2;
+
+template <class T, class Op, unsigned FLAGS>
+hipError_t go(const char *in, char *acc, char *dst, size_t count, hipStream_t s)
+{
+    // acc is touched unless INIT|FINAL; dst only with FINAL.
+    constexpr bool kUsesAcc = FLAGS != (XRED_STEP_INIT | XRED_STEP_FINAL);
+    constexpr bool kUsesDst = (FLAGS & XRED_STEP_FINAL) != 0;
+    uintptr_t bits = (uintptr_t)in;
+    if (kUsesAcc) bits |= (uintptr_t)acc;
+    if (kUsesDst) bits |= (uintptr_t)dst;
+    const bool vec = (bits & 15u) == 0;
+    if (vec) {
+        const size_t nvec = count / T::kVec;
+        const size_t tail = count % T::kVec;
+        constexpr size_t kTile = (size_t)kBlock * kU;
+        const uint64_t tiles = (nvec + kTile - 1) / kTile + (tail ? 1 : 0);
+        hipLaunchKernelGGL((step_kernel<T, Op, FLAGS, kU, true>), dim3(grid_for(tiles)),
+                           dim3(kBlock), 0, s, in, acc, dst, nvec, tail);
+    } else {
+        hipLaunchKernelGGL((step_kernel<T, Op, FLAGS, kU, false>),
+                           dim3(grid_for((count + kBlock - 1) / kBlock)), dim3(kBlock), 0, s, in,
+                           acc, dst, (size_t)0, count);
+    }
+    return hipGetLastError();
+}
+
+template <class T, class Op>
+hipError_t go_flags(unsigned flags, const char *in, char *acc, char *dst, size_t count,
+                    hipStream_t s)
+{
+    switch (flags) {
+    case 0: return go<T, Op, 0u>(in, acc, dst, count, s);
+    case XRED_STEP_INIT: return go<T, Op, XRED_STEP_INIT>(in, acc, dst, count, s);
+    case XRED_STEP_FINAL: return go<T, Op, XRED_STEP_FINAL>(in, acc, dst, count, s);
+    default: return go<T, Op, XRED_STEP_INIT | XRED_STEP_FINAL>(in, acc, dst, count, s);
+    }
+}
+
+template <class T>
+hipError_t go_op(xred_op op, unsigned flags, const char *in, char *acc, char *dst, size_t count,
+                 hipStream_t s)
+{
+    switch (op) {
+    case XRED_SUM: return go_flags<T, OpSum>(flags, in, acc, dst, count, s);
+    case XRED_PROD: return go_flags<T, OpProd>(flags, in, acc, dst, count, s);
+    case XRED_MAX: return go_flags<T, OpMax>(flags, in, acc, dst, count, s);
+    case XRED_MIN: return go_flags<T, OpMin>(flags, in, acc, dst, count, s);
+    }
+    return hipErrorInvalidValue;
+}
+
+template <class T>
+hipError_t go_cast(const char *acc, char *dst, size_t count, hipStream_t s)
+{
+    if ((((uintptr_t)acc | (uintptr_t)dst) & 15u) == 0) {
+        const size_t nvec = count / T::kVec;
+        const size_t tail = count % T::kVec;
+        constexpr size_t kTile = (size_t)kBlock * kU;
+        const uint64_t tiles = (nvec + kTile - 1) / kTile + (tail ? 1 : 0);
+        hipLaunchKernelGGL((acc_cast_kernel<T, kU, true>), dim3(grid_for(tiles)), dim3(kBlock),
+                           0, s, acc, dst, nvec, tail);
+    } else {
+        hipLaunchKernelGGL((acc_cast_kernel<T, kU, false>),
+                           dim3(grid_for((count + kBlock - 1) / kBlock)), dim3(kBlock), 0, s, acc,
+                           dst, (size_t)0, count);
+    }
+    return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_step(xred_dtype dtype, xred_op op, unsigned flags, const char *in, char *acc,
+                       char *dst, size_t count, hipStream_t stream)
+{
+    switch (dtype) {
+    case XRED_FLOAT32: return go_op<TF32>(op, flags, in, acc, dst, count, stream);
+    case XRED_BFLOAT16: return go_op<TBF16>(op, flags, in, acc, dst, count, stream);
+    case XRED_INT32: return go_op<TI32>(op, flags, in, acc, dst, count, stream);
+    case XRED_UINT32: return go_op<TU32>(op, flags, in, acc, dst, count, stream);
+    default: return hipErrorInvalidValue;
+    }
+}
+
+hipError_t launch_acc_cast(xred_dtype dtype, const char *acc, char *dst, size_t count,
+                           hipStream_t stream)
+{
+    switch (dtype) {
+    case XRED_FLOAT32: return go_cast<TF32>(acc, dst, count, stream);
+    case XRED_BFLOAT16: return go_cast<TBF16>(acc, dst, count, stream);
+    case XRED_INT32: return go_cast<TI32>(acc, dst, count, stream);
+    case XRED_UINT32: return go_cast<TU32>(acc, dst, count, stream);
+    default: return hipErrorInvalidValue;
+    }
+}
+
+}  // namespace xred

@@ -1,0 +1,371 @@
+"""GPU parity: every entry point of libxred against the CPU oracle, element by
+element, on the same seeded inputs.  The bar is bit-exact equality (the fold
+order is fixed, so float results are deterministic); NaN payloads of float
+sum/prod are not specified and compare by NaN-ness only.
+
+Covered: the six workloads at full size in the launch configuration the
+benchmark times (c1, c2, c3, c5a, c5b fully; c4 on a sample of items plus
+host/device-descriptor agreement on all items), and an edge matrix of sizes
+(empty, ragged, several tiles), source counts 1..64, every dtype x op with
+special values (+-0, +-inf, subnormals, NaN, overflow), misaligned buffers,
+in-place calls, guard bands around outputs, and every step-wise flag.
+"""
+import ctypes
+import os
+
+import numpy as np
+import pytest
+
+import gpu_util as gu
+import pins
+import workloads as wl
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+DTYPES = ("f32", "bf16", "i32", "u32")
+OPS = ("sum", "prod", "max", "min")
+CORES = min(16, len(os.sched_getaffinity(0)))
+
+
+@pytest.fixture(scope="module")
+def xr():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU visible")
+    import paper_2510_20171_amd as xr
+    xr.load()   # raises if libxred.so is missing: there is no fallback
+    return xr
+
+
+def _run_allreduce(xr, srcs_np, dtype, op, **kw):
+    srcs = [gu.to_dev(s, dtype) for s in srcs_np]
+    out = torch.empty_like(srcs[0])
+    xr.allreduce_local(srcs, out, op, dtype=dtype, **kw)
+    torch.cuda.synchronize()
+    return out
+
+
+def test_native_library_is_loaded(xr):
+    maps = open("/proc/self/maps").read()
+    assert str(xr._lib.LIB_PATH) in maps or "libxred.so" in maps
+
+
+# ------------------------------------------------------------ workloads --
+
+def test_c1_full(xr, orc):
+    w = wl.WORKLOADS["c1"]
+    srcs = wl.sources(w)
+    got = _run_allreduce(xr, srcs, w.dtype, w.op)
+    exp = orc.allreduce_local(srcs, w.dtype, w.op, nthreads=CORES)
+    gu.assert_parity(got, exp, w.dtype, w.op, "c1")
+
+
+def test_c2_full(xr, orc):
+    w = wl.WORKLOADS["c2"]
+    srcs = wl.sources(w)
+    got = _run_allreduce(xr, srcs, w.dtype, w.op)
+    exp = orc.allreduce_local(srcs, w.dtype, w.op, nthreads=CORES)
+    gu.assert_parity(got, exp, w.dtype, w.op, "c2")
+
+
+@pytest.mark.parametrize("name", ["c5a", "c5b"])
+def test_c5_full(xr, orc, name):
+    w = wl.WORKLOADS[name]
+    srcs = wl.sources(w)
+    got = _run_allreduce(xr, srcs, w.dtype, w.op)
+    exp = orc.allreduce_local(srcs, w.dtype, w.op, nthreads=CORES)
+    gu.assert_parity(got, exp, w.dtype, w.op, name)
+    if name == "c5b":
+        # the structured blocks: +-0 columns give +0 unless all -0; one +inf wins
+        b = gu.bits(got, "f32")
+        assert np.all(b[wl.C5B_BLOCK:2 * wl.C5B_BLOCK] == 0x7F800000)
+
+
+def test_c3_stepwise_full(xr, orc):
+    w = wl.WORKLOADS["c3"]
+    chunks = wl.stepwise_chunks(w)
+    d = [gu.to_dev(c, w.dtype) for c in chunks]
+    acc = torch.empty(w.count, dtype=torch.float32, device="cuda")
+    out = torch.empty_like(d[0])
+    xr.reduce_copy_step(d[0], acc, None, w.op, init=True)
+    for c in d[1:]:
+        xr.reduce_copy_step(c, acc, None, w.op)
+    xr.acc_cast(acc, out)
+    # the same sequence with the last step fused into FINAL
+    acc2 = torch.empty_like(acc)
+    out2 = torch.empty_like(out)
+    xr.reduce_copy_step(d[0], acc2, None, w.op, init=True)
+    for c in d[1:-1]:
+        xr.reduce_copy_step(c, acc2, None, w.op)
+    xr.reduce_copy_step(d[-1], acc2, out2, w.op, final=True)
+    torch.cuda.synchronize()
+    oacc = orc.reduce_copy_step(chunks[0], None, w.dtype, w.op, init=True)
+    for c in chunks[1:]:
+        oacc = orc.reduce_copy_step(c, oacc, w.dtype, w.op)
+    gu.assert_parity(acc, oacc, "f32", w.op, "c3 accumulator")
+    exp = orc.acc_cast(oacc, w.dtype)
+    gu.assert_parity(out, exp, w.dtype, w.op, "c3 cast")
+    gu.assert_parity(out2, exp, w.dtype, w.op, "c3 final")
+    # and it equals the fused 16-source reduce of the chunks
+    fused = torch.empty_like(out)
+    xr.allreduce_local(d, fused, w.op)
+    torch.cuda.synchronize()
+    gu.assert_parity(fused, exp, w.dtype, w.op, "c3 fused")
+
+
+def _c4_device_descriptors(xr, arena_dev, offs, sizes, outs, es):
+    """Device-resident xred_item array + per-item device pointer arrays."""
+    base = arena_dev.data_ptr()
+    P = offs.shape[1]
+    ptrs = torch.tensor((base + offs * es).reshape(-1).astype(np.int64), device="cuda")
+    items = np.zeros(len(sizes), xr.ITEM_DTYPE)
+    items["srcs"] = ptrs.data_ptr() + 8 * P * np.arange(len(sizes), dtype=np.uint64)
+    items["dst"] = [o.data_ptr() for o in outs]
+    items["count"] = sizes
+    items["nsrc"] = P
+    dev_items = torch.from_numpy(items.view(np.uint8).copy()).to("cuda")
+    return dev_items, ptrs
+
+
+def test_c4_batched_full(xr, orc):
+    w = wl.WORKLOADS["c4"]
+    sizes = wl.batched_sizes(w)
+    arena, offs = wl.batched_arena(w, sizes)
+    es = wl.ELEM_SIZE[w.dtype]
+    arena_dev = gu.to_dev(arena, w.dtype)
+    outs = [torch.empty(int(n), dtype=torch.bfloat16, device="cuda") for n in sizes]
+    items = [([arena_dev[o:o + int(n)] for o in offs[k]], outs[k])
+             for k, n in enumerate(sizes)]
+    xr.batched_reduce(items, w.op, dtype=w.dtype)
+    torch.cuda.synchronize()
+    # sampled items against the oracle, one by one
+    rng = np.random.default_rng(44)
+    sample = sorted(set(rng.choice(len(sizes), 64, replace=False).tolist())
+                    | {0, len(sizes) - 1, int(np.argmax(sizes)), int(np.argmin(sizes))})
+    for k in sample:
+        n = int(sizes[k])
+        srcs = [arena[o:o + n] for o in offs[k]]
+        exp = orc.allreduce_local(srcs, w.dtype, w.op)
+        gu.assert_parity(outs[k], exp, w.dtype, w.op, f"c4 item {k}")
+    # device-resident descriptors give the same bits on every item
+    outs2 = [torch.full_like(o, float("nan")) for o in outs]
+    dev_items, keep = _c4_device_descriptors(xr, arena_dev, offs, sizes, outs2, es)
+    xr.batched_reduce(dev_items, w.op, dtype=w.dtype)
+    torch.cuda.synchronize()
+    a = torch.cat(outs).view(torch.int16)
+    b = torch.cat(outs2).view(torch.int16)
+    assert torch.equal(a, b)
+    del keep
+
+
+# ---------------------------------------------------------- edge matrix --
+
+SIZES = [1, 7, 8, 9, 63, 64, 65, 1023, 4096 + 5, (1 << 17) + 3]
+NSRCS = [1, 2, 3, 4, 5, 7, 8, 9, 16, 31, 32, 33, 64]
+
+
+@pytest.mark.parametrize("dtype", DTYPES)
+@pytest.mark.parametrize("op", OPS)
+def test_edge_matrix(xr, orc, dtype, op):
+    rng = np.random.default_rng(10 * DTYPES.index(dtype) + OPS.index(op))
+    for P in NSRCS:
+        for n in SIZES:
+            if P * n > (1 << 21):
+                continue
+            srcs = [pins.random_column_values(rng, dtype, n) for _ in range(P)]
+            got = _run_allreduce(xr, srcs, dtype, op)
+            exp = orc.allreduce_local(srcs, dtype, op)
+            gu.assert_parity(got, exp, dtype, op, f"{dtype} {op} P={P} n={n}")
+
+
+def test_empty_is_noop(xr):
+    a = torch.zeros(0, dtype=torch.bfloat16, device="cuda")
+    xr.allreduce_local([a, a], a)
+    acc = torch.zeros(0, dtype=torch.float32, device="cuda")
+    xr.reduce_copy_step(a, acc, None, init=True)
+    xr.acc_cast(acc, a)
+    xr.batched_reduce([], dtype="bf16")
+    torch.cuda.synchronize()
+
+
+@pytest.mark.parametrize("dtype", DTYPES)
+def test_misaligned_and_guard_bands(xr, orc, dtype):
+    rng = np.random.default_rng(5)
+    n = 70001
+    G = 4096          # guard elements on each side of dst
+    for P in (1, 3, 8, 33):
+        for shift in (1, 3):
+            srcs = [pins.random_column_values(rng, dtype, n) for _ in range(P)]
+            big = [gu.to_dev(np.concatenate([np.zeros(shift, s.dtype), s]), dtype) for s in srcs]
+            views = [b[shift:] for b in big]
+            canary = 0x5A
+            store = torch.full((n + 2 * G,), 0, dtype=gu.torch_dtype(dtype), device="cuda")
+            store.view(torch.uint8).fill_(canary)
+            out = store[G + shift:G + shift + n]
+            xr.allreduce_local(views, out, "sum", dtype=dtype)
+            torch.cuda.synchronize()
+            exp = orc.allreduce_local(srcs, dtype, "sum")
+            gu.assert_parity(out, exp, dtype, "sum", f"misaligned {dtype} P={P} shift={shift}")
+            raw = store.view(torch.uint8).cpu().numpy()
+            es = out.element_size()
+            assert np.all(raw[:(G + shift) * es] == canary)
+            assert np.all(raw[(G + shift + n) * es:] == canary)
+
+
+@pytest.mark.parametrize("dtype", DTYPES)
+def test_in_place(xr, orc, dtype):
+    rng = np.random.default_rng(8)
+    n = (1 << 16) + 5
+    for P in (2, 8, 20):
+        for k in (0, P - 1):
+            srcs = [pins.random_column_values(rng, dtype, n) for _ in range(P)]
+            d = [gu.to_dev(s, dtype) for s in srcs]
+            xr.allreduce_local(d, d[k], "sum", dtype=dtype)
+            torch.cuda.synchronize()
+            exp = orc.allreduce_local(srcs, dtype, "sum")
+            gu.assert_parity(d[k], exp, dtype, "sum", f"in place k={k} P={P}")
+
+
+@pytest.mark.parametrize("dtype", DTYPES)
+@pytest.mark.parametrize("recvcount", [1000003, 1 << 18, 1])
+def test_reduce_scatter(xr, orc, dtype, recvcount):
+    rng = np.random.default_rng(recvcount)
+    P = 5
+    srcs = [pins.random_column_values(rng, dtype, P * recvcount) for _ in range(P)]
+    d = [gu.to_dev(s, dtype) for s in srcs]
+    full = _run_allreduce(xr, srcs, dtype, "max")
+    shards = []
+    for r in range(P):
+        out = torch.empty(recvcount, dtype=d[0].dtype, device="cuda")
+        xr.reduce_scatter_local(d, r, out, "max", dtype=dtype)
+        torch.cuda.synchronize()
+        exp = orc.reduce_scatter_local(srcs, r, dtype, "max")
+        gu.assert_parity(out, exp, dtype, "max", f"rs rank {r}")
+        shards.append(out)
+    gu.assert_parity(torch.cat(shards), gu.bits(full, dtype), dtype, "max", "rs concat")
+    # in place: rank r's result lands in its own slice of srcs[r]
+    r = 2
+    d2 = [gu.to_dev(s, dtype) for s in srcs]
+    xr.reduce_scatter_local(d2, r, d2[r][r * recvcount:(r + 1) * recvcount], "sum", dtype=dtype)
+    torch.cuda.synchronize()
+    exp = orc.reduce_scatter_local(srcs, r, dtype, "sum")
+    gu.assert_parity(d2[r][r * recvcount:(r + 1) * recvcount], exp, dtype, "sum", "rs in place")
+
+
+@pytest.mark.parametrize("dtype", DTYPES)
+@pytest.mark.parametrize("op", OPS)
+def test_step_all_flags(xr, orc, dtype, op):
+    rng = np.random.default_rng(3)
+    for n, shift in ((4096 * 3 + 7, 0), (1 << 15, 0), (999, 1)):
+        chunks = [pins.random_column_values(rng, dtype, n) for _ in range(6)]
+        dev = []
+        for c in chunks:
+            b = gu.to_dev(np.concatenate([np.zeros(shift, c.dtype), c]), dtype)
+            dev.append(b[shift:])
+        accbuf = torch.empty(n + shift, dtype=torch.float32 if dtype in ("f32", "bf16")
+                             else torch.int32, device="cuda")
+        acc = accbuf[shift:]
+        xr.reduce_copy_step(dev[0], acc, None, op, init=True, dtype=dtype)
+        for c in dev[1:-1]:
+            xr.reduce_copy_step(c, acc, None, op, dtype=dtype)
+        outbuf = torch.empty(n + shift, dtype=dev[0].dtype, device="cuda")
+        out = outbuf[shift:]
+        acc_before = acc.clone()
+        xr.reduce_copy_step(dev[-1], acc, out, op, final=True, dtype=dtype)
+        single = torch.empty_like(out)
+        xr.reduce_copy_step(dev[0], None, single, op, init=True, final=True, dtype=dtype)
+        torch.cuda.synchronize()
+        assert torch.equal(acc.view(torch.int32), acc_before.view(torch.int32)), "FINAL wrote acc"
+        oacc = orc.reduce_copy_step(chunks[0], None, dtype, op, init=True)
+        for c in chunks[1:-1]:
+            oacc = orc.reduce_copy_step(c, oacc, dtype, op)
+        accd = "f32" if dtype in ("f32", "bf16") else "u32"
+        gu.assert_parity(acc, oacc, accd, op, f"step acc {dtype} {op} n={n}")
+        exp = orc.reduce_copy_step(chunks[-1], oacc.copy(), dtype, op, final=True)
+        gu.assert_parity(out, exp, dtype, op, f"step final {dtype} {op} n={n}")
+        gu.assert_parity(single, orc.reduce_copy_step(chunks[0], None, dtype, op, init=True,
+                                                      final=True), dtype, op, "init|final")
+        cast = torch.empty_like(out)
+        xr.acc_cast(acc, cast, dtype=dtype)
+        torch.cuda.synchronize()
+        gu.assert_parity(cast, orc.acc_cast(oacc, dtype), dtype, op, "cast")
+
+
+@pytest.mark.parametrize("dtype", ("bf16", "f32", "i32"))
+def test_batched_mixed(xr, orc, dtype):
+    """Mixed source counts, ragged and misaligned items, zero-length items,
+    host and device descriptors."""
+    rng = np.random.default_rng(21)
+    specs = []
+    for k in range(300):
+        P = int(rng.choice([1, 2, 3, 8, 9, 17, 64]))
+        n = int(rng.choice([0, 1, 7, 100, 4095, 4096, 4097, 20000, 70001]))
+        shift = int(rng.integers(0, 2)) if k % 3 == 0 else 0
+        specs.append((P, n, shift))
+    host_srcs, items, outs = [], [], []
+    for P, n, shift in specs:
+        s = [pins.random_column_values(rng, dtype, n) for _ in range(P)]
+        host_srcs.append(s)
+        d = [gu.to_dev(np.concatenate([np.zeros(shift, x.dtype), x]), dtype)[shift:] for x in s]
+        ob = torch.zeros(n + shift, dtype=gu.torch_dtype(dtype), device="cuda")
+        outs.append(ob[shift:])
+        items.append((d, outs[-1]))
+    xr.batched_reduce(items, "sum", dtype=dtype)
+    torch.cuda.synchronize()
+    for k, (s, o) in enumerate(zip(host_srcs, outs)):
+        if s[0].size == 0:
+            continue
+        gu.assert_parity(o, orc.allreduce_local(s, dtype, "sum"), dtype, "sum", f"item {k}")
+    # device descriptors, plus items that must be skipped (dst untouched)
+    keep, rows = [], []
+    outs2 = [torch.zeros_like(o) for o in outs]
+    for (d, _), o in zip(items, outs2):
+        pa = torch.tensor([x.data_ptr() for x in d], dtype=torch.int64, device="cuda")
+        keep.append(pa)
+        rows.append((pa.data_ptr(), o.data_ptr(), o.numel(), len(d), 0))
+    bad_out = torch.full((4096,), 7, dtype=gu.torch_dtype(dtype), device="cuda")
+    nullp = torch.zeros(3, dtype=torch.int64, device="cuda")
+    good_p = keep[0]
+    rows += [(good_p.data_ptr(), bad_out.data_ptr(), 4096, 0, 0),      # nsrc 0
+             (good_p.data_ptr(), bad_out.data_ptr(), 4096, 65, 0),     # nsrc > 64
+             (good_p.data_ptr(), bad_out.data_ptr(), 4096, 1, 1),      # reserved != 0
+             (0, bad_out.data_ptr(), 4096, 1, 0),                      # srcs NULL
+             (nullp.data_ptr(), bad_out.data_ptr(), 4096, 3, 0)]       # NULL source
+    arr = np.zeros(len(rows), xr.ITEM_DTYPE)
+    for k, r in enumerate(rows):
+        arr[k] = r
+    dev_items = torch.from_numpy(arr.view(np.uint8).copy()).to("cuda")
+    xr.batched_reduce(dev_items, "sum", dtype=dtype)
+    torch.cuda.synchronize()
+    for k, (o1, o2) in enumerate(zip(outs, outs2)):
+        assert np.array_equal(gu.bits(o1, dtype), gu.bits(o2, dtype)), k
+    assert torch.all(bad_out == 7)
+    del keep
+
+
+def test_specials_exact(xr):
+    """Hand-picked columns through the GPU: -0 columns, overflow, subnormal sums,
+    NaN canonicalisation for max/min, bf16 ties."""
+    cases = [
+        ("f32", "sum", [0x80000000, 0x80000000], 0x80000000),
+        ("f32", "sum", [0x00000001, 0x00000001], 0x00000002),
+        ("f32", "sum", [0x7F7FFFFF, 0x7F7FFFFF, 0xFF7FFFFF], 0x7F800000),
+        ("f32", "sum", [0x3F800000, 0x33800000, 0x33800000], 0x3F800000),
+        ("f32", "max", [0x80000000, 0x00000000], 0x00000000),
+        ("f32", "min", [0x00000000, 0x80000000], 0x80000000),
+        ("f32", "max", [0x3F800000, 0x7FC00001], 0x7FC00000),
+        ("f32", "min", [0xFFC00000, 0x3F800000], 0x7FC00000),
+        ("bf16", "sum", [0x3F80, 0x3B80, 0x3B80], 0x3F81),
+        ("bf16", "sum", [0x3F80, 0x3B80], 0x3F80),
+        ("bf16", "sum", [0x7F7F, 0x7F7F], 0x7F80),
+        ("bf16", "sum", [0x0001, 0x0001], 0x0002),
+        ("bf16", "max", [0x8000, 0x0000], 0x0000),
+        ("bf16", "max", [0x7FC1, 0x0000], 0x7FC0),
+    ]
+    for dtype, op, col, expect in cases:
+        n = 4096 + 3   # vector body and scalar tail both see the column
+        srcs = [np.full(n, v, gu.NP_BITS[dtype]).view(wl.NP_TYPES[dtype]) for v in col]
+        got = gu.bits(_run_allreduce(xr, srcs, dtype, op), dtype)
+        assert np.all(got == expect), (dtype, op, [hex(c) for c in col], hex(int(got[0])),
+                                       hex(int(got[-1])))

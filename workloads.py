@@ -6,8 +6,11 @@ lays them out.  The shapes follow the message sizes the paper quotes for its
 collectives (8 MB FTAR chunks, gradient buckets, small inference messages;
 Sections 5 and 6), since the paper's own workloads are proprietary traces.
 
-Generator: numpy ``Generator(PCG64(seed))``.  Float values are drawn in
-binary32; bf16 inputs are those binary32 draws converted by PyTorch's CPU
+Generator: a stream ``seed`` of n values is cut into chunks of 2^22
+elements; chunk c is drawn from numpy ``Generator(PCG64(SeedSequence([seed,
+c])))``, so chunks can be drawn in parallel threads and any prefix of a
+stream is the same whatever n is.  Float values are drawn in binary32; bf16
+inputs are those binary32 draws converted by PyTorch's CPU
 ``to(torch.bfloat16)`` (a library conversion, round to nearest even).  bf16
 arrays are carried as uint16 bit patterns.
 
@@ -23,6 +26,8 @@ Workloads (M = 2^20, K = 2^10 elements):
 from __future__ import annotations
 
 import math
+import threading
+from concurrent.futures import ThreadPoolExecutor
 from dataclasses import dataclass
 
 import numpy as np
@@ -74,37 +79,72 @@ def _rng(seed: int) -> np.random.Generator:
     return np.random.Generator(np.random.PCG64(seed))
 
 
-def draw(dist: str, n: int, seed: int, dtype: str) -> np.ndarray:
-    """n values of distribution ``dist`` from stream ``seed`` in element type ``dtype``."""
-    g = _rng(seed)
+CHUNK = 1 << 22
+_tls = threading.local()
+
+
+def _scratch(n: int) -> np.ndarray:
+    """Per-thread float32 scratch of at least n elements (reused across chunks)."""
+    buf = getattr(_tls, "buf", None)
+    if buf is None or buf.size < n:
+        buf = np.empty(max(n, CHUNK), np.float32)
+        _tls.buf = buf
+    return buf[:n]
+
+
+def _fill_chunk(dist: str, out: np.ndarray, seed: int, c: int, dtype: str) -> None:
+    """Draw chunk c of stream ``seed`` into ``out`` (len(out) values)."""
+    g = np.random.Generator(np.random.PCG64(np.random.SeedSequence([seed, c])))
+    n = out.size
     if dist == "int32":
-        v = g.integers(-(2**31), 2**31, size=n, dtype=np.int64).astype(np.int32)
-        return v if dtype == "i32" else v.view(np.uint32)
-    if dist == "uniform":
-        x = g.uniform(-1.0, 1.0, size=n).astype(np.float32)
+        v = g.integers(-(2**31), 2**31, size=n, dtype=np.int32)
+        out[:] = v if dtype == "i32" else v.view(np.uint32)
+        return
+    x = out if dtype == "f32" else _scratch(n)
+    if dist == "uniform":                       # U[-1, 1)
+        g.random(out=x, dtype=np.float32)
+        x *= np.float32(2.0)
+        x -= np.float32(1.0)
     elif dist == "normal":
-        x = g.standard_normal(size=n, dtype=np.float32)
+        g.standard_normal(out=x, dtype=np.float32)
     elif dist == "normal_1e-3":
-        x = g.standard_normal(size=n, dtype=np.float32) * np.float32(1e-3)
+        g.standard_normal(out=x, dtype=np.float32)
+        x *= np.float32(1e-3)
     elif dist == "normal_specials":
         # per element: 1% +-inf, 1% +-0.0 (signs 50/50), otherwise N(0,1)
-        x = g.standard_normal(size=n, dtype=np.float32)
-        u = g.random(size=n)
-        sgn = g.random(size=n) < 0.5
+        g.standard_normal(out=x, dtype=np.float32)
+        u = g.random(size=n, dtype=np.float32)
+        neg = g.random(size=n, dtype=np.float32) < 0.5
         x[u < 0.01] = np.float32(np.inf)
-        zero = (u >= 0.01) & (u < 0.02)
-        x[zero] = np.float32(0.0)
-        special = u < 0.02
-        x[special & sgn] = -x[special & sgn]
+        x[(u >= 0.01) & (u < 0.02)] = np.float32(0.0)
+        flip = (u < 0.02) & neg
+        x[flip] = -x[flip]
     elif dist == "ones":
-        x = np.ones(n, np.float32)
+        x[:] = np.float32(1.0)
     else:
         raise ValueError(dist)
     if dtype == "bf16":
-        return to_bf16_bits(x)
-    if dtype == "f32":
-        return x
-    raise ValueError(f"float distribution {dist} for {dtype}")
+        out[:] = to_bf16_bits(x)
+    elif dtype != "f32":
+        raise ValueError(f"float distribution {dist} for {dtype}")
+
+
+def draw(dist: str, n: int, seed: int, dtype: str, threads: int = 16) -> np.ndarray:
+    """n values of distribution ``dist`` from stream ``seed`` in element type ``dtype``."""
+    out = np.empty(n, NP_TYPES[dtype])
+    nchunks = (n + CHUNK - 1) // CHUNK
+
+    def fill(c):
+        lo = c * CHUNK
+        _fill_chunk(dist, out[lo:min(n, lo + CHUNK)], seed, c, dtype)
+
+    if nchunks <= 1:
+        for c in range(nchunks):
+            fill(c)
+    else:
+        with ThreadPoolExecutor(max_workers=min(threads, nchunks)) as ex:
+            list(ex.map(fill, range(nchunks)))
+    return out
 
 
 # Blocks of structured extremes in c5b: [0, 64K) every source is +-0.0 with a
