@@ -22,7 +22,8 @@
  *                    addition modulo 2^32;
  *          XRED_PROD binary32 multiply, or the low 32 bits of the product;
  *          XRED_MAX / XRED_MIN  float: total order -inf < ... < -0 < +0 < ...
- *                    < +inf, any NaN operand gives the quiet NaN 0x7FC00000;
+ *                    < +inf; a NaN among the reduced values gives the quiet
+ *                    NaN 0x7FC00000 (also for P = 1 and the INIT step);
  *                    int32 signed, uint32 unsigned;
  *   - the accumulator starts from up(src[0][i]) (never from zero), so a column
  *     of -0.0 sums to -0.0;

@@ -28,8 +28,10 @@
  * notes):
  *   - the accumulator starts from up(src[0][i]), never from 0, so a column of
  *     -0.0 sums to -0.0;
- *   - MAX/MIN use the total order -inf < ... < -0 < +0 < ... < +inf; any NaN
- *     operand gives the canonical quiet NaN 0x7FC00000;
+ *   - MAX/MIN use the total order -inf < ... < -0 < +0 < ... < +inf; a NaN
+ *     among the reduced values gives the canonical quiet NaN 0x7FC00000,
+ *     whatever their number (also for a single source and for the INIT step
+ *     of the step-wise mode);
  *   - NaN payloads of SUM/PROD are not specified ("parity unpinned" for NaN
  *     payloads: tests compare NaN-ness only);
  *   - down() of a NaN to bf16 keeps the sign and gives the quiet NaN 0x7FC0.
@@ -175,6 +177,14 @@ static uint32_t op_int(int op, int dtype, uint32_t a, uint32_t b)
     }
 }
 
+/* MAX/MIN results: a NaN anywhere among the reduced values is reported as the
+ * canonical quiet NaN, also when no binary operation was applied (P = 1). */
+static float settle(int op, float v)
+{
+    if ((op == XO_MAX || op == XO_MIN) && isnan(v)) return canonical_nan();
+    return v;
+}
+
 static int valid_dtype(int dtype) { return elem_size(dtype) != 0; }
 static int valid_op(int op) { return op >= XO_SUM && op <= XO_MIN; }
 
@@ -188,7 +198,7 @@ static void reduce_one(const void *const *srcs, int nsrc, uint64_t off, void *ds
         float acc = up_float(srcs[0], off + i, dtype);
         for (int p = 1; p < nsrc; ++p)
             acc = op_float(op, acc, up_float(srcs[p], off + i, dtype));
-        down_float(dst, i, dtype, acc);
+        down_float(dst, i, dtype, settle(op, acc));
     } else {
         uint32_t acc = up_int(srcs[0], off + i);
         for (int p = 1; p < nsrc; ++p)
@@ -246,6 +256,7 @@ int xo_reduce_copy_step(const void *in, void *acc, void *dst, uint64_t count, in
         if (is_float_type(dtype)) {
             float x = up_float(in, i, dtype);
             float a = init ? x : op_float(op, up_float(acc, i, XO_F32), x);
+            a = settle(op, a);
             if (fin) down_float(dst, i, dtype, a);
             else down_float(acc, i, XO_F32, a);
         } else {

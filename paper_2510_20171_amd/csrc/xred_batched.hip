@@ -136,7 +136,12 @@ __global__ __launch_bounds__(kBlock) void batched_kernel(const xred_item *items,
         const uint64_t g1 = total * (blockIdx.x + 1) / gridDim.x;
         if (g0 == g1) return;
         left = g1 - g0;
-        // find the item holding global tile g0
+        // find the item holding global tile g0 (if none is found the walk
+        // below starts past the last item and does nothing)
+        if (threadIdx.x == 0) {
+            s_start[0] = (uint64_t)nitems;
+            s_start[1] = 0;
+        }
         uint64_t base = 0;
         for (int w0 = 0; w0 < nitems; w0 += kBlock) {
             const int i = w0 + (int)threadIdx.x;

@@ -168,6 +168,8 @@ def reduce_column(vals_bits, dtype: str, op: str) -> int:
         acc = up(vals_bits[0])
         for v in vals_bits[1:]:
             acc = FOPS[op](acc, up(v))
+        if op in ("max", "min") and is_nan32(acc):
+            acc = CANON_NAN32      # a NaN among the values, whatever their number
         return f32_to_bf16(acc) if dtype == "bf16" else acc
     acc = vals_bits[0] & 0xFFFFFFFF
     for v in vals_bits[1:]:
