@@ -291,6 +291,8 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--no-secondary", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="also run 3 plain device copies of 1 GiB (for scaling HBM byte counters)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the reduce step runs on a single MI355X and "
@@ -347,6 +349,14 @@ def main() -> int:
                      "kernel": "reduce_vec_kernel<TBF16, OpSum, 8>",
                      "kernel_source_sha": kernel_source_sha()},
     }
+    if args.calibrate_copy:
+        a = torch.empty(1 << 29, dtype=torch.int16, device="cuda")
+        b = torch.empty_like(a)
+        for _ in range(3):
+            b.copy_(a)
+        torch.cuda.synchronize()
+        log("calibration: 3 copies of 1 GiB done")
+        del a, b
     if not args.no_cpu_baseline:
         log("timing the CPU oracle on a sample")
         sample = [s[: 1 << 22] for s in srcs_np]
