@@ -2,7 +2,7 @@
 //
 // Small messages are dominated by per-call overhead (the T_c term of the
 // LogP model in Section 6.2), so a batch of K reductions is run as one
-// kernel.  Work is cut into tiles of kBlock*kU 16-byte vectors of one item;
+// kernel.  Work is cut into tiles of kB*kU 16-byte vectors of one item;
 // the global tile sequence (item 0's tiles, then item 1's, ...) is split
 // into one contiguous range per workgroup, so each workgroup walks forward
 // through consecutive items and reads each descriptor once.
@@ -22,12 +22,14 @@
 namespace xred {
 namespace {
 
-constexpr int kU = 2;
+constexpr int kU = 1;
+constexpr int kB = 512;
 
 template <class T>
-constexpr uint64_t tile_vecs() { return (uint64_t)kBlock * kU; }
+constexpr uint64_t tile_vecs() { return (uint64_t)kB * kU; }
 template <class T>
 constexpr uint64_t tile_elems() { return tile_vecs<T>() * T::kVec; }
+constexpr uint32_t kTileBytes = (uint32_t)kB * kU * 16u;
 
 __device__ __forceinline__ bool item_runnable(const xred_item &it)
 {
@@ -49,27 +51,20 @@ __device__ __forceinline__ uint64_t uniform64(uint64_t x)
     return ((uint64_t)hi << 32) | lo;
 }
 
-// Inclusive prefix sum over the workgroup; s[kBlock-1] holds the total
-// until the next call.
+// Inclusive prefix sum over the workgroup; s[kB-1] holds the total until the
+// next call.
 __device__ uint64_t block_inclusive_scan(uint64_t v, uint64_t *s)
 {
     __syncthreads();
     s[threadIdx.x] = v;
     __syncthreads();
-    for (int off = 1; off < kBlock; off <<= 1) {
+    for (int off = 1; off < kB; off <<= 1) {
         const uint64_t t = threadIdx.x >= (unsigned)off ? s[threadIdx.x - off] : 0;
         __syncthreads();
         s[threadIdx.x] += t;
         __syncthreads();
     }
     return s[threadIdx.x];
-}
-
-template <class T, class Op, int NP>
-__device__ __forceinline__ void tile_np(const GlobalSrc &src, int nsrc, char *dst, size_t v0,
-                                        size_t nvec)
-{
-    reduce_vec_tile<T, Op, NP, kU, true, true, true>(src, nsrc, dst, v0, nvec);
 }
 
 // Tile lt of one item.
@@ -91,17 +86,24 @@ __device__ void batched_tile(const xred_item &it, uint64_t lt)
     const uint64_t count = it.count;
     if ((bits & 15u) == 0) {
         const size_t nvec = count / T::kVec;
-        const size_t v0 = lt * tile_vecs<T>() + threadIdx.x;
-        switch (nsrc) {
-        case 1: tile_np<T, Op, 1>(src, nsrc, dst, v0, nvec); break;
-        case 2: tile_np<T, Op, 2>(src, nsrc, dst, v0, nvec); break;
-        case 3: tile_np<T, Op, 3>(src, nsrc, dst, v0, nvec); break;
-        case 4: tile_np<T, Op, 4>(src, nsrc, dst, v0, nvec); break;
-        case 5: tile_np<T, Op, 5>(src, nsrc, dst, v0, nvec); break;
-        case 6: tile_np<T, Op, 6>(src, nsrc, dst, v0, nvec); break;
-        case 7: tile_np<T, Op, 7>(src, nsrc, dst, v0, nvec); break;
-        case 8: tile_np<T, Op, 8>(src, nsrc, dst, v0, nvec); break;
-        default: tile_np<T, Op, 0>(src, nsrc, dst, v0, nvec); break;
+        const size_t vbytes = nvec * 16;
+        const size_t off = lt * kTileBytes;
+        if (off < vbytes) {
+            const Tile tl{off, tile_nrec(vbytes, off, kTileBytes)};
+            switch (nsrc) {
+            case 1: reduce_tile<T, Op, 1, kU, kB>(src, nsrc, dst, tl); break;
+            case 2: reduce_tile<T, Op, 2, kU, kB>(src, nsrc, dst, tl); break;
+            case 3: reduce_tile<T, Op, 3, kU, kB>(src, nsrc, dst, tl); break;
+            case 4: reduce_tile<T, Op, 4, kU, kB>(src, nsrc, dst, tl); break;
+            case 5: reduce_tile<T, Op, 5, kU, kB>(src, nsrc, dst, tl); break;
+            case 6: reduce_tile<T, Op, 6, kU, kB>(src, nsrc, dst, tl); break;
+            case 7: reduce_tile<T, Op, 7, kU, kB>(src, nsrc, dst, tl); break;
+            case 8: reduce_tile<T, Op, 8, kU, kB>(src, nsrc, dst, tl); break;
+            case 16: reduce_tile<T, Op, 16, kU, kB>(src, nsrc, dst, tl); break;
+            case 32: reduce_tile<T, Op, 32, kU, kB>(src, nsrc, dst, tl); break;
+            case 64: reduce_tile<T, Op, 64, kU, kB>(src, nsrc, dst, tl); break;
+            default: reduce_tile<T, Op, 0, kU, kB>(src, nsrc, dst, tl); break;
+            }
         }
         // the item's last tile also takes the elements after its last full vector
         if ((lt + 1) * tile_elems<T>() >= count) {
@@ -111,15 +113,15 @@ __device__ void batched_tile(const xred_item &it, uint64_t lt)
     } else {
         const uint64_t e0 = lt * tile_elems<T>();
         const uint64_t e1 = count < e0 + tile_elems<T>() ? count : e0 + tile_elems<T>();
-        for (uint64_t i = e0 + threadIdx.x; i < e1; i += kBlock) reduce_elem<T, Op>(src, nsrc, dst, i);
+        for (uint64_t i = e0 + threadIdx.x; i < e1; i += kB) reduce_elem<T, Op>(src, nsrc, dst, i);
     }
 }
 
 template <class T, class Op, bool PLANNED>
-__global__ __launch_bounds__(kBlock) void batched_kernel(const xred_item *items, int nitems,
+__global__ __launch_bounds__(kB) void batched_kernel(const xred_item *items, int nitems,
                                                          const WgStart *wg)
 {
-    __shared__ uint64_t s_scan[kBlock];
+    __shared__ uint64_t s_scan[kB];
     __shared__ uint64_t s_start[2];
     uint64_t k, lt, left;
     if constexpr (PLANNED) {
@@ -129,9 +131,9 @@ __global__ __launch_bounds__(kBlock) void batched_kernel(const xred_item *items,
         left = w.ntiles;
     } else {
         uint64_t mine = 0;
-        for (int i = threadIdx.x; i < nitems; i += kBlock) mine += item_tiles<T, true>(items[i]);
+        for (int i = threadIdx.x; i < nitems; i += kB) mine += item_tiles<T, true>(items[i]);
         block_inclusive_scan(mine, s_scan);
-        const uint64_t total = s_scan[kBlock - 1];
+        const uint64_t total = s_scan[kB - 1];
         const uint64_t g0 = total * blockIdx.x / gridDim.x;
         const uint64_t g1 = total * (blockIdx.x + 1) / gridDim.x;
         if (g0 == g1) return;
@@ -143,7 +145,7 @@ __global__ __launch_bounds__(kBlock) void batched_kernel(const xred_item *items,
             s_start[1] = 0;
         }
         uint64_t base = 0;
-        for (int w0 = 0; w0 < nitems; w0 += kBlock) {
+        for (int w0 = 0; w0 < nitems; w0 += kB) {
             const int i = w0 + (int)threadIdx.x;
             const uint64_t c = i < nitems ? item_tiles<T, true>(items[i]) : 0;
             const uint64_t incl = block_inclusive_scan(c, s_scan);
@@ -152,7 +154,7 @@ __global__ __launch_bounds__(kBlock) void batched_kernel(const xred_item *items,
                 s_start[0] = (uint64_t)i;
                 s_start[1] = g0 - base - excl;
             }
-            const uint64_t wtot = s_scan[kBlock - 1];
+            const uint64_t wtot = s_scan[kB - 1];
             __syncthreads();
             if (base + wtot > g0) break;
             base += wtot;
@@ -182,10 +184,10 @@ hipError_t go(bool planned, const xred_item *d_items, int nitems, const WgStart 
               unsigned grid, hipStream_t s)
 {
     if (planned)
-        hipLaunchKernelGGL((batched_kernel<T, Op, true>), dim3(grid), dim3(kBlock), 0, s, d_items,
+        hipLaunchKernelGGL((batched_kernel<T, Op, true>), dim3(grid), dim3(kB), 0, s, d_items,
                            nitems, d_wg);
     else
-        hipLaunchKernelGGL((batched_kernel<T, Op, false>), dim3(grid), dim3(kBlock), 0, s,
+        hipLaunchKernelGGL((batched_kernel<T, Op, false>), dim3(grid), dim3(kB), 0, s,
                            d_items, nitems, d_wg);
     return hipGetLastError();
 }

@@ -6,7 +6,12 @@
 namespace xred {
 namespace {
 
-constexpr int kU = 2;  // 16-byte vectors per thread per tile
+// One 16-byte vector per thread, 512-thread workgroups: 8 KiB tiles of every
+// source.  Measured on MI355X against 2 and 4 vectors per thread and 256 or
+// 1024 threads; this shape was fastest or within noise of it for P = 8 and
+// P = 32, and has the most workgroups for mid-size messages.
+constexpr int kU = 1;    // 16-byte vectors per thread per tile
+constexpr int kB = 512;  // threads per workgroup
 
 template <class T, class Op, int NP, int MAXP>
 hipError_t go_vec(const char *const *srcs, int nsrc, char *dst, size_t count, hipStream_t s)
@@ -16,10 +21,10 @@ hipError_t go_vec(const char *const *srcs, int nsrc, char *dst, size_t count, hi
     for (int p = nsrc; p < MAXP; ++p) ks.p[p] = nullptr;
     const size_t nvec = count / T::kVec;
     const uint32_t tail = (uint32_t)(count % T::kVec);
-    constexpr size_t kTile = (size_t)kBlock * kU;
+    constexpr size_t kTile = (size_t)kB * kU;
     const uint64_t tiles = (nvec + kTile - 1) / kTile + (tail ? 1 : 0);
-    hipLaunchKernelGGL((reduce_vec_kernel<T, Op, NP, MAXP, kU, true, true>), dim3(grid_for(tiles)),
-                       dim3(kBlock), 0, s, ks, nsrc, dst, nvec, tail);
+    hipLaunchKernelGGL((reduce_vec_kernel<T, Op, NP, MAXP, kU, kB>), dim3(grid_for(tiles)),
+                       dim3(kB), 0, s, ks, nsrc, dst, nvec, tail);
     return hipGetLastError();
 }
 
@@ -32,8 +37,8 @@ hipError_t go(const char *const *srcs, int nsrc, char *dst, size_t count, hipStr
         KernargSrc<XRED_MAX_SRC> ks;
         for (int p = 0; p < nsrc; ++p) ks.p[p] = srcs[p];
         for (int p = nsrc; p < XRED_MAX_SRC; ++p) ks.p[p] = nullptr;
-        hipLaunchKernelGGL((reduce_scalar_kernel<T, Op>), dim3(grid_for((count + kBlock - 1) / kBlock)),
-                           dim3(kBlock), 0, s, ks, nsrc, dst, count);
+        hipLaunchKernelGGL((reduce_scalar_kernel<T, Op, kB>), dim3(grid_for((count + kB - 1) / kB)),
+                           dim3(kB), 0, s, ks, nsrc, dst, count);
         return hipGetLastError();
     }
     switch (nsrc) {
@@ -45,6 +50,9 @@ hipError_t go(const char *const *srcs, int nsrc, char *dst, size_t count, hipStr
     case 6: return go_vec<T, Op, 6, 8>(srcs, nsrc, dst, count, s);
     case 7: return go_vec<T, Op, 7, 8>(srcs, nsrc, dst, count, s);
     case 8: return go_vec<T, Op, 8, 8>(srcs, nsrc, dst, count, s);
+    case 16: return go_vec<T, Op, 16, 16>(srcs, nsrc, dst, count, s);
+    case 32: return go_vec<T, Op, 32, 32>(srcs, nsrc, dst, count, s);
+    case 64: return go_vec<T, Op, 64, 64>(srcs, nsrc, dst, count, s);
     default: return go_vec<T, Op, 0, XRED_MAX_SRC>(srcs, nsrc, dst, count, s);
     }
 }

@@ -13,6 +13,7 @@ namespace xred {
 namespace {
 
 constexpr int kU = 2;
+constexpr int kB = 256;
 
 template <class T, class Op, unsigned FLAGS>
 hipError_t go(const char *in, char *acc, char *dst, size_t count, hipStream_t s)
@@ -27,14 +28,14 @@ hipError_t go(const char *in, char *acc, char *dst, size_t count, hipStream_t s)
     if (vec) {
         const size_t nvec = count / T::kVec;
         const size_t tail = count % T::kVec;
-        constexpr size_t kTile = (size_t)kBlock * kU;
+        constexpr size_t kTile = (size_t)kB * kU;
         const uint64_t tiles = (nvec + kTile - 1) / kTile + (tail ? 1 : 0);
-        hipLaunchKernelGGL((step_kernel<T, Op, FLAGS, kU, true>), dim3(grid_for(tiles)),
-                           dim3(kBlock), 0, s, in, acc, dst, nvec, tail);
+        hipLaunchKernelGGL((step_kernel<T, Op, FLAGS, kU, kB, true>), dim3(grid_for(tiles)),
+                           dim3(kB), 0, s, in, acc, dst, nvec, tail);
     } else {
-        hipLaunchKernelGGL((step_kernel<T, Op, FLAGS, kU, false>),
-                           dim3(grid_for((count + kBlock - 1) / kBlock)), dim3(kBlock), 0, s, in,
-                           acc, dst, (size_t)0, count);
+        hipLaunchKernelGGL((step_kernel<T, Op, FLAGS, kU, kB, false>),
+                           dim3(grid_for((count + kB - 1) / kB)), dim3(kB), 0, s, in, acc, dst,
+                           (size_t)0, count);
     }
     return hipGetLastError();
 }
@@ -70,14 +71,14 @@ hipError_t go_cast(const char *acc, char *dst, size_t count, hipStream_t s)
     if ((((uintptr_t)acc | (uintptr_t)dst) & 15u) == 0) {
         const size_t nvec = count / T::kVec;
         const size_t tail = count % T::kVec;
-        constexpr size_t kTile = (size_t)kBlock * kU;
+        constexpr size_t kTile = (size_t)kB * kU;
         const uint64_t tiles = (nvec + kTile - 1) / kTile + (tail ? 1 : 0);
-        hipLaunchKernelGGL((acc_cast_kernel<T, kU, true>), dim3(grid_for(tiles)), dim3(kBlock),
-                           0, s, acc, dst, nvec, tail);
+        hipLaunchKernelGGL((acc_cast_kernel<T, kU, kB, true>), dim3(grid_for(tiles)), dim3(kB), 0,
+                           s, acc, dst, nvec, tail);
     } else {
-        hipLaunchKernelGGL((acc_cast_kernel<T, kU, false>),
-                           dim3(grid_for((count + kBlock - 1) / kBlock)), dim3(kBlock), 0, s, acc,
-                           dst, (size_t)0, count);
+        hipLaunchKernelGGL((acc_cast_kernel<T, kU, kB, false>),
+                           dim3(grid_for((count + kB - 1) / kB)), dim3(kB), 0, s, acc, dst,
+                           (size_t)0, count);
     }
     return hipGetLastError();
 }
