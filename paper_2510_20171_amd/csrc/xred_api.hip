@@ -11,6 +11,7 @@
 #include <stdlib.h>
 #include <string.h>
 
+#include <algorithm>
 #include <atomic>
 #include <mutex>
 
@@ -144,7 +145,10 @@ xred_status batched_host(const xred_item *items, int nitems, xred_dtype dtype, x
     }
     if (total_tiles == 0) return XRED_SUCCESS;
 
-    const unsigned grid = grid_for(total_tiles);
+    // Persistent workgroups (at most batched_device_grid()), each walking a
+    // contiguous range of tiles: one descriptor prologue per workgroup
+    // instead of one per tile.
+    const unsigned grid = (unsigned)std::min<uint64_t>(total_tiles, batched_device_grid());
     const size_t items_bytes = sizeof(xred_item) * (size_t)nitems;
     const size_t wg_bytes = sizeof(WgStart) * (size_t)grid;
     const size_t need = items_bytes + wg_bytes + 8 * (size_t)total_ptrs;
@@ -252,7 +256,7 @@ unsigned grid_for(uint64_t tiles)
 
 unsigned batched_device_grid()
 {
-    static const long per_cu = env_long("XRED_BATCH_WG_PER_CU", 8);
+    static const long per_cu = env_long("XRED_BATCH_WG_PER_CU", 16);
     return grid_for((uint64_t)device_cus() * (uint64_t)per_cu);
 }
 

@@ -44,6 +44,19 @@ __device__ __forceinline__ uint64_t item_tiles(const xred_item &it)
     return (it.count + tile_elems<T>() - 1) / tile_elems<T>();
 }
 
+// Descriptor of item k, loaded field by field with scalar loads.
+__device__ __forceinline__ xred_item load_item(const xred_item *items, uint64_t k)
+{
+    const xred_item *p = items + k;
+    xred_item it;
+    it.srcs = sload(&p->srcs);
+    it.dst = sload(&p->dst);
+    it.count = sload(&p->count);
+    it.nsrc = sload(&p->nsrc);
+    it.reserved = sload(&p->reserved);
+    return it;
+}
+
 __device__ __forceinline__ uint64_t uniform64(uint64_t x)
 {
     const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)x);
@@ -76,7 +89,7 @@ __device__ void batched_tile(const xred_item &it, uint64_t lt)
     uintptr_t bits = (uintptr_t)it.dst;
     bool null_src = false;
     for (int p = 0; p < nsrc; ++p) {
-        const uintptr_t q = (uintptr_t)sp[p];
+        const uintptr_t q = (uintptr_t)sload(sp + p);
         bits |= q;
         null_src |= q == 0;
     }
@@ -125,10 +138,10 @@ __global__ __launch_bounds__(kB) void batched_kernel(const xred_item *items, int
     __shared__ uint64_t s_start[2];
     uint64_t k, lt, left;
     if constexpr (PLANNED) {
-        const WgStart w = wg[blockIdx.x];
-        k = w.item;
-        lt = w.local_tile;
-        left = w.ntiles;
+        const WgStart *w = wg + blockIdx.x;
+        k = sload(&w->item);
+        lt = sload(&w->local_tile);
+        left = sload(&w->ntiles);
     } else {
         uint64_t mine = 0;
         for (int i = threadIdx.x; i < nitems; i += kB) mine += item_tiles<T, true>(items[i]);
@@ -166,7 +179,8 @@ __global__ __launch_bounds__(kB) void batched_kernel(const xred_item *items, int
     lt = uniform64(lt);
     left = uniform64(left);
     while (left > 0 && k < (uint64_t)nitems) {
-        const xred_item it = items[k];
+        k = uniform64(k);
+        const xred_item it = load_item(items, k);
         const uint64_t nt = item_tiles<T, !PLANNED>(it);
         if (lt >= nt) {
             ++k;

@@ -70,10 +70,20 @@ struct KernargSrc {
     __device__ __forceinline__ const char *operator()(int i) const { return p[i]; }
 };
 
+// Scalar load of a value every lane of the wavefront reads at the same
+// address: going through the constant address space makes the compiler use
+// s_load into SGPRs, so buffer descriptors built from the value are uniform
+// (a vector load would force a readfirstlane loop around every buffer access).
+template <class V>
+__device__ __forceinline__ V sload(const V *p)
+{
+    return *(const __attribute__((address_space(4))) V *)p;
+}
+
 // Source pointers read from a device array (batched descriptors).
 struct GlobalSrc {
     const char *const *p;
-    __device__ __forceinline__ const char *operator()(int i) const { return p[i]; }
+    __device__ __forceinline__ const char *operator()(int i) const { return sload(p + i); }
 };
 
 // Geometry of one tile of one 16-byte-vector stream: the byte offset of the
