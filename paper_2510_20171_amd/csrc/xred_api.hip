@@ -144,14 +144,21 @@ xred_status batched_host(const xred_item *items, int nitems, xred_dtype dtype, x
         total_ptrs += it.nsrc;
     }
     if (total_tiles == 0) return XRED_SUCCESS;
+    if (total_tiles >= 0xFFFFFFFFull)
+        return fail(XRED_INVALID_ARGUMENT, "batch has %llu tiles; at most 2^32-2 are supported",
+                    (unsigned long long)total_tiles);
 
-    // Persistent workgroups (at most batched_device_grid()), each walking a
-    // contiguous range of tiles: one descriptor prologue per workgroup
-    // instead of one per tile.
-    const unsigned grid = (unsigned)std::min<uint64_t>(total_tiles, batched_device_grid());
+    // Round-robin layout (batches up to batched_rr_max_items() items):
+    //     items | tile-start prefix (nitems + 1 u32, padded to 8 B) | source pointers
+    // Range layout (larger batches):
+    //     items | per-workgroup starts | source pointers
+    const bool rr = nitems <= batched_rr_max_items();
+    const unsigned grid =
+        rr ? 0u : (unsigned)std::min<uint64_t>(total_tiles, batched_device_grid());
     const size_t items_bytes = sizeof(xred_item) * (size_t)nitems;
-    const size_t wg_bytes = sizeof(WgStart) * (size_t)grid;
-    const size_t need = items_bytes + wg_bytes + 8 * (size_t)total_ptrs;
+    const size_t plan_bytes = rr ? (4 * ((size_t)nitems + 1) + 7) / 8 * 8
+                                 : sizeof(WgStart) * (size_t)grid;
+    const size_t need = items_bytes + plan_bytes + 8 * (size_t)total_ptrs;
 
     int dev = 0;
     hipError_t e = hipGetDevice(&dev);
@@ -183,13 +190,11 @@ xred_status batched_host(const xred_item *items, int nitems, xred_dtype dtype, x
     if (!s.done && (e = hipEventCreateWithFlags(&s.done, hipEventDisableTiming)) != hipSuccess)
         return hip_fail(e, "hipEventCreate");
 
-    // Layout: items | per-workgroup starts | source pointer arrays.
     char *h = (char *)s.host;
     char *d = (char *)s.dev;
     xred_item *h_items = (xred_item *)h;
-    WgStart *h_wg = (WgStart *)(h + items_bytes);
-    const void **h_ptrs = (const void **)(h + items_bytes + wg_bytes);
-    const char *d_ptrs = d + items_bytes + wg_bytes;
+    const void **h_ptrs = (const void **)(h + items_bytes + plan_bytes);
+    const char *d_ptrs = d + items_bytes + plan_bytes;
     uint64_t pos = 0;
     for (int k = 0; k < nitems; ++k) {
         const xred_item &it = items[k];
@@ -204,25 +209,40 @@ xred_status batched_host(const xred_item *items, int nitems, xred_dtype dtype, x
         for (uint32_t p = 0; p < it.nsrc; ++p) h_ptrs[pos + p] = it.srcs[p];
         pos += it.nsrc;
     }
-    // Workgroup b takes global tiles [total*b/grid, total*(b+1)/grid).
-    uint64_t k = 0, k_first = 0;  // item cursor and its first global tile
-    for (unsigned b = 0; b < grid; ++b) {
-        const uint64_t g0 = (uint64_t)((unsigned __int128)total_tiles * b / grid);
-        const uint64_t g1 = (uint64_t)((unsigned __int128)total_tiles * (b + 1) / grid);
-        for (;;) {
-            const uint64_t nt = (items[k].count + te - 1) / te;
-            if (g0 < k_first + nt) break;
-            k_first += nt;
-            ++k;
+    if (rr) {
+        uint32_t *h_pre = (uint32_t *)(h + items_bytes);
+        uint64_t acc = 0;
+        for (int k = 0; k < nitems; ++k) {
+            h_pre[k] = (uint32_t)acc;
+            acc += (items[k].count + te - 1) / te;
         }
-        h_wg[b].item = (uint32_t)k;
-        h_wg[b].ntiles = (uint32_t)(g1 - g0);
-        h_wg[b].local_tile = g0 - k_first;
+        h_pre[nitems] = (uint32_t)acc;
+    } else {
+        // Workgroup b takes global tiles [total*b/grid, total*(b+1)/grid).
+        WgStart *h_wg = (WgStart *)(h + items_bytes);
+        uint64_t k = 0, k_first = 0;  // item cursor and its first global tile
+        for (unsigned b = 0; b < grid; ++b) {
+            const uint64_t g0 = (uint64_t)((unsigned __int128)total_tiles * b / grid);
+            const uint64_t g1 = (uint64_t)((unsigned __int128)total_tiles * (b + 1) / grid);
+            for (;;) {
+                const uint64_t nt = (items[k].count + te - 1) / te;
+                if (g0 < k_first + nt) break;
+                k_first += nt;
+                ++k;
+            }
+            h_wg[b].item = (uint32_t)k;
+            h_wg[b].ntiles = (uint32_t)(g1 - g0);
+            h_wg[b].local_tile = g0 - k_first;
+        }
     }
     e = hipMemcpyAsync(s.dev, s.host, need, hipMemcpyHostToDevice, stream);
     if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync(descriptors)");
-    e = launch_batched_planned(dtype, op, (const xred_item *)d, nitems,
-                               (const WgStart *)(d + items_bytes), grid, stream);
+    if (rr)
+        e = launch_batched_rr(dtype, op, (const xred_item *)d, nitems,
+                              (const uint32_t *)(d + items_bytes), stream);
+    else
+        e = launch_batched_planned(dtype, op, (const xred_item *)d, nitems,
+                                   (const WgStart *)(d + items_bytes), grid, stream);
     if (e != hipSuccess) return hip_fail(e, "batched launch");
     e = hipEventRecord(s.done, stream);
     if (e != hipSuccess) return hip_fail(e, "hipEventRecord(staging slot)");
@@ -258,6 +278,12 @@ unsigned batched_device_grid()
 {
     static const long per_cu = env_long("XRED_BATCH_WG_PER_CU", 16);
     return grid_for((uint64_t)device_cus() * (uint64_t)per_cu);
+}
+
+unsigned batched_rr_grid(int fit_per_cu)
+{
+    static const long per_cu = env_long("XRED_RR_WG_PER_CU", 0);
+    return grid_for((uint64_t)device_cus() * (uint64_t)(per_cu > 0 ? per_cu : fit_per_cu));
 }
 
 bool supported(xred_dtype dtype, xred_op op)
@@ -398,8 +424,11 @@ XRED_API xred_status xred_batched_reduce(const xred_item *items, int nitems, xre
     if (flags & XRED_ITEMS_ON_DEVICE) {
         if ((uintptr_t)items % alignof(xred_item))
             return fail(XRED_INVALID_ARGUMENT, "items is not %zu-byte aligned", alignof(xred_item));
-        const hipError_t e = launch_batched_device(dtype, op, items, nitems, batched_device_grid(),
-                                                   (hipStream_t)hip_stream);
+        const hipError_t e =
+            nitems <= batched_rr_max_items()
+                ? launch_batched_rr(dtype, op, items, nitems, nullptr, (hipStream_t)hip_stream)
+                : launch_batched_device(dtype, op, items, nitems, batched_device_grid(),
+                                        (hipStream_t)hip_stream);
         return e == hipSuccess ? XRED_SUCCESS : hip_fail(e, "batched launch");
     }
     return batched_host(items, nitems, dtype, op, (hipStream_t)hip_stream);

@@ -112,9 +112,9 @@ __device__ void batched_tile(const xred_item &it, uint64_t lt)
             case 6: reduce_tile<T, Op, 6, kU, kB>(src, nsrc, dst, tl); break;
             case 7: reduce_tile<T, Op, 7, kU, kB>(src, nsrc, dst, tl); break;
             case 8: reduce_tile<T, Op, 8, kU, kB>(src, nsrc, dst, tl); break;
-            case 16: reduce_tile<T, Op, 16, kU, kB>(src, nsrc, dst, tl); break;
-            case 32: reduce_tile<T, Op, 32, kU, kB>(src, nsrc, dst, tl); break;
-            case 64: reduce_tile<T, Op, 64, kU, kB>(src, nsrc, dst, tl); break;
+            // more than 8 sources: the compact group loop (the pipelined
+            // 16/32/64 bodies would raise every batched kernel's register
+            // count and cut its occupancy)
             default: reduce_tile<T, Op, 0, kU, kB>(src, nsrc, dst, tl); break;
             }
         }
@@ -193,6 +193,180 @@ __global__ __launch_bounds__(kB) void batched_kernel(const xred_item *items, int
     }
 }
 
+// ------------------------------------------------------ round-robin variant --
+// Global tile g is processed by workgroup g mod G (G = the workgroups that fit
+// on the chip at once), so the tiles in flight form one moving window over
+// the batch, as in the fused kernel, instead of G scattered ranges.  Each
+// workgroup keeps the batch's tile-start prefix in LDS (copied from the host
+// plan, or computed by a block scan over device-resident descriptors), finds
+// the (item, tile) of each of its tiles by binary search in parallel, and
+// while one tile's loads are in flight fetches the next tile's descriptor and
+// source pointers with scalar loads.
+constexpr int kListMax = 1024;     // tiles a workgroup plans per pass
+constexpr int kRrMaxItems = 8192;  // items whose prefix fits the LDS budget
+
+struct TileDesc {
+    const char *p[8];         // sources 0..7 (valid below nsrc)
+    const char *const *srcs;  // the item's source array
+    char *dst;
+    uint64_t count;
+    uint64_t lt;              // tile within the item
+    uint32_t k;               // item
+    int nsrc;
+    bool fast;                // nsrc <= 8, no NULL source, all pointers 16-byte aligned
+};
+
+__device__ __forceinline__ void fetch_desc(TileDesc &d, const xred_item *items, const uint2 *s_list,
+                                           int j)
+{
+    const uint32_t k = __builtin_amdgcn_readfirstlane(s_list[j].x);
+    const uint32_t lt = __builtin_amdgcn_readfirstlane(s_list[j].y);
+    const xred_item *it = items + k;
+    d.k = k;
+    d.lt = lt;
+    d.srcs = (const char *const *)sload(&it->srcs);
+    d.dst = (char *)sload(&it->dst);
+    d.count = sload(&it->count);
+    d.nsrc = (int)sload(&it->nsrc);
+    uintptr_t bits = (uintptr_t)d.dst;
+    bool null_src = false;
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+        d.p[q] = q < d.nsrc ? sload(d.srcs + q) : nullptr;
+        bits |= (uintptr_t)d.p[q];
+        null_src |= q < d.nsrc && d.p[q] == nullptr;
+    }
+    d.fast = d.nsrc <= 8 && !null_src && (bits & 15u) == 0;
+}
+
+template <class T, class Op, bool PLANNED>
+__global__ __launch_bounds__(kB) void batched_rr_kernel(const xred_item *items, int nitems,
+                                                        const uint32_t *tile_start)
+{
+    extern __shared__ uint2 s_dyn[];
+    __shared__ uint64_t s_scan[kB];
+    uint2 *s_list = s_dyn;                             // kListMax entries
+    uint32_t *s_pre = (uint32_t *)(s_dyn + kListMax);  // nitems + 1 entries
+    if constexpr (PLANNED) {
+        for (int i = threadIdx.x; i <= nitems; i += kB) s_pre[i] = tile_start[i];
+    } else {
+        uint64_t base = 0;
+        for (int w0 = 0; w0 < nitems; w0 += kB) {
+            const int i = w0 + (int)threadIdx.x;
+            const uint64_t c = i < nitems ? item_tiles<T, true>(items[i]) : 0;
+            const uint64_t incl = block_inclusive_scan(c, s_scan);
+            if (i < nitems) s_pre[i] = (uint32_t)(base + incl - c);
+            base += s_scan[kB - 1];
+        }
+        if (base >= 0xFFFFFFFFull) return;   // more tiles than the plan can index: run nothing
+        if (threadIdx.x == 0) s_pre[nitems] = (uint32_t)base;
+    }
+    __syncthreads();
+    const uint64_t total = s_pre[nitems];
+    const uint64_t G = gridDim.x;
+    for (uint64_t g0 = blockIdx.x; g0 < total; g0 += (uint64_t)kListMax * G) {
+        const uint64_t left = (total - g0 + G - 1) / G;
+        const int n = left < (uint64_t)kListMax ? (int)left : kListMax;
+        for (int j = threadIdx.x; j < n; j += kB) {
+            const uint64_t g = g0 + (uint64_t)j * G;
+            int lo = 0, hi = nitems;   // s_pre[lo] <= g < s_pre[hi]
+            while (hi - lo > 1) {
+                const int mid = (lo + hi) >> 1;
+                if (s_pre[mid] <= g) lo = mid;
+                else hi = mid;
+            }
+            s_list[j] = uint2{(uint32_t)lo, (uint32_t)(g - s_pre[lo])};
+        }
+        __syncthreads();
+        TileDesc cur, nxt;
+        fetch_desc(cur, items, s_list, 0);
+        for (int j = 0; j < n; ++j) {
+            // Issue the current tile's loads.  Straight-line code: sources
+            // beyond nsrc, and tiles not on the fast path, get a zero-length
+            // buffer range, so their loads return 0 without touching memory
+            // and their store is dropped.
+            const size_t nvec = cur.count / T::kVec;
+            const size_t vbytes = nvec * 16, toff = cur.lt * kTileBytes;
+            const uint32_t nrec = cur.fast && toff < vbytes ? tile_nrec(vbytes, toff, kTileBytes) : 0u;
+            u32x4 in[8];
+#pragma unroll
+            for (int q = 0; q < 8; ++q) {
+                const bool on = q < cur.nsrc;
+                in[q] = bload<kLoadStream>(make_rsrc((on ? cur.p[q] : cur.dst) + toff, on ? nrec : 0u),
+                                           (uint32_t)threadIdx.x * 16u);
+            }
+            // fetch the next tile's descriptor while those loads are in flight
+            if (j + 1 < n) fetch_desc(nxt, items, s_list, j + 1);
+            // fold (unused sources skipped by a uniform select) and store
+            typename T::Acc acc[T::kVec];
+            up_vec<T>(in[0], acc);
+#pragma unroll
+            for (int q = 1; q < 8; ++q) {
+                const bool on = q < cur.nsrc;
+                typename T::Acc b[T::kVec];
+                up_vec<T>(in[q], b);
+#pragma unroll
+                for (int e = 0; e < T::kVec; ++e) {
+                    const typename T::Acc c = combine<T, Op>(acc[e], b[e]);
+                    acc[e] = on ? c : acc[e];
+                }
+            }
+            bstore<kStoreOut>(down_vec<T, Op>(acc), make_rsrc(cur.dst + toff, nrec),
+                              (uint32_t)threadIdx.x * 16u);
+            if (cur.fast) {
+                if ((cur.lt + 1) * tile_elems<T>() >= cur.count) {
+                    const uint32_t tail = (uint32_t)(cur.count % T::kVec);
+                    if (threadIdx.x < tail)
+                        reduce_elem<T, Op>(GlobalSrc{cur.srcs}, cur.nsrc, cur.dst,
+                                           nvec * T::kVec + threadIdx.x);
+                }
+            } else {
+                batched_tile<T, Op>(load_item(items, cur.k), cur.lt);
+            }
+            cur = nxt;
+        }
+        __syncthreads();
+    }
+}
+
+constexpr size_t rr_lds_bytes(int nitems)
+{
+    return sizeof(uint2) * kListMax + sizeof(uint32_t) * ((size_t)nitems + 1);
+}
+
+template <class T, class Op>
+hipError_t go_rr(bool planned, const xred_item *d_items, int nitems, const uint32_t *d_tile_start,
+                 hipStream_t s)
+{
+    const void *fn = planned ? (const void *)batched_rr_kernel<T, Op, true>
+                             : (const void *)batched_rr_kernel<T, Op, false>;
+    const size_t lds = rr_lds_bytes(nitems);
+    int per_cu = 0;
+    hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, kB, lds);
+    if (e != hipSuccess) return e;
+    const unsigned grid = batched_rr_grid(per_cu > 0 ? per_cu : 1);
+    if (planned)
+        hipLaunchKernelGGL((batched_rr_kernel<T, Op, true>), dim3(grid), dim3(kB), lds, s,
+                           d_items, nitems, d_tile_start);
+    else
+        hipLaunchKernelGGL((batched_rr_kernel<T, Op, false>), dim3(grid), dim3(kB), lds, s,
+                           d_items, nitems, d_tile_start);
+    return hipGetLastError();
+}
+
+template <class T>
+hipError_t go_rr_op(xred_op op, bool planned, const xred_item *d_items, int nitems,
+                    const uint32_t *d_tile_start, hipStream_t s)
+{
+    switch (op) {
+    case XRED_SUM: return go_rr<T, OpSum>(planned, d_items, nitems, d_tile_start, s);
+    case XRED_PROD: return go_rr<T, OpProd>(planned, d_items, nitems, d_tile_start, s);
+    case XRED_MAX: return go_rr<T, OpMax>(planned, d_items, nitems, d_tile_start, s);
+    case XRED_MIN: return go_rr<T, OpMin>(planned, d_items, nitems, d_tile_start, s);
+    }
+    return hipErrorInvalidValue;
+}
+
 template <class T, class Op>
 hipError_t go(bool planned, const xred_item *d_items, int nitems, const WgStart *d_wg,
               unsigned grid, hipStream_t s)
@@ -255,6 +429,21 @@ hipError_t launch_batched_device(xred_dtype dtype, xred_op op, const xred_item *
                                  int nitems, unsigned grid, hipStream_t stream)
 {
     return dispatch(dtype, op, false, d_items, nitems, nullptr, grid, stream);
+}
+
+int batched_rr_max_items() { return kRrMaxItems; }
+
+hipError_t launch_batched_rr(xred_dtype dtype, xred_op op, const xred_item *d_items, int nitems,
+                             const uint32_t *d_tile_start, hipStream_t stream)
+{
+    const bool planned = d_tile_start != nullptr;
+    switch (dtype) {
+    case XRED_FLOAT32: return go_rr_op<TF32>(op, planned, d_items, nitems, d_tile_start, stream);
+    case XRED_BFLOAT16: return go_rr_op<TBF16>(op, planned, d_items, nitems, d_tile_start, stream);
+    case XRED_INT32: return go_rr_op<TI32>(op, planned, d_items, nitems, d_tile_start, stream);
+    case XRED_UINT32: return go_rr_op<TU32>(op, planned, d_items, nitems, d_tile_start, stream);
+    default: return hipErrorInvalidValue;
+    }
 }
 
 }  // namespace xred

@@ -56,4 +56,15 @@ hipError_t launch_batched_device(xred_dtype dtype, xred_op op, const xred_item *
 // Grid used for device-resident batches (fixed: the host cannot see sizes).
 unsigned batched_device_grid();
 
+// Round-robin batched kernel (batches of at most batched_rr_max_items()
+// items).  d_tile_start: the host plan (nitems + 1 exclusive tile-start
+// prefix values), or NULL to have every workgroup compute it from the
+// device-resident descriptors.
+int batched_rr_max_items();
+hipError_t launch_batched_rr(xred_dtype dtype, xred_op op, const xred_item *d_items, int nitems,
+                             const uint32_t *d_tile_start, hipStream_t stream);
+
+// Workgroups for the round-robin kernel given how many fit on one CU.
+unsigned batched_rr_grid(int fit_per_cu);
+
 }  // namespace xred

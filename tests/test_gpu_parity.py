@@ -369,3 +369,45 @@ def test_specials_exact(xr):
         got = gu.bits(_run_allreduce(xr, srcs, dtype, op), dtype)
         assert np.all(got == expect), (dtype, op, [hex(c) for c in col], hex(int(got[0])),
                                        hex(int(got[-1])))
+
+
+@pytest.mark.parametrize("on_device", [False, True])
+def test_batched_beyond_round_robin_limit(xr, orc, on_device):
+    """More items than the round-robin plan holds (8192): the range-walking
+    kernels take over; every item against the oracle."""
+    rng = np.random.default_rng(77)
+    K = 9000
+    sizes = rng.integers(1, 600, size=K)
+    nsrcs = rng.integers(1, 5, size=K)
+    total_in = int(sum(int(n) * int(p) for n, p in zip(sizes, nsrcs)))
+    flat = pins.random_column_values(rng, "bf16", total_in)
+    src_dev = gu.to_dev(flat, "bf16")
+    out_dev = torch.zeros(int(sizes.sum()), dtype=torch.bfloat16, device="cuda")
+    items, host_srcs, outs = [], [], []
+    pos = opos = 0
+    for n, P in zip(sizes.tolist(), nsrcs.tolist()):
+        s = [flat[pos + q * n: pos + (q + 1) * n] for q in range(P)]
+        d = [src_dev[pos + q * n: pos + (q + 1) * n] for q in range(P)]
+        pos += n * P
+        o = out_dev[opos: opos + n]
+        opos += n
+        host_srcs.append(s)
+        items.append((d, o))
+        outs.append(o)
+    if on_device:
+        keep, rows = [], []
+        for d, o in items:
+            pa = torch.tensor([x.data_ptr() for x in d], dtype=torch.int64, device="cuda")
+            keep.append(pa)
+            rows.append((pa.data_ptr(), o.data_ptr(), o.numel(), len(d), 0))
+        arr = np.zeros(len(rows), xr.ITEM_DTYPE)
+        for k, r in enumerate(rows):
+            arr[k] = r
+        xr.batched_reduce(torch.from_numpy(arr.view(np.uint8).copy()).to("cuda"), "sum",
+                          dtype="bf16")
+    else:
+        xr.batched_reduce(items, "sum", dtype="bf16")
+    torch.cuda.synchronize()
+    got = gu.bits(out_dev, "bf16")
+    exp = np.concatenate([orc.allreduce_local(s, "bf16", "sum") for s in host_srcs])
+    gu.assert_parity(got, exp, "bf16", "sum", f"{K} items, device={on_device}")
