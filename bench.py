@@ -34,28 +34,30 @@ sys.path.insert(0, str(ROOT))
 
 METRIC = "reduce-copy GB/s (read+write) and % HBM peak at 1 GPU; small-msg µs/call"
 HBM_PEAK_GBS = 8000.0     # MI355X HBM3E, published
-PROFILE = ROOT / "profiles" / "reduce_bf16_sum_p8_64M.md"
-KERNEL_SOURCES = ["paper_2510_20171_amd/csrc/xred_device.hpp",
-                  "paper_2510_20171_amd/csrc/xred_kernels.hpp",
-                  "paper_2510_20171_amd/csrc/xred_reduce.hip"]
+CSRC = "paper_2510_20171_amd/csrc/"
+KERNEL_SOURCES = {
+    "reduce": [CSRC + "xred_device.hpp", CSRC + "xred_kernels.hpp", CSRC + "xred_reduce.hip"],
+    "step": [CSRC + "xred_device.hpp", CSRC + "xred_kernels.hpp", CSRC + "xred_step.hip"],
+    "batched": [CSRC + "xred_device.hpp", CSRC + "xred_kernels.hpp", CSRC + "xred_batched.hip"],
+}
 
 
-def kernel_source_sha() -> str:
+def kernel_source_sha(family: str = "reduce") -> str:
     h = hashlib.sha256()
-    for f in KERNEL_SOURCES:
+    for f in KERNEL_SOURCES[family]:
         h.update((ROOT / f).read_bytes())
     return h.hexdigest()[:16]
 
 
-def committed_traffic():
-    """HBM bytes per launch from the committed counter summary, if it still
+def committed_traffic(profile: Path, family: str):
+    """HBM bytes per launch from a committed counter summary, if it still
     describes the current kernel sources."""
-    if not PROFILE.exists():
+    if not profile.exists():
         return None
-    text = PROFILE.read_text()
+    text = profile.read_text()
     sha = re.search(r"kernel_source_sha:\s*([0-9a-f]+)", text)
     tb = re.search(r"traffic_bytes_per_launch:\s*([0-9.eE+]+)", text)
-    if not sha or not tb or sha.group(1) != kernel_source_sha():
+    if not sha or not tb or sha.group(1) != kernel_source_sha(family):
         return None
     return float(tb.group(1))
 
@@ -284,11 +286,109 @@ def secondary(torch, xr, L, timer, wl, flush):
     return res
 
 
+def build_workload(name, torch, xr, L, wl):
+    """Inputs resident in HBM and one step of workload `name`.
+
+    Returns a dict with the step callable, algorithmic bytes per step, the
+    dominant kernel, its source family and committed profile, a config
+    description, and a callable timing the CPU oracle on a bounded sample."""
+    import numpy as np
+    w = wl.WORKLOADS[name]
+    stream = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    if w.kind == "allreduce":
+        log(f"generating {name} inputs (P={w.nsrc} x {w.count} {w.dtype})")
+        srcs_np = wl.sources(w)
+        d = [dev_any(torch, s, w.dtype) for s in srcs_np]
+        out = torch.empty_like(d[0])
+        step = reduce_call(L, xr, d, out, w.dtype, w.op)
+        step._keep_inputs = (d, out)
+        es = wl.ELEM_SIZE[w.dtype]
+        np_ = w.nsrc if w.nsrc <= 8 or w.nsrc in (16, 32, 64) else 0
+        res = dict(step=step, alg_bytes=w.alg_bytes(), family="reduce",
+                   kernel=f"reduce_vec_kernel<{w.dtype}, {w.op}, NP={np_}>",
+                   profile=ROOT / "profiles" / f"reduce_{w.dtype}_{name}.md",
+                   config={"workload": f"{name}: allreduce_local P={w.nsrc} x {w.count} {w.dtype}, "
+                                       f"{w.op}, fixed rank order", "P": w.nsrc, "N": w.count,
+                           "io_dtype": w.dtype})
+        sample_n = min(w.count, (1 << 25) // w.nsrc)
+        res["cpu"] = lambda: cpu_baseline([s[:sample_n] for s in srcs_np], w.dtype, w.op,
+                                          w.nsrc, es)
+        return res
+    if w.kind == "stepwise":
+        log(f"generating {name} inputs (16 chunks x {w.count} bf16)")
+        chunks_np = wl.stepwise_chunks(w)
+        chunks = [dev_bf16(torch, c.copy()) for c in chunks_np]
+        acc = torch.empty(w.count, dtype=torch.float32, device="cuda")
+        out = torch.empty_like(chunks[0])
+        cp = [ctypes.c_void_p(c.data_ptr()) for c in chunks]
+        ap, op_ = ctypes.c_void_p(acc.data_ptr()), ctypes.c_void_p(out.data_ptr())
+
+        def step():
+            L.xred_reduce_copy_step(cp[0], ap, None, w.count, 1, 0, 1, stream)
+            for c in cp[1:]:
+                L.xred_reduce_copy_step(c, ap, None, w.count, 1, 0, 0, stream)
+            L.xred_acc_cast(ap, op_, w.count, 1, stream)
+        step._keep_inputs = (chunks, acc, out)
+        res = dict(step=step, alg_bytes=17 * w.count * 2, family="step",
+                   kernel="step_kernel<bf16, sum, 0>",
+                   profile=ROOT / "profiles" / f"step_bf16_{name}.md",
+                   config={"workload": f"{name}: INIT + 15 reduce_copy_step + acc_cast, "
+                                       f"16 chunks x {w.count} bf16, fp32 accumulator",
+                           "chunks": 16, "N": w.count, "io_dtype": "bf16"})
+        res["cpu"] = lambda: cpu_baseline([c.copy() for c in chunks_np], "bf16", "sum", 16, 2)
+        return res
+    # batched
+    sizes = wl.batched_sizes(w)
+    log(f"generating {name} inputs ({len(sizes)} items, P={w.nsrc})")
+    arena, offs = wl.batched_arena(w, sizes)
+    arena_d = dev_bf16(torch, arena)
+    base = arena_d.data_ptr()
+    ends = np.cumsum((sizes + 127) // 128 * 128)
+    opos = np.concatenate([[0], ends[:-1]]).astype(np.int64)
+    outs = torch.empty(int(ends[-1]), dtype=torch.bfloat16, device="cuda")
+    assert int(opos[-1]) + int(sizes[-1]) <= outs.numel()
+    P, K = offs.shape[1], len(sizes)
+    rows = [(ctypes.c_void_p * P)(*[base + int(o) * 2 for o in offs[k]]) for k in range(K)]
+    items = xr.pack_items([(ctypes.addressof(rows[k]), outs.data_ptr() + int(opos[k]) * 2,
+                            int(sizes[k]), P) for k in range(K)])
+
+    def step():
+        st = L.xred_batched_reduce(items, K, 1, 0, 0, stream)
+        if st:
+            xr._lib.check(st)
+    step._keep_inputs = (arena_d, outs, rows, items)
+    res = dict(step=step, alg_bytes=w.alg_bytes(sizes), family="batched",
+               kernel="batched_rr_kernel<bf16, sum, planned>",
+               profile=ROOT / "profiles" / f"batched_bf16_{name}.md",
+               config={"workload": f"{name}: batched_reduce of {K} items, P={P} bf16, sizes "
+                                   "log-uniform 8 KiB-1 MiB per source, host descriptors",
+                       "items": K, "P": P, "io_dtype": "bf16"})
+    sample = [[arena[o:o + int(sizes[k])] for o in offs[k]] for k in range(64)]
+
+    def cpu():
+        import oracle
+        orc = oracle.load()
+        t0 = time.perf_counter()
+        reps = 0
+        while time.perf_counter() - t0 < 10.0:
+            for s in sample:
+                orc.allreduce_local(s, "bf16", "sum")
+            reps += 1
+        el = time.perf_counter() - t0
+        ab = sum((P + 1) * s[0].size * 2 for s in sample) * reps
+        return {"value": round(ab / el / 1e9, 3), "unit": "GB/s", "cores": 1, "kind": "oracle",
+                "sample": f"first 64 items, {reps} reps, {el:.1f} s, one thread"}
+    res["cpu"] = cpu
+    return res
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="c2", choices=["c1", "c2", "c3", "c4", "c5a", "c5b"],
+                    help="which workload one step runs (default: the c2 gradient bucket)")
     ap.add_argument("--no-secondary", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--calibrate-copy", action="store_true",
@@ -310,13 +410,8 @@ def main() -> int:
         return 1
     L = xr.load()
     timer = Timer(torch)
-    w = wl.WORKLOADS["c2"]
-    log("generating c2 inputs (P=8 x 64M bf16)")
-    srcs_np = wl.sources(w)
-    d = [dev_bf16(torch, s) for s in srcs_np]
-    out = torch.empty_like(d[0])
-    step = reduce_call(L, xr, d, out, "bf16", "sum")
-    ab = w.alg_bytes()
+    wk = build_workload(args.workload, torch, xr, L, wl)
+    step, ab = wk["step"], wk["alg_bytes"]
 
     log(f"timing {args.steps} steps after {args.warmup} warmup")
     for _ in range(args.warmup):
@@ -332,22 +427,20 @@ def main() -> int:
     ms = timer.e0.elapsed_time(timer.e1) / args.steps
     gbs = ab / (ms * 1e-3) / 1e9
 
+    config = dict(wk["config"], accumulate="f32" if wk["config"].get("io_dtype") in ("bf16", "f32")
+                  else "u32", alg_bytes_per_step=ab, parallelism="single GPU")
     result = {
         "metric": METRIC, "value": round(gbs, 1), "unit": "GB/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 5),
-        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
-        "data": "synthetic",
-        "config": {"workload": "gradient bucket: allreduce_local P=8 x 2^26 bf16, sum, "
-                               "binary32 accumulation in rank order, bf16 out",
-                   "P": 8, "N": w.count, "io_dtype": "bf16", "accumulate": "f32",
-                   "alg_bytes_per_step": ab, "parallelism": "single GPU"},
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": config["accumulate"], "data": "synthetic", "config": config,
         "pct_hbm_peak": round(100 * gbs / HBM_PEAK_GBS, 2),
         "wall_s_timed": round(wall, 4),
         "roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4),
-                     "traffic": committed_traffic(),
-                     "kernel": "reduce_vec_kernel<TBF16, OpSum, 8>",
-                     "kernel_source_sha": kernel_source_sha()},
+                     "traffic": committed_traffic(wk["profile"], wk["family"]),
+                     "kernel": wk["kernel"],
+                     "kernel_source_sha": kernel_source_sha(wk["family"])},
     }
     if args.calibrate_copy:
         a = torch.empty(1 << 29, dtype=torch.int16, device="cuda")
@@ -359,11 +452,10 @@ def main() -> int:
         del a, b
     if not args.no_cpu_baseline:
         log("timing the CPU oracle on a sample")
-        sample = [s[: 1 << 22] for s in srcs_np]
-        result["cpu_baseline"] = cpu_baseline(sample, "bf16", "sum", 8, 2)
-    del d, out, srcs_np
+        result["cpu_baseline"] = wk["cpu"]()
+    del wk, step
     torch.cuda.empty_cache()
-    if not args.no_secondary:
+    if not args.no_secondary and args.workload == "c2":
         log("secondary workloads")
         flush = torch.empty(1 << 28, dtype=torch.float32, device="cuda")
         result["secondary"] = secondary(torch, xr, L, timer, wl, flush)
