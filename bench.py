@@ -39,6 +39,7 @@ KERNEL_SOURCES = {
     "reduce": [CSRC + "xred_device.hpp", CSRC + "xred_kernels.hpp", CSRC + "xred_reduce.hip"],
     "step": [CSRC + "xred_device.hpp", CSRC + "xred_kernels.hpp", CSRC + "xred_step.hip"],
     "batched": [CSRC + "xred_device.hpp", CSRC + "xred_kernels.hpp", CSRC + "xred_batched.hip"],
+    "ring": [CSRC + "xred_device.hpp", CSRC + "xred_kernels.hpp", CSRC + "xred_ring.hip"],
 }
 
 
@@ -95,6 +96,31 @@ class Timer:
             self.e1.synchronize()
             out.append(self.e0.elapsed_time(self.e1))
         return out
+
+
+class PinnedWords:
+    """n uint32 words of hipHostMalloc'd host memory, with their device address."""
+
+    def __init__(self, n: int):
+        self.hip = ctypes.CDLL("libamdhip64.so")
+        self.hip.hipHostMalloc.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_size_t,
+                                           ctypes.c_uint]
+        self.hip.hipHostGetDevicePointer.argtypes = [ctypes.POINTER(ctypes.c_void_p),
+                                                     ctypes.c_void_p, ctypes.c_uint]
+        self.hip.hipHostFree.argtypes = [ctypes.c_void_p]
+        self.host, self.dev = ctypes.c_void_p(), ctypes.c_void_p()
+        if self.hip.hipHostMalloc(ctypes.byref(self.host), 4 * n, 0) != 0:
+            raise RuntimeError("hipHostMalloc failed")
+        if self.hip.hipHostGetDevicePointer(ctypes.byref(self.dev), self.host, 0) != 0:
+            raise RuntimeError("hipHostGetDevicePointer failed")
+        self.words = (ctypes.c_uint32 * n).from_address(self.host.value)
+        for i in range(n):
+            self.words[i] = 0
+
+    def free(self):
+        if self.host:
+            self.hip.hipHostFree(self.host)
+            self.host = None
 
 
 def median(xs):
@@ -202,6 +228,29 @@ def secondary(torch, xr, L, timer, wl, flush):
     fused = torch.empty_like(out)
     ffn = reduce_call(L, xr, chunks, fused, "bf16", "sum")
     fused_ms = timer.loop_ms(ffn, 50)
+    ring_arr = xr._lib.ptr_array([c.data_ptr() for c in chunks])
+    ring_out = ctypes.c_void_p(fused.data_ptr())
+    ring_ms = timer.loop_ms(lambda: L.xred_ring_reduce(ring_arr, 16, ring_out, w.count, 1, 0, None,
+                                                       1, 0, None, stream), 50)
+    flags = PinnedWords(16)
+    for i in range(16):
+        flags.words[i] = 1
+    ring_flag_ms = timer.loop_ms(lambda: L.xred_ring_reduce(ring_arr, 16, ring_out, w.count, 1, 0,
+                                                            flags.dev, 1, 0, None, stream), 50)
+    # per-step cost of observing an already-set host flag: 64 steps on one tile
+    tiny = [torch.ones(4096, dtype=torch.bfloat16, device="cuda") for _ in range(64)]
+    tiny_arr = xr._lib.ptr_array([c.data_ptr() for c in tiny])
+    tiny_out = torch.empty_like(tiny[0])
+    flags64 = PinnedWords(64)
+    for i in range(64):
+        flags64.words[i] = 1
+    t_none = timer.loop_ms(lambda: L.xred_ring_reduce(tiny_arr, 64, ctypes.c_void_p(tiny_out.data_ptr()),
+                                                      4096, 1, 0, None, 1, 0, None, stream), 50)
+    t_flag = timer.loop_ms(lambda: L.xred_ring_reduce(tiny_arr, 64, ctypes.c_void_p(tiny_out.data_ptr()),
+                                                      4096, 1, 0, flags64.dev, 1, 0, None, stream), 50)
+    torch.cuda.synchronize()
+    flags.free()
+    flags64.free()
     moved = 16 * w.count * 2 + 15 * w.count * 8 + w.count * 4 + w.count * 4 + w.count * 2
     res["c3"] = {"us_per_step": round(st_ms * 1e3, 2),
                  "step_GBs_moved": round(w.count * 10 / st_ms / 1e6, 1),
@@ -209,7 +258,13 @@ def secondary(torch, xr, L, timer, wl, flush):
                  "sequence_GBs_alg": round(17 * w.count * 2 / seq_ms / 1e6, 1),
                  "sequence_GBs_moved": round(moved / seq_ms / 1e6, 1),
                  "fused_16src_us": round(fused_ms * 1e3, 2),
-                 "fused_16src_GBs": round(17 * w.count * 2 / fused_ms / 1e6, 1)}
+                 "fused_16src_GBs": round(17 * w.count * 2 / fused_ms / 1e6, 1),
+                 "ring_one_launch_us": round(ring_ms * 1e3, 2),
+                 "ring_one_launch_GBs": round(17 * w.count * 2 / ring_ms / 1e6, 1),
+                 "ring_host_flags_preset_us": round(ring_flag_ms * 1e3, 2),
+                 "ring_64_steps_1_tile_us": round(t_none * 1e3, 2),
+                 "ring_64_steps_1_tile_host_flags_us": round(t_flag * 1e3, 2),
+                 "host_flag_poll_us_per_step": round((t_flag - t_none) * 1e3 / 64, 3)}
     del chunks, acc, out, fused
 
     # c5a / c5b: P=32 x 8M
@@ -293,8 +348,29 @@ def build_workload(name, torch, xr, L, wl):
     dominant kernel, its source family and committed profile, a config
     description, and a callable timing the CPU oracle on a bounded sample."""
     import numpy as np
-    w = wl.WORKLOADS[name]
+    w = wl.WORKLOADS["c3" if name == "c3ring" else name]
     stream = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    if name == "c3ring":
+        log(f"generating c3 inputs for the one-launch ring (16 chunks x {w.count} bf16)")
+        chunks_np = [c.copy() for c in wl.stepwise_chunks(w)]
+        chunks = [dev_bf16(torch, c) for c in chunks_np]
+        out = torch.empty_like(chunks[0])
+        arr = xr._lib.ptr_array([c.data_ptr() for c in chunks])
+        dptr = ctypes.c_void_p(out.data_ptr())
+
+        def step():
+            st = L.xred_ring_reduce(arr, 16, dptr, w.count, 1, 0, None, 1, 0, None, stream)
+            if st:
+                xr._lib.check(st)
+        step._keep_inputs = (chunks, out, arr)
+        res = dict(step=step, alg_bytes=17 * w.count * 2, family="ring",
+                   kernel="ring_kernel<bf16, sum>",
+                   profile=ROOT / "profiles" / "ring_bf16_c3ring.md",
+                   config={"workload": "c3 in one launch: xred_ring_reduce of 16 chunks x "
+                                       f"{w.count} bf16, accumulator on chip",
+                           "chunks": 16, "N": w.count, "io_dtype": "bf16"})
+        res["cpu"] = lambda: cpu_baseline(chunks_np, "bf16", "sum", 16, 2)
+        return res
     if w.kind == "allreduce":
         log(f"generating {name} inputs (P={w.nsrc} x {w.count} {w.dtype})")
         srcs_np = wl.sources(w)
@@ -387,7 +463,7 @@ def main() -> int:
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default="c2", choices=["c1", "c2", "c3", "c4", "c5a", "c5b"],
+    ap.add_argument("--workload", default="c2", choices=["c1", "c2", "c3", "c3ring", "c4", "c5a", "c5b"],
                     help="which workload one step runs (default: the c2 gradient bucket)")
     ap.add_argument("--no-secondary", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")

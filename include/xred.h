@@ -177,6 +177,37 @@ XRED_API xred_status xred_acc_cast(const void *acc, void *dst, size_t count, xre
 XRED_API xred_status xred_batched_reduce(const xred_item *items, int nitems, xred_dtype dtype,
                                          xred_op op, unsigned flags, void *hip_stream);
 
+/*
+ * All steps of a ring's ReduceCopy in one persistent launch: the FTAR
+ * pipeline's in-kernel reduce (Section 5) gated by producer/consumer flags
+ * in host-pinned or device memory (the host-kernel coordinated mode of
+ * Section 4).  Computes dst[i] = down(fold_{s=0..nchunks-1} up(chunks[s][i])),
+ * the same definition and fold order as xred_allreduce_local over the
+ * chunks, with the accumulator kept on chip (LDS) between steps, so only
+ * the chunks are read and only dst is written.
+ *   chunks     host array of nchunks (1..XRED_MAX_SRC) device pointers to count
+ *              elements each; all buffers 16-byte aligned (else XRED_UNSUPPORTED)
+ *   count      at most xred_ring_max_count(dtype) (else XRED_UNSUPPORTED)
+ *   ready      NULL: every chunk is ready at launch.  Otherwise nchunks
+ *              uint32 words the GPU can read coherently (hipHostMalloc'd or
+ *              device memory); chunk s is read only once
+ *              (int32_t)(ready[s] - epoch) >= 0, observed with a system-scope
+ *              acquire, so data written before the flag is seen.
+ *   timeout_us bound on each wait (0: one second; capped at 60 s).  A
+ *              workgroup whose wait times out writes 1 to *status (if status
+ *              is not NULL) and stops; dst is then unspecified.  The caller
+ *              zeroes *status before the call if it wants to check it.
+ * Errors: as xred_allreduce_local; XRED_UNSUPPORTED for misaligned buffers or
+ * counts beyond the capacity.
+ */
+XRED_API xred_status xred_ring_reduce(const void *const *chunks, int nchunks, void *dst,
+                                      size_t count, xred_dtype dtype, xred_op op,
+                                      const uint32_t *ready, uint32_t epoch, uint64_t timeout_us,
+                                      uint32_t *status, void *hip_stream);
+
+/* Largest count xred_ring_reduce accepts for dtype on the current device. */
+XRED_API size_t xred_ring_max_count(xred_dtype dtype);
+
 /* Bytes per accumulator element for dtype: 4 (binary32 or uint32), 0 if unknown. */
 XRED_API size_t xred_acc_elem_size(xred_dtype dtype);
 

@@ -23,7 +23,7 @@ from ._lib import (ALIAS, DTYPE, EXPORTS, HIP_ERROR, INVALID_ARGUMENT, ITEM_DTYP
                    UNSUPPORTED, XredError, XredItem, check, load, ptr_array)
 
 __all__ = ["allreduce_local", "reduce_scatter_local", "reduce_copy_step", "acc_cast",
-           "batched_reduce", "pack_items", "acc_elem_size", "version", "release", "XredError",
+           "batched_reduce", "ring_reduce", "ring_max_count", "pack_items", "acc_elem_size", "version", "release", "XredError",
            "load", "EXPORTS"]
 
 
@@ -125,6 +125,23 @@ def batched_reduce(items, op: str = "sum", *, dtype: str, stream=None, device=No
     dev_t = items[0][1] if items else None
     st = _stream(dev_t, stream) if dev_t is not None else ctypes.c_void_p(0)
     check(L.xred_batched_reduce(arr, len(rows), DTYPE[dtype], OP[op], 0, st))
+
+
+def ring_reduce(chunks, out, op: str = "sum", *, ready=None, epoch: int = 1,
+                timeout_us: int = 0, status=None, dtype=None, stream=None) -> None:
+    """All steps of a ring ReduceCopy in one launch (xred_ring_reduce).
+
+    ready: None, or a tensor of len(chunks) uint32/int32 flags in pinned host
+    or device memory; status: None or a 1-element int32 tensor (pinned or
+    device) that receives 1 if a wait timed out."""
+    L = load()
+    check(L.xred_ring_reduce(ptr_array([c.data_ptr() for c in chunks]), len(chunks), _ptr(out),
+                             out.numel(), _dtype(out, dtype), OP[op], _ptr(ready),
+                             epoch & 0xFFFFFFFF, timeout_us, _ptr(status), _stream(out, stream)))
+
+
+def ring_max_count(dtype: str) -> int:
+    return int(load().xred_ring_max_count(DTYPE[dtype]))
 
 
 def acc_elem_size(dtype: str) -> int:

@@ -35,8 +35,9 @@ class XredItem(ctypes.Structure):
 
 
 EXPORTS = ("xred_allreduce_local", "xred_reduce_scatter_local", "xred_reduce_copy_step",
-           "xred_acc_cast", "xred_batched_reduce", "xred_acc_elem_size", "xred_status_string",
-           "xred_last_error", "xred_version", "xred_release")
+           "xred_acc_cast", "xred_batched_reduce", "xred_ring_reduce", "xred_ring_max_count",
+           "xred_acc_elem_size", "xred_status_string", "xred_last_error", "xred_version",
+           "xred_release")
 
 _lib = None
 
@@ -65,8 +66,12 @@ def load(path: Path = LIB_PATH) -> ctypes.CDLL:
     L.xred_reduce_copy_step.argtypes = [vp, vp, vp, sz, i32, i32, u32, vp]
     L.xred_acc_cast.argtypes = [vp, vp, sz, i32, vp]
     L.xred_batched_reduce.argtypes = [vp, i32, i32, i32, u32, vp]
+    L.xred_ring_reduce.argtypes = [vp, i32, vp, sz, i32, i32, vp, ctypes.c_uint32,
+                                   ctypes.c_uint64, vp, vp]
+    L.xred_ring_max_count.argtypes = [i32]
+    L.xred_ring_max_count.restype = sz
     for f in ("xred_allreduce_local", "xred_reduce_scatter_local", "xred_reduce_copy_step",
-              "xred_acc_cast", "xred_batched_reduce"):
+              "xred_acc_cast", "xred_batched_reduce", "xred_ring_reduce"):
         getattr(L, f).restype = ctypes.c_int
     L.xred_acc_elem_size.argtypes = [i32]
     L.xred_acc_elem_size.restype = sz

@@ -286,6 +286,16 @@ unsigned batched_rr_grid(int fit_per_cu)
     return grid_for((uint64_t)device_cus() * (uint64_t)(per_cu > 0 ? per_cu : fit_per_cu));
 }
 
+uint64_t wall_ticks_per_us()
+{
+    int dev = 0, khz = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, dev) != hipSuccess ||
+        khz <= 0)
+        return 100;   // 100 MHz, the usual s_memrealtime rate
+    return (uint64_t)khz / 1000 > 0 ? (uint64_t)khz / 1000 : 1;
+}
+
 bool supported(xred_dtype dtype, xred_op op)
 {
     return (dtype == XRED_FLOAT32 || dtype == XRED_BFLOAT16 || dtype == XRED_INT32 ||
@@ -432,6 +442,50 @@ XRED_API xred_status xred_batched_reduce(const xred_item *items, int nitems, xre
         return e == hipSuccess ? XRED_SUCCESS : hip_fail(e, "batched launch");
     }
     return batched_host(items, nitems, dtype, op, (hipStream_t)hip_stream);
+}
+
+XRED_API xred_status xred_ring_reduce(const void *const *chunks, int nchunks, void *dst,
+                                      size_t count, xred_dtype dtype, xred_op op,
+                                      const uint32_t *ready, uint32_t epoch, uint64_t timeout_us,
+                                      uint32_t *status, void *hip_stream)
+{
+    if (nchunks < 1 || nchunks > XRED_MAX_SRC)
+        return fail(XRED_INVALID_ARGUMENT, "nchunks = %d outside 1..%d", nchunks, XRED_MAX_SRC);
+    xred_status st = check_types(dtype, op);
+    if (st != XRED_SUCCESS) return st;
+    if (count == 0) return XRED_SUCCESS;
+    if (chunks == nullptr) return fail(XRED_INVALID_ARGUMENT, "chunks is NULL");
+    const size_t es = elem_size(dtype);
+    if (mul_overflows(count, es)) return fail(XRED_INVALID_ARGUMENT, "count * size overflows");
+    const size_t bytes = count * es;
+    if ((st = check_buf(dst, bytes, es, "dst", 0)) != XRED_SUCCESS) return st;
+    uintptr_t bits = (uintptr_t)dst;
+    for (int p = 0; p < nchunks; ++p) {
+        if ((st = check_buf(chunks[p], bytes, es, "chunks", p)) != XRED_SUCCESS) return st;
+        if (bad_overlap(dst, bytes, chunks[p], bytes, true))
+            return fail(XRED_ALIAS, "dst partially overlaps chunks[%d]", p);
+        bits |= (uintptr_t)chunks[p];
+    }
+    if (bits & 15u)
+        return fail(XRED_UNSUPPORTED, "xred_ring_reduce needs 16-byte aligned buffers");
+    if (ready != nullptr && ((uintptr_t)ready & 3u))
+        return fail(XRED_INVALID_ARGUMENT, "ready is not 4-byte aligned");
+    if (status != nullptr && ((uintptr_t)status & 3u))
+        return fail(XRED_INVALID_ARGUMENT, "status is not 4-byte aligned");
+    if (count > ring_max_count(dtype))
+        return fail(XRED_UNSUPPORTED, "count %zu exceeds the on-chip accumulator capacity %llu",
+                    count, (unsigned long long)ring_max_count(dtype));
+    if (timeout_us == 0) timeout_us = 1000000;
+    if (timeout_us > 60000000ull) timeout_us = 60000000ull;
+    const hipError_t e =
+        launch_ring(dtype, op, (const char *const *)chunks, nchunks, (char *)dst, count, ready,
+                    epoch, timeout_us * wall_ticks_per_us(), status, (hipStream_t)hip_stream);
+    return e == hipSuccess ? XRED_SUCCESS : hip_fail(e, "ring launch");
+}
+
+XRED_API size_t xred_ring_max_count(xred_dtype dtype)
+{
+    return known_dtype(dtype) && dtype != XRED_FLOAT16 ? (size_t)ring_max_count(dtype) : 0;
 }
 
 XRED_API size_t xred_acc_elem_size(xred_dtype dtype)

@@ -67,4 +67,13 @@ hipError_t launch_batched_rr(xred_dtype dtype, xred_op op, const xred_item *d_it
 // Workgroups for the round-robin kernel given how many fit on one CU.
 unsigned batched_rr_grid(int fit_per_cu);
 
+// All steps of a ring ReduceCopy in one persistent launch (xred_ring_reduce).
+uint64_t ring_max_count(xred_dtype dtype);
+hipError_t launch_ring(xred_dtype dtype, xred_op op, const char *const *chunks, int nchunks,
+                       char *dst, size_t count, const uint32_t *ready, uint32_t epoch,
+                       uint64_t timeout_ticks, uint32_t *status, hipStream_t stream);
+
+// Device wall-clock ticks per microsecond of the current device.
+uint64_t wall_ticks_per_us();
+
 }  // namespace xred
