@@ -326,6 +326,23 @@ def secondary(torch, xr, L, timer, wl, flush):
                  "separate_calls_GBs": round(ab / sep_ms / 1e6, 1)}
     del arena_d, outs, items_d, ptrs_d, singles
 
+    # CU budget: GB/s of the P=8 bf16 reduce on FTAR-sized 8 MiB chunks
+    # (4M elements per source) as the workgroup budget grows
+    n = 4 << 20
+    d = [torch.randn(n, device="cuda").to(torch.bfloat16) for _ in range(8)]
+    out = torch.empty_like(d[0])
+    fn = reduce_call(L, xr, d, out, "bf16", "sum")
+    curve = {}
+    for cap in (1, 2, 4, 8, 16, 32, 64, 128, 256, 512, 1024, 0):
+        prev = L.xred_set_max_workgroups(cap)
+        try:
+            ms = timer.loop_ms(fn, 20 if cap == 0 or cap >= 8 else 5, warm=1)
+        finally:
+            L.xred_set_max_workgroups(prev)
+        curve[str(cap) if cap else "all"] = round(9 * n * 2 / ms / 1e6, 1)
+    res["cu_budget_p8_bf16_8MiB_GBs"] = curve
+    del d, out
+
     # small-message latency: P=8 bf16, back-to-back and single call
     lat = {}
     for kib in (8, 64, 1024, 8192):

@@ -208,6 +208,16 @@ XRED_API xred_status xred_ring_reduce(const void *const *chunks, int nchunks, vo
 /* Largest count xred_ring_reduce accepts for dtype on the current device. */
 XRED_API size_t xred_ring_max_count(xred_dtype dtype);
 
+/*
+ * CU budget: at most max_workgroups workgroups per launch of the fused,
+ * reduce-scatter, step-wise, cast and batched kernels (0 = no limit, the
+ * default), so a reduction can run beside compute kernels on the rest of the
+ * chip -- the paper's FTAR kernel uses two thread blocks and stays hidden
+ * behind the network (Section 5).  Results do not depend on it.  Process-wide;
+ * returns the previous value.  xred_ring_reduce sizes its own persistent grid.
+ */
+XRED_API unsigned xred_set_max_workgroups(unsigned max_workgroups);
+
 /* Bytes per accumulator element for dtype: 4 (binary32 or uint32), 0 if unknown. */
 XRED_API size_t xred_acc_elem_size(xred_dtype dtype);
 

@@ -23,7 +23,7 @@ from ._lib import (ALIAS, DTYPE, EXPORTS, HIP_ERROR, INVALID_ARGUMENT, ITEM_DTYP
                    UNSUPPORTED, XredError, XredItem, check, load, ptr_array)
 
 __all__ = ["allreduce_local", "reduce_scatter_local", "reduce_copy_step", "acc_cast",
-           "batched_reduce", "ring_reduce", "ring_max_count", "pack_items", "acc_elem_size", "version", "release", "XredError",
+           "batched_reduce", "ring_reduce", "ring_max_count", "set_max_workgroups", "pack_items", "acc_elem_size", "version", "release", "XredError",
            "load", "EXPORTS"]
 
 
@@ -142,6 +142,11 @@ def ring_reduce(chunks, out, op: str = "sum", *, ready=None, epoch: int = 1,
 
 def ring_max_count(dtype: str) -> int:
     return int(load().xred_ring_max_count(DTYPE[dtype]))
+
+
+def set_max_workgroups(n: int) -> int:
+    """CU budget for later launches (0 = none); returns the previous value."""
+    return int(load().xred_set_max_workgroups(n))
 
 
 def acc_elem_size(dtype: str) -> int:

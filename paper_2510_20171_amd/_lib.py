@@ -36,8 +36,8 @@ class XredItem(ctypes.Structure):
 
 EXPORTS = ("xred_allreduce_local", "xred_reduce_scatter_local", "xred_reduce_copy_step",
            "xred_acc_cast", "xred_batched_reduce", "xred_ring_reduce", "xred_ring_max_count",
-           "xred_acc_elem_size", "xred_status_string", "xred_last_error", "xred_version",
-           "xred_release")
+           "xred_set_max_workgroups", "xred_acc_elem_size", "xred_status_string",
+           "xred_last_error", "xred_version", "xred_release")
 
 _lib = None
 
@@ -73,6 +73,8 @@ def load(path: Path = LIB_PATH) -> ctypes.CDLL:
     for f in ("xred_allreduce_local", "xred_reduce_scatter_local", "xred_reduce_copy_step",
               "xred_acc_cast", "xred_batched_reduce", "xred_ring_reduce"):
         getattr(L, f).restype = ctypes.c_int
+    L.xred_set_max_workgroups.argtypes = [ctypes.c_uint]
+    L.xred_set_max_workgroups.restype = ctypes.c_uint
     L.xred_acc_elem_size.argtypes = [i32]
     L.xred_acc_elem_size.restype = sz
     L.xred_status_string.argtypes = [i32]

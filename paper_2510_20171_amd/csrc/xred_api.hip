@@ -267,10 +267,15 @@ int device_cus()
     return c;
 }
 
+// Workgroup budget: 0 = none.  Set by xred_set_max_workgroups (or the
+// XRED_MAX_WORKGROUPS environment variable at load); read on every launch.
+std::atomic<unsigned> g_max_workgroups{(unsigned)env_long("XRED_MAX_WORKGROUPS", 0)};
+
 unsigned grid_for(uint64_t tiles)
 {
-    static const long cap = env_long("XRED_MAX_WORKGROUPS", 0x7FFFFFFF);
-    uint64_t g = tiles < (uint64_t)cap ? tiles : (uint64_t)cap;
+    const unsigned cap = g_max_workgroups.load(std::memory_order_relaxed);
+    uint64_t g = (cap != 0 && tiles > cap) ? cap : tiles;
+    if (g > 0x7FFFFFFFull) g = 0x7FFFFFFFull;
     return g == 0 ? 1u : (unsigned)g;
 }
 
@@ -486,6 +491,11 @@ XRED_API xred_status xred_ring_reduce(const void *const *chunks, int nchunks, vo
 XRED_API size_t xred_ring_max_count(xred_dtype dtype)
 {
     return known_dtype(dtype) && dtype != XRED_FLOAT16 ? (size_t)ring_max_count(dtype) : 0;
+}
+
+XRED_API unsigned xred_set_max_workgroups(unsigned max_workgroups)
+{
+    return g_max_workgroups.exchange(max_workgroups);
 }
 
 XRED_API size_t xred_acc_elem_size(xred_dtype dtype)
