@@ -86,6 +86,16 @@ class Timer:
         self.e1.synchronize()
         return self.e0.elapsed_time(self.e1) / reps
 
+    def single_ms(self, fn, reps: int) -> list:
+        out = []
+        for _ in range(reps):
+            self.e0.record()
+            fn()
+            self.e1.record()
+            self.e1.synchronize()
+            out.append(self.e0.elapsed_time(self.e1))
+        return out
+
     def cold_ms(self, fn, reps: int, flush) -> list:
         out = []
         for _ in range(reps):
@@ -173,9 +183,28 @@ def cpu_baseline(srcs_np, dtype, op, P, es, target_s=10.0):
         orc.allreduce_local(srcs_np, dtype, op, nthreads=cores)
     el = time.perf_counter() - t0
     gbs = (P + 1) * n * es * reps / el / 1e9
+    # the same oracle on one core, for about 3 s
+    t0 = time.perf_counter()
+    reps1 = 0
+    while time.perf_counter() - t0 < 3.0:
+        orc.allreduce_local(srcs_np, dtype, op, nthreads=1)
+        reps1 += 1
+    el1 = time.perf_counter() - t0
     return {"value": round(gbs, 3), "unit": "GB/s", "cores": cores, "kind": "oracle",
             "sample": f"first {n} elements of each of the P={P} sources, {reps} reps, "
-                      f"{el:.1f} s, OpenMP over elements"}
+                      f"{el:.1f} s, OpenMP over elements",
+            "one_core_value": round((P + 1) * n * es * reps1 / el1 / 1e9, 3),
+            "host_cores_available": oracle.host_cores(), "cpu_model": cpu_model()}
+
+
+def cpu_model() -> str:
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
 
 
 def secondary(torch, xr, L, timer, wl, flush):
@@ -345,12 +374,13 @@ def secondary(torch, xr, L, timer, wl, flush):
 
     # small-message latency: P=8 bf16, back-to-back and single call
     lat = {}
-    for kib in (8, 64, 1024, 8192):
+    # 16 MiB per source is one GPU's share of a c2 bucket reduce-scattered over 8 GPUs
+    for kib in (8, 64, 1024, 8192, 16384, 32768, 131072):
         n = kib * 1024 // 2
         d = [torch.randn(n, device="cuda").to(torch.bfloat16) for _ in range(8)]
         out = torch.empty_like(d[0])
         fn = reduce_call(L, xr, d, out, "bf16", "sum")
-        ms = timer.loop_ms(fn, 1000 if kib <= 1024 else 200)
+        ms = timer.loop_ms(fn, 1000 if kib <= 1024 else 200 if kib <= 16384 else 50)
         lat[f"{kib}KiB"] = {"us_per_call": round(ms * 1e3, 2),
                             "GBs": round(9 * n * 2 / ms / 1e6, 1)}
         del d, out
@@ -519,6 +549,18 @@ def main() -> int:
     wall = time.perf_counter() - t0
     ms = timer.e0.elapsed_time(timer.e1) / args.steps
     gbs = ab / (ms * 1e-3) / 1e9
+    # per-call spread (with the secondary figures only, so that profiled runs
+    # hold the timed loop's calls alone): each call between its own events,
+    # back to back and after evicting L2 and the MALL
+    per_call = None
+    if not args.no_secondary:
+        flush = torch.empty(1 << 28, dtype=torch.float32, device="cuda")
+        single = sorted(timer.single_ms(step, max(10, args.steps)))
+        cold = sorted(timer.cold_ms(step, max(10, min(args.steps, 30)), flush))
+        pct = lambda xs, q: round(xs[min(len(xs) - 1, int(q * len(xs)))] * 1e3, 2)
+        per_call = {"p10_us": pct(single, 0.1), "p50_us": pct(single, 0.5),
+                    "p90_us": pct(single, 0.9), "cold_p50_us": pct(cold, 0.5),
+                    "cold_p90_us": pct(cold, 0.9)}
 
     config = dict(wk["config"], accumulate="f32" if wk["config"].get("io_dtype") in ("bf16", "f32")
                   else "u32", alg_bytes_per_step=ab, parallelism="single GPU")
@@ -529,6 +571,7 @@ def main() -> int:
         "dtype": config["accumulate"], "data": "synthetic", "config": config,
         "pct_hbm_peak": round(100 * gbs / HBM_PEAK_GBS, 2),
         "wall_s_timed": round(wall, 4),
+        "per_call": per_call,
         "roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": round(gbs / HBM_PEAK_GBS, 4),
                      "traffic": committed_traffic(wk["profile"], wk["family"]),

@@ -70,11 +70,15 @@ class Oracle:
         L.xo_reduce_copy_step.argtypes = [vp, vp, vp, u64, i32, i32, ctypes.c_uint]
         L.xo_acc_cast.argtypes = [vp, vp, u64, i32]
         L.xo_batched_reduce.argtypes = [i32, vp, vp, vp, vp, vp, i32, i32, i32]
+        L.xo_sim_chunk.argtypes = [u64, i32]
+        L.xo_sim_chunk.restype = u64
+        L.xo_ring_allreduce_sim.argtypes = [vp, vp, i32, u64, i32, i32, i32]
+        L.xo_rhd_allreduce_sim.argtypes = [vp, vp, i32, u64, i32, i32, i32]
         L.xo_f32_bits_to_bf16.argtypes = [vp, vp, u64]
         L.xo_bf16_to_f32_bits.argtypes = [vp, vp, u64]
         for fn in ("xo_allreduce_local", "xo_reduce_scatter_local", "xo_reduce_copy_step",
-                   "xo_acc_cast", "xo_batched_reduce", "xo_selfcheck", "xo_max_threads",
-                   "xo_version"):
+                   "xo_acc_cast", "xo_batched_reduce", "xo_ring_allreduce_sim",
+                   "xo_rhd_allreduce_sim", "xo_selfcheck", "xo_max_threads", "xo_version"):
             getattr(L, fn).restype = ctypes.c_int
         self._L = L
 
@@ -179,6 +183,27 @@ class Oracle:
             raise OracleError(f"xo_batched_reduce rc={rc}")
         return outs
 
+    def sim_chunk(self, count: int, nranks: int) -> int:
+        """Chunk length of the simulated schedules (ceil(count/G) rounded up to 64)."""
+        return int(self._L.xo_sim_chunk(count, nranks))
+
+    def allreduce_sim(self, sends, dtype: str, op: str, algo: str = "ring", nthreads: int = 1):
+        """A whole AllReduce over len(sends) simulated ranks, message by message
+        (``algo`` "ring" or "rhd"); returns every rank's output buffer."""
+        sends = list(sends)
+        self._check_arrays(sends, dtype)
+        n = sends[0].size
+        if any(s.size != n for s in sends):
+            raise OracleError("send buffers differ in length")
+        outs = [np.empty(n, DTYPES[dtype][1]) for _ in sends]
+        fn = {"ring": self._L.xo_ring_allreduce_sim, "rhd": self._L.xo_rhd_allreduce_sim}[algo]
+        rc = fn(ctypes.cast(self._ptr_table(sends), ctypes.c_void_p),
+                ctypes.cast(self._ptr_table(outs), ctypes.c_void_p), len(sends), n,
+                DTYPES[dtype][0], OPS[op], nthreads)
+        if rc != 0:
+            raise OracleError(f"{algo} allreduce simulation rc={rc}")
+        return outs
+
     def f32_bits_to_bf16(self, bits: np.ndarray) -> np.ndarray:
         bits = np.ascontiguousarray(bits, np.uint32)
         out = np.empty(bits.size, np.uint16)
@@ -199,7 +224,7 @@ def load() -> Oracle:
     """Load the built oracle, building it with gcc only if nothing is built."""
     global _default
     if _default is None:
-        if not LIB.exists():
+        if not LIB.exists() or LIB.stat().st_mtime < SRC.stat().st_mtime:
             build()
         _default = Oracle(LIB)
         if _default.selfcheck() != 0:

@@ -39,11 +39,18 @@
  * Step-wise ring mode (the ReduceCopy of the FTAR pipeline, Section 5 FTAR):
  * acc <- up(in) on INIT, acc <- acc (+) up(in) otherwise, and on FINAL the
  * result is written as down(...) to dst instead of to acc.
+ *
+ * Simulated schedules: a whole ring (or recursive halving-doubling)
+ * AllReduce over G ranks held in this process, message by message, each hop
+ * being the definition with two sources (received, own) and every message
+ * kept in the I/O dtype, so the fold order of an element is the order in
+ * which the schedule's messages reach it.
  */
 #include <math.h>
 #include <stdint.h>
 #include <string.h>
 #include <stddef.h>
+#include <stdlib.h>
 #ifdef _OPENMP
 #include <omp.h>
 #endif
@@ -295,6 +302,193 @@ int xo_batched_reduce(int nitems, const void *const *item_srcs, const uint64_t *
     return XO_OK;
 }
 
+/* ------------------------------------- simulated multi-rank schedules --- */
+/*
+ * A whole AllReduce over G ranks whose buffers all live in this process,
+ * following a schedule step by step, with every message held in a wire
+ * buffer of the I/O dtype.  Each hop's reduction is the definition above
+ * with two sources, received message first:  down(up(received) (+) up(own)),
+ * so a partial is rounded to the I/O dtype every time it travels.
+ *
+ * Chunks: M = ceil(count / G) rounded up to a multiple of 64 elements; chunk
+ * c is [c*M, min(count, (c+1)*M)), so trailing chunks may be short or empty.
+ */
+#define XO_SIM_ALIGN 64u
+
+uint64_t xo_sim_chunk(uint64_t count, int G)
+{
+    if (G < 1) return 0;
+    uint64_t m = (count + (uint64_t)G - 1) / (uint64_t)G;
+    return (m + XO_SIM_ALIGN - 1) / XO_SIM_ALIGN * XO_SIM_ALIGN;
+}
+
+static uint64_t clampu(uint64_t v, uint64_t hi) { return v < hi ? v : hi; }
+static int mod_rank(int r, int G) { return ((r % G) + G) % G; }
+static char *elem_at(const void *base, uint64_t i, int dtype)
+{
+    return (char *)base + i * elem_size(dtype);
+}
+
+/* dst[0..n) = down(up(received[0..n)) (+) up(own[0..n))) */
+static void hop_reduce(const void *received, const void *own, void *dst, uint64_t n, int dtype,
+                       int op, int nthreads)
+{
+    const void *two[2] = {received, own};
+    reduce_range(two, 2, 0, dst, n, dtype, op, nthreads);
+}
+
+static void **alloc_bufs(int G, uint64_t bytes)
+{
+    void **b = (void **)calloc((size_t)G, sizeof(void *));
+    if (!b) return NULL;
+    for (int r = 0; r < G; ++r) {
+        b[r] = malloc(bytes ? bytes : 1);
+        if (!b[r]) {
+            for (int q = 0; q < r; ++q) free(b[q]);
+            free(b);
+            return NULL;
+        }
+    }
+    return b;
+}
+
+static void free_bufs(void **b, int G)
+{
+    if (!b) return;
+    for (int r = 0; r < G; ++r) free(b[r]);
+    free(b);
+}
+
+/*
+ * Ring AllReduce (the ring of the FTAR pipeline, Section 5): rank r sends to
+ * rank r+1 and receives from rank r-1.
+ *   ReduceScatter phase, G-1 steps after the first send:
+ *     sendCopy  rank r puts its own chunk r-1 on the wire;
+ *     step s    rank r receives chunk r-1-s;
+ *               RedCopy (s < G-1): forwards down(up(received) (+) up(own));
+ *               Reduce  (s = G-1): the chunk is r, the result goes to recv[r].
+ *   AllGather phase: rank r sends its reduced chunk r; at step t it receives
+ *     chunk r-t and writes it to recv[r]; RecvCopy (t < G-1) also forwards it,
+ *     Recv (t = G-1) does not.
+ * So chunk c is folded in arrival order c+1, c+2, ..., c+G-1, c (mod G), and
+ * every rank ends with the same bits.  With G = 1 recv[0] is a copy of
+ * send[0].  recv[r] may equal send[r] (in place): inputs are copied first.
+ */
+int xo_ring_allreduce_sim(const void *const *send, void *const *recv, int G, uint64_t count,
+                          int dtype, int op, int nthreads)
+{
+    if (G < 1 || !valid_dtype(dtype) || !valid_op(op)) return XO_BAD;
+    if (count == 0) return XO_OK;
+    const size_t es = elem_size(dtype);
+    const uint64_t M = xo_sim_chunk(count, G);
+    void **own = alloc_bufs(G, count * es);
+    void **wire = alloc_bufs(G, M * es);
+    void **next = alloc_bufs(G, M * es);
+    if (!own || !wire || !next) {
+        free_bufs(own, G); free_bufs(wire, G); free_bufs(next, G);
+        return XO_BAD;
+    }
+    for (int r = 0; r < G; ++r) memcpy(own[r], send[r], count * es);
+    if (G == 1) {
+        memcpy(recv[0], own[0], count * es);
+    } else {
+#define LO(c) clampu((uint64_t)(c) * M, count)
+#define LEN(c) (LO((c) + 1) - LO(c))
+        /* ReduceScatter */
+        for (int r = 0; r < G; ++r) {                      /* sendCopy */
+            const int c = mod_rank(r - 1, G);
+            memcpy(wire[r], elem_at(own[r], LO(c), dtype), LEN(c) * es);
+        }
+        for (int s = 1; s <= G - 1; ++s) {
+            for (int r = 0; r < G; ++r) {
+                const int c = mod_rank(r - 1 - s, G);
+                const void *in = wire[mod_rank(r - 1, G)];
+                if (s < G - 1)                              /* RedCopy */
+                    hop_reduce(in, elem_at(own[r], LO(c), dtype), next[r], LEN(c), dtype, op,
+                               nthreads);
+                else                                        /* Reduce */
+                    hop_reduce(in, elem_at(own[r], LO(c), dtype), elem_at(recv[r], LO(c), dtype),
+                               LEN(c), dtype, op, nthreads);
+            }
+            void **t = wire; wire = next; next = t;
+        }
+        /* AllGather */
+        for (int r = 0; r < G; ++r)
+            memcpy(wire[r], elem_at(recv[r], LO(r), dtype), LEN(r) * es);
+        for (int t = 1; t <= G - 1; ++t) {
+            for (int r = 0; r < G; ++r) {
+                const int c = mod_rank(r - t, G);
+                const void *in = wire[mod_rank(r - 1, G)];
+                memcpy(elem_at(recv[r], LO(c), dtype), in, LEN(c) * es);   /* Recv */
+                if (t < G - 1) memcpy(next[r], in, LEN(c) * es);           /* ...Copy */
+            }
+            void **tt = wire; wire = next; next = tt;
+        }
+#undef LEN
+#undef LO
+    }
+    free_bufs(own, G); free_bufs(wire, G); free_bufs(next, G);
+    return XO_OK;
+}
+
+/*
+ * Recursive halving-doubling AllReduce (the RHD ReduceScatter the paper
+ * lists beside the ring, Section 2.2), G a power of two.  ReduceScatter by
+ * recursive halving: with distance d = G/2, G/4, ..., 1, rank r and its
+ * partner r^d split their common region of blocks in two; the rank whose bit
+ * d is clear keeps the lower half, the other the upper half; each sends the
+ * half it gives up and reduces the received message into the half it keeps,
+ * down(up(received) (+) up(own)).  Afterwards rank r holds block r.
+ * AllGather by recursive doubling: with d = 1, 2, ..., G/2 each rank sends
+ * its region to r^d, which stores it.  Blocks are the chunks defined above.
+ */
+int xo_rhd_allreduce_sim(const void *const *send, void *const *recv, int G, uint64_t count,
+                         int dtype, int op, int nthreads)
+{
+    if (G < 1 || (G & (G - 1)) != 0 || !valid_dtype(dtype) || !valid_op(op)) return XO_BAD;
+    if (count == 0) return XO_OK;
+    const size_t es = elem_size(dtype);
+    const uint64_t M = xo_sim_chunk(count, G);
+    void **work = alloc_bufs(G, count * es);
+    void **msg = alloc_bufs(G, count * es);
+    int *lo = (int *)calloc((size_t)G, sizeof(int));
+    if (!work || !msg || !lo) {
+        free_bufs(work, G); free_bufs(msg, G); free(lo);
+        return XO_BAD;
+    }
+#define EL(b) clampu((uint64_t)(b) * M, count)
+    for (int r = 0; r < G; ++r) memcpy(work[r], send[r], count * es);
+    int nblk = G;
+    for (int d = G / 2; d >= 1; d /= 2) {
+        const int half = nblk / 2;
+        for (int r = 0; r < G; ++r) {                       /* send the half given up */
+            const int give = (r & d) ? lo[r] : lo[r] + half;
+            memcpy(msg[r], elem_at(work[r], EL(give), dtype), (EL(give + half) - EL(give)) * es);
+        }
+        for (int r = 0; r < G; ++r) {                       /* reduce into the half kept */
+            const int keep = (r & d) ? lo[r] + half : lo[r];
+            void *mine = elem_at(work[r], EL(keep), dtype);
+            hop_reduce(msg[r ^ d], mine, mine, EL(keep + half) - EL(keep), dtype, op, nthreads);
+            lo[r] = keep;
+        }
+        nblk = half;
+    }
+    for (int d = 1; d < G; d *= 2) {
+        for (int r = 0; r < G; ++r)
+            memcpy(msg[r], elem_at(work[r], EL(lo[r]), dtype), (EL(lo[r] + nblk) - EL(lo[r])) * es);
+        for (int r = 0; r < G; ++r) {
+            const int p = r ^ d;
+            memcpy(elem_at(work[r], EL(lo[p]), dtype), msg[p], (EL(lo[p] + nblk) - EL(lo[p])) * es);
+        }
+        for (int r = 0; r < G; ++r) lo[r] = lo[r] < lo[r ^ d] ? lo[r] : lo[r ^ d];
+        nblk *= 2;
+    }
+#undef EL
+    for (int r = 0; r < G; ++r) memcpy(recv[r], work[r], count * es);
+    free_bufs(work, G); free_bufs(msg, G); free(lo);
+    return XO_OK;
+}
+
 /* Bulk conversions, exposed so tests can check down()/up() on their own. */
 void xo_f32_bits_to_bf16(const uint32_t *in, uint16_t *out, uint64_t n)
 {
@@ -331,4 +525,4 @@ int xo_max_threads(void)
 #endif
 }
 
-int xo_version(void) { return 1; }
+int xo_version(void) { return 2; }

@@ -325,10 +325,112 @@ def pin_composition(orc, seed: int = 17) -> None:
         assert np.array_equal(out[~nan], exp[~nan])
 
 
+# ------------------------------------------------ simulated schedules --
+
+def sim_chunk_len(count: int, nranks: int) -> int:
+    """The schedules' chunk length: ceil(count / G) rounded up to 64 elements."""
+    m = -(-count // nranks)
+    return -(-m // 64) * 64
+
+
+def brute_ring_element(col, c: int, dtype: str, op: str) -> int:
+    """One element of chunk c after a ring AllReduce over len(col) ranks: the
+    partial starts as rank c+1's value and travels c+2, ..., c+G-1, c, each hop
+    being a two-source reduce (received, own) rounded to the I/O dtype."""
+    G = len(col)
+    if G == 1:
+        return col[0]
+    v = col[(c + 1) % G]
+    for j in range(2, G + 1):
+        v = brute.reduce_column([v, col[(c + j) % G]], dtype, op)
+    return v
+
+
+def brute_rhd_element(col, b: int, dtype: str, op: str) -> int:
+    """One element of block b after recursive halving: at distance d every
+    rank combines its partner's value (received) with its own; block b ends at
+    rank b."""
+    G = len(col)
+    w = list(col)
+    d = G // 2
+    while d >= 1:
+        w = [brute.reduce_column([w[r ^ d], w[r]], dtype, op) for r in range(G)]
+        d //= 2
+    return w[b]
+
+
+def pin_sim_bruteforce(orc, seed: int = 23, per_case: int = 12) -> None:
+    """Every rank's output of the simulated ring / halving-doubling AllReduce
+    equals the exact rational chain of hops, element by element, on ragged
+    sizes whose trailing chunks are short or empty; all ranks hold the same bits."""
+    rng = np.random.default_rng(seed)
+    for algo, sizes, brute_el in (("ring", (1, 2, 3, 5, 8), brute_ring_element),
+                                  ("rhd", (1, 2, 4, 8), brute_rhd_element)):
+        for dtype in DTYPES:
+            for op in OPS:
+                for G in sizes:
+                    n = 64 * G + 70 if G > 1 else 37
+                    sends = [random_column_values(rng, dtype, n) for _ in range(G)]
+                    outs = [_bits(o) for o in orc.allreduce_sim(sends, dtype, op, algo)]
+                    for r in range(1, G):
+                        assert np.array_equal(outs[r], outs[0]), f"{algo} G={G}: ranks differ"
+                    M = sim_chunk_len(n, G)
+                    idx = {0, n - 1} | {min(n - 1, k * M + e) for k in range(1, G) for e in (-1, 0)}
+                    idx |= set(rng.integers(0, n, per_case).tolist())
+                    sb = [_bits(s) for s in sends]
+                    for i in sorted(idx):
+                        col = [int(x[i]) for x in sb]
+                        exp = brute_el(col, i // M, dtype, op)
+                        assert _same(int(outs[0][i]), exp, dtype, op), (
+                            f"{algo} {dtype} {op} G={G} i={i} got={int(outs[0][i]):#x} exp={exp:#x}")
+
+
+def pin_sim_closed_forms(orc, n: int = 5003, seed: int = 29) -> None:
+    """Closed forms and invariants of the simulated schedules: integer-valued
+    inputs whose every partial is exact give the int64 sum at every rank
+    (bf16 too, as |partials| <= 128 are exact there); int32 sums wrap to the
+    numpy int64 sum mod 2^32; max/min equal the order-free fused reduce; one
+    rank copies its buffer bit for bit; with two ranks the ring and the
+    halving-doubling schedules perform the same single hop per element."""
+    import torch
+    rng = np.random.default_rng(seed)
+    for algo, G in (("ring", 8), ("ring", 7), ("rhd", 8)):
+        ints = [rng.integers(-16, 17, size=n) for _ in range(G)]
+        exact = np.sum(np.stack(ints), axis=0)
+        f32 = orc.allreduce_sim([x.astype(np.float32) for x in ints], "f32", "sum", algo)
+        bf = orc.allreduce_sim([torch.from_numpy(x.astype(np.float32)).to(torch.bfloat16)
+                                .view(torch.int16).numpy().view(np.uint16) for x in ints],
+                               "bf16", "sum", algo)
+        exp16 = torch.from_numpy(exact.astype(np.float32)).to(torch.bfloat16).view(torch.int16)
+        for r in range(G):
+            assert np.array_equal(f32[r], exact.astype(np.float32)), f"{algo} f32 closed form"
+            assert np.array_equal(bf[r], exp16.numpy().view(np.uint16)), f"{algo} bf16 closed form"
+        wide = [rng.integers(-2**31, 2**31, size=n).astype(np.int32) for _ in range(G)]
+        wsum = (np.sum(np.stack(wide).astype(np.int64), axis=0) & 0xFFFFFFFF).astype(np.uint32)
+        for o in orc.allreduce_sim(wide, "i32", "sum", algo):
+            assert np.array_equal(o.view(np.uint32), wsum), f"{algo} int32 wrap"
+        for op in ("max", "min"):
+            vals = [random_column_values(rng, "f32", n) for _ in range(G)]
+            fused = _bits(orc.allreduce_local(vals, "f32", op))
+            for o in orc.allreduce_sim(vals, "f32", op, algo):
+                assert np.array_equal(_bits(o), fused), f"{algo} {op} order-free"
+    one = random_column_values(rng, "bf16", 1000)
+    one[:4] = [0x7F81, 0xFF81, 0x8000, 0x0001]           # NaN payloads and -0 survive a copy
+    for algo in ("ring", "rhd"):
+        assert np.array_equal(orc.allreduce_sim([one], "bf16", "sum", algo)[0], one)
+    two = [random_column_values(rng, "bf16", 777) for _ in range(2)]
+    a = orc.allreduce_sim(two, "bf16", "sum", "ring")
+    b = orc.allreduce_sim(two, "bf16", "sum", "rhd")
+    for x, y in zip(a, b):
+        nan = np.array([_is_nan_bits(int(v), "bf16") for v in x], bool)
+        assert np.array_equal(x[~nan], y[~nan]) and np.all(
+            [_is_nan_bits(int(v), "bf16") for v in y[nan]]), "G=2 ring vs rhd"
+
+
 def pin_selfcheck(orc) -> None:
     assert orc.selfcheck() == 0, "floating-point environment"
 
 
 FAST_PINS = [pin_selfcheck, pin_golden_reduce, pin_golden_bf16, pin_bf16_vs_brute,
              pin_up_bf16, pin_integer_closed_form, pin_int_mod32, pin_invariants,
-             pin_composition, pin_bruteforce]
+             pin_composition, pin_bruteforce, pin_sim_closed_forms, pin_sim_bruteforce]

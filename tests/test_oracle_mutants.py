@@ -56,6 +56,22 @@ MUTANTS = [
      "for (int p = 1; p < nsrc; ++p)\n            acc = op_float(op, acc, up_float(srcs[p], off + i, dtype));",
      "for (int p = nsrc - 2; p >= 0; --p)\n            acc = op_float(op, acc, up_float(srcs[p], off + i, dtype));",
      1, ()),
+    # simulated schedules
+    ("ring_sendcopy_own_chunk", "const int c = mod_rank(r - 1, G);\n            memcpy(wire[r]",
+     "const int c = mod_rank(r, G);\n            memcpy(wire[r]", 1, ()),
+    ("ring_reduce_drops_own",
+     "hop_reduce(in, elem_at(own[r], LO(c), dtype), elem_at(recv[r], LO(c), dtype),",
+     "hop_reduce(in, in, elem_at(recv[r], LO(c), dtype),", 1, ()),
+    ("ring_allgather_wrong_slot", "const int c = mod_rank(r - t, G);",
+     "const int c = mod_rank(r - t + 1, G);", 1, ()),
+    ("ring_recvcopy_does_not_forward", "if (t < G - 1) memcpy(next[r], in, LEN(c) * es);",
+     "if (t < G - 1) memcpy(next[r], elem_at(recv[r], LO(r), dtype), LEN(c) * es);", 1, ()),
+    ("rhd_keeps_given_half", "const int keep = (r & d) ? lo[r] + half : lo[r];",
+     "const int keep = (r & d) ? lo[r] : lo[r] + half;", 1, ()),
+    ("rhd_reduces_own_message", "hop_reduce(msg[r ^ d], mine, mine,", "hop_reduce(msg[r], mine, mine,",
+     1, ()),
+    ("sim_chunks_unaligned", "return (m + XO_SIM_ALIGN - 1) / XO_SIM_ALIGN * XO_SIM_ALIGN;",
+     "return m;", 1, ()),
     # a fast-math build flushes subnormals (and loads code that sets FTZ/DAZ for
     # the whole process, which is why every mutant runs in a child process)
     ("fast_math_build", None, None, 0, ("-ffast-math",)),
