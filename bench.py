@@ -40,6 +40,7 @@ KERNEL_SOURCES = {
     "step": [CSRC + "xred_device.hpp", CSRC + "xred_kernels.hpp", CSRC + "xred_step.hip"],
     "batched": [CSRC + "xred_device.hpp", CSRC + "xred_kernels.hpp", CSRC + "xred_batched.hip"],
     "ring": [CSRC + "xred_device.hpp", CSRC + "xred_kernels.hpp", CSRC + "xred_ring.hip"],
+    "sim": [CSRC + "xred_device.hpp", CSRC + "xred_kernels.hpp", CSRC + "xred_sim.hip"],
 }
 
 
@@ -372,6 +373,24 @@ def secondary(torch, xr, L, timer, wl, flush):
     res["cu_budget_p8_bf16_8MiB_GBs"] = curve
     del d, out
 
+    # simulated AllReduce schedules on one GPU: 8 ranks, ring and halving-doubling,
+    # at the bucket size and at 1 MiB per rank
+    sim = {}
+    for label, n in (("64M", 64 << 20), ("512K", 512 << 10)):
+        sends = [torch.randn(n, device="cuda").to(torch.bfloat16) for _ in range(8)]
+        recvs = [torch.empty_like(x) for x in sends]
+        arr_s = xr._lib.ptr_array([x.data_ptr() for x in sends])
+        arr_r = xr._lib.ptr_array([x.data_ptr() for x in recvs])
+        stream = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+        for sched in ("ring", "rhd"):
+            fn = (lambda sc=xr.SCHEDULE[sched]:
+                  L.xred_allreduce_sim(arr_s, arr_r, 8, n, 1, 0, sc, stream))
+            ms = timer.loop_ms(fn, 20 if n > (1 << 20) else 200)
+            sim[f"{sched}_{label}"] = {"us": round(ms * 1e3, 2),
+                                       "GBs": round(5 * 7 * n * 2 / ms / 1e6, 1)}
+        del sends, recvs
+    res["sim_g8_bf16"] = sim
+
     # small-message latency: P=8 bf16, back-to-back and single call
     lat = {}
     # 16 MiB per source is one GPU's share of a c2 bucket reduce-scattered over 8 GPUs
@@ -436,6 +455,46 @@ def build_workload(name, torch, xr, L, wl):
         sample_n = min(w.count, (1 << 25) // w.nsrc)
         res["cpu"] = lambda: cpu_baseline([s[:sample_n] for s in srcs_np], w.dtype, w.op,
                                           w.nsrc, es)
+        return res
+    if w.kind == "sim":
+        G, N = w.nsrc, w.count
+        log(f"generating {name} inputs ({G} ranks x {N} {w.dtype})")
+        sends_np = wl.sources(w)
+        sends = [dev_bf16(torch, s) for s in sends_np]
+        recvs = [torch.empty_like(s) for s in sends]
+        arr_s = xr._lib.ptr_array([s.data_ptr() for s in sends])
+        arr_r = xr._lib.ptr_array([r.data_ptr() for r in recvs])
+
+        def step():
+            st = L.xred_allreduce_sim(arr_s, arr_r, G, N, 1, 0, xr.SCHEDULE["ring"], stream)
+            if st:
+                xr._lib.check(st)
+        step._keep_inputs = (sends, recvs, arr_s, arr_r)
+        res = dict(step=step, alg_bytes=w.alg_bytes(), family="sim",
+                   kernel="whole ring schedule: 7 x sim_step_vec_kernel<bf16, sum, reduce> + "
+                          "7 x sim_step_vec_kernel<bf16, sum, copy>",
+                   profile=ROOT / "profiles" / f"sim_bf16_{name}.md",
+                   config={"workload": f"{name}: ring AllReduce of {G} simulated ranks x {N} bf16 "
+                                       "on one GPU (2(G-1) steps, zero-copy messages)",
+                           "ranks": G, "N": N, "io_dtype": "bf16", "schedule": "ring"})
+        sample = [s[:1 << 22] for s in sends_np]
+
+        def cpu():
+            import oracle
+            orc = oracle.load()
+            cores = min(16, oracle.host_cores())
+            t0 = time.perf_counter()
+            reps = 0
+            while time.perf_counter() - t0 < 10.0:
+                orc.allreduce_sim(sample, "bf16", "sum", "ring", nthreads=cores)
+                reps += 1
+            el = time.perf_counter() - t0
+            ab = 5 * (G - 1) * sample[0].size * 2 * reps
+            return {"value": round(ab / el / 1e9, 3), "unit": "GB/s", "cores": cores,
+                    "kind": "oracle",
+                    "sample": f"first {sample[0].size} elements of each rank, {reps} reps, "
+                              f"{el:.1f} s, OpenMP over elements within each hop"}
+        res["cpu"] = cpu
         return res
     if w.kind == "stepwise":
         log(f"generating {name} inputs (16 chunks x {w.count} bf16)")
@@ -510,7 +569,8 @@ def main() -> int:
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--workload", default="c2", choices=["c1", "c2", "c3", "c3ring", "c4", "c5a", "c5b"],
+    ap.add_argument("--workload", default="c2",
+                    choices=["c1", "c2", "c3", "c3ring", "c4", "c5a", "c5b", "sim"],
                     help="which workload one step runs (default: the c2 gradient bucket)")
     ap.add_argument("--no-secondary", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")

@@ -208,6 +208,51 @@ XRED_API xred_status xred_ring_reduce(const void *const *chunks, int nchunks, vo
 /* Largest count xred_ring_reduce accepts for dtype on the current device. */
 XRED_API size_t xred_ring_max_count(xred_dtype dtype);
 
+/* Schedules of xred_allreduce_sim. */
+typedef enum {
+    XRED_SCHEDULE_RING = 0,  /* ring: 2(G-1) steps */
+    XRED_SCHEDULE_RHD = 1    /* recursive halving-doubling, G a power of two: 2 log2(G) steps */
+} xred_schedule;
+
+/*
+ * A whole AllReduce over nranks = G simulated ranks whose buffers all live on
+ * this GPU, step by step: the ring of the FTAR pipeline (Section 5:
+ * sendCopy, RedCopy, Reduce, RecvCopy, Recv) or the recursive
+ * halving-doubling schedule (Section 2.2).  Each step is one launch holding
+ * every rank's work of that step.
+ *
+ * Every hop is the two-source reduce down(up(received) (+) up(own)), so a
+ * partial is rounded to the I/O dtype each time it travels.  In the ring,
+ * chunk c is folded in arrival order c+1, c+2, ..., c+G-1, c (mod G); in
+ * halving-doubling, at distance d = G/2, ..., 1 every rank combines its
+ * partner's partial with its own.  Messages are zero-copy: the partial a
+ * rank forwards is stored once, in that rank's own recvbuf at the chunk's
+ * place, and the next rank reads it there; a reduced chunk is forwarded from
+ * where it was written.  No staging buffer and no extra store per hop.
+ *
+ *   sendbufs, recvbufs  host arrays of G device pointers to count elements
+ *              each, consumed before return.  recvbufs[r] may equal
+ *              sendbufs[r] (in place); a recvbuf must not overlap any other
+ *              buffer.  Sends may overlap each other.
+ *   G          1..XRED_MAX_SRC; a power of two for XRED_SCHEDULE_RHD.  With
+ *              one rank recvbufs[0] becomes a bitwise copy of sendbufs[0].
+ *   chunks     xred_sim_chunk(count, G) elements each, i.e. ceil(count / G)
+ *              rounded up to a multiple of 64; trailing chunks are short or
+ *              empty.  (RHD blocks are the same chunks.)
+ * When the stream reaches the end of the call every recvbufs[r] holds the
+ * same bits.  Buffers that are all 16-byte aligned take the vector path,
+ * others (element-aligned) a scalar path with the same results.
+ * Errors: XRED_INVALID_ARGUMENT (G out of range, unknown schedule, RHD with G
+ * not a power of two, NULL or misaligned pointer, size overflow),
+ * XRED_UNSUPPORTED, XRED_ALIAS, XRED_HIP_ERROR.
+ */
+XRED_API xred_status xred_allreduce_sim(const void *const *sendbufs, void *const *recvbufs,
+                                        int nranks, size_t count, xred_dtype dtype, xred_op op,
+                                        xred_schedule schedule, void *hip_stream);
+
+/* Chunk length of xred_allreduce_sim's schedules (0 when nranks < 1). */
+XRED_API size_t xred_sim_chunk(size_t count, int nranks);
+
 /*
  * CU budget: at most max_workgroups workgroups per launch of the fused,
  * reduce-scatter, step-wise, cast and batched kernels (0 = no limit, the

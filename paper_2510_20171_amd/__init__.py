@@ -19,12 +19,13 @@ from __future__ import annotations
 import ctypes
 
 from ._lib import (ALIAS, DTYPE, EXPORTS, HIP_ERROR, INVALID_ARGUMENT, ITEM_DTYPE,
-                   ITEMS_ON_DEVICE, MAX_SRC, OP, OUT_OF_MEMORY, STEP_FINAL, STEP_INIT, SUCCESS,
-                   UNSUPPORTED, XredError, XredItem, check, load, ptr_array)
+                   ITEMS_ON_DEVICE, MAX_SRC, OP, OUT_OF_MEMORY, SCHEDULE, STEP_FINAL, STEP_INIT,
+                   SUCCESS, UNSUPPORTED, XredError, XredItem, check, load, ptr_array)
 
 __all__ = ["allreduce_local", "reduce_scatter_local", "reduce_copy_step", "acc_cast",
-           "batched_reduce", "ring_reduce", "ring_max_count", "set_max_workgroups", "pack_items", "acc_elem_size", "version", "release", "XredError",
-           "load", "EXPORTS"]
+           "batched_reduce", "ring_reduce", "ring_max_count", "allreduce_sim", "sim_chunk",
+           "set_max_workgroups", "pack_items", "acc_elem_size", "version", "release",
+           "XredError", "load", "EXPORTS"]
 
 
 def _torch_dtype_name(t) -> str:
@@ -138,6 +139,25 @@ def ring_reduce(chunks, out, op: str = "sum", *, ready=None, epoch: int = 1,
     check(L.xred_ring_reduce(ptr_array([c.data_ptr() for c in chunks]), len(chunks), _ptr(out),
                              out.numel(), _dtype(out, dtype), OP[op], _ptr(ready),
                              epoch & 0xFFFFFFFF, timeout_us, _ptr(status), _stream(out, stream)))
+
+
+def allreduce_sim(sends, recvs, op: str = "sum", *, schedule: str = "ring", dtype=None,
+                  stream=None) -> None:
+    """A whole AllReduce over len(sends) simulated ranks on this GPU
+    (xred_allreduce_sim): recvs[r] receives the reduced buffer at every rank.
+    schedule: "ring" or "rhd" (recursive halving-doubling)."""
+    L = load()
+    if len(sends) != len(recvs):
+        raise XredError(INVALID_ARGUMENT, "one recv buffer per send buffer")
+    out = recvs[0]
+    check(L.xred_allreduce_sim(ptr_array([s.data_ptr() for s in sends]),
+                               ptr_array([r.data_ptr() for r in recvs]), len(sends), out.numel(),
+                               _dtype(out, dtype), OP[op], SCHEDULE[schedule],
+                               _stream(out, stream)))
+
+
+def sim_chunk(count: int, nranks: int) -> int:
+    return int(load().xred_sim_chunk(count, nranks))
 
 
 def ring_max_count(dtype: str) -> int:

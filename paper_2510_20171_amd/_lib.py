@@ -22,6 +22,7 @@ SUCCESS, INVALID_ARGUMENT, UNSUPPORTED, ALIAS, HIP_ERROR, OUT_OF_MEMORY = range(
 MAX_SRC = 64
 STEP_INIT, STEP_FINAL = 1, 2
 ITEMS_ON_DEVICE = 1
+SCHEDULE = {"ring": 0, "rhd": 1}
 
 # struct xred_item (32 bytes)
 ITEM_DTYPE = np.dtype([("srcs", "<u8"), ("dst", "<u8"), ("count", "<u8"), ("nsrc", "<u4"),
@@ -36,7 +37,7 @@ class XredItem(ctypes.Structure):
 
 EXPORTS = ("xred_allreduce_local", "xred_reduce_scatter_local", "xred_reduce_copy_step",
            "xred_acc_cast", "xred_batched_reduce", "xred_ring_reduce", "xred_ring_max_count",
-           "xred_set_max_workgroups", "xred_acc_elem_size", "xred_status_string",
+           "xred_allreduce_sim", "xred_sim_chunk", "xred_set_max_workgroups", "xred_acc_elem_size", "xred_status_string",
            "xred_last_error", "xred_version", "xred_release")
 
 _lib = None
@@ -68,10 +69,13 @@ def load(path: Path = LIB_PATH) -> ctypes.CDLL:
     L.xred_batched_reduce.argtypes = [vp, i32, i32, i32, u32, vp]
     L.xred_ring_reduce.argtypes = [vp, i32, vp, sz, i32, i32, vp, ctypes.c_uint32,
                                    ctypes.c_uint64, vp, vp]
+    L.xred_allreduce_sim.argtypes = [vp, vp, i32, sz, i32, i32, i32, vp]
+    L.xred_sim_chunk.argtypes = [sz, i32]
+    L.xred_sim_chunk.restype = sz
     L.xred_ring_max_count.argtypes = [i32]
     L.xred_ring_max_count.restype = sz
     for f in ("xred_allreduce_local", "xred_reduce_scatter_local", "xred_reduce_copy_step",
-              "xred_acc_cast", "xred_batched_reduce", "xred_ring_reduce"):
+              "xred_acc_cast", "xred_batched_reduce", "xred_ring_reduce", "xred_allreduce_sim"):
         getattr(L, f).restype = ctypes.c_int
     L.xred_set_max_workgroups.argtypes = [ctypes.c_uint]
     L.xred_set_max_workgroups.restype = ctypes.c_uint

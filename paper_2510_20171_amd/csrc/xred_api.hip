@@ -493,6 +493,48 @@ XRED_API size_t xred_ring_max_count(xred_dtype dtype)
     return known_dtype(dtype) && dtype != XRED_FLOAT16 ? (size_t)ring_max_count(dtype) : 0;
 }
 
+XRED_API xred_status xred_allreduce_sim(const void *const *sendbufs, void *const *recvbufs,
+                                        int nranks, size_t count, xred_dtype dtype, xred_op op,
+                                        xred_schedule schedule, void *hip_stream)
+{
+    if (nranks < 1 || nranks > XRED_MAX_SRC)
+        return fail(XRED_INVALID_ARGUMENT, "nranks = %d outside 1..%d", nranks, XRED_MAX_SRC);
+    if (schedule != XRED_SCHEDULE_RING && schedule != XRED_SCHEDULE_RHD)
+        return fail(XRED_INVALID_ARGUMENT, "unknown schedule %d", (int)schedule);
+    if (schedule == XRED_SCHEDULE_RHD && (nranks & (nranks - 1)) != 0)
+        return fail(XRED_INVALID_ARGUMENT, "halving-doubling needs a power-of-two nranks, not %d",
+                    nranks);
+    xred_status st = check_types(dtype, op);
+    if (st != XRED_SUCCESS) return st;
+    if (count == 0) return XRED_SUCCESS;
+    if (sendbufs == nullptr || recvbufs == nullptr)
+        return fail(XRED_INVALID_ARGUMENT, "sendbufs or recvbufs is NULL");
+    const size_t es = elem_size(dtype);
+    if (mul_overflows(count, es)) return fail(XRED_INVALID_ARGUMENT, "count * size overflows");
+    const size_t bytes = count * es;
+    for (int r = 0; r < nranks; ++r) {
+        if ((st = check_buf(sendbufs[r], bytes, es, "sendbufs", r)) != XRED_SUCCESS) return st;
+        if ((st = check_buf(recvbufs[r], bytes, es, "recvbufs", r)) != XRED_SUCCESS) return st;
+    }
+    for (int r = 0; r < nranks; ++r) {
+        for (int q = 0; q < nranks; ++q) {
+            if (bad_overlap(recvbufs[r], bytes, sendbufs[q], bytes, q == r))
+                return fail(XRED_ALIAS, "recvbufs[%d] overlaps sendbufs[%d]", r, q);
+            if (q != r && bad_overlap(recvbufs[r], bytes, recvbufs[q], bytes, false))
+                return fail(XRED_ALIAS, "recvbufs[%d] overlaps recvbufs[%d]", r, q);
+        }
+    }
+    const hipError_t e = launch_sim(dtype, op, (const char *const *)sendbufs,
+                                    (char *const *)recvbufs, nranks, count, schedule,
+                                    (hipStream_t)hip_stream);
+    return e == hipSuccess ? XRED_SUCCESS : hip_fail(e, "schedule step launch");
+}
+
+XRED_API size_t xred_sim_chunk(size_t count, int nranks)
+{
+    return (size_t)sim_chunk(count, nranks);
+}
+
 XRED_API unsigned xred_set_max_workgroups(unsigned max_workgroups)
 {
     return g_max_workgroups.exchange(max_workgroups);

@@ -73,6 +73,12 @@ hipError_t launch_ring(xred_dtype dtype, xred_op op, const char *const *chunks, 
                        char *dst, size_t count, const uint32_t *ready, uint32_t epoch,
                        uint64_t timeout_ticks, uint32_t *status, hipStream_t stream);
 
+// A whole AllReduce over nranks simulated ranks on this GPU, one launch per
+// step of the ring or halving-doubling schedule (xred_allreduce_sim).
+uint64_t sim_chunk(uint64_t count, int nranks);
+hipError_t launch_sim(xred_dtype dtype, xred_op op, const char *const *send, char *const *recv,
+                      int nranks, size_t count, xred_schedule schedule, hipStream_t stream);
+
 // Device wall-clock ticks per microsecond of the current device.
 uint64_t wall_ticks_per_us();
 

@@ -1,0 +1,252 @@
+// xred_sim.hip -- a whole AllReduce over G simulated ranks on one GPU
+// (xred_allreduce_sim), one launch per step of the schedule.
+//
+// Ring (the FTAR pipeline's ring, Section 5).  Rank q receives from q-1.
+// ReduceScatter step j = 1..G-1: rank q folds chunk c = q-1-j, reading the
+// message from rank q-1 and its own contribution, and stores the result in
+// recv[q] at chunk c:
+//   j = 1        the message is send[q-1] at chunk c (sendCopy is zero-copy:
+//                the receiver reads the sender's buffer),
+//   1 < j < G-1  the message is recv[q-1] at chunk c, stored there by rank
+//                q-1 in step j-1 (RedCopy: reduce and forward in one store),
+//   j = G-1      c = q: the store is rank q's reduced chunk (Reduce).
+// AllGather step t = 1..G-1: rank q copies chunk q-t from recv[q-1] into
+// recv[q] (RecvCopy; the copy is also the message rank q+1 reads next).
+//
+// Recursive halving-doubling (Section 2.2), G a power of two.  Halving step
+// at distance d = G/2, ..., 1: rank q keeps the aligned group of d blocks that
+// contains block q, and folds its partner q^d's partial of that group into
+// its own (both read from the send buffers at the first step, from the recv
+// buffers after).  Doubling step at d = 1, ..., G/2: rank q copies its
+// partner's aligned group of d blocks from recv[q^d].
+//
+// Within a step no rank writes what another rank reads, and each rank reads
+// its own elements before overwriting them, so recv[q] may be send[q].  Every
+// hop computes down(up(received) (+) up(own)) with the fused kernel's tile
+// code (two sources, fold order received-then-own); copies move bits.
+#include "xred_internal.hpp"
+#include "xred_kernels.hpp"
+
+namespace xred {
+namespace {
+
+constexpr int kB = 256;    // threads per workgroup
+constexpr int kU = 1;      // 16-byte vectors per thread per tile
+
+// One step: rank q's message, own contribution and output, already offset to
+// the chunk (or group of blocks) the rank works on, and its length.
+struct SimStep {
+    const char *in[XRED_MAX_SRC];
+    const char *own[XRED_MAX_SRC];
+    char *out[XRED_MAX_SRC];
+    uint64_t len[XRED_MAX_SRC];
+};
+
+template <class T>
+__device__ __forceinline__ void copy_elem(const char *in, char *out, size_t i)
+{
+    if constexpr (T::kSize == 2)
+        ((uint16_t *)out)[i] = ((const uint16_t *)in)[i];
+    else
+        ((uint32_t *)out)[i] = ((const uint32_t *)in)[i];
+}
+
+// Work item w of a step: rank w % G, tile w / G of that rank's range.  Vector
+// tiles cover the 16-byte part; one extra tile per rank does the last
+// (len % kVec) elements.  COPY: out = in bit for bit; otherwise out =
+// down(up(in) (+) up(own)).
+template <class T, class Op, bool COPY>
+__global__ __launch_bounds__(kB) void sim_step_vec_kernel(SimStep a, int G, uint64_t tiles)
+{
+    constexpr uint32_t kTileBytes = (uint32_t)kB * kU * 16u;
+    const uint64_t work = tiles * (uint64_t)G;
+    for (uint64_t w = blockIdx.x; w < work; w += gridDim.x) {
+        const int q = (int)(w % (uint64_t)G);
+        const uint64_t t = w / (uint64_t)G;
+        const uint64_t len = a.len[q];
+        const uint64_t nvec = len / T::kVec;
+        const size_t vbytes = nvec * 16;
+        const uint64_t vtiles = (vbytes + kTileBytes - 1) / kTileBytes;
+        if (t < vtiles) {
+            const size_t off = t * kTileBytes;
+            const Tile tl{off, tile_nrec(vbytes, off, kTileBytes)};
+            if constexpr (COPY) {
+                const rsrc_t r = make_rsrc(a.in[q] + off, tl.nrec);
+                const rsrc_t o = make_rsrc(a.out[q] + off, tl.nrec);
+#pragma unroll
+                for (int u = 0; u < kU; ++u) {
+                    const uint32_t b = (uint32_t)(u * kB + threadIdx.x) * 16u;
+                    bstore<kStoreOut>(bload<kLoadStream>(r, b), o, b);
+                }
+            } else {
+                KernargSrc<2> src;
+                src.p[0] = a.in[q];
+                src.p[1] = a.own[q];
+                reduce_tile<T, Op, 2, kU, kB>(src, 2, a.out[q], tl);
+            }
+        } else if (t == vtiles && threadIdx.x < len - nvec * T::kVec) {
+            const size_t i = nvec * T::kVec + threadIdx.x;
+            if constexpr (COPY) {
+                copy_elem<T>(a.in[q], a.out[q], i);
+            } else {
+                KernargSrc<2> src;
+                src.p[0] = a.in[q];
+                src.p[1] = a.own[q];
+                reduce_elem<T, Op>(src, 2, a.out[q], i);
+            }
+        }
+    }
+}
+
+// Element-aligned buffers: one element per thread, tiles of kB elements.
+template <class T, class Op, bool COPY>
+__global__ __launch_bounds__(kB) void sim_step_scalar_kernel(SimStep a, int G, uint64_t tiles)
+{
+    const uint64_t work = tiles * (uint64_t)G;
+    for (uint64_t w = blockIdx.x; w < work; w += gridDim.x) {
+        const int q = (int)(w % (uint64_t)G);
+        const size_t i = (size_t)(w / (uint64_t)G) * kB + threadIdx.x;
+        if (i >= a.len[q]) continue;
+        if constexpr (COPY) {
+            copy_elem<T>(a.in[q], a.out[q], i);
+        } else {
+            KernargSrc<2> src;
+            src.p[0] = a.in[q];
+            src.p[1] = a.own[q];
+            reduce_elem<T, Op>(src, 2, a.out[q], i);
+        }
+    }
+}
+
+template <class T, class Op, bool COPY>
+hipError_t launch_sim_step(const SimStep &a, int G, bool vec, hipStream_t s)
+{
+    uint64_t maxlen = 0;
+    for (int q = 0; q < G; ++q) maxlen = a.len[q] > maxlen ? a.len[q] : maxlen;
+    if (maxlen == 0) return hipSuccess;
+    uint64_t tiles;
+    if (vec) {
+        constexpr uint64_t kTileElems = (uint64_t)kB * kU * T::kVec;
+        tiles = (maxlen / T::kVec * T::kVec + kTileElems - 1) / kTileElems + 1;   // + tail tile
+        hipLaunchKernelGGL((sim_step_vec_kernel<T, Op, COPY>), dim3(grid_for(tiles * G)),
+                           dim3(kB), 0, s, a, G, tiles);
+    } else {
+        tiles = (maxlen + kB - 1) / kB;
+        hipLaunchKernelGGL((sim_step_scalar_kernel<T, Op, COPY>), dim3(grid_for(tiles * G)),
+                           dim3(kB), 0, s, a, G, tiles);
+    }
+    return hipGetLastError();
+}
+
+int rank_mod(int r, int G) { return ((r % G) + G) % G; }
+
+template <class T, class Op>
+hipError_t run(const char *const *send, char *const *recv, int G, size_t count,
+               xred_schedule sched, hipStream_t s)
+{
+    constexpr size_t es = T::kSize;
+    const uint64_t M = sim_chunk(count, G);
+    uintptr_t bits = 0;
+    for (int q = 0; q < G; ++q) bits |= (uintptr_t)send[q] | (uintptr_t)recv[q];
+    const bool vec = (bits & 15u) == 0;
+    auto el = [&](uint64_t blk) { return blk * M < count ? blk * M : (uint64_t)count; };
+    SimStep a;
+    hipError_t e = hipSuccess;
+    if (G == 1) {
+        if (send[0] == recv[0]) return hipSuccess;
+        a.in[0] = send[0];
+        a.own[0] = nullptr;
+        a.out[0] = recv[0];
+        a.len[0] = count;
+        return launch_sim_step<T, Op, true>(a, 1, vec, s);
+    }
+    if (sched == XRED_SCHEDULE_RING) {
+        for (int j = 1; j <= G - 1 && e == hipSuccess; ++j) {
+            for (int q = 0; q < G; ++q) {
+                const int c = rank_mod(q - 1 - j, G);
+                const uint64_t lo = el(c), len = el(c + 1) - lo;
+                const int p = rank_mod(q - 1, G);
+                a.in[q] = (j == 1 ? send[p] : recv[p]) + lo * es;
+                a.own[q] = send[q] + lo * es;
+                a.out[q] = recv[q] + lo * es;
+                a.len[q] = len;
+            }
+            e = launch_sim_step<T, Op, false>(a, G, vec, s);
+        }
+        for (int t = 1; t <= G - 1 && e == hipSuccess; ++t) {
+            for (int q = 0; q < G; ++q) {
+                const int c = rank_mod(q - t, G);
+                const uint64_t lo = el(c), len = el(c + 1) - lo;
+                a.in[q] = recv[rank_mod(q - 1, G)] + lo * es;
+                a.own[q] = nullptr;
+                a.out[q] = recv[q] + lo * es;
+                a.len[q] = len;
+            }
+            e = launch_sim_step<T, Op, true>(a, G, vec, s);
+        }
+        return e;
+    }
+    // recursive halving, then recursive doubling
+    for (int d = G / 2; d >= 1 && e == hipSuccess; d /= 2) {
+        const bool first = d == G / 2;
+        for (int q = 0; q < G; ++q) {
+            const int p = q ^ d;
+            const uint64_t b0 = (uint64_t)(q & ~(d - 1));
+            const uint64_t lo = el(b0), len = el(b0 + d) - lo;
+            a.in[q] = (first ? send[p] : recv[p]) + lo * es;
+            a.own[q] = (first ? send[q] : recv[q]) + lo * es;
+            a.out[q] = recv[q] + lo * es;
+            a.len[q] = len;
+        }
+        e = launch_sim_step<T, Op, false>(a, G, vec, s);
+    }
+    for (int d = 1; d < G && e == hipSuccess; d *= 2) {
+        for (int q = 0; q < G; ++q) {
+            const int p = q ^ d;
+            const uint64_t b0 = (uint64_t)(p & ~(d - 1));
+            const uint64_t lo = el(b0), len = el(b0 + d) - lo;
+            a.in[q] = recv[p] + lo * es;
+            a.own[q] = nullptr;
+            a.out[q] = recv[q] + lo * es;
+            a.len[q] = len;
+        }
+        e = launch_sim_step<T, Op, true>(a, G, vec, s);
+    }
+    return e;
+}
+
+template <class T>
+hipError_t run_op(xred_op op, const char *const *send, char *const *recv, int G, size_t count,
+                  xred_schedule sched, hipStream_t s)
+{
+    switch (op) {
+    case XRED_SUM: return run<T, OpSum>(send, recv, G, count, sched, s);
+    case XRED_PROD: return run<T, OpProd>(send, recv, G, count, sched, s);
+    case XRED_MAX: return run<T, OpMax>(send, recv, G, count, sched, s);
+    case XRED_MIN: return run<T, OpMin>(send, recv, G, count, sched, s);
+    }
+    return hipErrorInvalidValue;
+}
+
+}  // namespace
+
+uint64_t sim_chunk(uint64_t count, int nranks)
+{
+    if (nranks < 1) return 0;
+    const uint64_t m = (count + (uint64_t)nranks - 1) / (uint64_t)nranks;
+    return (m + 63) / 64 * 64;
+}
+
+hipError_t launch_sim(xred_dtype dtype, xred_op op, const char *const *send, char *const *recv,
+                      int nranks, size_t count, xred_schedule schedule, hipStream_t stream)
+{
+    switch (dtype) {
+    case XRED_FLOAT32: return run_op<TF32>(op, send, recv, nranks, count, schedule, stream);
+    case XRED_BFLOAT16: return run_op<TBF16>(op, send, recv, nranks, count, schedule, stream);
+    case XRED_INT32: return run_op<TI32>(op, send, recv, nranks, count, schedule, stream);
+    case XRED_UINT32: return run_op<TU32>(op, send, recv, nranks, count, schedule, stream);
+    default: return hipErrorInvalidValue;
+    }
+}
+
+}  // namespace xred

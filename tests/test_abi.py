@@ -109,6 +109,23 @@ def ptrs(*xs):
     (lambda L: L.xred_ring_reduce(ptrs(A), 1, S(A + 8), 16, 1, 0, None, 1, 0, None, None), 3),
     (lambda L: L.xred_ring_reduce(ptrs(A), 1, S(A + 4096), 16, 1, 0, S(A + 1), 1, 0, None, None), 1),
     (lambda L: L.xred_ring_reduce(ptrs(A), 1, S(A + 4096), 16, 2, 0, None, 1, 0, None, None), 2),
+    # xred_allreduce_sim(sends, recvs, nranks, count, dtype, op, schedule, stream)
+    (lambda L: L.xred_allreduce_sim(ptrs(A), ptrs(A + 8192), 0, 16, 1, 0, 0, None), 1),
+    (lambda L: L.xred_allreduce_sim(ptrs(A), ptrs(A + 8192), 65, 16, 1, 0, 0, None), 1),
+    (lambda L: L.xred_allreduce_sim(ptrs(A), ptrs(A + 8192), 1, 16, 1, 0, 2, None), 1),
+    (lambda L: L.xred_allreduce_sim(ptrs(A, A + 4096, A + 8192), ptrs(A + 16384, A + 20480, A + 24576),
+                                    3, 16, 1, 0, 1, None), 1),
+    (lambda L: L.xred_allreduce_sim(None, ptrs(A + 8192), 1, 16, 1, 0, 0, None), 1),
+    (lambda L: L.xred_allreduce_sim(ptrs(A, A + 4096), ptrs(A + 8192, 0), 2, 16, 1, 0, 0, None), 1),
+    (lambda L: L.xred_allreduce_sim(ptrs(A, A + 4097), ptrs(A + 8192, A + 12288), 2, 16, 1, 0, 0,
+                                    None), 1),
+    (lambda L: L.xred_allreduce_sim(ptrs(A, A + 4096), ptrs(A + 8192, A + 16), 2, 16, 1, 0, 0, None), 3),
+    (lambda L: L.xred_allreduce_sim(ptrs(A, A + 4096), ptrs(A + 8192, A + 8200), 2, 16, 1, 0, 0,
+                                    None), 3),
+    (lambda L: L.xred_allreduce_sim(ptrs(A, A + 4096), ptrs(A + 8, A + 12288), 2, 16, 1, 0, 0, None), 3),
+    (lambda L: L.xred_allreduce_sim(ptrs(A, A + 4096), ptrs(A + 8192, A + 12288), 2, 16, 2, 0, 0,
+                                    None), 2),
+    (lambda L: L.xred_allreduce_sim(ptrs(A), ptrs(A + 8192), 1, 2**62, 0, 0, 0, None), 1),
 ])
 def test_validation_rejects_before_launch(L, case, expect):
     assert case(L) == expect
@@ -148,6 +165,17 @@ def test_zero_counts_succeed_without_launch(L):
     p = ptrs(A)
     it = (type(_item(p, A, 0, 1)) * 2)(_item(p, A + 4096, 0, 1), _item(None, 0, 0, 0))
     assert L.xred_batched_reduce(it, 2, 1, 0, 0, None) == 0
+    assert L.xred_allreduce_sim(ptrs(A, A + 4096), ptrs(A + 8192, A + 12288), 2, 0, 1, 0, 0,
+                                None) == 0
+
+
+def test_sim_chunk_rule(L):
+    """ceil(count / G) rounded up to 64 elements, as the oracle's schedules use."""
+    import pins
+    for count in (0, 1, 63, 64, 65, 1000, 64 * 8 + 70, (1 << 26) + 5):
+        for G in (1, 2, 3, 7, 8, 64):
+            assert L.xred_sim_chunk(count, G) == pins.sim_chunk_len(count, G)
+    assert L.xred_sim_chunk(100, 0) == 0
 
 
 def test_python_layer_raises(L):

@@ -1,0 +1,123 @@
+"""GPU parity of xred_allreduce_sim: a whole ring or halving-doubling
+AllReduce over G simulated ranks on one GPU, against the oracle's
+message-by-message simulation of the same schedule.
+
+Every rank's output must equal the oracle's bit for bit (NaN payloads of
+float sum/prod compare by NaN-ness only), and all ranks must hold the same
+bits.  Covered: every dtype x op; ring G = 1, 2, 3, 5, 8, 13 and
+halving-doubling G = 1, 2, 4, 8, 16; sizes from one element to several tiles
+per chunk with short and empty trailing chunks; in place; element-aligned
+(not 16-byte aligned) buffers; a CU budget; the full G=8 x 2^26 bf16 bucket
+the benchmark times, for both schedules.
+"""
+import os
+
+import numpy as np
+import pytest
+
+import gpu_util as gu
+import pins
+import workloads as wl
+
+pytestmark = pytest.mark.gpu
+torch = pytest.importorskip("torch")
+
+DTYPES = ("f32", "bf16", "i32", "u32")
+OPS = ("sum", "prod", "max", "min")
+CORES = min(16, len(os.sched_getaffinity(0)))
+
+
+@pytest.fixture(scope="module")
+def xr():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU visible")
+    import paper_2510_20171_amd as xr
+    xr.load()
+    yield xr
+    xr.set_max_workgroups(0)
+
+
+def _check(outs, exp, dtype, op, what):
+    b0 = gu.bits(outs[0], dtype)
+    for r, o in enumerate(outs):
+        assert np.array_equal(gu.bits(o, dtype), b0), f"{what}: rank {r} differs from rank 0"
+        gu.assert_parity(o, exp[r], dtype, op, f"{what} rank {r}")
+
+
+def _run(xr, sends_np, dtype, op, schedule, in_place=False):
+    sends = [gu.to_dev(s, dtype) for s in sends_np]
+    recvs = sends if in_place else [torch.empty_like(s) for s in sends]
+    xr.allreduce_sim(sends, recvs, op, schedule=schedule, dtype=dtype)
+    torch.cuda.synchronize()
+    return recvs
+
+
+def _sizes(G):
+    return (1, 37, 64 * G + 70, 4096 * 5 + 3, (1 << 17) + 5)
+
+
+@pytest.mark.parametrize("dtype", DTYPES)
+@pytest.mark.parametrize("op", OPS)
+def test_ring_and_rhd_parity(xr, orc, dtype, op):
+    rng = np.random.default_rng(61 + 10 * DTYPES.index(dtype) + OPS.index(op))
+    for schedule, ranks in (("ring", (1, 2, 3, 5, 8, 13)), ("rhd", (1, 2, 4, 8, 16))):
+        for G in ranks:
+            for n in _sizes(G):
+                if G * n > (1 << 21):
+                    continue
+                sends = [pins.random_column_values(rng, dtype, n) for _ in range(G)]
+                outs = _run(xr, sends, dtype, op, schedule)
+                exp = orc.allreduce_sim(sends, dtype, op, schedule)
+                _check(outs, exp, dtype, op, f"{schedule} {dtype} {op} G={G} n={n}")
+
+
+@pytest.mark.parametrize("schedule", ["ring", "rhd"])
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_in_place(xr, orc, schedule, dtype):
+    rng = np.random.default_rng(7)
+    for G, n in ((2, 999), (4, 64 * 4 + 70), (8, (1 << 16) + 3)):
+        sends = [pins.random_column_values(rng, dtype, n) for _ in range(G)]
+        outs = _run(xr, sends, dtype, "sum", schedule, in_place=True)
+        _check(outs, orc.allreduce_sim(sends, dtype, "sum", schedule), dtype, "sum",
+               f"in place {schedule} G={G}")
+
+
+@pytest.mark.parametrize("schedule", ["ring", "rhd"])
+def test_element_aligned_buffers(xr, orc, schedule):
+    """Buffers one element off 16-byte alignment take the scalar path."""
+    rng = np.random.default_rng(8)
+    G, n = 4, 64 * 4 * 3 + 11
+    for dtype in ("bf16", "f32", "i32"):
+        sends_np = [pins.random_column_values(rng, dtype, n) for _ in range(G)]
+        big = [gu.to_dev(np.concatenate([np.zeros(1, s.dtype), s]), dtype) for s in sends_np]
+        sends = [b[1:] for b in big]
+        rbig = [torch.empty_like(b) for b in big]
+        recvs = [b[1:] for b in rbig]
+        xr.allreduce_sim(sends, recvs, "max", schedule=schedule, dtype=dtype)
+        torch.cuda.synchronize()
+        _check(recvs, orc.allreduce_sim(sends_np, dtype, "max", schedule), dtype, "max",
+               f"element-aligned {schedule} {dtype}")
+
+
+def test_budget_does_not_change_results(xr, orc):
+    rng = np.random.default_rng(9)
+    G, n = 8, (1 << 15) + 77
+    sends = [pins.random_column_values(rng, "bf16", n) for _ in range(G)]
+    exp = orc.allreduce_sim(sends, "bf16", "sum", "ring")
+    for budget in (1, 7, 0):
+        prev = xr.set_max_workgroups(budget)
+        try:
+            outs = _run(xr, sends, "bf16", "sum", "ring")
+        finally:
+            xr.set_max_workgroups(prev)
+        _check(outs, exp, "bf16", "sum", f"budget {budget}")
+
+
+@pytest.mark.parametrize("schedule", ["ring", "rhd"])
+def test_full_bucket(xr, orc, schedule):
+    """The benchmark's workload: 8 ranks x 2^26 bf16, both schedules."""
+    w = wl.WORKLOADS["sim"]
+    sends = wl.sources(w)
+    outs = _run(xr, sends, w.dtype, w.op, schedule)
+    exp = orc.allreduce_sim(sends, w.dtype, w.op, schedule, nthreads=CORES)
+    _check(outs, exp, w.dtype, w.op, f"sim {schedule}")

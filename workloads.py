@@ -22,6 +22,9 @@ Workloads (M = 2^20, K = 2^10 elements):
                         log-uniform on [8 KiB, 1 MiB]
   c5a  allreduce_local  P=32 x 8M  i32  sum   uniform over all int32
   c5b  allreduce_local  P=32 x 8M  f32  max   N(0,1) with +-inf and +-0 mixed in
+  sim  allreduce_sim    G=8 ranks x 64M bf16 sum N(0,1)*1e-3 per rank (a c2-sized
+                        gradient bucket AllReduced over 8 simulated ranks; the
+                        send buffer of rank r is source r)
 """
 from __future__ import annotations
 
@@ -41,7 +44,7 @@ ELEM_SIZE = {"f32": 4, "bf16": 2, "i32": 4, "u32": 4}
 @dataclass(frozen=True)
 class Workload:
     name: str
-    kind: str          # "allreduce" | "stepwise" | "batched"
+    kind: str          # "allreduce" | "stepwise" | "batched" | "sim"
     dtype: str
     op: str
     nsrc: int
@@ -55,6 +58,10 @@ class Workload:
         es = ELEM_SIZE[self.dtype]
         if self.kind == "batched":
             return int(sum((self.nsrc + 1) * int(n) * es for n in sizes))
+        if self.kind == "sim":
+            # G-1 reduce steps reading two chunks and writing one, G-1 copy
+            # steps reading one and writing one, every chunk once per step
+            return 5 * (self.nsrc - 1) * self.count * es
         return (self.nsrc + 1) * self.count * es
 
 
@@ -65,6 +72,7 @@ WORKLOADS = {
     "c4": Workload("c4", "batched", "bf16", "sum", 8, 0, "uniform", 4000, nitems=4096),
     "c5a": Workload("c5a", "allreduce", "i32", "sum", 32, 8 * M, "int32", 5000),
     "c5b": Workload("c5b", "allreduce", "f32", "max", 32, 8 * M, "normal_specials", 5100),
+    "sim": Workload("sim", "sim", "bf16", "sum", 8, 64 * M, "normal_1e-3", 7000),
 }
 
 
