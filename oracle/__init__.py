@@ -13,8 +13,10 @@ follows the definition in the C file's header: a left fold in source order
 AllReduce semantics of Section 2.2).
 
 Element arrays are numpy arrays: float32 for ``f32``, uint16 bit patterns for
-``bf16``, int32 for ``i32`` and uint32 for ``u32``.  Step-wise accumulators
-are float32 arrays for float dtypes and uint32 arrays for integer dtypes.
+``bf16`` and ``f16``, uint8 bit patterns for ``e4m3`` and ``e5m2``, int32 /
+uint32 / int64 / uint64 for the integer types.  Step-wise accumulators are
+float32 arrays for float dtypes, uint32 for 32-bit and uint64 for 64-bit
+integer dtypes.
 """
 from __future__ import annotations
 
@@ -36,10 +38,13 @@ CFLAGS = [
     "-ffp-contract=off", "-fno-fast-math", "-fno-finite-math-only",
 ]
 
-DTYPES = {"f32": (10, np.float32), "bf16": (11, np.uint16), "i32": (13, np.int32),
-          "u32": (14, np.uint32)}
-OPS = {"sum": 20, "prod": 21, "max": 22, "min": 23}
-ACC_NP = {"f32": np.float32, "bf16": np.float32, "i32": np.uint32, "u32": np.uint32}
+DTYPES = {"f32": (10, np.float32), "bf16": (11, np.uint16), "f16": (12, np.uint16),
+          "i32": (13, np.int32), "u32": (14, np.uint32), "i64": (15, np.int64),
+          "u64": (16, np.uint64), "e4m3": (17, np.uint8), "e5m2": (18, np.uint8)}
+OPS = {"sum": 20, "prod": 21, "max": 22, "min": 23, "avg": 24}
+ACC_NP = {"f32": np.float32, "bf16": np.float32, "f16": np.float32, "e4m3": np.float32,
+          "e5m2": np.float32, "i32": np.uint32, "u32": np.uint32, "i64": np.uint64,
+          "u64": np.uint64}
 _INIT, _FINAL = 1, 2
 
 
@@ -75,6 +80,8 @@ class Oracle:
         L.xo_ring_allreduce_sim.argtypes = [vp, vp, i32, u64, i32, i32, i32]
         L.xo_rhd_allreduce_sim.argtypes = [vp, vp, i32, u64, i32, i32, i32]
         L.xo_f32_bits_to_bf16.argtypes = [vp, vp, u64]
+        L.xo_small_to_f32_bits.argtypes = [vp, i32, vp, u64, i32]
+        L.xo_f32_bits_to_small.argtypes = [vp, vp, u64, i32]
         L.xo_bf16_to_f32_bits.argtypes = [vp, vp, u64]
         for fn in ("xo_allreduce_local", "xo_reduce_scatter_local", "xo_reduce_copy_step",
                    "xo_acc_cast", "xo_batched_reduce", "xo_ring_allreduce_sim",
@@ -208,6 +215,22 @@ class Oracle:
         bits = np.ascontiguousarray(bits, np.uint32)
         out = np.empty(bits.size, np.uint16)
         self._L.xo_f32_bits_to_bf16(_ptr(bits), _ptr(out), bits.size)
+        return out
+
+    def small_to_f32_bits(self, h: np.ndarray, dtype: str) -> np.ndarray:
+        """Exact widening of f16 / e4m3 / e5m2 bit patterns to binary32 bits."""
+        np_t = DTYPES[dtype][1]
+        h = np.ascontiguousarray(h, np_t)
+        out = np.empty(h.size, np.uint32)
+        self._L.xo_small_to_f32_bits(_ptr(h), np.dtype(np_t).itemsize, _ptr(out), h.size,
+                                     DTYPES[dtype][0])
+        return out
+
+    def f32_bits_to_small(self, bits: np.ndarray, dtype: str) -> np.ndarray:
+        """binary32 bits -> f16 / e4m3 / e5m2 bits (round to nearest even)."""
+        bits = np.ascontiguousarray(bits, np.uint32)
+        out = np.empty(bits.size, DTYPES[dtype][1])
+        self._L.xo_f32_bits_to_small(_ptr(bits), _ptr(out), bits.size, DTYPES[dtype][0])
         return out
 
     def bf16_to_f32_bits(self, h: np.ndarray) -> np.ndarray:

@@ -16,8 +16,10 @@
  * for every element index i independently, where fold is a LEFT fold in
  * source order 0..P-1 (the paper never states an order; a fixed rank order is
  * the reading taken), up() converts an input element to the accumulator type
- * (binary32 for bf16/fp32, uint32 for int32/uint32: the paper names no
- * accumulator type), and down() converts back with round-to-nearest-even.
+ * (binary32 for bf16/fp16/fp8/fp32, uint32 for int32/uint32, uint64 for
+ * int64/uint64: the paper names no accumulator type), and down() converts
+ * back with round-to-nearest-even.  AVG (float types) is the SUM fold
+ * followed by one binary32 division by P.
  *
  * Arithmetic is carried out in binary32 because the definition being checked
  * is binary32 accumulation; this file is compiled with -ffp-contract=off and
@@ -56,8 +58,9 @@
 #endif
 
 /* The oracle's own codes; the Python loader maps dtype/op names onto them. */
-enum { XO_F32 = 10, XO_BF16 = 11, XO_I32 = 13, XO_U32 = 14 };
-enum { XO_SUM = 20, XO_PROD = 21, XO_MAX = 22, XO_MIN = 23 };
+enum { XO_F32 = 10, XO_BF16 = 11, XO_F16 = 12, XO_I32 = 13, XO_U32 = 14, XO_I64 = 15,
+       XO_U64 = 16, XO_E4M3 = 17, XO_E5M2 = 18 };
+enum { XO_SUM = 20, XO_PROD = 21, XO_MAX = 22, XO_MIN = 23, XO_AVG = 24 };
 enum { XO_INIT = 1u, XO_FINAL = 2u };
 enum { XO_OK = 0, XO_BAD = -1 };
 
@@ -66,15 +69,127 @@ enum { XO_OK = 0, XO_BAD = -1 };
 static uint32_t f2u(float f) { uint32_t u; memcpy(&u, &f, 4); return u; }
 static float u2f(uint32_t u) { float f; memcpy(&f, &u, 4); return f; }
 
-static int is_float_type(int dtype) { return dtype == XO_F32 || dtype == XO_BF16; }
+static int is_float_type(int dtype)
+{
+    return dtype == XO_F32 || dtype == XO_BF16 || dtype == XO_F16 || dtype == XO_E4M3 ||
+           dtype == XO_E5M2;
+}
+
+static int is_int64_type(int dtype) { return dtype == XO_I64 || dtype == XO_U64; }
 
 static size_t elem_size(int dtype)
 {
     switch (dtype) {
     case XO_F32: case XO_I32: case XO_U32: return 4;
-    case XO_BF16: return 2;
+    case XO_BF16: case XO_F16: return 2;
+    case XO_E4M3: case XO_E5M2: return 1;
+    case XO_I64: case XO_U64: return 8;
     default: return 0;
     }
+}
+
+/* ------------------------------------------------ narrow float formats --- */
+/*
+ * fp16  IEEE 754 binary16: exponent 5 bits (bias 15), fraction 10 bits.
+ * e5m2  OCP 8-bit E5M2: exponent 5 bits (bias 15), fraction 2 bits; infinities
+ *       and NaNs as in binary16.
+ * e4m3  OCP 8-bit E4M3 ("FN"): exponent 4 bits (bias 7), fraction 3 bits; no
+ *       infinity; exponent field 15 with fraction 7 is NaN, so the largest
+ *       finite magnitude is 1.75 * 2^8 = 448.
+ */
+struct small_fmt {
+    int mbits, ebits, bias, has_inf;
+    uint32_t max_finite;   /* magnitude bits of the largest finite value */
+    uint32_t qnan;         /* magnitude bits of the quiet NaN produced */
+};
+static const struct small_fmt FMT_F16 = {10, 5, 15, 1, 0x7BFFu, 0x7E00u};
+static const struct small_fmt FMT_E5M2 = {2, 5, 15, 1, 0x7Bu, 0x7Eu};
+static const struct small_fmt FMT_E4M3 = {3, 4, 7, 0, 0x7Eu, 0x7Fu};
+
+static const struct small_fmt *small_fmt_of(int dtype)
+{
+    switch (dtype) {
+    case XO_F16: return &FMT_F16;
+    case XO_E5M2: return &FMT_E5M2;
+    case XO_E4M3: return &FMT_E4M3;
+    default: return NULL;
+    }
+}
+
+/* Exact widening: sign, biased exponent and fraction read from the fields. */
+static float small_to_f32(uint32_t bits, const struct small_fmt *f)
+{
+    const uint32_t sign = (bits >> (f->mbits + f->ebits)) & 1u;
+    const uint32_t e = (bits >> f->mbits) & ((1u << f->ebits) - 1u);
+    const uint32_t m = bits & ((1u << f->mbits) - 1u);
+    const uint32_t etop = (1u << f->ebits) - 1u;
+    float mag;
+    if (f->has_inf && e == etop)
+        mag = m ? NAN : INFINITY;
+    else if (!f->has_inf && e == etop && m == (1u << f->mbits) - 1u)
+        mag = NAN;
+    else if (e == 0)
+        mag = ldexpf((float)m, 1 - f->bias - f->mbits);
+    else
+        mag = ldexpf((float)(m | (1u << f->mbits)), (int)e - f->bias - f->mbits);
+    return sign ? -mag : mag;
+}
+
+/*
+ * binary32 -> narrow format, round to nearest, ties to even, subnormals kept.
+ * |x| = M * 2^E exactly (M < 2^24).  The result's quantum is 2^Q with
+ * Q = max(floor(log2 |x|), emin) - mbits; M * 2^(E-Q) is rounded to an integer
+ * n by its dropped bits, and n * 2^Q is encoded.  Past the largest finite
+ * value the result is infinity for formats that have one and the largest
+ * finite magnitude for e4m3 (saturation; an infinite input saturates too).
+ * NaN gives the format's quiet NaN with the sign kept.
+ */
+static uint32_t f32_to_small(float x, const struct small_fmt *f)
+{
+    const uint32_t b = f2u(x);
+    const uint32_t sbit = (b >> 31) << (f->mbits + f->ebits);
+    const uint32_t etop = (1u << f->ebits) - 1u;
+    const uint32_t overflow = f->has_inf ? (etop << f->mbits) : f->max_finite;
+    if (isnan(x)) return sbit | f->qnan;
+    if (isinf(x)) return sbit | overflow;
+    uint32_t M = b & 0x7FFFFFu;
+    const uint32_t ef = (b >> 23) & 0xFFu;
+    int E;
+    if (ef == 0) {
+        if (M == 0) return sbit;
+        E = -149;
+    } else {
+        M |= 0x800000u;
+        E = (int)ef - 150;
+    }
+    int msb = 31;
+    while (!(M >> msb)) --msb;
+    const int k = E + msb;                     /* floor(log2 |x|) */
+    const int emin = 1 - f->bias;
+    int Q = (k > emin ? k : emin) - f->mbits;
+    const int shift = Q - E;                   /* bits of M below the quantum */
+    uint64_t n;
+    if (shift <= 0) {
+        n = (uint64_t)M << (-shift);
+    } else if (shift > 25) {
+        n = 0;                                 /* below half a quantum */
+    } else {
+        n = (uint64_t)M >> shift;
+        const uint64_t rem = (uint64_t)M & ((1ull << shift) - 1u);
+        const uint64_t half = 1ull << (shift - 1);
+        if (rem > half || (rem == half && (n & 1u))) n += 1;
+    }
+    if (n == 0) return sbit;
+    if (n >= (2ull << f->mbits)) {             /* carried into the next binade */
+        n >>= 1;
+        Q += 1;
+    }
+    if (n < (1ull << f->mbits)) return sbit | (uint32_t)n;   /* subnormal */
+    const int efield = Q + f->mbits + f->bias;
+    if (efield > (int)etop) return sbit | overflow;
+    const uint32_t mag = ((uint32_t)efield << f->mbits) | (uint32_t)(n - (1ull << f->mbits));
+    if (mag > f->max_finite) return sbit | overflow;
+    return sbit | mag;
 }
 
 /* ---------------------------------------------------------------- up() --- */
@@ -89,6 +204,13 @@ static float up_float(const void *base, uint64_t i, int dtype)
         memcpy(&h, (const char *)base + 2 * i, 2);
         return bf16_to_f32(h);
     }
+    if (dtype == XO_F16) {
+        uint16_t h;
+        memcpy(&h, (const char *)base + 2 * i, 2);
+        return small_to_f32(h, &FMT_F16);
+    }
+    if (dtype == XO_E4M3 || dtype == XO_E5M2)
+        return small_to_f32(((const uint8_t *)base)[i], small_fmt_of(dtype));
     float f;
     memcpy(&f, (const char *)base + 4 * i, 4);
     return f;
@@ -98,6 +220,13 @@ static uint32_t up_int(const void *base, uint64_t i)
 {
     uint32_t u;
     memcpy(&u, (const char *)base + 4 * i, 4);
+    return u;
+}
+
+static uint64_t up_int64(const void *base, uint64_t i)
+{
+    uint64_t u;
+    memcpy(&u, (const char *)base + 8 * i, 8);
     return u;
 }
 
@@ -125,9 +254,19 @@ static void down_float(void *base, uint64_t i, int dtype, float v)
     if (dtype == XO_BF16) {
         uint16_t h = f32_to_bf16(v);
         memcpy((char *)base + 2 * i, &h, 2);
+    } else if (dtype == XO_F16) {
+        uint16_t h = (uint16_t)f32_to_small(v, &FMT_F16);
+        memcpy((char *)base + 2 * i, &h, 2);
+    } else if (dtype == XO_E4M3 || dtype == XO_E5M2) {
+        ((uint8_t *)base)[i] = (uint8_t)f32_to_small(v, small_fmt_of(dtype));
     } else {
         memcpy((char *)base + 4 * i, &v, 4);
     }
+}
+
+static void down_int64(void *base, uint64_t i, uint64_t v)
+{
+    memcpy((char *)base + 8 * i, &v, 8);
 }
 
 static void down_int(void *base, uint64_t i, uint32_t v)
@@ -184,6 +323,21 @@ static uint32_t op_int(int op, int dtype, uint32_t a, uint32_t b)
     }
 }
 
+/* 64-bit integers: sum and product wrap modulo 2^64; max/min signed for XO_I64. */
+static uint64_t op_int64(int op, int dtype, uint64_t a, uint64_t b)
+{
+    switch (op) {
+    case XO_SUM: return a + b;
+    case XO_PROD: return a * b;
+    case XO_MAX:
+        if (dtype == XO_I64) return ((int64_t)a > (int64_t)b) ? a : b;
+        return a > b ? a : b;
+    default:
+        if (dtype == XO_I64) return ((int64_t)a < (int64_t)b) ? a : b;
+        return a < b ? a : b;
+    }
+}
+
 /* MAX/MIN results: a NaN anywhere among the reduced values is reported as the
  * canonical quiet NaN, also when no binary operation was applied (P = 1). */
 static float settle(int op, float v)
@@ -193,19 +347,32 @@ static float settle(int op, float v)
 }
 
 static int valid_dtype(int dtype) { return elem_size(dtype) != 0; }
-static int valid_op(int op) { return op >= XO_SUM && op <= XO_MIN; }
+static int valid_op(int op) { return op >= XO_SUM && op <= XO_AVG; }
+/* AVG is defined for float types only. */
+static int valid_pair(int dtype, int op)
+{
+    return valid_dtype(dtype) && valid_op(op) && (op != XO_AVG || is_float_type(dtype));
+}
 
 /* ------------------------------------------------------ the definition --- */
 
-/* out[i] = down(fold_op(up(srcs[0][off+i]), ..., up(srcs[P-1][off+i]))) */
+/* out[i] = down(fold_op(up(srcs[0][off+i]), ..., up(srcs[P-1][off+i])));
+ * AVG is the SUM fold followed by one binary32 division by P. */
 static void reduce_one(const void *const *srcs, int nsrc, uint64_t off, void *dst,
                        uint64_t i, int dtype, int op)
 {
     if (is_float_type(dtype)) {
+        const int fop = op == XO_AVG ? XO_SUM : op;
         float acc = up_float(srcs[0], off + i, dtype);
         for (int p = 1; p < nsrc; ++p)
-            acc = op_float(op, acc, up_float(srcs[p], off + i, dtype));
+            acc = op_float(fop, acc, up_float(srcs[p], off + i, dtype));
+        if (op == XO_AVG) acc = acc / (float)nsrc;
         down_float(dst, i, dtype, settle(op, acc));
+    } else if (is_int64_type(dtype)) {
+        uint64_t acc = up_int64(srcs[0], off + i);
+        for (int p = 1; p < nsrc; ++p)
+            acc = op_int64(op, dtype, acc, up_int64(srcs[p], off + i));
+        down_int64(dst, i, acc);
     } else {
         uint32_t acc = up_int(srcs[0], off + i);
         for (int p = 1; p < nsrc; ++p)
@@ -217,7 +384,7 @@ static void reduce_one(const void *const *srcs, int nsrc, uint64_t off, void *ds
 static int reduce_range(const void *const *srcs, int nsrc, uint64_t off, void *dst,
                         uint64_t count, int dtype, int op, int nthreads)
 {
-    if (nsrc < 1 || !valid_dtype(dtype) || !valid_op(op)) return XO_BAD;
+    if (nsrc < 1 || !valid_pair(dtype, op)) return XO_BAD;
     if (count == 0) return XO_OK;
     if (nthreads < 1) nthreads = 1;
     /* Elements are independent; splitting the index range over threads does
@@ -257,10 +424,15 @@ int xo_reduce_scatter_local(const void *const *srcs, int nsrc, int rank, void *d
 int xo_reduce_copy_step(const void *in, void *acc, void *dst, uint64_t count, int dtype,
                         int op, unsigned flags)
 {
-    if (!valid_dtype(dtype) || !valid_op(op)) return XO_BAD;
+    if (!valid_pair(dtype, op) || op == XO_AVG) return XO_BAD;
     int init = (flags & XO_INIT) != 0, fin = (flags & XO_FINAL) != 0;
     for (uint64_t i = 0; i < count; ++i) {
-        if (is_float_type(dtype)) {
+        if (is_int64_type(dtype)) {
+            uint64_t x = up_int64(in, i);
+            uint64_t a = init ? x : op_int64(op, dtype, up_int64(acc, i), x);
+            if (fin) down_int64(dst, i, a);
+            else down_int64(acc, i, a);
+        } else if (is_float_type(dtype)) {
             float x = up_float(in, i, dtype);
             float a = init ? x : op_float(op, up_float(acc, i, XO_F32), x);
             a = settle(op, a);
@@ -282,6 +454,7 @@ int xo_acc_cast(const void *acc, void *dst, uint64_t count, int dtype)
     if (!valid_dtype(dtype)) return XO_BAD;
     for (uint64_t i = 0; i < count; ++i) {
         if (is_float_type(dtype)) down_float(dst, i, dtype, up_float(acc, i, XO_F32));
+        else if (is_int64_type(dtype)) down_int64(dst, i, up_int64(acc, i));
         else down_int(dst, i, up_int(acc, i));
     }
     return XO_OK;
@@ -377,7 +550,8 @@ static void free_bufs(void **b, int G)
 int xo_ring_allreduce_sim(const void *const *send, void *const *recv, int G, uint64_t count,
                           int dtype, int op, int nthreads)
 {
-    if (G < 1 || !valid_dtype(dtype) || !valid_op(op)) return XO_BAD;
+    /* AVG is not a hop operation (each hop would halve); it is not simulated. */
+    if (G < 1 || !valid_pair(dtype, op) || op == XO_AVG) return XO_BAD;
     if (count == 0) return XO_OK;
     const size_t es = elem_size(dtype);
     const uint64_t M = xo_sim_chunk(count, G);
@@ -445,7 +619,7 @@ int xo_ring_allreduce_sim(const void *const *send, void *const *recv, int G, uin
 int xo_rhd_allreduce_sim(const void *const *send, void *const *recv, int G, uint64_t count,
                          int dtype, int op, int nthreads)
 {
-    if (G < 1 || (G & (G - 1)) != 0 || !valid_dtype(dtype) || !valid_op(op)) return XO_BAD;
+    if (G < 1 || (G & (G - 1)) != 0 || !valid_pair(dtype, op) || op == XO_AVG) return XO_BAD;
     if (count == 0) return XO_OK;
     const size_t es = elem_size(dtype);
     const uint64_t M = xo_sim_chunk(count, G);
@@ -525,4 +699,24 @@ int xo_max_threads(void)
 #endif
 }
 
-int xo_version(void) { return 2; }
+int xo_version(void) { return 3; }
+
+/* Narrow float conversions on their own, for the pins. */
+void xo_small_to_f32_bits(const uint8_t *in, int in_size, uint32_t *out, uint64_t n, int dtype)
+{
+    const struct small_fmt *f = small_fmt_of(dtype);
+    for (uint64_t i = 0; i < n; ++i) {
+        uint32_t v = in_size == 2 ? (uint32_t)((const uint16_t *)in)[i] : in[i];
+        out[i] = f2u(small_to_f32(v, f));
+    }
+}
+
+void xo_f32_bits_to_small(const uint32_t *in, uint8_t *out, uint64_t n, int dtype)
+{
+    const struct small_fmt *f = small_fmt_of(dtype);
+    for (uint64_t i = 0; i < n; ++i) {
+        uint32_t v = f32_to_small(u2f(in[i]), f);
+        if (f->mbits + f->ebits + 1 == 16) ((uint16_t *)out)[i] = (uint16_t)v;
+        else out[i] = (uint8_t)v;
+    }
+}

@@ -14,6 +14,12 @@ from fractions import Fraction
 
 F32 = dict(p=24, emin=-126, emax=127, ebits=8, bias=127, total=32)
 BF16 = dict(p=8, emin=-126, emax=127, ebits=8, bias=127, total=16)
+# IEEE binary16, OCP FP8 E5M2 (binary16-like), OCP FP8 E4M3 "FN": no
+# infinity, the all-ones pattern is the only NaN, largest finite 448.
+F16 = dict(p=11, emin=-14, emax=15, ebits=5, bias=15, total=16, qnan=0x7E00)
+E5M2 = dict(p=3, emin=-14, emax=15, ebits=5, bias=15, total=8, qnan=0x7E)
+E4M3 = dict(p=4, emin=-6, emax=8, ebits=4, bias=7, total=8, qnan=0x7F, fn=True)
+NARROW = {"f16": F16, "e5m2": E5M2, "e4m3": E4M3}
 CANON_NAN32 = 0x7FC00000
 
 
@@ -23,7 +29,10 @@ def decode(bits: int, fmt=F32):
     s = (bits >> (fmt["total"] - 1)) & 1
     e = (bits >> mbits) & ((1 << fmt["ebits"]) - 1)
     m = bits & ((1 << mbits) - 1)
-    if e == (1 << fmt["ebits"]) - 1:
+    if fmt.get("fn") and e == (1 << fmt["ebits"]) - 1:
+        if m == (1 << mbits) - 1:
+            return ("nan",)
+    elif e == (1 << fmt["ebits"]) - 1:
         return ("nan",) if m else ("inf", s)
     if e == 0:
         mag = Fraction(m) * Fraction(2) ** (fmt["emin"] - mbits)
@@ -65,6 +74,60 @@ def encode_rounded(sign: int, mag: Fraction, fmt=F32) -> int:
     if n < (1 << mbits):       # subnormal (only possible at e == emin) or zero
         return sbit | n
     return sbit | ((e + fmt["bias"]) << mbits) | (n - (1 << mbits))
+
+
+def _fn_max(fmt) -> int:
+    """Magnitude bits of the largest finite value of an "FN" format."""
+    return (((1 << fmt["ebits"]) - 1) << (fmt["p"] - 1)) | ((1 << (fmt["p"] - 1)) - 2)
+
+
+def f32_to_narrow(b: int, dtype: str) -> int:
+    """Correctly rounded binary32 -> f16 / e5m2 / e4m3.  NaN keeps its sign and
+    becomes the format's quiet NaN; e4m3 saturates at 448 (also for infinities)."""
+    fmt = NARROW[dtype]
+    sbit = ((b >> 31) & 1) << (fmt["total"] - 1)
+    d = decode(b)
+    if d[0] == "nan":
+        return sbit | fmt["qnan"]
+    if fmt.get("fn"):
+        # every magnitude >= the largest finite value rounds to it or past it,
+        # and past it saturates: the result is the largest finite value
+        top = Fraction(2 * (1 << (fmt["p"] - 1)) - 2, 1 << (fmt["p"] - 1)) * Fraction(2) ** fmt["emax"]
+        if d[0] == "inf" or d[2] >= top:
+            return sbit | _fn_max(fmt)
+        return encode_rounded(d[1], d[2], fmt)
+    if d[0] == "inf":
+        return sbit | (((1 << fmt["ebits"]) - 1) << (fmt["p"] - 1))
+    return encode_rounded(d[1], d[2], fmt)
+
+
+def narrow_to_f32(h: int, dtype: str) -> int:
+    """Exact widening of f16 / e5m2 / e4m3 bits to binary32 bits."""
+    d = decode(h, NARROW[dtype])
+    if d[0] == "nan":
+        return CANON_NAN32
+    if d[0] == "inf":
+        return (d[1] << 31) | 0x7F800000
+    return encode_rounded(d[1], d[2], F32)
+
+
+def div32(a: int, b: int) -> int:
+    """Correctly rounded binary32 division a / b."""
+    A, B = decode(a), decode(b)
+    if A[0] == "nan" or B[0] == "nan":
+        return CANON_NAN32
+    s = A[1] ^ B[1]
+    if A[0] == "inf":
+        return CANON_NAN32 if B[0] == "inf" else (s << 31) | 0x7F800000
+    if B[0] == "inf":
+        return s << 31
+    if B[2] == 0:
+        return CANON_NAN32 if A[2] == 0 else (s << 31) | 0x7F800000
+    return encode_rounded(s, A[2] / B[2])
+
+
+def f32_bits_of_int(k: int) -> int:
+    return encode_rounded(0 if k >= 0 else 1, Fraction(abs(k)))
 
 
 def add32(a: int, b: int) -> int:
@@ -161,16 +224,50 @@ def iop(op: str, dtype: str, a: int, b: int) -> int:
     return max(a, b) if op == "max" else min(a, b)
 
 
+def iop64(op: str, dtype: str, a: int, b: int) -> int:
+    """64-bit integer op on uint64 bit patterns (sum/prod modulo 2^64)."""
+    m = (1 << 64) - 1
+    if op == "sum":
+        return (a + b) & m
+    if op == "prod":
+        return (a * b) & m
+    if dtype == "i64":
+        sa = a - (1 << 64) if a >> 63 else a
+        sb = b - (1 << 64) if b >> 63 else b
+        r = max(sa, sb) if op == "max" else min(sa, sb)
+        return r & m
+    return max(a, b) if op == "max" else min(a, b)
+
+
+FLOAT_DTYPES = ("f32", "bf16", "f16", "e4m3", "e5m2")
+
+
 def reduce_column(vals_bits, dtype: str, op: str) -> int:
-    """Left fold of one column of bit patterns; returns the output bit pattern."""
-    if dtype in ("f32", "bf16"):
-        up = bf16_to_f32 if dtype == "bf16" else (lambda x: x & 0xFFFFFFFF)
+    """Left fold of one column of bit patterns; returns the output bit pattern.
+    AVG: the SUM fold, then one binary32 division by the number of values."""
+    if dtype in FLOAT_DTYPES:
+        if dtype == "bf16":
+            up, down = bf16_to_f32, f32_to_bf16
+        elif dtype == "f32":
+            up, down = (lambda x: x & 0xFFFFFFFF), (lambda x: x)
+        else:
+            up = lambda x: narrow_to_f32(x, dtype)          # noqa: E731
+            down = lambda x: f32_to_narrow(x, dtype)        # noqa: E731
+        fop = FOPS["sum" if op == "avg" else op]
         acc = up(vals_bits[0])
         for v in vals_bits[1:]:
-            acc = FOPS[op](acc, up(v))
+            acc = fop(acc, up(v))
+        if op == "avg":
+            acc = div32(acc, f32_bits_of_int(len(vals_bits)))
         if op in ("max", "min") and is_nan32(acc):
             acc = CANON_NAN32      # a NaN among the values, whatever their number
-        return f32_to_bf16(acc) if dtype == "bf16" else acc
+        return down(acc)
+    if dtype in ("i64", "u64"):
+        m = (1 << 64) - 1
+        acc = vals_bits[0] & m
+        for v in vals_bits[1:]:
+            acc = iop64(op, dtype, acc, v & m)
+        return acc
     acc = vals_bits[0] & 0xFFFFFFFF
     for v in vals_bits[1:]:
         acc = iop(op, dtype, acc, v & 0xFFFFFFFF)

@@ -30,9 +30,17 @@ import numpy as np
 import brute
 
 GOLDEN = Path(__file__).resolve().parent / "golden"
-NP = {"f32": np.float32, "bf16": np.uint16, "i32": np.int32, "u32": np.uint32}
+NP = {"f32": np.float32, "bf16": np.uint16, "i32": np.int32, "u32": np.uint32,
+      "f16": np.uint16, "e4m3": np.uint8, "e5m2": np.uint8, "i64": np.int64, "u64": np.uint64}
 DTYPES = ("f32", "bf16", "i32", "u32")
 OPS = ("sum", "prod", "max", "min")
+# the further element types and AVG (float types only)
+MORE_DTYPES = ("f16", "e4m3", "e5m2", "i64", "u64")
+FLOATS = ("f32", "bf16", "f16", "e4m3", "e5m2")
+
+
+def ops_for(dtype: str):
+    return OPS + ("avg",) if dtype in FLOATS else OPS
 
 F32_SPECIALS = [
     0x00000000, 0x80000000, 0x7F800000, 0xFF800000, 0x7F7FFFFF, 0xFF7FFFFF,
@@ -47,7 +55,7 @@ BF16_SPECIALS = [
 
 
 def _bits(a: np.ndarray) -> np.ndarray:
-    return a.view(np.uint32) if a.dtype.itemsize == 4 else a.view(np.uint16)
+    return a.view({1: np.uint8, 2: np.uint16, 4: np.uint32, 8: np.uint64}[a.dtype.itemsize])
 
 
 def _is_nan_bits(b: int, dtype: str) -> bool:
@@ -55,12 +63,18 @@ def _is_nan_bits(b: int, dtype: str) -> bool:
         return (b & 0x7F80) == 0x7F80 and (b & 0x7F) != 0
     if dtype == "f32":
         return brute.is_nan32(b)
+    if dtype == "f16":
+        return (b & 0x7C00) == 0x7C00 and (b & 0x3FF) != 0
+    if dtype == "e5m2":
+        return (b & 0x7C) == 0x7C and (b & 0x3) != 0
+    if dtype == "e4m3":
+        return (b & 0x7F) == 0x7F
     return False
 
 
 def _same(got: int, exp: int, dtype: str, op: str) -> bool:
-    """Bitwise equality, except that NaN payloads of sum/prod are unpinned."""
-    if dtype in ("f32", "bf16") and op in ("sum", "prod") and _is_nan_bits(exp, dtype):
+    """Bitwise equality, except that NaN payloads of sum/prod/avg are unpinned."""
+    if dtype in FLOATS and op in ("sum", "prod", "avg") and _is_nan_bits(exp, dtype):
         return _is_nan_bits(got, dtype)
     return got == exp
 
@@ -84,6 +98,29 @@ def random_column_values(rng, dtype: str, n: int) -> np.ndarray:
         pick = rng.integers(0, 4, size=n)
         return np.where(pick == 0, pool[rng.integers(0, pool.size, n)],
                         np.where(pick == 1, rb, np.where(pick == 2, near, tiny))).astype(np.uint16)
+    if dtype == "f16":
+        pool = np.array([0x0000, 0x8000, 0x7C00, 0xFC00, 0x7BFF, 0xFBFF, 0x0001, 0x8001, 0x03FF,
+                         0x0400, 0x3C00, 0xBC00, 0x3C01, 0x1400, 0x7E00, 0x7C01, 0x3800], np.uint16)
+        rb = rng.integers(0, 2**16, size=n, dtype=np.uint32).astype(np.uint16)
+        near = rng.standard_normal(n).astype(np.float16).view(np.uint16)
+        tiny = rng.integers(0, 0x0800, size=n, dtype=np.uint32).astype(np.uint16)
+        pick = rng.integers(0, 4, size=n)
+        return np.where(pick == 0, pool[rng.integers(0, pool.size, n)],
+                        np.where(pick == 1, rb, np.where(pick == 2, near, tiny))).astype(np.uint16)
+    if dtype in ("e4m3", "e5m2"):
+        # every byte is a value; weight small magnitudes so sums stay in range
+        rb = rng.integers(0, 256, size=n, dtype=np.uint32).astype(np.uint8)
+        mid = (rng.integers(0x20, 0x48, size=n, dtype=np.uint32).astype(np.uint8)
+               | (rng.integers(0, 2, size=n, dtype=np.uint32).astype(np.uint8) << 7))
+        return np.where(rng.integers(0, 2, size=n) == 0, rb, mid).astype(np.uint8)
+    if dtype in ("i64", "u64"):
+        sp = np.array([0, 1, 2**64 - 1, 2**63 - 1, 2**63, 2, 2**32, 2**32 - 1], np.uint64)
+        rb = rng.integers(0, 2**64, size=n, dtype=np.uint64)
+        small = rng.integers(0, 8, size=n, dtype=np.uint64)
+        pick = rng.integers(0, 3, size=n)
+        out = np.where(pick == 0, sp[rng.integers(0, sp.size, n)],
+                       np.where(pick == 1, rb, small)).astype(np.uint64)
+        return out.view(np.int64) if dtype == "i64" else out
     specials = np.array([0, 1, 0xFFFFFFFF, 0x7FFFFFFF, 0x80000000, 2, 0x10000], np.uint32)
     rb = rng.integers(0, 2**32, size=n, dtype=np.uint64).astype(np.uint32)
     small = rng.integers(0, 8, size=n, dtype=np.uint32)
@@ -427,10 +464,112 @@ def pin_sim_closed_forms(orc, n: int = 5003, seed: int = 29) -> None:
             [_is_nan_bits(int(v), "bf16") for v in y[nan]]), "G=2 ring vs rhd"
 
 
+# ------------------------------------------- further types and AVG --
+
+def pin_more_types_bruteforce(orc, seed: int = 31, ncols: int = 32,
+                              nsrc_list=(1, 2, 3, 5, 8)) -> None:
+    """fp16, fp8 e4m3/e5m2, int64, uint64 with every op, and AVG on every float
+    type, against the exact rational brute force."""
+    rng = np.random.default_rng(seed)
+    cases = [(d, o) for d in MORE_DTYPES for o in ops_for(d)] + [("f32", "avg"), ("bf16", "avg")]
+    for dtype, op in cases:
+        for P in nsrc_list:
+            srcs = [random_column_values(rng, dtype, ncols) for _ in range(P)]
+            got = _bits(orc.allreduce_local(srcs, dtype, op))
+            sb = [_bits(s) for s in srcs]
+            for i in range(ncols):
+                col = [int(s[i]) for s in sb]
+                exp = brute.reduce_column(col, dtype, op)
+                assert _same(int(got[i]), exp, dtype, op), (
+                    f"{dtype} {op} P={P} col={[hex(c) for c in col]} "
+                    f"got={int(got[i]):#x} exp={exp:#x}")
+
+
+def pin_narrow_vs_torch(orc, n_random: int = 1 << 16, seed: int = 37) -> None:
+    """Widening of every f16 / e4m3 / e5m2 pattern and narrowing of random and
+    boundary binary32 patterns against PyTorch's CPU conversions.  They agree
+    everywhere except e4m3 overflow, where PyTorch gives NaN and the definition
+    saturates at +-448 (checked separately: every |x| >= 448 gives 448)."""
+    import torch
+    tt = {"f16": torch.float16, "e4m3": torch.float8_e4m3fn, "e5m2": torch.float8_e5m2}
+    rng = np.random.default_rng(seed)
+    bits = np.concatenate([
+        rng.integers(0, 2**32, n_random, dtype=np.uint64).astype(np.uint32),
+        rng.integers(0x30000000, 0x48000000, n_random, dtype=np.uint64).astype(np.uint32),
+        np.arange(0, 1 << 16, dtype=np.uint32) << 16 | 0x8000,      # exact ties
+        np.arange(0, 1 << 16, dtype=np.uint32) << 16]).astype(np.uint32)
+    f = bits.view(np.float32)
+    for dt, t in tt.items():
+        itemsize = 2 if dt == "f16" else 1
+        pats = np.arange(1 << (8 * itemsize), dtype=np.uint64).astype(NP[dt])
+        wide = orc.small_to_f32_bits(pats, dt)
+        ref = torch.from_numpy(pats.view(np.int16) if itemsize == 2 else pats).view(t)
+        ref = ref.float().numpy().view(np.uint32)
+        nan = np.isnan(ref.view(np.float32))
+        assert np.array_equal(np.isnan(wide.view(np.float32)), nan), f"{dt} widening NaN set"
+        assert np.array_equal(wide[~nan], ref[~nan]), f"{dt} widening"
+        got = orc.f32_bits_to_small(bits, dt)
+        tr = torch.from_numpy(f.copy()).to(t)
+        exp = (tr.view(torch.int16).numpy().view(np.uint16) if itemsize == 2
+               else tr.view(torch.uint8).numpy())
+        keep = ~np.isnan(f)
+        if dt == "e4m3":
+            over = np.abs(f) >= 448.0
+            assert np.all(got[over & keep] == np.where(np.signbit(f[over & keep]), 0xFE, 0x7E)), \
+                "e4m3 saturation"
+            keep &= ~over
+        assert np.array_equal(got[keep], exp[keep]), f"{dt} narrowing"
+        gn = got[np.isnan(f)]
+        assert all(_is_nan_bits(int(v), dt) for v in gn), f"{dt} NaN stays NaN"
+
+
+def pin_more_types_closed_forms(orc, n: int = 1 << 15, seed: int = 41) -> None:
+    """AVG of integer-valued inputs over a power-of-two P is the exact mean;
+    fp8 and fp16 sums of small integers are exact before the final rounding,
+    so they equal PyTorch's conversion of the int64 sum; int64/uint64 sums
+    and products wrap like numpy's 64-bit arithmetic; max/min are permutation
+    invariant."""
+    import torch
+    rng = np.random.default_rng(seed)
+    for P in (2, 4, 8):
+        ints = [rng.integers(-64, 65, size=n) for _ in range(P)]
+        tot = np.sum(np.stack(ints), axis=0)
+        got = orc.allreduce_local([x.astype(np.float32) for x in ints], "f32", "avg")
+        assert np.array_equal(got, (tot / P).astype(np.float32)), f"avg closed form P={P}"
+    for dt, t in (("f16", torch.float16), ("e4m3", torch.float8_e4m3fn),
+                  ("e5m2", torch.float8_e5m2)):
+        ints = [rng.integers(-8, 9, size=n) for _ in range(8)]
+        srcs = []
+        for x in ints:
+            tx = torch.from_numpy(x.astype(np.float32)).to(t)
+            srcs.append(tx.view(torch.int16).numpy().view(np.uint16) if dt == "f16"
+                        else tx.view(torch.uint8).numpy())
+        tot = torch.from_numpy(np.sum(np.stack(ints), axis=0).astype(np.float32)).to(t)
+        exp = (tot.view(torch.int16).numpy().view(np.uint16) if dt == "f16"
+               else tot.view(torch.uint8).numpy())
+        assert np.array_equal(orc.allreduce_local(srcs, dt, "sum"), exp), f"{dt} integer sums"
+    a = [rng.integers(-2**63, 2**63, size=n, dtype=np.int64) for _ in range(5)]
+    with np.errstate(over="ignore"):
+        assert np.array_equal(orc.allreduce_local(a, "i64", "sum"), np.sum(np.stack(a), axis=0))
+        assert np.array_equal(orc.allreduce_local(a, "i64", "prod"), np.prod(np.stack(a), axis=0))
+        u = [x.view(np.uint64) for x in a]
+        assert np.array_equal(orc.allreduce_local(u, "u64", "sum"), np.sum(np.stack(u), axis=0))
+    assert np.array_equal(orc.allreduce_local(a, "i64", "max"), np.max(np.stack(a), axis=0))
+    assert np.array_equal(orc.allreduce_local([x.view(np.uint64) for x in a], "u64", "min"),
+                          np.min(np.stack([x.view(np.uint64) for x in a]), axis=0))
+    for dt in ("f16", "e4m3", "e5m2"):
+        srcs = [random_column_values(rng, dt, 4096) for _ in range(6)]
+        for op in ("max", "min"):
+            ref = orc.allreduce_local(srcs, dt, op)
+            perm = [srcs[k] for k in rng.permutation(6)]
+            assert np.array_equal(orc.allreduce_local(perm, dt, op), ref), f"{dt} {op} order"
+
+
 def pin_selfcheck(orc) -> None:
     assert orc.selfcheck() == 0, "floating-point environment"
 
 
 FAST_PINS = [pin_selfcheck, pin_golden_reduce, pin_golden_bf16, pin_bf16_vs_brute,
              pin_up_bf16, pin_integer_closed_form, pin_int_mod32, pin_invariants,
-             pin_composition, pin_bruteforce, pin_sim_closed_forms, pin_sim_bruteforce]
+             pin_composition, pin_bruteforce, pin_sim_closed_forms, pin_sim_bruteforce,
+             pin_narrow_vs_torch, pin_more_types_closed_forms, pin_more_types_bruteforce]

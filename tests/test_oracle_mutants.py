@@ -49,12 +49,12 @@ MUTANTS = [
     ("step_final_writes_acc", "if (fin) down_float(dst, i, dtype, a);\n            else down_float(acc, i, XO_F32, a);",
      "down_float(acc, i, XO_F32, a);\n            if (fin) down_float(dst, i, dtype, a);", 1, ()),
     ("bf16_accumulates_in_bf16",
-     "acc = op_float(op, acc, up_float(srcs[p], off + i, dtype));",
-     "{ acc = op_float(op, acc, up_float(srcs[p], off + i, dtype)); "
+     "acc = op_float(fop, acc, up_float(srcs[p], off + i, dtype));",
+     "{ acc = op_float(fop, acc, up_float(srcs[p], off + i, dtype)); "
      "if (dtype == XO_BF16) acc = bf16_to_f32(f32_to_bf16(acc)); }", 1, ()),
     ("reverse_fold_order",
-     "for (int p = 1; p < nsrc; ++p)\n            acc = op_float(op, acc, up_float(srcs[p], off + i, dtype));",
-     "for (int p = nsrc - 2; p >= 0; --p)\n            acc = op_float(op, acc, up_float(srcs[p], off + i, dtype));",
+     "for (int p = 1; p < nsrc; ++p)\n            acc = op_float(fop, acc, up_float(srcs[p], off + i, dtype));",
+     "for (int p = nsrc - 2; p >= 0; --p)\n            acc = op_float(fop, acc, up_float(srcs[p], off + i, dtype));",
      1, ()),
     # simulated schedules
     ("ring_sendcopy_own_chunk", "const int c = mod_rank(r - 1, G);\n            memcpy(wire[r]",
@@ -72,6 +72,33 @@ MUTANTS = [
      1, ()),
     ("sim_chunks_unaligned", "return (m + XO_SIM_ALIGN - 1) / XO_SIM_ALIGN * XO_SIM_ALIGN;",
      "return m;", 1, ()),
+    # further types and AVG
+    ("narrow_ties_away", "if (rem > half || (rem == half && (n & 1u))) n += 1;",
+     "if (rem >= half) n += 1;", 1, ()),
+    ("narrow_flushes_subnormals", "if (n < (1ull << f->mbits)) return sbit | (uint32_t)n;",
+     "if (n < (1ull << f->mbits)) return sbit;", 1, ()),
+    ("e4m3_overflow_to_nan",
+     "const uint32_t overflow = f->has_inf ? (etop << f->mbits) : f->max_finite;",
+     "const uint32_t overflow = f->has_inf ? (etop << f->mbits) : f->qnan;", 1, ()),
+    ("e5m2_without_infinity", "FMT_E5M2 = {2, 5, 15, 1, 0x7Bu, 0x7Eu};",
+     "FMT_E5M2 = {2, 5, 15, 0, 0x7Bu, 0x7Eu};", 1, ()),
+    ("f16_wrong_bias", "FMT_F16 = {10, 5, 15, 1, 0x7BFFu, 0x7E00u};",
+     "FMT_F16 = {10, 5, 14, 1, 0x7BFFu, 0x7E00u};", 1, ()),
+    ("avg_divides_by_p_minus_1", "if (op == XO_AVG) acc = acc / (float)nsrc;",
+     "if (op == XO_AVG) acc = acc / (float)(nsrc > 1 ? nsrc - 1 : 1);", 1, ()),
+    ("avg_premultiplies",
+     "float acc = up_float(srcs[0], off + i, dtype);\n        for (int p = 1; p < nsrc; ++p)\n"
+     "            acc = op_float(fop, acc, up_float(srcs[p], off + i, dtype));\n"
+     "        if (op == XO_AVG) acc = acc / (float)nsrc;",
+     "const float sc = op == XO_AVG ? 1.0f / (float)nsrc : 1.0f;\n"
+     "        float acc = op == XO_AVG ? up_float(srcs[0], off + i, dtype) * sc : up_float(srcs[0], off + i, dtype);\n"
+     "        for (int p = 1; p < nsrc; ++p)\n"
+     "            acc = op_float(fop, acc, op == XO_AVG ? up_float(srcs[p], off + i, dtype) * sc : up_float(srcs[p], off + i, dtype));",
+     1, ()),
+    ("int64_truncated", "uint64_t acc = up_int64(srcs[0], off + i);",
+     "uint64_t acc = (uint32_t)up_int64(srcs[0], off + i);", 1, ()),
+    ("i64_max_unsigned", "if (dtype == XO_I64) return ((int64_t)a > (int64_t)b) ? a : b;",
+     "if (dtype == XO_I64) return a > b ? a : b;", 1, ()),
     # a fast-math build flushes subnormals (and loads code that sets FTZ/DAZ for
     # the whole process, which is why every mutant runs in a child process)
     ("fast_math_build", None, None, 0, ("-ffast-math",)),

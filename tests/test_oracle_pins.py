@@ -19,6 +19,15 @@ def test_bruteforce_wide(orc):
     pins.pin_bruteforce(orc, seed=101, ncols=64, nsrc_list=(4, 16, 33))
 
 
+def test_narrow_formats_vs_torch_wide(orc):
+    """fp16 / e4m3 / e5m2 conversions against PyTorch on 2 x 2^21 random patterns."""
+    pins.pin_narrow_vs_torch(orc, n_random=1 << 21, seed=43)
+
+
+def test_more_types_bruteforce_wide(orc):
+    pins.pin_more_types_bruteforce(orc, seed=47, ncols=48, nsrc_list=(4, 16, 33))
+
+
 def test_bf16_down_vs_torch(orc):
     """Every sign/exponent/high-mantissa half with each class of dropped bits,
     plus 2^20 random patterns, against PyTorch's CPU conversion."""
