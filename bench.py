@@ -35,12 +35,17 @@ sys.path.insert(0, str(ROOT))
 METRIC = "reduce-copy GB/s (read+write) and % HBM peak at 1 GPU; small-msg µs/call"
 HBM_PEAK_GBS = 8000.0     # MI355X HBM3E, published
 CSRC = "paper_2510_20171_amd/csrc/"
+_COMMON = [CSRC + "xred_device.hpp", CSRC + "xred_kernels.hpp", CSRC + "xred_dispatch.hpp"]
 KERNEL_SOURCES = {
-    "reduce": [CSRC + "xred_device.hpp", CSRC + "xred_kernels.hpp", CSRC + "xred_reduce.hip"],
-    "step": [CSRC + "xred_device.hpp", CSRC + "xred_kernels.hpp", CSRC + "xred_step.hip"],
-    "batched": [CSRC + "xred_device.hpp", CSRC + "xred_kernels.hpp", CSRC + "xred_batched.hip"],
-    "ring": [CSRC + "xred_device.hpp", CSRC + "xred_kernels.hpp", CSRC + "xred_ring.hip"],
-    "sim": [CSRC + "xred_device.hpp", CSRC + "xred_kernels.hpp", CSRC + "xred_sim.hip"],
+    "reduce": _COMMON + [CSRC + f for f in ("xred_reduce.hpp", "xred_reduce.hip",
+                                           "xred_reduce_float.hip", "xred_reduce_fp8.hip",
+                                           "xred_reduce_int.hip")],
+    "step": _COMMON + [CSRC + "xred_step.hip"],
+    "batched": _COMMON + [CSRC + f for f in ("xred_batched.hpp", "xred_batched.hip",
+                                            "xred_batched_float.hip", "xred_batched_fp8.hip",
+                                            "xred_batched_int.hip")],
+    "ring": _COMMON + [CSRC + "xred_ring.hip"],
+    "sim": _COMMON + [CSRC + "xred_sim.hip"],
 }
 
 
@@ -149,6 +154,8 @@ def dev_any(torch, a, dtype):
     if dtype == "bf16":
         return dev_bf16(torch, a)
     if dtype == "f32":
+        return torch.from_numpy(a).to("cuda")
+    if dtype == "e4m3":
         return torch.from_numpy(a).to("cuda")
     return torch.from_numpy(a.view(np.int32)).to("cuda")
 
@@ -373,6 +380,32 @@ def secondary(torch, xr, L, timer, wl, flush):
     res["cu_budget_p8_bf16_8MiB_GBs"] = curve
     del d, out
 
+    # further element types and AVG at the gradient-bucket footprint: P=8
+    # sources of 128 MiB each (random bytes; fp8 bytes masked to finite values)
+    more = {}
+    for dt, es, op in (("f16", 2, "sum"), ("e4m3", 1, "sum"), ("e5m2", 1, "sum"),
+                       ("i64", 8, "sum"), ("bf16", 2, "avg"), ("f32", 4, "avg")):
+        n = (128 << 20) // es
+        d = []
+        for _ in range(8):
+            x = torch.randint(0, 256, (n * es,), dtype=torch.uint8, device="cuda")
+            if dt in ("e4m3", "e5m2"):
+                x &= 0x3F if dt == "e4m3" else 0x3B     # finite magnitudes below 1
+            elif dt in ("f16", "bf16", "f32"):
+                x.view(torch.int16 if es == 2 else torch.int32).bitwise_and_(
+                    0x3BFF if dt == "f16" else (0x3F7F if dt == "bf16" else 0x3F7FFFFF))
+            d.append(x)
+        out = torch.empty_like(d[0])
+        arr = xr._lib.ptr_array([x.data_ptr() for x in d])
+        stream = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+        fn = (lambda a=arr, o=out, nn=n, t=xr.DTYPE[dt], oo=xr.OP[op]:
+              L.xred_allreduce_local(a, 8, ctypes.c_void_p(o.data_ptr()), nn, t, oo, stream))
+        ms = timer.loop_ms(fn, 20)
+        more[f"{dt}_{op}_p8_128MiB"] = {"us": round(ms * 1e3, 2),
+                                        "GBs": round(9 * n * es / ms / 1e6, 1)}
+        del d, out
+    res["more_types"] = more
+
     # simulated AllReduce schedules on one GPU: 8 ranks, ring and halving-doubling,
     # at the bucket size and at 1 MiB per rank
     sim = {}
@@ -570,7 +603,7 @@ def main() -> int:
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="c2",
-                    choices=["c1", "c2", "c3", "c3ring", "c4", "c5a", "c5b", "sim"],
+                    choices=["c1", "c2", "c3", "c3ring", "c4", "c5a", "c5b", "c2fp8", "sim"],
                     help="which workload one step runs (default: the c2 gradient bucket)")
     ap.add_argument("--no-secondary", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -622,8 +655,10 @@ def main() -> int:
                     "p90_us": pct(single, 0.9), "cold_p50_us": pct(cold, 0.5),
                     "cold_p90_us": pct(cold, 0.9)}
 
-    config = dict(wk["config"], accumulate="f32" if wk["config"].get("io_dtype") in ("bf16", "f32")
-                  else "u32", alg_bytes_per_step=ab, parallelism="single GPU")
+    io = wk["config"].get("io_dtype")
+    acc = ("f32" if io in ("bf16", "f32", "f16", "e4m3", "e5m2")
+           else "u64" if io in ("i64", "u64") else "u32")
+    config = dict(wk["config"], accumulate=acc, alg_bytes_per_step=ab, parallelism="single GPU")
     result = {
         "metric": METRIC, "value": round(gbs, 1), "unit": "GB/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 5),

@@ -16,19 +16,25 @@
  *
  *   - a LEFT fold in source order 0..P-1 (the order is fixed, so float
  *     results are deterministic and bit-reproducible);
- *   - up(): bf16 -> binary32 (exact), fp32 -> binary32, int32/uint32 -> uint32;
- *     the accumulator is binary32 for float types and uint32 for integer types;
+ *   - up(): bf16, fp16, fp8 e4m3 / e5m2 -> binary32 (exact), fp32 -> binary32,
+ *     int32/uint32 -> uint32, int64/uint64 -> uint64; the accumulator is
+ *     binary32 for float types and uint32 / uint64 for integer types;
  *   - (+): XRED_SUM  binary32 add (round to nearest even, subnormals kept) or
- *                    addition modulo 2^32;
- *          XRED_PROD binary32 multiply, or the low 32 bits of the product;
+ *                    addition modulo 2^32 / 2^64;
+ *          XRED_PROD binary32 multiply, or the low 32 / 64 bits of the product;
  *          XRED_MAX / XRED_MIN  float: total order -inf < ... < -0 < +0 < ...
  *                    < +inf; a NaN among the reduced values gives the quiet
  *                    NaN 0x7FC00000 (also for P = 1 and the INIT step);
- *                    int32 signed, uint32 unsigned;
+ *                    int32/int64 signed, uint32/uint64 unsigned;
+ *          XRED_AVG  (float types only) the XRED_SUM fold, then one binary32
+ *                    division by P, rounded to nearest even;
  *   - the accumulator starts from up(src[0][i]) (never from zero), so a column
  *     of -0.0 sums to -0.0;
- *   - down(): binary32 -> bf16 round to nearest even (overflow to +-inf),
- *     identity otherwise.  NaN payloads of SUM/PROD results are unspecified.
+ *   - down(): binary32 -> bf16 / fp16 / e5m2 round to nearest even with
+ *     subnormals and overflow to +-inf; binary32 -> e4m3 (OCP "FN": no
+ *     infinity, largest finite 448) round to nearest even, saturating at
+ *     +-448 on overflow and for infinities; identity otherwise.  NaN stays
+ *     NaN; NaN payloads of SUM/PROD/AVG results are unspecified.
  *
  * Conventions shared by every call:
  *   - All functions are thread-safe, never print and never abort.
@@ -60,12 +66,18 @@ extern "C" {
 typedef enum {
     XRED_FLOAT32 = 0,
     XRED_BFLOAT16 = 1,
-    XRED_FLOAT16 = 2,   /* reserved: currently returns XRED_UNSUPPORTED */
+    XRED_FLOAT16 = 2,   /* IEEE binary16 */
     XRED_INT32 = 3,
-    XRED_UINT32 = 4
+    XRED_UINT32 = 4,
+    XRED_INT64 = 5,
+    XRED_UINT64 = 6,
+    XRED_FP8_E4M3 = 7,  /* OCP 8-bit E4M3 ("FN"), saturating */
+    XRED_FP8_E5M2 = 8   /* OCP 8-bit E5M2 */
 } xred_dtype;
 
-typedef enum { XRED_SUM = 0, XRED_PROD = 1, XRED_MAX = 2, XRED_MIN = 3 } xred_op;
+/* XRED_AVG: float types only, and only where the whole reduction happens in
+ * one call (fused, reduce-scatter and batched); elsewhere XRED_UNSUPPORTED. */
+typedef enum { XRED_SUM = 0, XRED_PROD = 1, XRED_MAX = 2, XRED_MIN = 3, XRED_AVG = 4 } xred_op;
 
 typedef enum {
     XRED_SUCCESS = 0,
@@ -130,8 +142,10 @@ XRED_API xred_status xred_reduce_scatter_local(const void *const *srcs, int nsrc
  *   INIT | FINAL             dst[i] = down(up(in[i]))              (acc unused)
  *   in       count elements of dtype
  *   acc      count accumulator elements of xred_acc_elem_size(dtype) bytes
- *            (binary32 for float dtypes, uint32 for integer dtypes), 4-byte
- *            aligned; may be NULL only for INIT|FINAL
+ *            (binary32 for float dtypes, uint32 / uint64 for 32- / 64-bit
+ *            integer dtypes), aligned to that size; may be NULL only for
+ *            INIT|FINAL
+ *   op       not XRED_AVG (a step does not know P; use XRED_SUM and divide)
  *   dst      count elements of dtype, used only with FINAL (may be NULL otherwise)
  * Buffers must not overlap, except dst == in exactly.
  * Errors: XRED_INVALID_ARGUMENT (unknown flag bits, NULL/misaligned pointer,
@@ -263,7 +277,8 @@ XRED_API size_t xred_sim_chunk(size_t count, int nranks);
  */
 XRED_API unsigned xred_set_max_workgroups(unsigned max_workgroups);
 
-/* Bytes per accumulator element for dtype: 4 (binary32 or uint32), 0 if unknown. */
+/* Bytes per accumulator element for dtype: 4 (binary32 or uint32), 8 (uint64
+ * for int64/uint64), 0 if unknown. */
 XRED_API size_t xred_acc_elem_size(xred_dtype dtype);
 
 /* Static, human-readable name of a status code. */

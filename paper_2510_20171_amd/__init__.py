@@ -10,9 +10,11 @@ current HIP stream of the tensor's device is used unless one is given.
     out = torch.empty_like(srcs[0])
     xr.allreduce_local(srcs, out)                     # out = srcs[0] + ... + srcs[7]
 
-Element types are taken from the tensors (float32, bfloat16, int32, uint32)
-or forced with ``dtype=`` ("f32", "bf16", "i32", "u32"), e.g. to treat int32
-storage as uint32.
+Element types are taken from the tensors (float32, bfloat16, float16,
+float8_e4m3fn, float8_e5m2, int32, uint32, int64, uint64) or forced with
+``dtype=`` ("f32", "bf16", "f16", "e4m3", "e5m2", "i32", "u32", "i64",
+"u64"), e.g. to treat int32 storage as uint32.  Ops: "sum", "prod", "max",
+"min" and, for float types where the whole fold is one call, "avg".
 """
 from __future__ import annotations
 
@@ -31,9 +33,11 @@ __all__ = ["allreduce_local", "reduce_scatter_local", "reduce_copy_step", "acc_c
 def _torch_dtype_name(t) -> str:
     import torch
     m = {torch.float32: "f32", torch.bfloat16: "bf16", torch.int32: "i32",
-         torch.float16: "f16"}
-    if hasattr(torch, "uint32"):
-        m[torch.uint32] = "u32"
+         torch.float16: "f16", torch.int64: "i64"}
+    for name, code in (("uint32", "u32"), ("uint64", "u64"), ("float8_e4m3fn", "e4m3"),
+                       ("float8_e5m2", "e5m2")):
+        if hasattr(torch, name):
+            m[getattr(torch, name)] = code
     try:
         return m[t.dtype]
     except KeyError:

@@ -12,6 +12,7 @@ into paper_2510_20171_amd/libxred.so.  Flags:
 """
 from __future__ import annotations
 
+import os
 import subprocess
 import sys
 from concurrent.futures import ThreadPoolExecutor
@@ -42,13 +43,15 @@ def _run(cmd):
         print(err, file=sys.stderr)
 
 
-def build(jobs: int = 4, verbose: bool = False) -> Path:
+def build(jobs: int = 0, verbose: bool = False) -> Path:
     """Compile every csrc/*.hip and link libxred.so; returns its path."""
     BUILD.mkdir(exist_ok=True)
     sources = sorted(CSRC.glob("*.hip"))
     objs = [BUILD / (s.stem + ".o") for s in sources]
     cmds = [[HIPCC, *HIPFLAGS, "-c", str(s), "-o", str(o)] for s, o in zip(sources, objs)]
-    with ThreadPoolExecutor(max_workers=max(1, jobs)) as ex:
+    if jobs <= 0:
+        jobs = min(16, os.cpu_count() or 4)
+    with ThreadPoolExecutor(max_workers=jobs) as ex:
         list(ex.map(_run, cmds))
     tmp = OUT.with_suffix(".so.tmp")
     _run([HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", *map(str, objs), "-o", str(tmp)])

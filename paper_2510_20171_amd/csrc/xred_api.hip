@@ -37,8 +37,21 @@ xred_status hip_fail(hipError_t e, const char *what)
     return fail(XRED_HIP_ERROR, "%s: %s", what, hipGetErrorString(e));
 }
 
-bool known_dtype(xred_dtype d) { return d >= XRED_FLOAT32 && d <= XRED_UINT32; }
-bool known_op(xred_op o) { return o >= XRED_SUM && o <= XRED_MIN; }
+bool known_dtype(xred_dtype d) { return d >= XRED_FLOAT32 && d <= XRED_FP8_E5M2; }
+bool known_op(xred_op o) { return o >= XRED_SUM && o <= XRED_AVG; }
+
+// Entry points whose kernels see only part of the fold (one step, a chunk at
+// a time, or a hop) cannot divide by P: AVG is unsupported there.
+xred_status check_no_avg(xred_op op, const char *entry)
+{
+    if (op == XRED_AVG)
+        return fail(XRED_UNSUPPORTED, "%s does not support XRED_AVG (it never sees the whole fold)",
+                    entry);
+    return XRED_SUCCESS;
+}
+
+// Accumulator element bytes: uint64 for 64-bit integers, else 4.
+size_t acc_size(xred_dtype d) { return d == XRED_INT64 || d == XRED_UINT64 ? 8 : 4; }
 
 // Checks shared by every entry point on dtype and op.
 xred_status check_types(xred_dtype dtype, xred_op op)
@@ -303,9 +316,10 @@ uint64_t wall_ticks_per_us()
 
 bool supported(xred_dtype dtype, xred_op op)
 {
-    return (dtype == XRED_FLOAT32 || dtype == XRED_BFLOAT16 || dtype == XRED_INT32 ||
-            dtype == XRED_UINT32) &&
-           known_op(op);
+    const bool is_float = dtype == XRED_FLOAT32 || dtype == XRED_BFLOAT16 ||
+                          dtype == XRED_FLOAT16 || dtype == XRED_FP8_E4M3 ||
+                          dtype == XRED_FP8_E5M2;
+    return known_dtype(dtype) && known_op(op) && (op != XRED_AVG || is_float);
 }
 
 size_t elem_size(xred_dtype dtype)
@@ -313,6 +327,8 @@ size_t elem_size(xred_dtype dtype)
     switch (dtype) {
     case XRED_FLOAT32: case XRED_INT32: case XRED_UINT32: return 4;
     case XRED_BFLOAT16: case XRED_FLOAT16: return 2;
+    case XRED_INT64: case XRED_UINT64: return 8;
+    case XRED_FP8_E4M3: case XRED_FP8_E5M2: return 1;
     default: return 0;
     }
 }
@@ -385,15 +401,16 @@ XRED_API xred_status xred_reduce_copy_step(const void *in, void *acc, void *dst,
         return fail(XRED_INVALID_ARGUMENT, "unknown flag bits 0x%x", flags);
     xred_status st = check_types(dtype, op);
     if (st != XRED_SUCCESS) return st;
+    if ((st = check_no_avg(op, "xred_reduce_copy_step")) != XRED_SUCCESS) return st;
     if (count == 0) return XRED_SUCCESS;
-    const size_t es = elem_size(dtype);
-    if (mul_overflows(count, 4)) return fail(XRED_INVALID_ARGUMENT, "count * 4 overflows");
-    const size_t bytes = count * es, acc_bytes = count * 4;
+    const size_t es = elem_size(dtype), as = acc_size(dtype);
+    if (mul_overflows(count, as)) return fail(XRED_INVALID_ARGUMENT, "count * %zu overflows", as);
+    const size_t bytes = count * es, acc_bytes = count * as;
     const bool uses_acc = flags != (XRED_STEP_INIT | XRED_STEP_FINAL);
     const bool uses_dst = (flags & XRED_STEP_FINAL) != 0;
     if ((st = check_buf(in, bytes, es, "in", 0)) != XRED_SUCCESS) return st;
     if (uses_acc) {
-        if ((st = check_buf(acc, acc_bytes, 4, "acc", 0)) != XRED_SUCCESS) return st;
+        if ((st = check_buf(acc, acc_bytes, as, "acc", 0)) != XRED_SUCCESS) return st;
         if (bad_overlap(acc, acc_bytes, in, bytes, false))
             return fail(XRED_ALIAS, "acc overlaps in");
     }
@@ -415,11 +432,11 @@ XRED_API xred_status xred_acc_cast(const void *acc, void *dst, size_t count, xre
     xred_status st = check_types(dtype, XRED_SUM);
     if (st != XRED_SUCCESS) return st;
     if (count == 0) return XRED_SUCCESS;
-    const size_t es = elem_size(dtype);
-    if (mul_overflows(count, 4)) return fail(XRED_INVALID_ARGUMENT, "count * 4 overflows");
-    if ((st = check_buf(acc, count * 4, 4, "acc", 0)) != XRED_SUCCESS) return st;
+    const size_t es = elem_size(dtype), as = acc_size(dtype);
+    if (mul_overflows(count, as)) return fail(XRED_INVALID_ARGUMENT, "count * %zu overflows", as);
+    if ((st = check_buf(acc, count * as, as, "acc", 0)) != XRED_SUCCESS) return st;
     if ((st = check_buf(dst, count * es, es, "dst", 0)) != XRED_SUCCESS) return st;
-    if (bad_overlap(acc, count * 4, dst, count * es, false))
+    if (bad_overlap(acc, count * as, dst, count * es, false))
         return fail(XRED_ALIAS, "dst overlaps acc");
     const hipError_t e =
         launch_acc_cast(dtype, (const char *)acc, (char *)dst, count, (hipStream_t)hip_stream);
@@ -458,6 +475,7 @@ XRED_API xred_status xred_ring_reduce(const void *const *chunks, int nchunks, vo
         return fail(XRED_INVALID_ARGUMENT, "nchunks = %d outside 1..%d", nchunks, XRED_MAX_SRC);
     xred_status st = check_types(dtype, op);
     if (st != XRED_SUCCESS) return st;
+    if ((st = check_no_avg(op, "xred_ring_reduce")) != XRED_SUCCESS) return st;
     if (count == 0) return XRED_SUCCESS;
     if (chunks == nullptr) return fail(XRED_INVALID_ARGUMENT, "chunks is NULL");
     const size_t es = elem_size(dtype);
@@ -490,7 +508,7 @@ XRED_API xred_status xred_ring_reduce(const void *const *chunks, int nchunks, vo
 
 XRED_API size_t xred_ring_max_count(xred_dtype dtype)
 {
-    return known_dtype(dtype) && dtype != XRED_FLOAT16 ? (size_t)ring_max_count(dtype) : 0;
+    return known_dtype(dtype) ? (size_t)ring_max_count(dtype) : 0;
 }
 
 XRED_API xred_status xred_allreduce_sim(const void *const *sendbufs, void *const *recvbufs,
@@ -506,6 +524,7 @@ XRED_API xred_status xred_allreduce_sim(const void *const *sendbufs, void *const
                     nranks);
     xred_status st = check_types(dtype, op);
     if (st != XRED_SUCCESS) return st;
+    if ((st = check_no_avg(op, "xred_allreduce_sim")) != XRED_SUCCESS) return st;
     if (count == 0) return XRED_SUCCESS;
     if (sendbufs == nullptr || recvbufs == nullptr)
         return fail(XRED_INVALID_ARGUMENT, "sendbufs or recvbufs is NULL");
@@ -542,7 +561,7 @@ XRED_API unsigned xred_set_max_workgroups(unsigned max_workgroups)
 
 XRED_API size_t xred_acc_elem_size(xred_dtype dtype)
 {
-    return known_dtype(dtype) ? 4 : 0;
+    return known_dtype(dtype) ? acc_size(dtype) : 0;
 }
 
 XRED_API const char *xred_status_string(xred_status s)

@@ -1,445 +1,48 @@
-// xred_batched.hip -- many independent reductions in one launch.
-//
-// Small messages are dominated by per-call overhead (the T_c term of the
-// LogP model in Section 6.2), so a batch of K reductions is run as one
-// kernel.  Work is cut into tiles of kB*kU 16-byte vectors of one item;
-// the global tile sequence (item 0's tiles, then item 1's, ...) is split
-// into one contiguous range per workgroup, so each workgroup walks forward
-// through consecutive items and reads each descriptor once.
-//
-// Two ways to find a workgroup's range:
-//   planned  (host descriptors): the host computes each workgroup's first
-//            item, first tile and tile count and stages them with the items;
-//   device   (XRED_ITEMS_ON_DEVICE): descriptors are read only when the
-//            kernel runs (metadata by reference, Section 6.1), so every
-//            workgroup sums the tile counts itself (an LDS scan over the
-//            descriptors), then locates its first tile.  No state is kept
-//            between calls, so the kernel can be captured in a graph.
-
-#include "xred_internal.hpp"
-#include "xred_kernels.hpp"
+// xred_batched.hip -- many independent reductions in one launch: the entry
+// points used by the C ABI, dispatching to the kernels of the element type's
+// group (xred_batched_float.hip, xred_batched_fp8.hip, xred_batched_int.hip).
+#include "xred_batched.hpp"
 
 namespace xred {
+
+uint64_t batched_tile_elems(xred_dtype dtype)
+{
+    uint64_t n = 0;
+    (void)with_dtype(dtype, [&](auto t) {
+        n = tile_elems<decltype(t)>();
+        return hipSuccess;
+    });
+    return n;
+}
+
 namespace {
 
-constexpr int kU = 1;     // vectors per thread in one pass over a sub-tile
-constexpr int kB = 512;
-// Sub-tiles of kB*kU vectors per tile: two halve the per-tile descriptor
-// work (measured +5-6 % on batches of large or equal items, neutral on the
-// log-uniform 4096-item batch); four were no better.
-constexpr int kSub = 2;
-
-template <class T>
-constexpr uint64_t tile_vecs() { return (uint64_t)kB * kU * kSub; }
-template <class T>
-constexpr uint64_t tile_elems() { return tile_vecs<T>() * T::kVec; }
-constexpr uint32_t kTileBytes = (uint32_t)kB * kU * kSub * 16u;
-constexpr uint32_t kSubBytes = (uint32_t)kB * kU * 16u;
-
-__device__ __forceinline__ bool item_runnable(const xred_item &it)
+hipError_t range_dispatch(xred_dtype dtype, xred_op op, bool planned, const xred_item *d_items,
+                          int nitems, const WgStart *d_wg, unsigned grid, hipStream_t s)
 {
-    return it.nsrc >= 1 && it.nsrc <= XRED_MAX_SRC && it.reserved == 0 && it.srcs != nullptr &&
-           it.dst != nullptr;
-}
-
-template <class T, bool CHECK>
-__device__ __forceinline__ uint64_t item_tiles(const xred_item &it)
-{
-    if (CHECK && !item_runnable(it)) return 0;
-    return (it.count + tile_elems<T>() - 1) / tile_elems<T>();
-}
-
-// Descriptor of item k, loaded field by field with scalar loads.
-__device__ __forceinline__ xred_item load_item(const xred_item *items, uint64_t k)
-{
-    const xred_item *p = items + k;
-    xred_item it;
-    it.srcs = sload(&p->srcs);
-    it.dst = sload(&p->dst);
-    it.count = sload(&p->count);
-    it.nsrc = sload(&p->nsrc);
-    it.reserved = sload(&p->reserved);
-    return it;
-}
-
-__device__ __forceinline__ uint64_t uniform64(uint64_t x)
-{
-    const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)x);
-    const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(x >> 32));
-    return ((uint64_t)hi << 32) | lo;
-}
-
-// Inclusive prefix sum over the workgroup; s[kB-1] holds the total until the
-// next call.
-__device__ uint64_t block_inclusive_scan(uint64_t v, uint64_t *s)
-{
-    __syncthreads();
-    s[threadIdx.x] = v;
-    __syncthreads();
-    for (int off = 1; off < kB; off <<= 1) {
-        const uint64_t t = threadIdx.x >= (unsigned)off ? s[threadIdx.x - off] : 0;
-        __syncthreads();
-        s[threadIdx.x] += t;
-        __syncthreads();
-    }
-    return s[threadIdx.x];
-}
-
-// Tile lt of one item.
-template <class T, class Op>
-__device__ void batched_tile(const xred_item &it, uint64_t lt)
-{
-    const char *const *sp = (const char *const *)it.srcs;
-    const int nsrc = (int)it.nsrc;
-    uintptr_t bits = (uintptr_t)it.dst;
-    bool null_src = false;
-    for (int p = 0; p < nsrc; ++p) {
-        const uintptr_t q = (uintptr_t)sload(sp + p);
-        bits |= q;
-        null_src |= q == 0;
-    }
-    if (null_src) return;
-    char *dst = (char *)it.dst;
-    const GlobalSrc src{sp};
-    const uint64_t count = it.count;
-    if ((bits & 15u) == 0) {
-        const size_t nvec = count / T::kVec;
-        const size_t vbytes = nvec * 16;
-        for (int h = 0; h < kSub; ++h) {
-            const size_t off = lt * kTileBytes + (size_t)h * kSubBytes;
-            if (off >= vbytes) break;
-            const Tile tl{off, tile_nrec(vbytes, off, kSubBytes)};
-            switch (nsrc) {
-            case 1: reduce_tile<T, Op, 1, kU, kB>(src, nsrc, dst, tl); break;
-            case 2: reduce_tile<T, Op, 2, kU, kB>(src, nsrc, dst, tl); break;
-            case 3: reduce_tile<T, Op, 3, kU, kB>(src, nsrc, dst, tl); break;
-            case 4: reduce_tile<T, Op, 4, kU, kB>(src, nsrc, dst, tl); break;
-            case 5: reduce_tile<T, Op, 5, kU, kB>(src, nsrc, dst, tl); break;
-            case 6: reduce_tile<T, Op, 6, kU, kB>(src, nsrc, dst, tl); break;
-            case 7: reduce_tile<T, Op, 7, kU, kB>(src, nsrc, dst, tl); break;
-            case 8: reduce_tile<T, Op, 8, kU, kB>(src, nsrc, dst, tl); break;
-            // more than 8 sources: the compact group loop (the pipelined
-            // 16/32/64 bodies would raise every batched kernel's register
-            // count and cut its occupancy)
-            default: reduce_tile<T, Op, 0, kU, kB>(src, nsrc, dst, tl); break;
-            }
-        }
-        // the item's last tile also takes the elements after its last full vector
-        if ((lt + 1) * tile_elems<T>() >= count) {
-            const uint32_t tail = (uint32_t)(count % T::kVec);
-            if (threadIdx.x < tail) reduce_elem<T, Op>(src, nsrc, dst, nvec * T::kVec + threadIdx.x);
-        }
-    } else {
-        const uint64_t e0 = lt * tile_elems<T>();
-        const uint64_t e1 = count < e0 + tile_elems<T>() ? count : e0 + tile_elems<T>();
-        for (uint64_t i = e0 + threadIdx.x; i < e1; i += kB) reduce_elem<T, Op>(src, nsrc, dst, i);
-    }
-}
-
-template <class T, class Op, bool PLANNED>
-__global__ __launch_bounds__(kB) void batched_kernel(const xred_item *items, int nitems,
-                                                         const WgStart *wg)
-{
-    __shared__ uint64_t s_scan[kB];
-    __shared__ uint64_t s_start[2];
-    uint64_t k, lt, left;
-    if constexpr (PLANNED) {
-        const WgStart *w = wg + blockIdx.x;
-        k = sload(&w->item);
-        lt = sload(&w->local_tile);
-        left = sload(&w->ntiles);
-    } else {
-        uint64_t mine = 0;
-        for (int i = threadIdx.x; i < nitems; i += kB) mine += item_tiles<T, true>(items[i]);
-        block_inclusive_scan(mine, s_scan);
-        const uint64_t total = s_scan[kB - 1];
-        const uint64_t g0 = total * blockIdx.x / gridDim.x;
-        const uint64_t g1 = total * (blockIdx.x + 1) / gridDim.x;
-        if (g0 == g1) return;
-        left = g1 - g0;
-        // find the item holding global tile g0 (if none is found the walk
-        // below starts past the last item and does nothing)
-        if (threadIdx.x == 0) {
-            s_start[0] = (uint64_t)nitems;
-            s_start[1] = 0;
-        }
-        uint64_t base = 0;
-        for (int w0 = 0; w0 < nitems; w0 += kB) {
-            const int i = w0 + (int)threadIdx.x;
-            const uint64_t c = i < nitems ? item_tiles<T, true>(items[i]) : 0;
-            const uint64_t incl = block_inclusive_scan(c, s_scan);
-            const uint64_t excl = incl - c;
-            if (c > 0 && base + excl <= g0 && g0 < base + incl) {
-                s_start[0] = (uint64_t)i;
-                s_start[1] = g0 - base - excl;
-            }
-            const uint64_t wtot = s_scan[kB - 1];
-            __syncthreads();
-            if (base + wtot > g0) break;
-            base += wtot;
-        }
-        k = s_start[0];
-        lt = s_start[1];
-    }
-    k = uniform64(k);
-    lt = uniform64(lt);
-    left = uniform64(left);
-    while (left > 0 && k < (uint64_t)nitems) {
-        k = uniform64(k);
-        const xred_item it = load_item(items, k);
-        const uint64_t nt = item_tiles<T, !PLANNED>(it);
-        if (lt >= nt) {
-            ++k;
-            lt = 0;
-            continue;
-        }
-        batched_tile<T, Op>(it, lt);
-        ++lt;
-        --left;
-    }
-}
-
-// ------------------------------------------------------ round-robin variant --
-// Global tile g is processed by workgroup g mod G (G = the workgroups that fit
-// on the chip at once), so the tiles in flight form one moving window over
-// the batch, as in the fused kernel, instead of G scattered ranges.  Each
-// workgroup keeps the batch's tile-start prefix in LDS (copied from the host
-// plan, or computed by a block scan over device-resident descriptors), finds
-// the (item, tile) of each of its tiles by binary search in parallel, and
-// while one tile's loads are in flight fetches the next tile's descriptor and
-// source pointers with scalar loads.
-constexpr int kListMax = 1024;     // tiles a workgroup plans per pass
-constexpr int kRrMaxItems = 8192;  // items whose prefix fits the LDS budget
-
-struct TileDesc {
-    const char *p[8];         // sources 0..7 (valid below nsrc)
-    const char *const *srcs;  // the item's source array
-    char *dst;
-    uint64_t count;
-    uint64_t lt;              // tile within the item
-    uint32_t k;               // item
-    int nsrc;
-    bool fast;                // nsrc <= 8, no NULL source, all pointers 16-byte aligned
-};
-
-__device__ __forceinline__ void fetch_desc(TileDesc &d, const xred_item *items, const uint2 *s_list,
-                                           int j)
-{
-    const uint32_t k = __builtin_amdgcn_readfirstlane(s_list[j].x);
-    const uint32_t lt = __builtin_amdgcn_readfirstlane(s_list[j].y);
-    const xred_item *it = items + k;
-    d.k = k;
-    d.lt = lt;
-    d.srcs = (const char *const *)sload(&it->srcs);
-    d.dst = (char *)sload(&it->dst);
-    d.count = sload(&it->count);
-    d.nsrc = (int)sload(&it->nsrc);
-    uintptr_t bits = (uintptr_t)d.dst;
-    bool null_src = false;
-#pragma unroll
-    for (int q = 0; q < 8; ++q) {
-        d.p[q] = q < d.nsrc ? sload(d.srcs + q) : nullptr;
-        bits |= (uintptr_t)d.p[q];
-        null_src |= q < d.nsrc && d.p[q] == nullptr;
-    }
-    d.fast = d.nsrc <= 8 && !null_src && (bits & 15u) == 0;
-}
-
-template <class T, class Op, bool PLANNED>
-__global__ __launch_bounds__(kB) void batched_rr_kernel(const xred_item *items, int nitems,
-                                                        const uint32_t *tile_start)
-{
-    extern __shared__ uint2 s_dyn[];
-    __shared__ uint64_t s_scan[kB];
-    uint2 *s_list = s_dyn;                             // kListMax entries
-    uint32_t *s_pre = (uint32_t *)(s_dyn + kListMax);  // nitems + 1 entries
-    if constexpr (PLANNED) {
-        for (int i = threadIdx.x; i <= nitems; i += kB) s_pre[i] = tile_start[i];
-    } else {
-        uint64_t base = 0;
-        for (int w0 = 0; w0 < nitems; w0 += kB) {
-            const int i = w0 + (int)threadIdx.x;
-            const uint64_t c = i < nitems ? item_tiles<T, true>(items[i]) : 0;
-            const uint64_t incl = block_inclusive_scan(c, s_scan);
-            if (i < nitems) s_pre[i] = (uint32_t)(base + incl - c);
-            base += s_scan[kB - 1];
-        }
-        if (base >= 0xFFFFFFFFull) return;   // more tiles than the plan can index: run nothing
-        if (threadIdx.x == 0) s_pre[nitems] = (uint32_t)base;
-    }
-    __syncthreads();
-    const uint64_t total = s_pre[nitems];
-    const uint64_t G = gridDim.x;
-    for (uint64_t g0 = blockIdx.x; g0 < total; g0 += (uint64_t)kListMax * G) {
-        const uint64_t left = (total - g0 + G - 1) / G;
-        const int n = left < (uint64_t)kListMax ? (int)left : kListMax;
-        for (int j = threadIdx.x; j < n; j += kB) {
-            const uint64_t g = g0 + (uint64_t)j * G;
-            int lo = 0, hi = nitems;   // s_pre[lo] <= g < s_pre[hi]
-            while (hi - lo > 1) {
-                const int mid = (lo + hi) >> 1;
-                if (s_pre[mid] <= g) lo = mid;
-                else hi = mid;
-            }
-            s_list[j] = uint2{(uint32_t)lo, (uint32_t)(g - s_pre[lo])};
-        }
-        __syncthreads();
-        TileDesc cur, nxt;
-        fetch_desc(cur, items, s_list, 0);
-        for (int j = 0; j < n; ++j) {
-            // Issue the current tile's loads.  Straight-line code: sources
-            // beyond nsrc, and tiles not on the fast path, get a zero-length
-            // buffer range, so their loads return 0 without touching memory
-            // and their store is dropped.
-            const size_t nvec = cur.count / T::kVec;
-            const size_t vbytes = nvec * 16, toff = cur.lt * kTileBytes;
-            const uint32_t nrec = cur.fast && toff < vbytes ? tile_nrec(vbytes, toff, kTileBytes) : 0u;
-            u32x4 in[8][kSub];
-#pragma unroll
-            for (int q = 0; q < 8; ++q) {
-                const bool on = q < cur.nsrc;
-                const rsrc_t r = make_rsrc((on ? cur.p[q] : cur.dst) + toff, on ? nrec : 0u);
-#pragma unroll
-                for (int h = 0; h < kSub; ++h)
-                    in[q][h] = bload<kLoadStream>(r, (uint32_t)(h * kB + threadIdx.x) * 16u);
-            }
-            // fetch the next tile's descriptor while those loads are in flight
-            if (j + 1 < n) fetch_desc(nxt, items, s_list, j + 1);
-            // fold (unused sources skipped by a uniform select) and store
-            const rsrc_t w = make_rsrc(cur.dst + toff, nrec);
-#pragma unroll
-            for (int h = 0; h < kSub; ++h) {
-                typename T::Acc acc[T::kVec];
-                up_vec<T>(in[0][h], acc);
-#pragma unroll
-                for (int q = 1; q < 8; ++q) {
-                    const bool on = q < cur.nsrc;
-                    typename T::Acc b[T::kVec];
-                    up_vec<T>(in[q][h], b);
-#pragma unroll
-                    for (int e = 0; e < T::kVec; ++e) {
-                        const typename T::Acc c = combine<T, Op>(acc[e], b[e]);
-                        acc[e] = on ? c : acc[e];
-                    }
-                }
-                bstore<kStoreOut>(down_vec<T, Op>(acc), w, (uint32_t)(h * kB + threadIdx.x) * 16u);
-            }
-            if (cur.fast) {
-                if ((cur.lt + 1) * tile_elems<T>() >= cur.count) {
-                    const uint32_t tail = (uint32_t)(cur.count % T::kVec);
-                    if (threadIdx.x < tail)
-                        reduce_elem<T, Op>(GlobalSrc{cur.srcs}, cur.nsrc, cur.dst,
-                                           nvec * T::kVec + threadIdx.x);
-                }
-            } else {
-                batched_tile<T, Op>(load_item(items, cur.k), cur.lt);
-            }
-            cur = nxt;
-        }
-        __syncthreads();
-    }
-}
-
-constexpr size_t rr_lds_bytes(int nitems)
-{
-    return sizeof(uint2) * kListMax + sizeof(uint32_t) * ((size_t)nitems + 1);
-}
-
-template <class T, class Op>
-hipError_t go_rr(bool planned, const xred_item *d_items, int nitems, const uint32_t *d_tile_start,
-                 hipStream_t s)
-{
-    const void *fn = planned ? (const void *)batched_rr_kernel<T, Op, true>
-                             : (const void *)batched_rr_kernel<T, Op, false>;
-    const size_t lds = rr_lds_bytes(nitems);
-    int per_cu = 0;
-    hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, kB, lds);
-    if (e != hipSuccess) return e;
-    const unsigned grid = batched_rr_grid(per_cu > 0 ? per_cu : 1);
-    if (planned)
-        hipLaunchKernelGGL((batched_rr_kernel<T, Op, true>), dim3(grid), dim3(kB), lds, s,
-                           d_items, nitems, d_tile_start);
-    else
-        hipLaunchKernelGGL((batched_rr_kernel<T, Op, false>), dim3(grid), dim3(kB), lds, s,
-                           d_items, nitems, d_tile_start);
-    return hipGetLastError();
-}
-
-template <class T>
-hipError_t go_rr_op(xred_op op, bool planned, const xred_item *d_items, int nitems,
-                    const uint32_t *d_tile_start, hipStream_t s)
-{
-    switch (op) {
-    case XRED_SUM: return go_rr<T, OpSum>(planned, d_items, nitems, d_tile_start, s);
-    case XRED_PROD: return go_rr<T, OpProd>(planned, d_items, nitems, d_tile_start, s);
-    case XRED_MAX: return go_rr<T, OpMax>(planned, d_items, nitems, d_tile_start, s);
-    case XRED_MIN: return go_rr<T, OpMin>(planned, d_items, nitems, d_tile_start, s);
-    }
-    return hipErrorInvalidValue;
-}
-
-template <class T, class Op>
-hipError_t go(bool planned, const xred_item *d_items, int nitems, const WgStart *d_wg,
-              unsigned grid, hipStream_t s)
-{
-    if (planned)
-        hipLaunchKernelGGL((batched_kernel<T, Op, true>), dim3(grid), dim3(kB), 0, s, d_items,
-                           nitems, d_wg);
-    else
-        hipLaunchKernelGGL((batched_kernel<T, Op, false>), dim3(grid), dim3(kB), 0, s,
-                           d_items, nitems, d_wg);
-    return hipGetLastError();
-}
-
-template <class T>
-hipError_t go_op(xred_op op, bool planned, const xred_item *d_items, int nitems,
-                 const WgStart *d_wg, unsigned grid, hipStream_t s)
-{
-    switch (op) {
-    case XRED_SUM: return go<T, OpSum>(planned, d_items, nitems, d_wg, grid, s);
-    case XRED_PROD: return go<T, OpProd>(planned, d_items, nitems, d_wg, grid, s);
-    case XRED_MAX: return go<T, OpMax>(planned, d_items, nitems, d_wg, grid, s);
-    case XRED_MIN: return go<T, OpMin>(planned, d_items, nitems, d_wg, grid, s);
-    }
-    return hipErrorInvalidValue;
-}
-
-hipError_t dispatch(xred_dtype dtype, xred_op op, bool planned, const xred_item *d_items,
-                    int nitems, const WgStart *d_wg, unsigned grid, hipStream_t s)
-{
-    switch (dtype) {
-    case XRED_FLOAT32: return go_op<TF32>(op, planned, d_items, nitems, d_wg, grid, s);
-    case XRED_BFLOAT16: return go_op<TBF16>(op, planned, d_items, nitems, d_wg, grid, s);
-    case XRED_INT32: return go_op<TI32>(op, planned, d_items, nitems, d_wg, grid, s);
-    case XRED_UINT32: return go_op<TU32>(op, planned, d_items, nitems, d_wg, grid, s);
-    default: return hipErrorInvalidValue;
+    switch (group_of(dtype)) {
+    case TypeGroup::kFloat:
+        return launch_batched_range_float(dtype, op, planned, d_items, nitems, d_wg, grid, s);
+    case TypeGroup::kFp8:
+        return launch_batched_range_fp8(dtype, op, planned, d_items, nitems, d_wg, grid, s);
+    default:
+        return launch_batched_range_int(dtype, op, planned, d_items, nitems, d_wg, grid, s);
     }
 }
 
 }  // namespace
 
-uint64_t batched_tile_elems(xred_dtype dtype)
-{
-    switch (dtype) {
-    case XRED_BFLOAT16: return tile_elems<TBF16>();
-    case XRED_FLOAT32: return tile_elems<TF32>();
-    case XRED_INT32: return tile_elems<TI32>();
-    case XRED_UINT32: return tile_elems<TU32>();
-    default: return 0;
-    }
-}
-
 hipError_t launch_batched_planned(xred_dtype dtype, xred_op op, const xred_item *d_items,
                                   int nitems, const WgStart *d_wg, unsigned grid,
                                   hipStream_t stream)
 {
-    return dispatch(dtype, op, true, d_items, nitems, d_wg, grid, stream);
+    return range_dispatch(dtype, op, true, d_items, nitems, d_wg, grid, stream);
 }
 
 hipError_t launch_batched_device(xred_dtype dtype, xred_op op, const xred_item *d_items,
                                  int nitems, unsigned grid, hipStream_t stream)
 {
-    return dispatch(dtype, op, false, d_items, nitems, nullptr, grid, stream);
+    return range_dispatch(dtype, op, false, d_items, nitems, nullptr, grid, stream);
 }
 
 int batched_rr_max_items() { return kRrMaxItems; }
@@ -447,13 +50,13 @@ int batched_rr_max_items() { return kRrMaxItems; }
 hipError_t launch_batched_rr(xred_dtype dtype, xred_op op, const xred_item *d_items, int nitems,
                              const uint32_t *d_tile_start, hipStream_t stream)
 {
-    const bool planned = d_tile_start != nullptr;
-    switch (dtype) {
-    case XRED_FLOAT32: return go_rr_op<TF32>(op, planned, d_items, nitems, d_tile_start, stream);
-    case XRED_BFLOAT16: return go_rr_op<TBF16>(op, planned, d_items, nitems, d_tile_start, stream);
-    case XRED_INT32: return go_rr_op<TI32>(op, planned, d_items, nitems, d_tile_start, stream);
-    case XRED_UINT32: return go_rr_op<TU32>(op, planned, d_items, nitems, d_tile_start, stream);
-    default: return hipErrorInvalidValue;
+    switch (group_of(dtype)) {
+    case TypeGroup::kFloat:
+        return launch_batched_rr_float(dtype, op, d_items, nitems, d_tile_start, stream);
+    case TypeGroup::kFp8:
+        return launch_batched_rr_fp8(dtype, op, d_items, nitems, d_tile_start, stream);
+    default:
+        return launch_batched_rr_int(dtype, op, d_items, nitems, d_tile_start, stream);
     }
 }
 

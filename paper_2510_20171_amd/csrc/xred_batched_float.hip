@@ -1,0 +1,19 @@
+// xred_batched_float.hip -- batched-reduce kernels for fp32, bf16 and fp16.
+#include "xred_batched.hpp"
+
+namespace xred {
+
+hipError_t launch_batched_range_float(xred_dtype dtype, xred_op op, bool planned,
+                                 const xred_item *d_items, int nitems, const WgStart *d_wg,
+                                 unsigned grid, hipStream_t stream)
+{
+    return batched_group<TF32, TBF16, TF16>(dtype, op, planned, d_items, nitems, d_wg, grid, stream);
+}
+
+hipError_t launch_batched_rr_float(xred_dtype dtype, xred_op op, const xred_item *d_items,
+                              int nitems, const uint32_t *d_tile_start, hipStream_t stream)
+{
+    return batched_rr_group<TF32, TBF16, TF16>(dtype, op, d_items, nitems, d_tile_start, stream);
+}
+
+}  // namespace xred

@@ -1,0 +1,19 @@
+// xred_batched_fp8.hip -- batched-reduce kernels for fp8 e4m3 and e5m2.
+#include "xred_batched.hpp"
+
+namespace xred {
+
+hipError_t launch_batched_range_fp8(xred_dtype dtype, xred_op op, bool planned,
+                                 const xred_item *d_items, int nitems, const WgStart *d_wg,
+                                 unsigned grid, hipStream_t stream)
+{
+    return batched_group<TE4M3, TE5M2>(dtype, op, planned, d_items, nitems, d_wg, grid, stream);
+}
+
+hipError_t launch_batched_rr_fp8(xred_dtype dtype, xred_op op, const xred_item *d_items,
+                              int nitems, const uint32_t *d_tile_start, hipStream_t stream)
+{
+    return batched_rr_group<TE4M3, TE5M2>(dtype, op, d_items, nitems, d_tile_start, stream);
+}
+
+}  // namespace xred

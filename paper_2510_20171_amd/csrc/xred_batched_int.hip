@@ -1,0 +1,19 @@
+// xred_batched_int.hip -- batched-reduce kernels for int32, uint32, int64 and uint64.
+#include "xred_batched.hpp"
+
+namespace xred {
+
+hipError_t launch_batched_range_int(xred_dtype dtype, xred_op op, bool planned,
+                                 const xred_item *d_items, int nitems, const WgStart *d_wg,
+                                 unsigned grid, hipStream_t stream)
+{
+    return batched_group<TI32, TU32, TI64, TU64>(dtype, op, planned, d_items, nitems, d_wg, grid, stream);
+}
+
+hipError_t launch_batched_rr_int(xred_dtype dtype, xred_op op, const xred_item *d_items,
+                              int nitems, const uint32_t *d_tile_start, hipStream_t stream)
+{
+    return batched_rr_group<TI32, TU32, TI64, TU64>(dtype, op, d_items, nitems, d_tile_start, stream);
+}
+
+}  // namespace xred

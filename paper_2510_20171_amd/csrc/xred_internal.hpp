@@ -25,6 +25,13 @@ size_t elem_size(xred_dtype dtype);
 // dst[i] = fold_p srcs[p][i], i < count.  srcs already include any shard offset.
 hipError_t launch_reduce(xred_dtype dtype, xred_op op, const char *const *srcs, int nsrc,
                          char *dst, size_t count, hipStream_t stream);
+// The same per group of element types (each in its own translation unit).
+hipError_t launch_reduce_float(xred_dtype dtype, xred_op op, const char *const *srcs, int nsrc,
+                               char *dst, size_t count, hipStream_t stream);
+hipError_t launch_reduce_fp8(xred_dtype dtype, xred_op op, const char *const *srcs, int nsrc,
+                             char *dst, size_t count, hipStream_t stream);
+hipError_t launch_reduce_int(xred_dtype dtype, xred_op op, const char *const *srcs, int nsrc,
+                             char *dst, size_t count, hipStream_t stream);
 
 hipError_t launch_step(xred_dtype dtype, xred_op op, unsigned flags, const char *in, char *acc,
                        char *dst, size_t count, hipStream_t stream);
@@ -63,6 +70,19 @@ unsigned batched_device_grid();
 int batched_rr_max_items();
 hipError_t launch_batched_rr(xred_dtype dtype, xred_op op, const xred_item *d_items, int nitems,
                              const uint32_t *d_tile_start, hipStream_t stream);
+
+// The batched launchers per group of element types (each in its own
+// translation unit).
+#define XRED_BATCHED_GROUP(G)                                                                  \
+    hipError_t launch_batched_range_##G(xred_dtype dtype, xred_op op, bool planned,            \
+                                        const xred_item *d_items, int nitems,                  \
+                                        const WgStart *d_wg, unsigned grid, hipStream_t s);    \
+    hipError_t launch_batched_rr_##G(xred_dtype dtype, xred_op op, const xred_item *d_items,   \
+                                     int nitems, const uint32_t *d_tile_start, hipStream_t s);
+XRED_BATCHED_GROUP(float)
+XRED_BATCHED_GROUP(fp8)
+XRED_BATCHED_GROUP(int)
+#undef XRED_BATCHED_GROUP
 
 // Workgroups for the round-robin kernel given how many fit on one CU.
 unsigned batched_rr_grid(int fit_per_cu);

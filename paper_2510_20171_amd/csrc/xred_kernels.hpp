@@ -180,6 +180,13 @@ __device__ __forceinline__ void reduce_tile(const Src &src, int nsrc, char *dst,
         default: break;
         }
     }
+    if constexpr (__is_same(Op, OpAvg)) {
+        const int n = NP > 0 ? NP : nsrc;
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+#pragma unroll
+            for (int j = 0; j < T::kVec; ++j) acc[u][j] = avg_scale<T, Op>(acc[u][j], n);
+    }
     const rsrc_t w = make_rsrc(dst + tl.off, tl.nrec);
 #pragma unroll
     for (int u = 0; u < U; ++u)
@@ -193,7 +200,7 @@ __device__ __forceinline__ void reduce_elem(const Src &src, int nsrc, char *dst,
 {
     typename T::Acc a = up1<T>(src(0), i);
     for (int p = 1; p < nsrc; ++p) a = combine<T, Op>(a, up1<T>(src(p), i));
-    down1<T, Op>(dst, i, a);
+    down1<T, Op>(dst, i, avg_scale<T, Op>(a, nsrc));
 }
 
 // ------------------------------------------------------ fused P-source --
@@ -226,14 +233,15 @@ __global__ __launch_bounds__(B) void reduce_scalar_kernel(KernargSrc<XRED_MAX_SR
 }
 
 // ------------------------------------------------------------ step-wise --
-// The accumulator holds kVec 4-byte values per 16-byte input vector, i.e.
-// kVec/4 16-byte accumulator vectors, contiguous.
+// The accumulator holds kVec values of T::Acc (4 or 8 bytes) per 16-byte
+// input vector, i.e. acc_vecs<T>() 16-byte accumulator vectors, contiguous.
 template <class T, class Op, unsigned FLAGS, int U, int B>
 __device__ __forceinline__ void step_tile(const char *in, char *acc, char *dst, size_t t,
                                           size_t nvec)
 {
     constexpr bool kInit = (FLAGS & XRED_STEP_INIT) != 0, kFinal = (FLAGS & XRED_STEP_FINAL) != 0;
-    constexpr int H = T::kVec / 4;                 // accumulator vectors per input vector
+    constexpr int H = acc_vecs<T>();               // accumulator vectors per input vector
+    constexpr int PV = acc_per_vec<T>();           // accumulator values per vector
     constexpr uint32_t kTileBytes = (uint32_t)B * U * 16u;
     const size_t off = t * kTileBytes;
     const uint32_t nrec = tile_nrec(nvec * 16, off, kTileBytes);
@@ -247,14 +255,9 @@ __device__ __forceinline__ void step_tile(const char *in, char *acc, char *dst, 
 #pragma unroll
         for (int u = 0; u < U; ++u) {
 #pragma unroll
-            for (int h = 0; h < H; ++h) {
-                const u32x4 y = bload<kLoadKeep>(racc, (uint32_t)((u * B + threadIdx.x) * H + h) * 16u);
-#pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    if constexpr (T::kFloat) a[u][4 * h + j] = __uint_as_float(y[j]);
-                    else a[u][4 * h + j] = y[j];
-                }
-            }
+            for (int h = 0; h < H; ++h)
+                unpack_acc<T>(bload<kLoadKeep>(racc, (uint32_t)((u * B + threadIdx.x) * H + h) * 16u),
+                              &a[u][PV * h]);
         }
     }
 #pragma unroll
@@ -272,13 +275,11 @@ __device__ __forceinline__ void step_tile(const char *in, char *acc, char *dst, 
         for (int u = 0; u < U; ++u) {
 #pragma unroll
             for (int h = 0; h < H; ++h) {
-                u32x4 y;
+                typename T::Acc f[PV];
 #pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    if constexpr (T::kFloat) y[j] = __float_as_uint(finalize<T, Op>(a[u][4 * h + j]));
-                    else y[j] = a[u][4 * h + j];
-                }
-                bstore<kStoreKeep>(y, racc, (uint32_t)((u * B + threadIdx.x) * H + h) * 16u);
+                for (int j = 0; j < PV; ++j) f[j] = finalize<T, Op>(a[u][PV * h + j]);
+                bstore<kStoreKeep>(pack_acc<T>(f), racc,
+                                   (uint32_t)((u * B + threadIdx.x) * H + h) * 16u);
             }
         }
     }
@@ -293,16 +294,12 @@ __device__ __forceinline__ void step_elem(const char *in, char *acc, char *dst, 
     if constexpr (kInit) {
         a = x;
     } else {
-        if constexpr (T::kFloat) a = ((const float *)acc)[i];
-        else a = ((const uint32_t *)acc)[i];
-        a = combine<T, Op>(a, x);
+        a = combine<T, Op>(((const typename T::Acc *)acc)[i], x);
     }
-    if constexpr (kFinal) {
+    if constexpr (kFinal)
         down1<T, Op>(dst, i, a);
-    } else {
-        if constexpr (T::kFloat) ((float *)acc)[i] = finalize<T, Op>(a);
-        else ((uint32_t *)acc)[i] = a;
-    }
+    else
+        ((typename T::Acc *)acc)[i] = finalize<T, Op>(a);
 }
 
 // One ReduceCopy step over nvec vectors + tail elements (16 B aligned) or,
@@ -331,7 +328,8 @@ __global__ __launch_bounds__(B) void acc_cast_kernel(const char *acc, char *dst,
                                                      size_t tail)
 {
     if constexpr (VEC) {
-        constexpr int H = T::kVec / 4;
+        constexpr int H = acc_vecs<T>();
+        constexpr int PV = acc_per_vec<T>();
         constexpr uint32_t kTileBytes = (uint32_t)B * U * 16u;
         const size_t vbytes = nvec * 16;
         const size_t ntiles = (vbytes + kTileBytes - 1) / kTileBytes;
@@ -344,33 +342,21 @@ __global__ __launch_bounds__(B) void acc_cast_kernel(const char *acc, char *dst,
             for (int u = 0; u < U; ++u) {
                 typename T::Acc a[T::kVec];
 #pragma unroll
-                for (int h = 0; h < H; ++h) {
-                    const u32x4 y =
-                        bload<kLoadStream>(racc, (uint32_t)((u * B + threadIdx.x) * H + h) * 16u);
-#pragma unroll
-                    for (int j = 0; j < 4; ++j) {
-                        if constexpr (T::kFloat) a[4 * h + j] = __uint_as_float(y[j]);
-                        else a[4 * h + j] = y[j];
-                    }
-                }
+                for (int h = 0; h < H; ++h)
+                    unpack_acc<T>(
+                        bload<kLoadStream>(racc, (uint32_t)((u * B + threadIdx.x) * H + h) * 16u),
+                        &a[PV * h]);
                 bstore<kStoreOut>(down_vec<T, OpSum>(a), rdst, (uint32_t)(u * B + threadIdx.x) * 16u);
             }
         }
         if (tail != 0 && blockIdx.x == ntiles % gridDim.x && threadIdx.x < tail) {
             const size_t i = nvec * T::kVec + threadIdx.x;
-            typename T::Acc a;
-            if constexpr (T::kFloat) a = ((const float *)acc)[i];
-            else a = ((const uint32_t *)acc)[i];
-            down1<T, OpSum>(dst, i, a);
+            down1<T, OpSum>(dst, i, ((const typename T::Acc *)acc)[i]);
         }
     } else {
         const size_t stride = (size_t)gridDim.x * B;
-        for (size_t i = (size_t)blockIdx.x * B + threadIdx.x; i < tail; i += stride) {
-            typename T::Acc a;
-            if constexpr (T::kFloat) a = ((const float *)acc)[i];
-            else a = ((const uint32_t *)acc)[i];
-            down1<T, OpSum>(dst, i, a);
-        }
+        for (size_t i = (size_t)blockIdx.x * B + threadIdx.x; i < tail; i += stride)
+            down1<T, OpSum>(dst, i, ((const typename T::Acc *)acc)[i]);
     }
 }
 

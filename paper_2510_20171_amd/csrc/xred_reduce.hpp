@@ -1,0 +1,148 @@
+// xred_reduce.hpp -- launch templates of the fused P-source reduce
+// (xred_allreduce_local and xred_reduce_scatter_local), instantiated per
+// group of element types by xred_reduce_{float,fp8,int}.hip so the groups
+// compile in parallel.
+#pragma once
+
+#include <stdlib.h>
+
+#include "xred_dispatch.hpp"
+#include "xred_internal.hpp"
+#include "xred_kernels.hpp"
+
+namespace xred {
+namespace {
+
+// Two tile shapes, both one 16-byte vector per thread:
+//
+// * Launches that fit on the chip in one round (every tile resident at
+//   once) are latency-bound: they use 512-thread workgroups, uncapped, so
+//   the whole message is in flight after the fewest workgroup dispatches
+//   (8 MiB per source at P=8 bf16: 10.1 us against 10.8 us with 128-thread
+//   workgroups, same process and buffers).
+// * Larger launches are bandwidth-bound: 128-thread workgroups with a
+//   bounded number of waves per CU.  HBM3E on MI355X delivers the most when
+//   a CU keeps a moderate number of loads in flight; more waves than that
+//   lower the rate (P=8 bf16, 2^26 elements per source: 168.6 us against
+//   190.7 us with uncapped 512-thread workgroups).  Waves per CU -> TB/s on
+//   32 MiB per source: P=4 is flat from 16 waves up; P=8 is flat between 8
+//   and 16 and falls at full occupancy; P=12 (runtime source count) wants
+//   ~16; P=16 ~10; P=32 ~6; P=64 ~4.  The cap is applied by giving each
+//   workgroup an LDS reservation it never touches, sized so that only the
+//   wanted number of workgroups fit on a CU.
+constexpr int kU = 1;          // 16-byte vectors per thread per tile
+constexpr int kB = 128;        // threads per workgroup, bandwidth-bound launches
+constexpr int kBWide = 512;    // threads per workgroup, one-round launches
+constexpr int kWideWgsPerCu = 4;   // resident 512-thread workgroups per CU
+
+// Waves per CU for a compile-time source count (0: runtime count); 0 = no cap.
+template <int NP>
+constexpr int waves_per_cu()
+{
+    return NP == 0 ? 16 : NP <= 4 ? 0 : NP <= 8 ? 12 : NP <= 16 ? 10 : NP <= 32 ? 6 : 4;
+}
+
+int lds_per_cu()
+{
+    static int bytes = [] {
+        int dev = 0, v = 0;
+        if (hipGetDevice(&dev) != hipSuccess ||
+            hipDeviceGetAttribute(&v, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor, dev) !=
+                hipSuccess ||
+            v <= 0)
+            v = 160 * 1024;
+        return v;
+    }();
+    return bytes;
+}
+
+// Dynamic LDS that leaves room for `waves` wavefronts per CU (0: no cap).
+size_t lds_for_waves(int waves)
+{
+    static const long force = [] {
+        const char *e = getenv("XRED_FUSED_WAVES_PER_CU");
+        return e && *e ? strtol(e, nullptr, 10) : 0L;
+    }();
+    if (force > 0) waves = (int)force;
+    if (waves <= 0) return 0;
+    const int wgs = waves / (kB / 64);
+    if (wgs <= 0 || wgs >= 16) return 0;     // at or beyond the natural occupancy
+    return (size_t)(lds_per_cu() / wgs) / 512 * 512;
+}
+
+template <class T, class Op, int NP, int MAXP>
+hipError_t go_vec(const char *const *srcs, int nsrc, char *dst, size_t count, hipStream_t s)
+{
+    KernargSrc<MAXP> ks;
+    for (int p = 0; p < nsrc; ++p) ks.p[p] = srcs[p];
+    for (int p = nsrc; p < MAXP; ++p) ks.p[p] = nullptr;
+    const size_t nvec = count / T::kVec;
+    const uint32_t tail = (uint32_t)(count % T::kVec);
+    constexpr size_t kTileWide = (size_t)kBWide * kU;
+    const uint64_t tiles_wide = (nvec + kTileWide - 1) / kTileWide + (tail ? 1 : 0);
+    if (tiles_wide <= (uint64_t)device_cus() * kWideWgsPerCu) {
+        hipLaunchKernelGGL((reduce_vec_kernel<T, Op, NP, MAXP, kU, kBWide>),
+                           dim3(grid_for(tiles_wide)), dim3(kBWide), 0, s, ks, nsrc, dst, nvec,
+                           tail);
+        return hipGetLastError();
+    }
+    constexpr size_t kTile = (size_t)kB * kU;
+    const uint64_t tiles = (nvec + kTile - 1) / kTile + (tail ? 1 : 0);
+    hipLaunchKernelGGL((reduce_vec_kernel<T, Op, NP, MAXP, kU, kB>), dim3(grid_for(tiles)),
+                       dim3(kB), lds_for_waves(waves_per_cu<NP>()), s, ks, nsrc, dst, nvec, tail);
+    return hipGetLastError();
+}
+
+template <class T, class Op>
+hipError_t go(const char *const *srcs, int nsrc, char *dst, size_t count, hipStream_t s)
+{
+    uintptr_t bits = (uintptr_t)dst;
+    for (int p = 0; p < nsrc; ++p) bits |= (uintptr_t)srcs[p];
+    if (bits & 15u) {
+        KernargSrc<XRED_MAX_SRC> ks;
+        for (int p = 0; p < nsrc; ++p) ks.p[p] = srcs[p];
+        for (int p = nsrc; p < XRED_MAX_SRC; ++p) ks.p[p] = nullptr;
+        hipLaunchKernelGGL((reduce_scalar_kernel<T, Op, kB>), dim3(grid_for((count + kB - 1) / kB)),
+                           dim3(kB), 0, s, ks, nsrc, dst, count);
+        return hipGetLastError();
+    }
+    constexpr bool kWide = is_core_type<T>() && !__is_same(Op, OpAvg);
+    switch (nsrc) {
+    case 1: return go_vec<T, Op, 1, 8>(srcs, nsrc, dst, count, s);
+    case 2: return go_vec<T, Op, 2, 8>(srcs, nsrc, dst, count, s);
+    case 3: return go_vec<T, Op, 3, 8>(srcs, nsrc, dst, count, s);
+    case 4: return go_vec<T, Op, 4, 8>(srcs, nsrc, dst, count, s);
+    case 5: return go_vec<T, Op, 5, 8>(srcs, nsrc, dst, count, s);
+    case 6: return go_vec<T, Op, 6, 8>(srcs, nsrc, dst, count, s);
+    case 7: return go_vec<T, Op, 7, 8>(srcs, nsrc, dst, count, s);
+    case 8: return go_vec<T, Op, 8, 8>(srcs, nsrc, dst, count, s);
+    case 16:
+        if constexpr (kWide) return go_vec<T, Op, 16, 16>(srcs, nsrc, dst, count, s);
+        break;
+    case 32:
+        if constexpr (kWide) return go_vec<T, Op, 32, 32>(srcs, nsrc, dst, count, s);
+        break;
+    case 64:
+        if constexpr (kWide) return go_vec<T, Op, 64, 64>(srcs, nsrc, dst, count, s);
+        break;
+    default: break;
+    }
+    return go_vec<T, Op, 0, XRED_MAX_SRC>(srcs, nsrc, dst, count, s);
+}
+
+
+// The fused launcher for the element types Ts (one translation unit each).
+template <class... Ts>
+hipError_t reduce_group(xred_dtype dtype, xred_op op, const char *const *srcs, int nsrc,
+                        char *dst, size_t count, hipStream_t stream)
+{
+    return with_dtype_among<Ts...>(dtype, [&](auto t) {
+        using T = decltype(t);
+        return with_op<T, true>(op, [&](auto o) {
+            return go<T, decltype(o)>(srcs, nsrc, dst, count, stream);
+        });
+    });
+}
+
+}  // namespace
+}  // namespace xred

@@ -18,6 +18,7 @@
 // acquire fence (an acquire per poll would invalidate L2 on every poll).
 // Every wait is bounded: after `timeout` device-clock ticks the workgroup
 // records 1 in *status (if given) and stops; dst is then unspecified.
+#include "xred_dispatch.hpp"
 #include "xred_internal.hpp"
 #include "xred_kernels.hpp"
 
@@ -27,14 +28,16 @@ namespace {
 constexpr int kB = 512;
 constexpr int kDepth = 8;            // chunks in flight per round
 constexpr int kMaxTilesPerWg = 4;    // tiles whose accumulators one workgroup holds
-constexpr int kLdsBytesPerTile = kB * 8 * 4;   // bf16: 8 binary32 accumulators per thread
+// LDS bytes of one tile's accumulators for element type T.
+template <class T>
+constexpr size_t lds_tile_bytes() { return (size_t)kB * acc_vecs<T>() * 16; }
 
-// Accumulator slot of thread `tid`, tile j, 4-value group h: [j][h][tid] as
-// 16-byte vectors, so consecutive lanes touch consecutive LDS addresses.
+// Accumulator slot of thread `tid`, tile j, 16-byte accumulator vector h:
+// [j][h][tid], so consecutive lanes touch consecutive LDS addresses.
 template <class T>
 __device__ __forceinline__ u32x4 *acc_slot(u32x4 *s_acc, int j, int h)
 {
-    return s_acc + ((size_t)j * (T::kVec / 4) + h) * kB + threadIdx.x;
+    return s_acc + ((size_t)j * acc_vecs<T>() + h) * kB + threadIdx.x;
 }
 
 template <class T, class Op>
@@ -47,7 +50,8 @@ __global__ __launch_bounds__(kB) void ring_kernel(KernargSrc<XRED_MAX_SRC> chunk
     extern __shared__ u32x4 s_acc[];
     __shared__ int s_upto;
     constexpr uint32_t kTileBytes = (uint32_t)kB * 16u;
-    constexpr int H = T::kVec / 4;
+    constexpr int H = acc_vecs<T>();
+    constexpr int PV = acc_per_vec<T>();
     const size_t vbytes = nvec * 16;
     const size_t ntiles = (nvec + kB - 1) / kB;
     int next = 0;
@@ -107,14 +111,7 @@ __global__ __launch_bounds__(kB) void ring_kernel(KernargSrc<XRED_MAX_SRC> chunk
                 up_vec<T>(in[0], a);
             } else {
 #pragma unroll
-                for (int h = 0; h < H; ++h) {
-                    const u32x4 y = *acc_slot<T>(s_acc, j, h);
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        if constexpr (T::kFloat) a[4 * h + e] = __uint_as_float(y[e]);
-                        else a[4 * h + e] = y[e];
-                    }
-                }
+                for (int h = 0; h < H; ++h) unpack_acc<T>(*acc_slot<T>(s_acc, j, h), &a[PV * h]);
             }
 #pragma unroll
             for (int q = 0; q < kDepth; ++q) {
@@ -132,15 +129,7 @@ __global__ __launch_bounds__(kB) void ring_kernel(KernargSrc<XRED_MAX_SRC> chunk
                                   (uint32_t)threadIdx.x * 16u);
             } else {
 #pragma unroll
-                for (int h = 0; h < H; ++h) {
-                    u32x4 y;
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        if constexpr (T::kFloat) y[e] = __float_as_uint(a[4 * h + e]);
-                        else y[e] = a[4 * h + e];
-                    }
-                    *acc_slot<T>(s_acc, j, h) = y;
-                }
+                for (int h = 0; h < H; ++h) *acc_slot<T>(s_acc, j, h) = pack_acc<T>(&a[PV * h]);
             }
         }
         next = upto;
@@ -162,7 +151,7 @@ hipError_t go(const char *const *chunks, int nchunks, char *dst, size_t count,
     const size_t nvec = count / T::kVec;
     const uint32_t tail = (uint32_t)(count % T::kVec);
     const size_t ntiles = (nvec + kB - 1) / kB;
-    const size_t lds_tile = (size_t)kB * T::kVec * 4;
+    const size_t lds_tile = lds_tile_bytes<T>();
     int per_cu = 0;
     hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(
         &per_cu, (const void *)ring_kernel<T, Op>, kB, lds_tile * kMaxTilesPerWg);
@@ -179,45 +168,40 @@ hipError_t go(const char *const *chunks, int nchunks, char *dst, size_t count,
 }
 
 template <class T>
-hipError_t go_op(xred_op op, const char *const *chunks, int nchunks, char *dst, size_t count,
-                 const uint32_t *ready, uint32_t epoch, uint64_t timeout, uint32_t *status,
-                 hipStream_t s)
+uint64_t max_count()
 {
-    switch (op) {
-    case XRED_SUM: return go<T, OpSum>(chunks, nchunks, dst, count, ready, epoch, timeout, status, s);
-    case XRED_PROD: return go<T, OpProd>(chunks, nchunks, dst, count, ready, epoch, timeout, status, s);
-    case XRED_MAX: return go<T, OpMax>(chunks, nchunks, dst, count, ready, epoch, timeout, status, s);
-    case XRED_MIN: return go<T, OpMin>(chunks, nchunks, dst, count, ready, epoch, timeout, status, s);
-    }
-    return hipErrorInvalidValue;
+    // the grid never exceeds what fits on the chip; each workgroup holds at
+    // most kMaxTilesPerWg tiles
+    int per_cu = 0;
+    (void)hipOccupancyMaxActiveBlocksPerMultiprocessor(
+        &per_cu, (const void *)ring_kernel<T, OpSum>, kB, lds_tile_bytes<T>() * kMaxTilesPerWg);
+    if (per_cu <= 0) per_cu = 1;
+    return (uint64_t)device_cus() * per_cu * kMaxTilesPerWg * kB * T::kVec;
 }
 
 }  // namespace
 
 uint64_t ring_max_count(xred_dtype dtype)
 {
-    const int vec = dtype == XRED_BFLOAT16 ? 8 : 4;
-    // the grid never exceeds what fits on the chip; each workgroup holds at
-    // most kMaxTilesPerWg tiles
-    int per_cu = 0;
-    (void)hipOccupancyMaxActiveBlocksPerMultiprocessor(
-        &per_cu, (const void *)ring_kernel<TBF16, OpSum>, kB,
-        (size_t)kLdsBytesPerTile * kMaxTilesPerWg);
-    if (per_cu <= 0) per_cu = 1;
-    return (uint64_t)device_cus() * per_cu * kMaxTilesPerWg * kB * vec;
+    uint64_t n = 0;
+    (void)with_dtype(dtype, [&](auto t) {
+        n = max_count<decltype(t)>();
+        return hipSuccess;
+    });
+    return n;
 }
 
 hipError_t launch_ring(xred_dtype dtype, xred_op op, const char *const *chunks, int nchunks,
                        char *dst, size_t count, const uint32_t *ready, uint32_t epoch,
                        uint64_t timeout_ticks, uint32_t *status, hipStream_t stream)
 {
-    switch (dtype) {
-    case XRED_FLOAT32: return go_op<TF32>(op, chunks, nchunks, dst, count, ready, epoch, timeout_ticks, status, stream);
-    case XRED_BFLOAT16: return go_op<TBF16>(op, chunks, nchunks, dst, count, ready, epoch, timeout_ticks, status, stream);
-    case XRED_INT32: return go_op<TI32>(op, chunks, nchunks, dst, count, ready, epoch, timeout_ticks, status, stream);
-    case XRED_UINT32: return go_op<TU32>(op, chunks, nchunks, dst, count, ready, epoch, timeout_ticks, status, stream);
-    default: return hipErrorInvalidValue;
-    }
+    return with_dtype(dtype, [&](auto t) {
+        using T = decltype(t);
+        return with_op<T, false>(op, [&](auto o) {
+            return go<T, decltype(o)>(chunks, nchunks, dst, count, ready, epoch, timeout_ticks,
+                                      status, stream);
+        });
+    });
 }
 
 }  // namespace xred

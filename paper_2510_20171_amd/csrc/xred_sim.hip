@@ -24,6 +24,7 @@
 // its own elements before overwriting them, so recv[q] may be send[q].  Every
 // hop computes down(up(received) (+) up(own)) with the fused kernel's tile
 // code (two sources, fold order received-then-own); copies move bits.
+#include "xred_dispatch.hpp"
 #include "xred_internal.hpp"
 #include "xred_kernels.hpp"
 
@@ -45,10 +46,14 @@ struct SimStep {
 template <class T>
 __device__ __forceinline__ void copy_elem(const char *in, char *out, size_t i)
 {
-    if constexpr (T::kSize == 2)
+    if constexpr (T::kSize == 1)
+        ((uint8_t *)out)[i] = ((const uint8_t *)in)[i];
+    else if constexpr (T::kSize == 2)
         ((uint16_t *)out)[i] = ((const uint16_t *)in)[i];
-    else
+    else if constexpr (T::kSize == 4)
         ((uint32_t *)out)[i] = ((const uint32_t *)in)[i];
+    else
+        ((uint64_t *)out)[i] = ((const uint64_t *)in)[i];
 }
 
 // Work item w of a step: rank w % G, tile w / G of that rank's range.  Vector
@@ -215,19 +220,6 @@ hipError_t run(const char *const *send, char *const *recv, int G, size_t count,
     return e;
 }
 
-template <class T>
-hipError_t run_op(xred_op op, const char *const *send, char *const *recv, int G, size_t count,
-                  xred_schedule sched, hipStream_t s)
-{
-    switch (op) {
-    case XRED_SUM: return run<T, OpSum>(send, recv, G, count, sched, s);
-    case XRED_PROD: return run<T, OpProd>(send, recv, G, count, sched, s);
-    case XRED_MAX: return run<T, OpMax>(send, recv, G, count, sched, s);
-    case XRED_MIN: return run<T, OpMin>(send, recv, G, count, sched, s);
-    }
-    return hipErrorInvalidValue;
-}
-
 }  // namespace
 
 uint64_t sim_chunk(uint64_t count, int nranks)
@@ -240,13 +232,12 @@ uint64_t sim_chunk(uint64_t count, int nranks)
 hipError_t launch_sim(xred_dtype dtype, xred_op op, const char *const *send, char *const *recv,
                       int nranks, size_t count, xred_schedule schedule, hipStream_t stream)
 {
-    switch (dtype) {
-    case XRED_FLOAT32: return run_op<TF32>(op, send, recv, nranks, count, schedule, stream);
-    case XRED_BFLOAT16: return run_op<TBF16>(op, send, recv, nranks, count, schedule, stream);
-    case XRED_INT32: return run_op<TI32>(op, send, recv, nranks, count, schedule, stream);
-    case XRED_UINT32: return run_op<TU32>(op, send, recv, nranks, count, schedule, stream);
-    default: return hipErrorInvalidValue;
-    }
+    return with_dtype(dtype, [&](auto t) {
+        using T = decltype(t);
+        return with_op<T, false>(op, [&](auto o) {
+            return run<T, decltype(o)>(send, recv, nranks, count, schedule, stream);
+        });
+    });
 }
 
 }  // namespace xred

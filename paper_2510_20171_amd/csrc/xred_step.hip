@@ -6,6 +6,7 @@
 // lookup and one kernel.  The grid is a pure function of count, so tile t of
 // the accumulator is processed by workgroup t on every step and therefore on
 // the same XCD, whose L2 may still hold it from the previous step.
+#include "xred_dispatch.hpp"
 #include "xred_internal.hpp"
 #include "xred_kernels.hpp"
 
@@ -53,19 +54,6 @@ hipError_t go_flags(unsigned flags, const char *in, char *acc, char *dst, size_t
 }
 
 template <class T>
-hipError_t go_op(xred_op op, unsigned flags, const char *in, char *acc, char *dst, size_t count,
-                 hipStream_t s)
-{
-    switch (op) {
-    case XRED_SUM: return go_flags<T, OpSum>(flags, in, acc, dst, count, s);
-    case XRED_PROD: return go_flags<T, OpProd>(flags, in, acc, dst, count, s);
-    case XRED_MAX: return go_flags<T, OpMax>(flags, in, acc, dst, count, s);
-    case XRED_MIN: return go_flags<T, OpMin>(flags, in, acc, dst, count, s);
-    }
-    return hipErrorInvalidValue;
-}
-
-template <class T>
 hipError_t go_cast(const char *acc, char *dst, size_t count, hipStream_t s)
 {
     if ((((uintptr_t)acc | (uintptr_t)dst) & 15u) == 0) {
@@ -88,25 +76,18 @@ hipError_t go_cast(const char *acc, char *dst, size_t count, hipStream_t s)
 hipError_t launch_step(xred_dtype dtype, xred_op op, unsigned flags, const char *in, char *acc,
                        char *dst, size_t count, hipStream_t stream)
 {
-    switch (dtype) {
-    case XRED_FLOAT32: return go_op<TF32>(op, flags, in, acc, dst, count, stream);
-    case XRED_BFLOAT16: return go_op<TBF16>(op, flags, in, acc, dst, count, stream);
-    case XRED_INT32: return go_op<TI32>(op, flags, in, acc, dst, count, stream);
-    case XRED_UINT32: return go_op<TU32>(op, flags, in, acc, dst, count, stream);
-    default: return hipErrorInvalidValue;
-    }
+    return with_dtype(dtype, [&](auto t) {
+        using T = decltype(t);
+        return with_op<T, false>(op, [&](auto o) {
+            return go_flags<T, decltype(o)>(flags, in, acc, dst, count, stream);
+        });
+    });
 }
 
 hipError_t launch_acc_cast(xred_dtype dtype, const char *acc, char *dst, size_t count,
                            hipStream_t stream)
 {
-    switch (dtype) {
-    case XRED_FLOAT32: return go_cast<TF32>(acc, dst, count, stream);
-    case XRED_BFLOAT16: return go_cast<TBF16>(acc, dst, count, stream);
-    case XRED_INT32: return go_cast<TI32>(acc, dst, count, stream);
-    case XRED_UINT32: return go_cast<TU32>(acc, dst, count, stream);
-    default: return hipErrorInvalidValue;
-    }
+    return with_dtype(dtype, [&](auto t) { return go_cast<decltype(t)>(acc, dst, count, stream); });
 }
 
 }  // namespace xred

@@ -58,6 +58,8 @@ def test_header_compiles(tmp_path, compiler, lang):
 def test_constants(L):
     assert L.xred_version() >= 100
     assert L.xred_acc_elem_size(0) == 4 and L.xred_acc_elem_size(1) == 4
+    assert L.xred_acc_elem_size(2) == 4 and L.xred_acc_elem_size(7) == 4
+    assert L.xred_acc_elem_size(5) == 8 and L.xred_acc_elem_size(6) == 8
     assert L.xred_acc_elem_size(99) == 0
     assert L.xred_status_string(0) == b"success"
     assert L.xred_status_string(3) == b"buffers overlap"
@@ -79,7 +81,10 @@ def ptrs(*xs):
     (lambda L: L.xred_allreduce_local(ptrs(A), 65, S(A + 4096), 16, 0, 0, None), 1),
     (lambda L: L.xred_allreduce_local(ptrs(A), 1, S(A + 4096), 16, 99, 0, None), 1),
     (lambda L: L.xred_allreduce_local(ptrs(A), 1, S(A + 4096), 16, 0, 9, None), 1),
-    (lambda L: L.xred_allreduce_local(ptrs(A), 1, S(A + 4096), 16, 2, 0, None), 2),  # f16
+    (lambda L: L.xred_allreduce_local(ptrs(A), 1, S(A + 4096), 16, 3, 4, None), 2),  # int AVG
+    (lambda L: L.xred_allreduce_local(ptrs(A), 1, S(A + 4096), 16, 9, 0, None), 1),
+    (lambda L: L.xred_allreduce_local(ptrs(A), 1, S(A + 4096), 16, 0, 5, None), 1),
+    (lambda L: L.xred_allreduce_local(ptrs(A + 4), 1, S(A + 4096), 16, 5, 0, None), 1),  # i64 align
     (lambda L: L.xred_allreduce_local(None, 1, S(A + 4096), 16, 0, 0, None), 1),
     (lambda L: L.xred_allreduce_local(ptrs(0), 1, S(A + 4096), 16, 0, 0, None), 1),
     (lambda L: L.xred_allreduce_local(ptrs(A), 1, S(0), 16, 0, 0, None), 1),
@@ -108,7 +113,9 @@ def ptrs(*xs):
     (lambda L: L.xred_ring_reduce(ptrs(A + 2), 1, S(A + 4096), 16, 1, 0, None, 1, 0, None, None), 2),
     (lambda L: L.xred_ring_reduce(ptrs(A), 1, S(A + 8), 16, 1, 0, None, 1, 0, None, None), 3),
     (lambda L: L.xred_ring_reduce(ptrs(A), 1, S(A + 4096), 16, 1, 0, S(A + 1), 1, 0, None, None), 1),
-    (lambda L: L.xred_ring_reduce(ptrs(A), 1, S(A + 4096), 16, 2, 0, None, 1, 0, None, None), 2),
+    (lambda L: L.xred_ring_reduce(ptrs(A), 1, S(A + 4096), 16, 1, 4, None, 1, 0, None, None), 2),
+    (lambda L: L.xred_reduce_copy_step(S(A), S(A + 4096), S(0), 16, 0, 4, 0, None), 2),  # AVG
+    (lambda L: L.xred_reduce_copy_step(S(A), S(A + 4100), S(0), 16, 5, 0, 0, None), 1),  # u64 acc
     # xred_allreduce_sim(sends, recvs, nranks, count, dtype, op, schedule, stream)
     (lambda L: L.xred_allreduce_sim(ptrs(A), ptrs(A + 8192), 0, 16, 1, 0, 0, None), 1),
     (lambda L: L.xred_allreduce_sim(ptrs(A), ptrs(A + 8192), 65, 16, 1, 0, 0, None), 1),
@@ -123,7 +130,7 @@ def ptrs(*xs):
     (lambda L: L.xred_allreduce_sim(ptrs(A, A + 4096), ptrs(A + 8192, A + 8200), 2, 16, 1, 0, 0,
                                     None), 3),
     (lambda L: L.xred_allreduce_sim(ptrs(A, A + 4096), ptrs(A + 8, A + 12288), 2, 16, 1, 0, 0, None), 3),
-    (lambda L: L.xred_allreduce_sim(ptrs(A, A + 4096), ptrs(A + 8192, A + 12288), 2, 16, 2, 0, 0,
+    (lambda L: L.xred_allreduce_sim(ptrs(A, A + 4096), ptrs(A + 8192, A + 12288), 2, 16, 1, 4, 0,
                                     None), 2),
     (lambda L: L.xred_allreduce_sim(ptrs(A), ptrs(A + 8192), 1, 2**62, 0, 0, 0, None), 1),
 ])

@@ -22,6 +22,9 @@ Workloads (M = 2^20, K = 2^10 elements):
                         log-uniform on [8 KiB, 1 MiB]
   c5a  allreduce_local  P=32 x 8M  i32  sum   uniform over all int32
   c5b  allreduce_local  P=32 x 8M  f32  max   N(0,1) with +-inf and +-0 mixed in
+  c2fp8 allreduce_local P=8  x 128M fp8 e4m3 sum, random sign, magnitudes
+                        log-uniform over [2^-9, 4) (the gradient bucket's
+                        footprint, 128 MiB per source, in e4m3)
   sim  allreduce_sim    G=8 ranks x 64M bf16 sum N(0,1)*1e-3 per rank (a c2-sized
                         gradient bucket AllReduced over 8 simulated ranks; the
                         send buffer of rank r is source r)
@@ -37,8 +40,9 @@ import numpy as np
 
 M = 1 << 20
 
-NP_TYPES = {"f32": np.float32, "bf16": np.uint16, "i32": np.int32, "u32": np.uint32}
-ELEM_SIZE = {"f32": 4, "bf16": 2, "i32": 4, "u32": 4}
+NP_TYPES = {"f32": np.float32, "bf16": np.uint16, "i32": np.int32, "u32": np.uint32,
+            "e4m3": np.uint8}
+ELEM_SIZE = {"f32": 4, "bf16": 2, "i32": 4, "u32": 4, "e4m3": 1}
 
 
 @dataclass(frozen=True)
@@ -73,6 +77,7 @@ WORKLOADS = {
     "c5a": Workload("c5a", "allreduce", "i32", "sum", 32, 8 * M, "int32", 5000),
     "c5b": Workload("c5b", "allreduce", "f32", "max", 32, 8 * M, "normal_specials", 5100),
     "sim": Workload("sim", "sim", "bf16", "sum", 8, 64 * M, "normal_1e-3", 7000),
+    "c2fp8": Workload("c2fp8", "allreduce", "e4m3", "sum", 8, 128 * M, "fp8_loguniform", 8000),
 }
 
 
@@ -107,6 +112,13 @@ def _fill_chunk(dist: str, out: np.ndarray, seed: int, c: int, dtype: str) -> No
     if dist == "int32":
         v = g.integers(-(2**31), 2**31, size=n, dtype=np.int32)
         out[:] = v if dtype == "i32" else v.view(np.uint32)
+        return
+    if dist == "fp8_loguniform":
+        # e4m3 bytes drawn as fields: random sign, exponent field 0..8 and
+        # fraction uniform, i.e. magnitudes log-uniform over [2^-9, 4)
+        code = g.integers(0, 9 * 8, size=n, dtype=np.uint8)
+        sign = g.integers(0, 2, size=n, dtype=np.uint8) << 7
+        out[:] = code | sign
         return
     x = out if dtype == "f32" else _scratch(n)
     if dist == "uniform":                       # U[-1, 1)
