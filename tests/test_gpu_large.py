@@ -1,0 +1,74 @@
+"""Buffers larger than 4 GiB: byte offsets past 2^32 on the fused, reduce-scatter
+and batched paths.  Inputs are random bit patterns drawn on the device by
+PyTorch's seeded generator (values from neither the oracle nor libxred); the
+oracle computes sampled columns one by one: random indices plus the elements
+around the 4 GiB byte boundary and the ragged tail.
+"""
+import numpy as np
+import pytest
+
+import gpu_util as gu
+
+pytestmark = pytest.mark.gpu
+torch = pytest.importorskip("torch")
+
+
+@pytest.fixture(scope="module")
+def xr():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU visible")
+    import paper_2510_20171_amd as xr
+    xr.load()
+    return xr
+
+
+def _random_bits(n, es, seed):
+    g = torch.Generator(device="cuda")
+    g.manual_seed(seed)
+    view = {1: torch.uint8, 2: torch.int16, 8: torch.int64}[es]
+    lo, hi = (0, 256) if es == 1 else (-(2 ** (8 * es - 1)), 2 ** (8 * es - 1) - 1)
+    return torch.randint(lo, hi, (n,), generator=g, dtype=view, device="cuda")
+
+
+def _samples(n, es, rng):
+    edge = (1 << 32) // es                       # first element past 4 GiB
+    idx = set(rng.integers(0, n, 1 << 16).tolist())
+    idx |= {i for i in range(edge - 64, edge + 64)} | {i for i in range(n - 64, n)} | {0}
+    return torch.tensor(sorted(i for i in idx if 0 <= i < n), dtype=torch.int64, device="cuda")
+
+
+@pytest.mark.parametrize("dtype,op,n", [("bf16", "sum", (1 << 31) + (1 << 20) + 3),
+                                        ("e4m3", "max", (1 << 32) + 4099),
+                                        ("i64", "sum", (1 << 29) + 777)])
+def test_fused_past_4gib(xr, orc, dtype, op, n):
+    es = {"bf16": 2, "e4m3": 1, "i64": 8}[dtype]
+    srcs = [_random_bits(n, es, 900 + p) for p in range(2)]
+    out = torch.empty_like(srcs[0])
+    xr.allreduce_local(srcs, out, op, dtype=dtype)
+    torch.cuda.synchronize()
+    idx = _samples(n, es, np.random.default_rng(5))
+    cols = [gu.bits(s[idx], dtype).copy() for s in srcs]
+    exp = orc.allreduce_local([c.view(gu.NP_BITS[dtype]) if dtype != "i64" else c.view(np.int64)
+                               for c in cols], dtype, op)
+    gu.assert_parity(out[idx], exp, dtype, op, f"{dtype} {op} n={n} (sampled)")
+    del srcs, out
+    torch.cuda.empty_cache()
+
+
+def test_reduce_scatter_and_batched_past_4gib(xr, orc):
+    """Rank 1's shard of P=2 send buffers of 2 x 2^31 + 10 bf16 (the shard starts
+    past 4 GiB), and the same reduction as one batched item."""
+    rc = (1 << 31) + 5
+    srcs = [_random_bits(2 * rc, 2, 950 + p) for p in range(2)]
+    out = torch.empty(rc, dtype=torch.int16, device="cuda")
+    xr.reduce_scatter_local(srcs, 1, out, "sum", dtype="bf16")
+    out_b = torch.empty(rc, dtype=torch.int16, device="cuda")
+    xr.batched_reduce([([s[rc:] for s in srcs], out_b)], "sum", dtype="bf16")
+    torch.cuda.synchronize()
+    idx = _samples(rc, 2, np.random.default_rng(6))
+    cols = [gu.bits(s[rc:][idx], "bf16").copy() for s in srcs]
+    exp = orc.allreduce_local(cols, "bf16", "sum")
+    gu.assert_parity(out[idx], exp, "bf16", "sum", "rs rank 1 past 4 GiB (sampled)")
+    gu.assert_parity(out_b[idx], exp, "bf16", "sum", "batched past 4 GiB (sampled)")
+    del srcs, out, out_b
+    torch.cuda.empty_cache()
