@@ -33,8 +33,6 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
-constexpr int kBlock = 256;   // threads per workgroup: 4 wavefronts of 64
-
 // ----------------------------------------------------------------- types --
 // kVec: elements per 16-byte vector; Acc: accumulator type; kSize: bytes.
 struct TF32 {
@@ -360,21 +358,6 @@ __device__ __forceinline__ u32x4 pack_acc(const typename T::Acc *a)
         for (int j = 0; j < 4; ++j) y[j] = a[j];
     }
     return y;
-}
-
-// ----------------------------------------------------------- memory ops --
-template <bool NT>
-__device__ __forceinline__ u32x4 load16(const char *p)
-{
-    if constexpr (NT) return __builtin_nontemporal_load((const u32x4 *)p);
-    else return *(const u32x4 *)p;
-}
-
-template <bool NT>
-__device__ __forceinline__ void store16(char *p, u32x4 v)
-{
-    if constexpr (NT) __builtin_nontemporal_store(v, (u32x4 *)p);
-    else *(u32x4 *)p = v;
 }
 
 }  // namespace xred

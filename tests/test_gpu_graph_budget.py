@@ -125,3 +125,56 @@ def test_graph_capture_and_replay(xr):
         for a, b in zip(got[2], ref_b):
             assert torch.equal(a.view(torch.int16), b.view(torch.int16)), r
     del keep
+
+
+def test_graph_capture_more_paths(xr):
+    """fp8 fused, fp16 AVG batched and the simulated ring (one launch per step)
+    captured once and replayed with eager input changes between replays."""
+    g_torch = torch.Generator(device="cuda")
+    g_torch.manual_seed(11)
+    n = (1 << 16) + 37
+    e4 = [torch.randint(0, 0x40, (n,), generator=g_torch, dtype=torch.uint8, device="cuda")
+          for _ in range(5)]
+    h = [torch.randn(n, device="cuda").to(torch.float16) for _ in range(4)]
+    sim_s = [torch.randn(n, device="cuda").to(torch.bfloat16) for _ in range(4)]
+    out_e4 = torch.empty_like(e4[0])
+    out_h = torch.empty_like(h[0])
+    sim_r = [torch.empty_like(x) for x in sim_s]
+    h_items, keep = _device_items(xr, [(h, out_h)])
+
+    def work():
+        xr.allreduce_local(e4, out_e4, "sum", dtype="e4m3")
+        xr.batched_reduce(h_items, "avg", dtype="f16")
+        xr.allreduce_sim(sim_s, sim_r, schedule="ring")
+
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        work()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        work()
+    torch.cuda.synchronize()
+    for r in range(4):
+        for x in e4:
+            x.add_(1).bitwise_and_(0x3F)
+        for x in h + sim_s:
+            x.mul_(0.5).add_(float(r))
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        got = (out_e4.clone(), out_h.clone(), [x.clone() for x in sim_r])
+        ref_e4 = torch.empty_like(out_e4)
+        xr.allreduce_local(e4, ref_e4, "sum", dtype="e4m3")
+        ref_h = torch.empty_like(out_h)
+        xr.batched_reduce([(h, ref_h)], "avg", dtype="f16")
+        ref_r = [torch.empty_like(x) for x in sim_s]
+        xr.allreduce_sim(sim_s, ref_r, schedule="ring")
+        torch.cuda.synchronize()
+        assert torch.equal(got[0], ref_e4), r
+        assert torch.equal(got[1].view(torch.int16), ref_h.view(torch.int16)), r
+        for a, b in zip(got[2], ref_r):
+            assert torch.equal(a.view(torch.int16), b.view(torch.int16)), r
+    del keep
