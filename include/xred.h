@@ -273,7 +273,8 @@ XRED_API size_t xred_sim_chunk(size_t count, int nranks);
  * default), so a reduction can run beside compute kernels on the rest of the
  * chip -- the paper's FTAR kernel uses two thread blocks and stays hidden
  * behind the network (Section 5).  Results do not depend on it.  Process-wide;
- * returns the previous value.  xred_ring_reduce sizes its own persistent grid.
+ * returns the previous value.  xred_ring_reduce applies it too, but never goes
+ * below the workgroups its on-chip accumulators need (one per 4 tiles).
  */
 XRED_API unsigned xred_set_max_workgroups(unsigned max_workgroups);
 
