@@ -103,9 +103,16 @@ class Timer:
         return out
 
     def cold_ms(self, fn, reps: int, flush) -> list:
+        """Each call after evicting L2 and the 256 MB MALL: 1 GiB is written and then
+        read, so the caches end up holding clean lines of the flush buffer only (a
+        write alone would leave dirty lines whose write-back the timed call pays)."""
         out = []
+        sink = getattr(self, "_sink", None)
+        if sink is None:
+            sink = self._sink = self.torch.empty((), dtype=flush.dtype, device=flush.device)
         for _ in range(reps):
-            flush.zero_()          # 1 GiB write evicts L2 and the 256 MB MALL
+            flush.zero_()
+            self.torch.sum(flush, dim=0, out=sink)
             self.e0.record()
             fn()
             self.e1.record()
