@@ -56,7 +56,7 @@ def test_header_compiles(tmp_path, compiler, lang):
 
 
 def test_constants(L):
-    assert L.xred_version() >= 100
+    assert L.xred_version() >= 200
     assert L.xred_acc_elem_size(0) == 4 and L.xred_acc_elem_size(1) == 4
     assert L.xred_acc_elem_size(2) == 4 and L.xred_acc_elem_size(7) == 4
     assert L.xred_acc_elem_size(5) == 8 and L.xred_acc_elem_size(6) == 8
@@ -191,6 +191,23 @@ def test_python_layer_raises(L):
         xr._lib.check(L.xred_allreduce_local(ptrs(A), 0, S(A), 16, 0, 0, None))
     assert e.value.name == "XRED_INVALID_ARGUMENT"
     assert "nsrc" in str(e.value)
+
+
+def test_torch_dtypes_map_to_codes():
+    """Element types taken from tensors: the new ones included."""
+    torch = pytest.importorskip("torch")
+    import paper_2510_20171_amd as xr
+    cases = {torch.float32: "f32", torch.bfloat16: "bf16", torch.float16: "f16",
+             torch.int32: "i32", torch.int64: "i64"}
+    for name, code in (("float8_e4m3fn", "e4m3"), ("float8_e5m2", "e5m2"), ("uint32", "u32"),
+                       ("uint64", "u64")):
+        if hasattr(torch, name):
+            cases[getattr(torch, name)] = code
+    for dt, code in cases.items():
+        assert xr._torch_dtype_name(torch.empty(1, dtype=dt)) == code
+        assert xr._dtype(torch.empty(1, dtype=dt), None) == xr.DTYPE[code]
+    with pytest.raises(xr.XredError):
+        xr._torch_dtype_name(torch.empty(1, dtype=torch.complex64))
 
 
 def test_product_does_not_import_oracle():
