@@ -414,7 +414,9 @@ def secondary(torch, xr, L, timer, wl, flush):
     res["more_types"] = more
 
     # simulated AllReduce schedules on one GPU: 8 ranks, ring and halving-doubling,
-    # at the bucket size and at 1 MiB per rank
+    # one launch per step and all steps in one launch ("ring1", "rhd1"), at the
+    # bucket size and at 1 MiB per rank; GB/s counts each form's own algorithmic
+    # bytes (5 (G-1) N per step schedule, 2 G N in one launch)
     sim = {}
     for label, n in (("64M", 64 << 20), ("512K", 512 << 10)):
         sends = [torch.randn(n, device="cuda").to(torch.bfloat16) for _ in range(8)]
@@ -422,12 +424,12 @@ def secondary(torch, xr, L, timer, wl, flush):
         arr_s = xr._lib.ptr_array([x.data_ptr() for x in sends])
         arr_r = xr._lib.ptr_array([x.data_ptr() for x in recvs])
         stream = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
-        for sched in ("ring", "rhd"):
+        for sched in ("ring", "rhd", "ring1", "rhd1"):
             fn = (lambda sc=xr.SCHEDULE[sched]:
                   L.xred_allreduce_sim(arr_s, arr_r, 8, n, 1, 0, sc, stream))
             ms = timer.loop_ms(fn, 20 if n > (1 << 20) else 200)
-            sim[f"{sched}_{label}"] = {"us": round(ms * 1e3, 2),
-                                       "GBs": round(5 * 7 * n * 2 / ms / 1e6, 1)}
+            ab = (2 * 8 if sched.endswith("1") else 5 * 7) * n * 2
+            sim[f"{sched}_{label}"] = {"us": round(ms * 1e3, 2), "GBs": round(ab / ms / 1e6, 1)}
         del sends, recvs
     res["sim_g8_bf16"] = sim
 
@@ -506,17 +508,24 @@ def build_workload(name, torch, xr, L, wl):
         arr_r = xr._lib.ptr_array([r.data_ptr() for r in recvs])
 
         def step():
-            st = L.xred_allreduce_sim(arr_s, arr_r, G, N, 1, 0, xr.SCHEDULE["ring"], stream)
+            st = L.xred_allreduce_sim(arr_s, arr_r, G, N, 1, 0, xr.SCHEDULE[w.schedule], stream)
             if st:
                 xr._lib.check(st)
         step._keep_inputs = (sends, recvs, arr_s, arr_r)
-        res = dict(step=step, alg_bytes=w.alg_bytes(), family="sim",
-                   kernel="whole ring schedule: 7 x sim_step_vec_kernel<bf16, sum, reduce> + "
-                          "7 x sim_step_vec_kernel<bf16, sum, copy>",
+        one = w.schedule.endswith("1")
+        base = w.schedule.rstrip("1")
+        if one:
+            kernel = f"sim_all_kernel<bf16, sum, {base}, vec> (every step in one launch)"
+            how = "every step in one launch, messages forwarded in registers"
+        else:
+            kernel = ("whole ring schedule: 7 x sim_step_vec_kernel<bf16, sum, reduce> + "
+                      "7 x sim_step_vec_kernel<bf16, sum, copy>")
+            how = "2(G-1) steps, zero-copy messages"
+        res = dict(step=step, alg_bytes=w.alg_bytes(), family="sim", kernel=kernel,
                    profile=ROOT / "profiles" / f"sim_bf16_{name}.md",
-                   config={"workload": f"{name}: ring AllReduce of {G} simulated ranks x {N} bf16 "
-                                       "on one GPU (2(G-1) steps, zero-copy messages)",
-                           "ranks": G, "N": N, "io_dtype": "bf16", "schedule": "ring"})
+                   config={"workload": f"{name}: {base} AllReduce of {G} simulated ranks x {N} "
+                                       f"bf16 on one GPU ({how})",
+                           "ranks": G, "N": N, "io_dtype": "bf16", "schedule": w.schedule})
         sample = [s[:1 << 22] for s in sends_np]
 
         def cpu():
@@ -526,10 +535,10 @@ def build_workload(name, torch, xr, L, wl):
             t0 = time.perf_counter()
             reps = 0
             while time.perf_counter() - t0 < 10.0:
-                orc.allreduce_sim(sample, "bf16", "sum", "ring", nthreads=cores)
+                orc.allreduce_sim(sample, "bf16", "sum", base, nthreads=cores)
                 reps += 1
             el = time.perf_counter() - t0
-            ab = 5 * (G - 1) * sample[0].size * 2 * reps
+            ab = w.alg_bytes() // N * sample[0].size * reps
             return {"value": round(ab / el / 1e9, 3), "unit": "GB/s", "cores": cores,
                     "kind": "oracle",
                     "sample": f"first {sample[0].size} elements of each rank, {reps} reps, "
@@ -610,7 +619,7 @@ def main() -> int:
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="c2",
-                    choices=["c1", "c2", "c3", "c3ring", "c4", "c5a", "c5b", "c2fp8", "sim"],
+                    choices=["c1", "c2", "c3", "c3ring", "c4", "c5a", "c5b", "c2fp8", "sim", "sim1"],
                     help="which workload one step runs (default: the c2 gradient bucket)")
     ap.add_argument("--no-secondary", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")

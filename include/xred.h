@@ -224,8 +224,11 @@ XRED_API size_t xred_ring_max_count(xred_dtype dtype);
 
 /* Schedules of xred_allreduce_sim. */
 typedef enum {
-    XRED_SCHEDULE_RING = 0,  /* ring: 2(G-1) steps */
-    XRED_SCHEDULE_RHD = 1    /* recursive halving-doubling, G a power of two: 2 log2(G) steps */
+    XRED_SCHEDULE_RING = 0,  /* ring: 2(G-1) steps, one launch each */
+    XRED_SCHEDULE_RHD = 1,   /* recursive halving-doubling, G a power of two: 2 log2(G)
+                                steps, one launch each */
+    XRED_SCHEDULE_RING_ONE_LAUNCH = 2, /* the ring, every step in one launch */
+    XRED_SCHEDULE_RHD_ONE_LAUNCH = 3   /* halving-doubling, every step in one launch */
 } xred_schedule;
 
 /*
@@ -253,6 +256,15 @@ typedef enum {
  *   chunks     xred_sim_chunk(count, G) elements each, i.e. ceil(count / G)
  *              rounded up to a multiple of 64; trailing chunks are short or
  *              empty.  (RHD blocks are the same chunks.)
+ * The ONE_LAUNCH schedules run every step in a single launch and give the
+ * same bits.  Each thread folds one element vector of one chunk in the
+ * schedule's order, handing every message to the next hop in registers,
+ * rounded to the I/O dtype exactly as when it is sent, and stores only the
+ * final bits into every recvbufs[r]: the messages the per-step schedule
+ * stores and then overwrites in its AllGather phase are never written (the
+ * intermediate stores ReduceCopy avoids, Section 5).  The call reads G N and
+ * writes G N elements instead of 5 (G-1) N, in one launch instead of
+ * 2 (G-1) or 2 log2(G).
  * When the stream reaches the end of the call every recvbufs[r] holds the
  * same bits.  Buffers that are all 16-byte aligned take the vector path,
  * others (element-aligned) a scalar path with the same results.

@@ -149,7 +149,8 @@ def allreduce_sim(sends, recvs, op: str = "sum", *, schedule: str = "ring", dtyp
                   stream=None) -> None:
     """A whole AllReduce over len(sends) simulated ranks on this GPU
     (xred_allreduce_sim): recvs[r] receives the reduced buffer at every rank.
-    schedule: "ring" or "rhd" (recursive halving-doubling)."""
+    schedule: "ring" or "rhd" (recursive halving-doubling), one launch per step, or
+    "ring1" / "rhd1", every step in one launch (same bits)."""
     L = load()
     if len(sends) != len(recvs):
         raise XredError(INVALID_ARGUMENT, "one recv buffer per send buffer")

@@ -23,7 +23,7 @@ SUCCESS, INVALID_ARGUMENT, UNSUPPORTED, ALIAS, HIP_ERROR, OUT_OF_MEMORY = range(
 MAX_SRC = 64
 STEP_INIT, STEP_FINAL = 1, 2
 ITEMS_ON_DEVICE = 1
-SCHEDULE = {"ring": 0, "rhd": 1}
+SCHEDULE = {"ring": 0, "rhd": 1, "ring1": 2, "rhd1": 3}   # 1: every step in one launch
 
 # struct xred_item (32 bytes)
 ITEM_DTYPE = np.dtype([("srcs", "<u8"), ("dst", "<u8"), ("count", "<u8"), ("nsrc", "<u4"),

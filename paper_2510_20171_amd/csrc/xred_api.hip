@@ -88,6 +88,7 @@ bool bad_overlap(const void *a, size_t na, const void *b, size_t nb, bool exact_
 bool mul_overflows(size_t a, size_t b) { return b != 0 && a > SIZE_MAX / b; }
 
 int cached_cus[kMaxDevices];
+int cached_ticks[kMaxDevices];
 
 long env_long(const char *name, long dflt)
 {
@@ -306,12 +307,19 @@ unsigned batched_rr_grid(int fit_per_cu)
 
 uint64_t wall_ticks_per_us()
 {
-    int dev = 0, khz = 0;
-    if (hipGetDevice(&dev) != hipSuccess ||
-        hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, dev) != hipSuccess ||
-        khz <= 0)
-        return 100;   // 100 MHz, the usual s_memrealtime rate
-    return (uint64_t)khz / 1000 > 0 ? (uint64_t)khz / 1000 : 1;
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return 100;
+    int t = __atomic_load_n(&cached_ticks[dev], __ATOMIC_RELAXED);
+    if (t <= 0) {
+        int khz = 0;
+        if (hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, dev) != hipSuccess ||
+            khz < 1000)
+            t = 100;   // 100 MHz, the usual device wall-clock rate
+        else
+            t = khz / 1000;
+        __atomic_store_n(&cached_ticks[dev], t, __ATOMIC_RELAXED);
+    }
+    return (uint64_t)t;
 }
 
 bool supported(xred_dtype dtype, xred_op op)
@@ -517,9 +525,10 @@ XRED_API xred_status xred_allreduce_sim(const void *const *sendbufs, void *const
 {
     if (nranks < 1 || nranks > XRED_MAX_SRC)
         return fail(XRED_INVALID_ARGUMENT, "nranks = %d outside 1..%d", nranks, XRED_MAX_SRC);
-    if (schedule != XRED_SCHEDULE_RING && schedule != XRED_SCHEDULE_RHD)
+    if (schedule < XRED_SCHEDULE_RING || schedule > XRED_SCHEDULE_RHD_ONE_LAUNCH)
         return fail(XRED_INVALID_ARGUMENT, "unknown schedule %d", (int)schedule);
-    if (schedule == XRED_SCHEDULE_RHD && (nranks & (nranks - 1)) != 0)
+    const bool rhd = schedule == XRED_SCHEDULE_RHD || schedule == XRED_SCHEDULE_RHD_ONE_LAUNCH;
+    if (rhd && (nranks & (nranks - 1)) != 0)
         return fail(XRED_INVALID_ARGUMENT, "halving-doubling needs a power-of-two nranks, not %d",
                     nranks);
     xred_status st = check_types(dtype, op);

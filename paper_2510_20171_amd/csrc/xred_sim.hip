@@ -1,5 +1,6 @@
 // xred_sim.hip -- a whole AllReduce over G simulated ranks on one GPU
-// (xred_allreduce_sim), one launch per step of the schedule.
+// (xred_allreduce_sim): one launch per step of the schedule, or every step in
+// one launch (see "one launch" below).
 //
 // Ring (the FTAR pipeline's ring, Section 5).  Rank q receives from q-1.
 // ReduceScatter step j = 1..G-1: rank q folds chunk c = q-1-j, reading the
@@ -143,6 +144,210 @@ hipError_t launch_sim_step(const SimStep &a, int G, bool vec, hipStream_t s)
     return hipGetLastError();
 }
 
+// ------------------------------------------------------------ one launch --
+// Every step in one launch.  Whatever the schedule, the bits every recv
+// buffer ends with at element i of chunk (block) c are one fold of the G
+// ranks' send values at i, in an order the schedule fixes, with the partial
+// rounded to the I/O type at every hop; every message stored during the
+// ReduceScatter phase is overwritten during the AllGather phase.  So one
+// thread folds element vector v of chunk c in that order, hands each message
+// to the next hop in registers (rounded exactly as when it is sent), and
+// stores only the final bits, once per rank: the intermediate forwarding
+// stores that ReduceCopy avoids (Section 5) are not made at all, and the call
+// moves 2 G N elements instead of the per-step schedule's 5 (G-1) N.
+//
+// Leaf k = 0..G-1 of chunk c is the send buffer of rank
+//   ring  (c+1+k) mod G, folded left to right: m = hop(m, leaf k), the
+//         message first and the receiving rank's own value second;
+//   RHD   c ^ bitrev(k), over log2 G bits.  The halving step at distance d
+//         makes, on rank c ^ y (y < d), hop(partial of rank c^(y+d), own
+//         partial): a pairwise tree over the leaves in bit-reversed order,
+//         the later subtree received, the earlier one own.  A binary counter
+//         evaluates it with one pending partial per tree level.
+// Leaves are loaded 8 at a time, all before the first store, so recv[r] may
+// be send[r].
+struct SimAll {
+    const char *send[XRED_MAX_SRC];
+    char *recv[XRED_MAX_SRC];
+};
+
+constexpr int kLeafBatch = 8;
+constexpr int kMaxLevels = 7;   // log2(XRED_MAX_SRC) + 1
+
+template <class T>
+__device__ __forceinline__ uint64_t load_bits(const char *base, size_t i)
+{
+    if constexpr (T::kSize == 1) return ((const uint8_t *)base)[i];
+    else if constexpr (T::kSize == 2) return ((const uint16_t *)base)[i];
+    else if constexpr (T::kSize == 4) return ((const uint32_t *)base)[i];
+    else return ((const uint64_t *)base)[i];
+}
+
+template <class T>
+__device__ __forceinline__ void store_bits(char *base, size_t i, uint64_t v)
+{
+    if constexpr (T::kSize == 1) ((uint8_t *)base)[i] = (uint8_t)v;
+    else if constexpr (T::kSize == 2) ((uint16_t *)base)[i] = (uint16_t)v;
+    else if constexpr (T::kSize == 4) ((uint32_t *)base)[i] = (uint32_t)v;
+    else ((uint64_t *)base)[i] = v;
+}
+
+// One lane's share of a work item: a 16-byte vector (VEC) or one element.
+template <class T, bool VEC>
+struct Lane;
+
+template <class T>
+struct Lane<T, true> {
+    using R = u32x4;
+    size_t off;      // byte offset of the tile in every buffer
+    uint32_t nrec;   // bytes of the tile in range
+    __device__ R load(const char *base, bool present) const
+    {
+        // an absent leaf reads through an empty descriptor: zeros, no access
+        return bload<kLoadStream>(make_rsrc(base + off, present ? nrec : 0u), threadIdx.x * 16u);
+    }
+    __device__ void store(R v, char *base) const
+    {
+        bstore<kStoreOut>(v, make_rsrc(base + off, nrec), threadIdx.x * 16u);
+    }
+    template <class Op>
+    __device__ static R hop(R in, R own)
+    {
+        typename T::Acc x[T::kVec];
+        up_vec<T>(in, x);
+        fold_vec<T, Op>(x, own);
+        return down_vec<T, Op>(x);
+    }
+};
+
+template <class T>
+struct Lane<T, false> {
+    using R = uint64_t;
+    size_t i;        // element index in every buffer
+    __device__ R load(const char *base, bool present) const
+    {
+        return present ? load_bits<T>(base, i) : 0;
+    }
+    __device__ void store(R v, char *base) const { store_bits<T>(base, i, v); }
+    template <class Op>
+    __device__ static R hop(R in, R own)
+    {
+        const typename T::Acc x =
+            combine<T, Op>(up1<T>((const char *)&in, 0), up1<T>((const char *)&own, 0));
+        R out = 0;
+        down1<T, Op>((char *)&out, 0, x);
+        return out;
+    }
+};
+
+template <class T, class Op, bool RHD, class L>
+__device__ __forceinline__ void fold_chunk(const SimAll &a, int G, int lg, int c, const L &lane)
+{
+    using R = typename L::R;
+    R m{};
+    R pending[kMaxLevels];
+    for (int k0 = 0; k0 < G; k0 += kLeafBatch) {
+        R v[kLeafBatch];
+#pragma unroll
+        for (int u = 0; u < kLeafBatch; ++u) {
+            const int k = k0 + u;
+            int rank = 0;
+            if (k < G)
+                rank = RHD ? c ^ (int)(__builtin_bitreverse32((uint32_t)k) >> (32 - lg))
+                           : (c + 1 + k) % G;
+            v[u] = lane.load(a.send[rank], k < G);
+        }
+#pragma unroll
+        for (int u = 0; u < kLeafBatch; ++u) {
+            const int k = k0 + u;
+            if (k >= G) break;
+            if constexpr (!RHD) {
+                m = k == 0 ? v[u] : L::template hop<Op>(m, v[u]);
+            } else {
+                R x = v[u];
+#pragma unroll
+                for (int l = 0; l < kMaxLevels; ++l) {
+                    if (((k >> l) & 1) == 0) {
+                        pending[l] = x;
+                        break;
+                    }
+                    x = L::template hop<Op>(x, pending[l]);
+                }
+            }
+        }
+    }
+    if constexpr (RHD) {
+#pragma unroll
+        for (int l = 0; l < kMaxLevels; ++l)
+            if (l == lg) m = pending[l];
+    }
+    for (int r = 0; r < G; ++r) lane.store(m, a.recv[r]);
+}
+
+// Work item w: chunk w % G, tile w / G of it (the last tile of each chunk
+// takes the elements after its last full vector).  VEC: 16-byte aligned
+// buffers; otherwise one element per thread.
+template <class T, class Op, bool RHD, bool VEC>
+__global__ __launch_bounds__(kB) void sim_all_kernel(SimAll a, int G, int lg, uint64_t M,
+                                                     uint64_t count, uint64_t tiles)
+{
+    constexpr uint32_t kTileBytes = (uint32_t)kB * 16u;
+    const uint64_t work = tiles * (uint64_t)G;
+    for (uint64_t w = blockIdx.x; w < work; w += gridDim.x) {
+        const int c = (int)(w % (uint64_t)G);
+        const uint64_t t = w / (uint64_t)G;
+        const uint64_t lo = (uint64_t)c * M < count ? (uint64_t)c * M : count;
+        const uint64_t hi = (uint64_t)(c + 1) * M < count ? (uint64_t)(c + 1) * M : count;
+        const uint64_t len = hi - lo;
+        if constexpr (VEC) {
+            const uint64_t nvec = len / T::kVec;
+            const size_t vbytes = nvec * 16;
+            const uint64_t vtiles = (vbytes + kTileBytes - 1) / kTileBytes;
+            if (t < vtiles) {
+                const size_t toff = t * kTileBytes;
+                fold_chunk<T, Op, RHD>(a, G, lg, c,
+                                       Lane<T, true>{lo * T::kSize + toff,
+                                                     tile_nrec(vbytes, toff, kTileBytes)});
+            } else if (t == vtiles && threadIdx.x < len - nvec * T::kVec) {
+                fold_chunk<T, Op, RHD>(a, G, lg, c,
+                                       Lane<T, false>{lo + nvec * T::kVec + threadIdx.x});
+            }
+        } else {
+            const uint64_t e = t * kB + threadIdx.x;
+            if (e < len) fold_chunk<T, Op, RHD>(a, G, lg, c, Lane<T, false>{lo + e});
+        }
+    }
+}
+
+template <class T, class Op>
+hipError_t launch_all(const char *const *send, char *const *recv, int G, size_t count, bool rhd,
+                      bool vec, hipStream_t s)
+{
+    SimAll a;
+    for (int q = 0; q < XRED_MAX_SRC; ++q) {
+        a.send[q] = q < G ? send[q] : nullptr;
+        a.recv[q] = q < G ? recv[q] : nullptr;
+    }
+    int lg = 0;
+    while ((1 << lg) < G) ++lg;
+    const uint64_t M = sim_chunk(count, G);
+    const uint64_t tiles = vec ? (M * T::kSize + kB * 16u - 1) / (kB * 16u) + 1 : (M + kB - 1) / kB;
+    const dim3 grid(grid_for(tiles * (uint64_t)G));
+    if (rhd && vec)
+        hipLaunchKernelGGL((sim_all_kernel<T, Op, true, true>), grid, dim3(kB), 0, s, a, G, lg, M,
+                           (uint64_t)count, tiles);
+    else if (rhd)
+        hipLaunchKernelGGL((sim_all_kernel<T, Op, true, false>), grid, dim3(kB), 0, s, a, G, lg, M,
+                           (uint64_t)count, tiles);
+    else if (vec)
+        hipLaunchKernelGGL((sim_all_kernel<T, Op, false, true>), grid, dim3(kB), 0, s, a, G, lg, M,
+                           (uint64_t)count, tiles);
+    else
+        hipLaunchKernelGGL((sim_all_kernel<T, Op, false, false>), grid, dim3(kB), 0, s, a, G, lg,
+                           M, (uint64_t)count, tiles);
+    return hipGetLastError();
+}
+
 int rank_mod(int r, int G) { return ((r % G) + G) % G; }
 
 template <class T, class Op>
@@ -165,6 +370,9 @@ hipError_t run(const char *const *send, char *const *recv, int G, size_t count,
         a.len[0] = count;
         return launch_sim_step<T, Op, true>(a, 1, vec, s);
     }
+    if (sched == XRED_SCHEDULE_RING_ONE_LAUNCH || sched == XRED_SCHEDULE_RHD_ONE_LAUNCH)
+        return launch_all<T, Op>(send, recv, G, count, sched == XRED_SCHEDULE_RHD_ONE_LAUNCH, vec,
+                                 s);
     if (sched == XRED_SCHEDULE_RING) {
         for (int j = 1; j <= G - 1 && e == hipSuccess; ++j) {
             for (int q = 0; q < G; ++q) {

@@ -119,9 +119,14 @@ def ptrs(*xs):
     # xred_allreduce_sim(sends, recvs, nranks, count, dtype, op, schedule, stream)
     (lambda L: L.xred_allreduce_sim(ptrs(A), ptrs(A + 8192), 0, 16, 1, 0, 0, None), 1),
     (lambda L: L.xred_allreduce_sim(ptrs(A), ptrs(A + 8192), 65, 16, 1, 0, 0, None), 1),
-    (lambda L: L.xred_allreduce_sim(ptrs(A), ptrs(A + 8192), 1, 16, 1, 0, 2, None), 1),
+    (lambda L: L.xred_allreduce_sim(ptrs(A), ptrs(A + 8192), 1, 16, 1, 0, 4, None), 1),
+    (lambda L: L.xred_allreduce_sim(ptrs(A), ptrs(A + 8192), 1, 16, 1, 0, -1, None), 1),
     (lambda L: L.xred_allreduce_sim(ptrs(A, A + 4096, A + 8192), ptrs(A + 16384, A + 20480, A + 24576),
                                     3, 16, 1, 0, 1, None), 1),
+    (lambda L: L.xred_allreduce_sim(ptrs(A, A + 4096, A + 8192), ptrs(A + 16384, A + 20480, A + 24576),
+                                    3, 16, 1, 0, 3, None), 1),
+    (lambda L: L.xred_allreduce_sim(ptrs(A, A + 4096), ptrs(A + 8192, A + 12288), 2, 16, 1, 4, 2,
+                                    None), 2),
     (lambda L: L.xred_allreduce_sim(None, ptrs(A + 8192), 1, 16, 1, 0, 0, None), 1),
     (lambda L: L.xred_allreduce_sim(ptrs(A, A + 4096), ptrs(A + 8192, 0), 2, 16, 1, 0, 0, None), 1),
     (lambda L: L.xred_allreduce_sim(ptrs(A, A + 4097), ptrs(A + 8192, A + 12288), 2, 16, 1, 0, 0,

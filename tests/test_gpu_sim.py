@@ -8,7 +8,9 @@ bits.  Covered: every dtype x op; ring G = 1, 2, 3, 5, 8, 13 and
 halving-doubling G = 1, 2, 4, 8, 16; sizes from one element to several tiles
 per chunk with short and empty trailing chunks; in place; element-aligned
 (not 16-byte aligned) buffers; a CU budget; the full G=8 x 2^26 bf16 bucket
-the benchmark times, for both schedules.
+the benchmark times, for both schedules.  Each schedule also runs with all of
+its steps in one launch ("ring1", "rhd1"), which must give the same bits as
+the oracle's simulation of that schedule.
 """
 import os
 
@@ -44,6 +46,10 @@ def _check(outs, exp, dtype, op, what):
         gu.assert_parity(o, exp[r], dtype, op, f"{what} rank {r}")
 
 
+def _oracle_schedule(schedule):
+    return schedule.rstrip("1")
+
+
 def _run(xr, sends_np, dtype, op, schedule, in_place=False):
     sends = [gu.to_dev(s, dtype) for s in sends_np]
     recvs = sends if in_place else [torch.empty_like(s) for s in sends]
@@ -66,23 +72,24 @@ def test_ring_and_rhd_parity(xr, orc, dtype, op):
                 if G * n > (1 << 21):
                     continue
                 sends = [pins.random_column_values(rng, dtype, n) for _ in range(G)]
-                outs = _run(xr, sends, dtype, op, schedule)
                 exp = orc.allreduce_sim(sends, dtype, op, schedule)
-                _check(outs, exp, dtype, op, f"{schedule} {dtype} {op} G={G} n={n}")
+                for variant in (schedule, schedule + "1"):
+                    outs = _run(xr, sends, dtype, op, variant)
+                    _check(outs, exp, dtype, op, f"{variant} {dtype} {op} G={G} n={n}")
 
 
-@pytest.mark.parametrize("schedule", ["ring", "rhd"])
+@pytest.mark.parametrize("schedule", ["ring", "rhd", "ring1", "rhd1"])
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
 def test_in_place(xr, orc, schedule, dtype):
     rng = np.random.default_rng(7)
     for G, n in ((2, 999), (4, 64 * 4 + 70), (8, (1 << 16) + 3)):
         sends = [pins.random_column_values(rng, dtype, n) for _ in range(G)]
         outs = _run(xr, sends, dtype, "sum", schedule, in_place=True)
-        _check(outs, orc.allreduce_sim(sends, dtype, "sum", schedule), dtype, "sum",
-               f"in place {schedule} G={G}")
+        _check(outs, orc.allreduce_sim(sends, dtype, "sum", _oracle_schedule(schedule)), dtype,
+               "sum", f"in place {schedule} G={G}")
 
 
-@pytest.mark.parametrize("schedule", ["ring", "rhd"])
+@pytest.mark.parametrize("schedule", ["ring", "rhd", "ring1", "rhd1"])
 def test_element_aligned_buffers(xr, orc, schedule):
     """Buffers one element off 16-byte alignment take the scalar path."""
     rng = np.random.default_rng(8)
@@ -95,8 +102,8 @@ def test_element_aligned_buffers(xr, orc, schedule):
         recvs = [b[1:] for b in rbig]
         xr.allreduce_sim(sends, recvs, "max", schedule=schedule, dtype=dtype)
         torch.cuda.synchronize()
-        _check(recvs, orc.allreduce_sim(sends_np, dtype, "max", schedule), dtype, "max",
-               f"element-aligned {schedule} {dtype}")
+        _check(recvs, orc.allreduce_sim(sends_np, dtype, "max", _oracle_schedule(schedule)),
+               dtype, "max", f"element-aligned {schedule} {dtype}")
 
 
 def test_budget_does_not_change_results(xr, orc):
@@ -105,19 +112,24 @@ def test_budget_does_not_change_results(xr, orc):
     sends = [pins.random_column_values(rng, "bf16", n) for _ in range(G)]
     exp = orc.allreduce_sim(sends, "bf16", "sum", "ring")
     for budget in (1, 7, 0):
-        prev = xr.set_max_workgroups(budget)
-        try:
-            outs = _run(xr, sends, "bf16", "sum", "ring")
-        finally:
-            xr.set_max_workgroups(prev)
-        _check(outs, exp, "bf16", "sum", f"budget {budget}")
+        for schedule in ("ring", "ring1"):
+            prev = xr.set_max_workgroups(budget)
+            try:
+                outs = _run(xr, sends, "bf16", "sum", schedule)
+            finally:
+                xr.set_max_workgroups(prev)
+            _check(outs, exp, "bf16", "sum", f"{schedule} budget {budget}")
 
 
 @pytest.mark.parametrize("schedule", ["ring", "rhd"])
 def test_full_bucket(xr, orc, schedule):
-    """The benchmark's workload: 8 ranks x 2^26 bf16, both schedules."""
+    """The benchmark's workload: 8 ranks x 2^26 bf16, both schedules, step by
+    step and in one launch."""
     w = wl.WORKLOADS["sim"]
     sends = wl.sources(w)
-    outs = _run(xr, sends, w.dtype, w.op, schedule)
     exp = orc.allreduce_sim(sends, w.dtype, w.op, schedule, nthreads=CORES)
-    _check(outs, exp, w.dtype, w.op, f"sim {schedule}")
+    for variant in (schedule, schedule + "1"):
+        outs = _run(xr, sends, w.dtype, w.op, variant)
+        _check(outs, exp, w.dtype, w.op, f"sim {variant}")
+        del outs
+        torch.cuda.empty_cache()

@@ -27,7 +27,10 @@ Workloads (M = 2^20, K = 2^10 elements):
                         footprint, 128 MiB per source, in e4m3)
   sim  allreduce_sim    G=8 ranks x 64M bf16 sum N(0,1)*1e-3 per rank (a c2-sized
                         gradient bucket AllReduced over 8 simulated ranks; the
-                        send buffer of rank r is source r)
+                        send buffer of rank r is source r), ring schedule, one
+                        launch per step
+  sim1 allreduce_sim    the same inputs, ring schedule with every step in one
+                        launch (messages forwarded in registers)
 """
 from __future__ import annotations
 
@@ -56,12 +59,17 @@ class Workload:
     dist: str
     seed_base: int
     nitems: int = 0
+    schedule: str = ""  # sim: "ring", "rhd", "ring1", "rhd1"
 
     def alg_bytes(self, sizes=None) -> int:
         """(P+1)*N*sizeof bytes of one pass (sizes: per-item counts for batched)."""
         es = ELEM_SIZE[self.dtype]
         if self.kind == "batched":
             return int(sum((self.nsrc + 1) * int(n) * es for n in sizes))
+        if self.kind == "sim" and self.schedule.endswith("1"):
+            # every step in one launch: each rank's send buffer read once,
+            # each rank's recv buffer written once
+            return 2 * self.nsrc * self.count * es
         if self.kind == "sim":
             # G-1 reduce steps reading two chunks and writing one, G-1 copy
             # steps reading one and writing one, every chunk once per step
@@ -76,7 +84,10 @@ WORKLOADS = {
     "c4": Workload("c4", "batched", "bf16", "sum", 8, 0, "uniform", 4000, nitems=4096),
     "c5a": Workload("c5a", "allreduce", "i32", "sum", 32, 8 * M, "int32", 5000),
     "c5b": Workload("c5b", "allreduce", "f32", "max", 32, 8 * M, "normal_specials", 5100),
-    "sim": Workload("sim", "sim", "bf16", "sum", 8, 64 * M, "normal_1e-3", 7000),
+    "sim": Workload("sim", "sim", "bf16", "sum", 8, 64 * M, "normal_1e-3", 7000,
+                    schedule="ring"),
+    "sim1": Workload("sim1", "sim", "bf16", "sum", 8, 64 * M, "normal_1e-3", 7000,
+                     schedule="ring1"),
     "c2fp8": Workload("c2fp8", "allreduce", "e4m3", "sum", 8, 128 * M, "fp8_loguniform", 8000),
 }
 
