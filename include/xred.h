@@ -43,9 +43,13 @@
  *   - Every call is stream-ordered and returns once the work is enqueued.
  *     Host arrays passed in (the srcs pointer array, host-side items) are
  *     consumed before the call returns and may be reused at once.
- *   - Every argument is validated before anything is enqueued: on any return
- *     other than XRED_SUCCESS nothing was enqueued and xred_last_error()
- *     describes the problem.  count == 0 succeeds with no launch.
+ *   - Every argument is validated before anything is enqueued: on
+ *     XRED_INVALID_ARGUMENT, XRED_UNSUPPORTED, XRED_ALIAS and
+ *     XRED_OUT_OF_MEMORY nothing was enqueued.  XRED_HIP_ERROR reports a
+ *     runtime failure while enqueueing; the work enqueued before it (earlier
+ *     launches of a multi-launch call, a descriptor copy) stays enqueued.
+ *     xred_last_error() describes the problem.  count == 0 succeeds with no
+ *     launch.
  *   - Device faults (e.g. a pointer to freed memory) surface at the caller's
  *     next synchronisation of the stream, as for any HIP kernel.
  *   - Element pointers must be aligned to the element size; 16-byte aligned

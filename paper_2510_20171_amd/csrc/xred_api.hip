@@ -251,16 +251,22 @@ xred_status batched_host(const xred_item *items, int nitems, xred_dtype dtype, x
     }
     e = hipMemcpyAsync(s.dev, s.host, need, hipMemcpyHostToDevice, stream);
     if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync(descriptors)");
+    hipError_t le;
     if (rr)
-        e = launch_batched_rr(dtype, op, (const xred_item *)d, nitems,
-                              (const uint32_t *)(d + items_bytes), stream);
+        le = launch_batched_rr(dtype, op, (const xred_item *)d, nitems,
+                               (const uint32_t *)(d + items_bytes), stream);
     else
-        e = launch_batched_planned(dtype, op, (const xred_item *)d, nitems,
-                                   (const WgStart *)(d + items_bytes), grid, stream);
-    if (e != hipSuccess) return hip_fail(e, "batched launch");
+        le = launch_batched_planned(dtype, op, (const xred_item *)d, nitems,
+                                    (const WgStart *)(d + items_bytes), grid, stream);
+    // The copy is enqueued whatever the launch did: the slot stays busy until
+    // the stream has passed it.
     e = hipEventRecord(s.done, stream);
-    if (e != hipSuccess) return hip_fail(e, "hipEventRecord(staging slot)");
+    if (e != hipSuccess) {
+        (void)hipStreamSynchronize(stream);
+        return hip_fail(e, "hipEventRecord(staging slot)");
+    }
     s.pending = true;
+    if (le != hipSuccess) return hip_fail(le, "batched launch");
     return XRED_SUCCESS;
 }
 
