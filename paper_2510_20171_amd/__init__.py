@@ -20,7 +20,8 @@ from __future__ import annotations
 
 import ctypes
 
-from ._lib import (ALIAS, DTYPE, EXPORTS, HIP_ERROR, INVALID_ARGUMENT, ITEM_DTYPE,
+from ._lib import (ACC_SIZE, ALIAS, DTYPE, ELEM_SIZE, EXPORTS, HIP_ERROR, INVALID_ARGUMENT,
+                   ITEM_DTYPE,
                    ITEMS_ON_DEVICE, MAX_SRC, OP, OUT_OF_MEMORY, SCHEDULE, STEP_FINAL, STEP_INIT,
                    SUCCESS, UNSUPPORTED, XredError, XredItem, check, load, ptr_array)
 
@@ -44,8 +45,38 @@ def _torch_dtype_name(t) -> str:
         raise XredError(INVALID_ARGUMENT, f"tensor dtype {t.dtype} is not supported") from None
 
 
+def _dtype_name(t, dtype) -> str:
+    name = dtype if dtype is not None else _torch_dtype_name(t)
+    if name not in DTYPE:
+        raise XredError(INVALID_ARGUMENT, f"unknown dtype {name!r}")
+    return name
+
+
 def _dtype(t, dtype):
-    return DTYPE[dtype] if dtype is not None else DTYPE[_torch_dtype_name(t)]
+    return DTYPE[_dtype_name(t, dtype)]
+
+
+def _require(tensors, n, es, what, device, host_ok=False):
+    """Every tensor: on `device` (or pinned host memory when host_ok),
+    contiguous, elements of es bytes and n elements (at least n when host_ok),
+    so that the kernels never touch memory outside it."""
+    for k, t in enumerate(tensors):
+        if t is None:
+            continue
+        if t.is_cuda:
+            if t.device != device:
+                raise XredError(INVALID_ARGUMENT, f"{what}[{k}] is on {t.device}, not {device}")
+        elif not (host_ok and t.is_pinned()):
+            raise XredError(INVALID_ARGUMENT, f"{what}[{k}] is not in GPU"
+                            + (" or pinned host" if host_ok else "") + " memory")
+        if not t.is_contiguous():
+            raise XredError(INVALID_ARGUMENT, f"{what}[{k}] is not contiguous")
+        if t.element_size() != es:
+            raise XredError(INVALID_ARGUMENT, f"{what}[{k}] has {t.element_size()}-byte elements,"
+                            f" the dtype needs {es}")
+        if t.numel() < n if host_ok else t.numel() != n:
+            raise XredError(INVALID_ARGUMENT, f"{what}[{k}] has {t.numel()} elements, expected "
+                            f"{'at least ' if host_ok else ''}{n}")
 
 
 def _stream(t, stream):
@@ -63,16 +94,22 @@ def allreduce_local(srcs, out, op: str = "sum", *, dtype=None, stream=None) -> N
     """out[i] = fold_op(srcs[0][i], ..., srcs[P-1][i]) in source order (xred_allreduce_local)."""
     L = load()
     n = out.numel()
+    dt = _dtype_name(out, dtype)
+    _require([out], n, ELEM_SIZE[dt], "out", out.device)
+    _require(srcs, n, ELEM_SIZE[dt], "srcs", out.device)
     check(L.xred_allreduce_local(ptr_array([s.data_ptr() for s in srcs]), len(srcs), _ptr(out),
-                                 n, _dtype(out, dtype), OP[op], _stream(out, stream)))
+                                 n, DTYPE[dt], OP[op], _stream(out, stream)))
 
 
 def reduce_scatter_local(srcs, rank: int, out, op: str = "sum", *, dtype=None,
                          stream=None) -> None:
     """Shard `rank` of a ReduceScatter over full send buffers srcs (xred_reduce_scatter_local)."""
     L = load()
+    dt = _dtype_name(out, dtype)
+    _require([out], out.numel(), ELEM_SIZE[dt], "out", out.device)
+    _require(srcs, out.numel() * len(srcs), ELEM_SIZE[dt], "srcs", out.device)
     check(L.xred_reduce_scatter_local(ptr_array([s.data_ptr() for s in srcs]), len(srcs), rank,
-                                      _ptr(out), out.numel(), _dtype(out, dtype), OP[op],
+                                      _ptr(out), out.numel(), DTYPE[dt], OP[op],
                                       _stream(out, stream)))
 
 
@@ -81,15 +118,28 @@ def reduce_copy_step(inp, acc, out=None, op: str = "sum", *, init: bool = False,
     """One ring ReduceCopy step into a 4-byte accumulator (xred_reduce_copy_step)."""
     L = load()
     flags = (STEP_INIT if init else 0) | (STEP_FINAL if final else 0)
-    check(L.xred_reduce_copy_step(_ptr(inp), _ptr(acc), _ptr(out), inp.numel(),
-                                  _dtype(inp, dtype), OP[op], flags, _stream(inp, stream)))
+    n = inp.numel()
+    dt = _dtype_name(inp, dtype)
+    _require([inp], n, ELEM_SIZE[dt], "in", inp.device)
+    if not (init and final):
+        if acc is None:
+            raise XredError(INVALID_ARGUMENT, "acc is required unless init and final")
+        _require([acc], n, ACC_SIZE[dt], "acc", inp.device)
+    if final:
+        if out is None:
+            raise XredError(INVALID_ARGUMENT, "out is required with final")
+        _require([out], n, ELEM_SIZE[dt], "out", inp.device)
+    check(L.xred_reduce_copy_step(_ptr(inp), _ptr(acc), _ptr(out), n, DTYPE[dt], OP[op], flags,
+                                  _stream(inp, stream)))
 
 
 def acc_cast(acc, out, *, dtype=None, stream=None) -> None:
     """out = down(acc): closing cast of a step-wise sequence (xred_acc_cast)."""
     L = load()
-    check(L.xred_acc_cast(_ptr(acc), _ptr(out), out.numel(), _dtype(out, dtype),
-                          _stream(out, stream)))
+    dt = _dtype_name(out, dtype)
+    _require([out], out.numel(), ELEM_SIZE[dt], "out", out.device)
+    _require([acc], out.numel(), ACC_SIZE[dt], "acc", out.device)
+    check(L.xred_acc_cast(_ptr(acc), _ptr(out), out.numel(), DTYPE[dt], _stream(out, stream)))
 
 
 def pack_items(items):
@@ -122,7 +172,11 @@ def batched_reduce(items, op: str = "sum", *, dtype: str, stream=None, device=No
         return
     keep = []
     rows = []
-    for srcs, out in items:
+    es = ELEM_SIZE[_dtype_name(None, dtype)]
+    dev = items[0][1].device if items else None
+    for k, (srcs, out) in enumerate(items):
+        _require([out], out.numel(), es, f"items[{k}].out", dev)
+        _require(srcs, out.numel(), es, f"items[{k}].srcs", dev)
         pa = ptr_array([s.data_ptr() for s in srcs])
         keep.append(pa)
         rows.append((ctypes.addressof(pa), out.data_ptr(), out.numel(), len(srcs)))
@@ -140,9 +194,14 @@ def ring_reduce(chunks, out, op: str = "sum", *, ready=None, epoch: int = 1,
     or device memory; status: None or a 1-element int32 tensor (pinned or
     device) that receives 1 if a wait timed out."""
     L = load()
+    dt = _dtype_name(out, dtype)
+    _require([out], out.numel(), ELEM_SIZE[dt], "out", out.device)
+    _require(chunks, out.numel(), ELEM_SIZE[dt], "chunks", out.device)
+    _require([ready], len(chunks), 4, "ready", out.device, host_ok=True)
+    _require([status], 1, 4, "status", out.device, host_ok=True)
     check(L.xred_ring_reduce(ptr_array([c.data_ptr() for c in chunks]), len(chunks), _ptr(out),
-                             out.numel(), _dtype(out, dtype), OP[op], _ptr(ready),
-                             epoch & 0xFFFFFFFF, timeout_us, _ptr(status), _stream(out, stream)))
+                             out.numel(), DTYPE[dt], OP[op], _ptr(ready), epoch & 0xFFFFFFFF,
+                             timeout_us, _ptr(status), _stream(out, stream)))
 
 
 def allreduce_sim(sends, recvs, op: str = "sum", *, schedule: str = "ring", dtype=None,
@@ -155,10 +214,12 @@ def allreduce_sim(sends, recvs, op: str = "sum", *, schedule: str = "ring", dtyp
     if len(sends) != len(recvs):
         raise XredError(INVALID_ARGUMENT, "one recv buffer per send buffer")
     out = recvs[0]
+    dt = _dtype_name(out, dtype)
+    _require(recvs, out.numel(), ELEM_SIZE[dt], "recvs", out.device)
+    _require(sends, out.numel(), ELEM_SIZE[dt], "sends", out.device)
     check(L.xred_allreduce_sim(ptr_array([s.data_ptr() for s in sends]),
                                ptr_array([r.data_ptr() for r in recvs]), len(sends), out.numel(),
-                               _dtype(out, dtype), OP[op], SCHEDULE[schedule],
-                               _stream(out, stream)))
+                               DTYPE[dt], OP[op], SCHEDULE[schedule], _stream(out, stream)))
 
 
 def sim_chunk(count: int, nranks: int) -> int:
