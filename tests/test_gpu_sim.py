@@ -5,7 +5,8 @@ message-by-message simulation of the same schedule.
 Every rank's output must equal the oracle's bit for bit (NaN payloads of
 float sum/prod compare by NaN-ness only), and all ranks must hold the same
 bits.  Covered: every dtype x op; ring G = 1, 2, 3, 5, 8, 13 and
-halving-doubling G = 1, 2, 4, 8, 16; sizes from one element to several tiles
+halving-doubling G = 1, 2, 4, 8, 16, and G = 32, 64 (the maximum) for three
+dtype x op pairs; sizes from one element to several tiles
 per chunk with short and empty trailing chunks; in place; element-aligned
 (not 16-byte aligned) buffers; a CU budget; the full G=8 x 2^26 bf16 bucket
 the benchmark times, for both schedules.  Each schedule also runs with all of
@@ -133,3 +134,19 @@ def test_full_bucket(xr, orc, schedule):
         _check(outs, exp, w.dtype, w.op, f"sim {variant}")
         del outs
         torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("G", [32, 64])
+def test_most_ranks(xr, orc, G):
+    """G = 32 and the maximum 64 (every tree level of the one-launch
+    halving-doubling, leaves loaded in 4 or 8 batches), all four schedules,
+    with a ragged last chunk and empty trailing chunks."""
+    rng = np.random.default_rng(70 + G)
+    for dtype, op in (("bf16", "sum"), ("f32", "max"), ("i32", "prod")):
+        for n in (64 * G + 70, 64 * (G - 3) + 1, 4096 * G + 3):
+            sends = [pins.random_column_values(rng, dtype, n) for _ in range(G)]
+            for schedule in ("ring", "rhd"):
+                exp = orc.allreduce_sim(sends, dtype, op, schedule)
+                for variant in (schedule, schedule + "1"):
+                    outs = _run(xr, sends, dtype, op, variant)
+                    _check(outs, exp, dtype, op, f"{variant} {dtype} {op} G={G} n={n}")
