@@ -269,6 +269,22 @@ def secondary(torch, xr, L, timer, wl, flush):
             L.xred_reduce_copy_step(c, ap, None, w.count, 1, 0, 0, stream)
     seq_ms = timer.loop_ms(seq, 50)
     st_ms = timer.loop_ms(steps15, 50) / 15
+    # the same sequence captured once in a HIP graph (17 kernel nodes) and
+    # replayed; its output is checked against the eager sequence's
+    seq()
+    eager = out.clone()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        cs = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+        L.xred_reduce_copy_step(cp[0], ap, None, w.count, 1, 0, 1, cs)
+        for c in cp[1:]:
+            L.xred_reduce_copy_step(c, ap, None, w.count, 1, 0, 0, cs)
+        L.xred_acc_cast(ap, op_, w.count, 1, cs)
+    out.zero_()
+    graph_ms = timer.loop_ms(graph.replay, 50)
+    torch.cuda.synchronize()
+    graph_ok = bool(torch.equal(out.view(torch.int16), eager.view(torch.int16)))
+    del graph
     fused = torch.empty_like(out)
     ffn = reduce_call(L, xr, chunks, fused, "bf16", "sum")
     fused_ms = timer.loop_ms(ffn, 50)
@@ -299,6 +315,8 @@ def secondary(torch, xr, L, timer, wl, flush):
     res["c3"] = {"us_per_step": round(st_ms * 1e3, 2),
                  "step_GBs_moved": round(w.count * 10 / st_ms / 1e6, 1),
                  "us_sequence": round(seq_ms * 1e3, 2),
+                 "us_sequence_graph_replay": round(graph_ms * 1e3, 2),
+                 "graph_replay_matches_eager": graph_ok,
                  "sequence_GBs_alg": round(17 * w.count * 2 / seq_ms / 1e6, 1),
                  "sequence_GBs_moved": round(moved / seq_ms / 1e6, 1),
                  "fused_16src_us": round(fused_ms * 1e3, 2),
