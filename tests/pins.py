@@ -175,6 +175,33 @@ def pin_golden_bf16(orc) -> None:
         assert int(g) == e, f"{x:#010x}: got {int(g):#06x} expected {e:#06x}"
 
 
+def _golden_rows(name):
+    for line in (GOLDEN / name).read_text().splitlines():
+        if line.strip() and not line.startswith("#"):
+            yield line.split()[:3]
+
+
+def pin_golden_narrow(orc) -> None:
+    """fp16 / fp8 down() and up() == the cases the formats' definitions fix
+    (tests/golden/narrow_cases.txt, tests/golden/widen_cases.txt)."""
+    rows = list(_golden_rows("narrow_cases.txt"))
+    for dt in ("f16", "e4m3", "e5m2"):
+        mine = [(int(f, 16), int(b, 16)) for d, f, b in rows if d == dt]
+        got = orc.f32_bits_to_small(np.array([f for f, _ in mine], np.uint32), dt)
+        for (f, e), g in zip(mine, got.tolist()):
+            assert g == e, f"{dt} down({f:#010x}): got {g:#x} expected {e:#x}"
+    rows = list(_golden_rows("widen_cases.txt"))
+    for dt in ("f16", "e4m3", "e5m2"):
+        mine = [(int(b, 16), w) for d, b, w in rows if d == dt]
+        got = orc.small_to_f32_bits(np.array([b for b, _ in mine]), dt)
+        for (b, e), g in zip(mine, got.tolist()):
+            if e == "nan":
+                ok = (g & 0x7F800000) == 0x7F800000 and (g & 0x7FFFFF) != 0
+            else:
+                ok = g == int(e, 16)
+            assert ok, f"{dt} up({b:#x}): got {g:#010x} expected {e}"
+
+
 def pin_bf16_vs_brute(orc, seed: int = 3, n: int = 4000) -> None:
     """down() == exact rational rounding on random and boundary patterns."""
     rng = np.random.default_rng(seed)
@@ -572,4 +599,5 @@ def pin_selfcheck(orc) -> None:
 FAST_PINS = [pin_selfcheck, pin_golden_reduce, pin_golden_bf16, pin_bf16_vs_brute,
              pin_up_bf16, pin_integer_closed_form, pin_int_mod32, pin_invariants,
              pin_composition, pin_bruteforce, pin_sim_closed_forms, pin_sim_bruteforce,
-             pin_narrow_vs_torch, pin_more_types_closed_forms, pin_more_types_bruteforce]
+             pin_narrow_vs_torch, pin_more_types_closed_forms, pin_more_types_bruteforce,
+             pin_golden_narrow]
