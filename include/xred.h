@@ -177,7 +177,9 @@ XRED_API xred_status xred_acc_cast(const void *acc, void *dst, size_t count, xre
  *            return (metadata by value).  Every item is validated as in
  *            xred_allreduce_local; the library stages the descriptors into
  *            device memory it owns (pinned staging slots reused once the
- *            launch that read them has completed).
+ *            launch that read them has completed).  Not capturable: on a
+ *            stream under graph capture the call returns XRED_UNSUPPORTED
+ *            (a replay would copy whatever a later call left in the slot).
  *   XRED_ITEMS_ON_DEVICE: `items` and every items[k].srcs are DEVICE memory,
  *            read when the kernels run, so an earlier kernel on the stream may
  *            still write them (metadata by reference, after the GPU-resident
@@ -189,7 +191,8 @@ XRED_API xred_status xred_acc_cast(const void *acc, void *dst, size_t count, xre
  *            otherwise trusted.
  *   Items of one batch must not write memory another item reads or writes.
  * Errors: XRED_INVALID_ARGUMENT (nitems < 0, bad item in host mode, unknown
- * flags), XRED_UNSUPPORTED, XRED_ALIAS (host mode, within an item),
+ * flags), XRED_UNSUPPORTED (also host mode under capture), XRED_ALIAS (host
+ * mode, within an item),
  * XRED_OUT_OF_MEMORY (staging or workspace allocation), XRED_HIP_ERROR.
  */
 XRED_API xred_status xred_batched_reduce(const xred_item *items, int nitems, xred_dtype dtype,

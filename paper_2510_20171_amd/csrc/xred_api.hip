@@ -161,6 +161,14 @@ xred_status batched_host(const xred_item *items, int nitems, xred_dtype dtype, x
     if (total_tiles >= 0xFFFFFFFFull)
         return fail(XRED_INVALID_ARGUMENT, "batch has %llu tiles; at most 2^32-2 are supported",
                     (unsigned long long)total_tiles);
+    // The descriptors go through staging slots that later calls reuse: a
+    // captured copy would replay whatever a later call left there.
+    hipStreamCaptureStatus capture = hipStreamCaptureStatusNone;
+    hipError_t e = hipStreamIsCapturing(stream, &capture);
+    if (e != hipSuccess) return hip_fail(e, "hipStreamIsCapturing");
+    if (capture != hipStreamCaptureStatusNone)
+        return fail(XRED_UNSUPPORTED, "host-side descriptors cannot be captured in a graph "
+                                      "(their staging is reused); use XRED_ITEMS_ON_DEVICE");
 
     // Round-robin layout (batches up to batched_rr_max_items() items):
     //     items | tile-start prefix (nitems + 1 u32, padded to 8 B) | source pointers
@@ -175,7 +183,7 @@ xred_status batched_host(const xred_item *items, int nitems, xred_dtype dtype, x
     const size_t need = items_bytes + plan_bytes + 8 * (size_t)total_ptrs;
 
     int dev = 0;
-    hipError_t e = hipGetDevice(&dev);
+    e = hipGetDevice(&dev);
     if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
     if (dev < 0 || dev >= kMaxDevices) return fail(XRED_UNSUPPORTED, "device %d", dev);
     Pool &pool = g_pool[dev];

@@ -178,3 +178,29 @@ def test_graph_capture_more_paths(xr):
         for a, b in zip(got[2], ref_r):
             assert torch.equal(a.view(torch.int16), b.view(torch.int16)), r
     del keep
+
+
+def test_host_descriptors_refuse_capture(xr):
+    """Host-mode batches are staged through reused slots, so capturing one is
+    refused before anything is enqueued; the same call works eagerly after."""
+    srcs = [torch.randn(3000, device="cuda").to(torch.bfloat16) for _ in range(3)]
+    out = torch.empty_like(srcs[0])
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        xr.batched_reduce([(srcs, out)], dtype="bf16")
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with pytest.raises(xr.XredError) as e:
+        with torch.cuda.graph(g):
+            xr.batched_reduce([(srcs, out)], dtype="bf16")
+    assert e.value.name == "XRED_UNSUPPORTED", e.value
+    torch.cuda.synchronize()
+    ref = torch.empty_like(out)
+    xr.allreduce_local(srcs, ref)
+    out.zero_()
+    xr.batched_reduce([(srcs, out)], dtype="bf16")
+    torch.cuda.synchronize()
+    assert torch.equal(out.view(torch.int16), ref.view(torch.int16))
+
