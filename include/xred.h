@@ -183,9 +183,9 @@ XRED_API xred_status xred_acc_cast(const void *acc, void *dst, size_t count, xre
  *   XRED_ITEMS_ON_DEVICE: `items` and every items[k].srcs are DEVICE memory,
  *            read when the kernels run, so an earlier kernel on the stream may
  *            still write them (metadata by reference, after the GPU-resident
- *            collectives of Section 6.1).  No host work per item; safe to
- *            capture in a HIP graph once a first call on the device has
- *            created the library's planning workspace.  Items that cannot be
+ *            collectives of Section 6.1).  No host work per item and no
+ *            allocation (each workgroup plans its share in the kernel), so
+ *            the call can be captured in a HIP graph.  Items that cannot be
  *            run safely (nsrc outside 1..64, a NULL pointer, reserved != 0)
  *            are skipped and their dst is left untouched; pointers are
  *            otherwise trusted.
@@ -193,7 +193,7 @@ XRED_API xred_status xred_acc_cast(const void *acc, void *dst, size_t count, xre
  * Errors: XRED_INVALID_ARGUMENT (nitems < 0, bad item in host mode, unknown
  * flags), XRED_UNSUPPORTED (also host mode under capture), XRED_ALIAS (host
  * mode, within an item),
- * XRED_OUT_OF_MEMORY (staging or workspace allocation), XRED_HIP_ERROR.
+ * XRED_OUT_OF_MEMORY (host mode: staging allocation), XRED_HIP_ERROR.
  */
 XRED_API xred_status xred_batched_reduce(const xred_item *items, int nitems, xred_dtype dtype,
                                          xred_op op, unsigned flags, void *hip_stream);
@@ -310,7 +310,7 @@ XRED_API const char *xred_last_error(void);
 /* Library version: major*10000 + minor*100 + patch. */
 XRED_API int xred_version(void);
 
-/* Frees the library's staging buffers and workspaces on every device after
+/* Frees the library's host-mode batch staging buffers on every device after
  * synchronising the device work that uses them.  Optional; later calls
  * re-create what they need. */
 XRED_API void xred_release(void);
