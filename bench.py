@@ -645,8 +645,8 @@ def main() -> int:
                     help="also run 3 plain device copies of 1 GiB (for scaling HBM byte counters)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU only: the reduce step runs on a single MI355X and "
-              "this build has no multi-GPU path; run with --gpus 1.", file=sys.stderr)
+        print("bench.py measures one GPU only: libxred's reduce step runs on a single MI355X "
+              "and has no multi-GPU path; run with --gpus 1.", file=sys.stderr)
         return 2
 
     import numpy as np
