@@ -34,9 +34,13 @@
  *     among the reduced values gives the canonical quiet NaN 0x7FC00000,
  *     whatever their number (also for a single source and for the INIT step
  *     of the step-wise mode);
- *   - NaN payloads of SUM/PROD are not specified ("parity unpinned" for NaN
- *     payloads: tests compare NaN-ness only);
- *   - down() of a NaN to bf16 keeps the sign and gives the quiet NaN 0x7FC0.
+ *   - NaN payloads of SUM/PROD/AVG are not specified ("parity unpinned" for
+ *     NaN payloads: tests compare NaN-ness only);
+ *   - down() of a NaN keeps the sign and gives the I/O type's quiet NaN
+ *     (bf16 0x7FC0, fp16 0x7E00, e5m2 0x7E, e4m3 0x7F);
+ *   - down() to fp16 or e5m2 overflows to +-inf as rounding dictates; e4m3
+ *     (the OCP "FN" format, no infinity) saturates: any magnitude that rounds
+ *     past 448, and an infinity, gives +-448.
  *
  * Step-wise ring mode (the ReduceCopy of the FTAR pipeline, Section 5 FTAR):
  * acc <- up(in) on INIT, acc <- acc (+) up(in) otherwise, and on FINAL the
