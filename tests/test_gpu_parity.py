@@ -61,12 +61,24 @@ def test_c1_full(xr, orc):
     gu.assert_parity(got, exp, w.dtype, w.op, "c1")
 
 
-def test_c2_full(xr, orc):
+@pytest.fixture(scope="module")
+def c2_sources():
+    return wl.sources(wl.WORKLOADS["c2"])
+
+
+def test_c2_full(xr, orc, c2_sources):
     w = wl.WORKLOADS["c2"]
-    srcs = wl.sources(w)
-    got = _run_allreduce(xr, srcs, w.dtype, w.op)
-    exp = orc.allreduce_local(srcs, w.dtype, w.op, nthreads=CORES)
+    got = _run_allreduce(xr, c2_sources, w.dtype, w.op)
+    exp = orc.allreduce_local(c2_sources, w.dtype, w.op, nthreads=CORES)
     gu.assert_parity(got, exp, w.dtype, w.op, "c2")
+
+
+@pytest.mark.parametrize("op", ["prod", "max", "min", "avg"])
+def test_c2_full_other_ops(xr, orc, c2_sources, op):
+    """The bucket's inputs and launch configuration with every other op."""
+    got = _run_allreduce(xr, c2_sources, "bf16", op)
+    exp = orc.allreduce_local(c2_sources, "bf16", op, nthreads=CORES)
+    gu.assert_parity(got, exp, "bf16", op, f"c2 {op}")
 
 
 @pytest.mark.parametrize("name", ["c5a", "c5b"])
