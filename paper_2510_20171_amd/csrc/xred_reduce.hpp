@@ -30,6 +30,11 @@ namespace {
 //   ~16; P=16 ~10; P=32 ~6; P=64 ~4.  The cap is applied by giving each
 //   workgroup an LDS reservation it never touches, sized so that only the
 //   wanted number of workgroups fit on a CU.
+// * Five to eight sources of several hundred MiB each want more loads in
+//   flight (P=8 bf16, one process per setting, best cap and time against the
+//   12-wave cap: 128 MiB per source 12; 256 MiB 16, 360 us against 374 us;
+//   512 MiB 24, 830 us against 963 us; 768 MiB 20-24, 1232 us against
+//   1346 us).  16 and 32 sources keep their caps up to 4.4 GB in all.
 constexpr int kU = 1;          // 16-byte vectors per thread per tile
 constexpr int kB = 128;        // threads per workgroup, bandwidth-bound launches
 constexpr int kBWide = 512;    // threads per workgroup, one-round launches
@@ -40,6 +45,17 @@ template <int NP>
 constexpr int waves_per_cu()
 {
     return NP == 0 ? 16 : NP <= 4 ? 0 : NP <= 8 ? 12 : NP <= 16 ? 10 : NP <= 32 ? 6 : 4;
+}
+
+// The cap of a bandwidth-bound launch with `bytes` per source.
+template <int NP>
+int waves_for(size_t bytes)
+{
+    if (NP >= 5 && NP <= 8) {
+        if (bytes > ((size_t)384 << 20)) return 24;
+        if (bytes > ((size_t)192 << 20)) return 16;
+    }
+    return waves_per_cu<NP>();
 }
 
 int lds_per_cu()
@@ -89,7 +105,8 @@ hipError_t go_vec(const char *const *srcs, int nsrc, char *dst, size_t count, hi
     constexpr size_t kTile = (size_t)kB * kU;
     const uint64_t tiles = (nvec + kTile - 1) / kTile + (tail ? 1 : 0);
     hipLaunchKernelGGL((reduce_vec_kernel<T, Op, NP, MAXP, kU, kB>), dim3(grid_for(tiles)),
-                       dim3(kB), lds_for_waves(waves_per_cu<NP>()), s, ks, nsrc, dst, nvec, tail);
+                       dim3(kB), lds_for_waves(waves_for<NP>(count * T::kSize)), s, ks, nsrc, dst,
+                       nvec, tail);
     return hipGetLastError();
 }
 

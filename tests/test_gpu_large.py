@@ -72,3 +72,20 @@ def test_reduce_scatter_and_batched_past_4gib(xr, orc):
     gu.assert_parity(out_b[idx], exp, "bf16", "sum", "batched past 4 GiB (sampled)")
     del srcs, out, out_b
     torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("mib", [256, 400])
+def test_fused_eight_large_sources(xr, orc, mib):
+    """Eight sources of several hundred MiB each (the launches with the larger
+    occupancy caps), ragged length, sampled columns."""
+    n = (mib << 20) // 2 + 5
+    srcs = [_random_bits(n, 2, 1200 + mib + p) for p in range(8)]
+    out = torch.empty_like(srcs[0])
+    xr.allreduce_local(srcs, out, "sum", dtype="bf16")
+    torch.cuda.synchronize()
+    idx = _samples(n, 2, np.random.default_rng(mib))
+    cols = [gu.bits(s[idx], "bf16").copy() for s in srcs]
+    exp = orc.allreduce_local(cols, "bf16", "sum")
+    gu.assert_parity(out[idx], exp, "bf16", "sum", f"P=8 x {mib} MiB (sampled)")
+    del srcs, out
+    torch.cuda.empty_cache()
