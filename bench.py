@@ -464,6 +464,19 @@ def secondary(torch, xr, L, timer, wl, flush):
                             "GBs": round(9 * n * 2 / ms / 1e6, 1)}
         del d, out
     res["latency_p8_bf16"] = lat
+
+    # messages larger than the bucket: 8 bf16 sources of 256 and 512 MiB (the
+    # launches whose occupancy cap grows with the bytes per source)
+    big = {}
+    for mib in (256, 512):
+        n = mib << 19
+        d = [torch.empty(n, dtype=torch.bfloat16, device="cuda").normal_() for _ in range(8)]
+        out = torch.empty_like(d[0])
+        ms = timer.loop_ms(reduce_call(L, xr, d, out, "bf16", "sum"), 10)
+        big[f"{mib}MiB"] = {"us": round(ms * 1e3, 1), "GBs": round(9 * n * 2 / ms / 1e6, 1)}
+        del d, out
+        torch.cuda.empty_cache()
+    res["large_p8_bf16"] = big
     return res
 
 
