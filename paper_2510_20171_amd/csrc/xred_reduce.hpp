@@ -30,11 +30,13 @@ namespace {
 //   ~16; P=16 ~10; P=32 ~6; P=64 ~4.  The cap is applied by giving each
 //   workgroup an LDS reservation it never touches, sized so that only the
 //   wanted number of workgroups fit on a CU.
-// * Five to eight sources of several hundred MiB each want more loads in
-//   flight (P=8 bf16, one process per setting, best cap and time against the
-//   12-wave cap: 128 MiB per source 12; 256 MiB 16, 360 us against 374 us;
-//   512 MiB 24, 830 us against 963 us; 768 MiB 20-24, 1232 us against
-//   1346 us).  16 and 32 sources keep their caps up to 4.4 GB in all.
+// * Five to eight sources want more loads in flight when each holds several
+//   hundred MiB, and when a launch is only a few rounds long (P=8 bf16, one
+//   process per setting, best cap and time against the 12-wave cap: 16 MiB
+//   per source 24, 25.5 us against 27.4 us back to back and 30.0 against
+//   32.0 us cold; 32 MiB 12 (24: +4 % cold); 128 MiB 12; 256 MiB 16, 360 us
+//   against 374 us; 512 MiB 24, 830 us against 963 us; 768 MiB 20-24, 1232 us
+//   against 1346 us).  16 and 32 sources keep their caps up to 4.4 GB.
 constexpr int kU = 1;          // 16-byte vectors per thread per tile
 constexpr int kB = 128;        // threads per workgroup, bandwidth-bound launches
 constexpr int kBWide = 512;    // threads per workgroup, one-round launches
@@ -54,6 +56,7 @@ int waves_for(size_t bytes)
     if (NP >= 5 && NP <= 8) {
         if (bytes > ((size_t)384 << 20)) return 24;
         if (bytes > ((size_t)192 << 20)) return 16;
+        if (bytes <= ((size_t)24 << 20)) return 24;
     }
     return waves_per_cu<NP>();
 }
