@@ -180,6 +180,8 @@ def test_graph_capture_more_paths(xr):
     del keep
 
 
+# the refused call enqueues nothing, so the captured graph is empty by design
+@pytest.mark.filterwarnings("ignore:The CUDA Graph is empty")
 def test_host_descriptors_refuse_capture(xr):
     """Host-mode batches are staged through reused slots, so capturing one is
     refused before anything is enqueued; the same call works eagerly after."""
