@@ -175,9 +175,10 @@ XRED_API xred_status xred_acc_cast(const void *acc, void *dst, size_t count, xre
  *   items    nitems descriptors.
  *   flags 0: `items` and every items[k].srcs are HOST memory, consumed before
  *            return (metadata by value).  Every item is validated as in
- *            xred_allreduce_local; the library stages the descriptors into
- *            device memory it owns (pinned staging slots reused once the
- *            launch that read them has completed).  Not capturable: on a
+ *            xred_allreduce_local; the library stages the descriptors, with
+ *            a list of every tile's item, into device memory it owns (pinned
+ *            staging slots reused once the launch that read them has
+ *            completed) and runs one workgroup per tile.  Not capturable: on a
  *            stream under graph capture the call returns XRED_UNSUPPORTED
  *            (a replay would copy whatever a later call left in the slot).
  *   XRED_ITEMS_ON_DEVICE: `items` and every items[k].srcs are DEVICE memory,

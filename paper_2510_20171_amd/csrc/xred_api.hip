@@ -134,7 +134,8 @@ xred_status batched_host(const xred_item *items, int nitems, xred_dtype dtype, x
 {
     const size_t es = elem_size(dtype);
     const uint64_t te = batched_tile_elems(dtype);
-    uint64_t total_tiles = 0, total_ptrs = 0;
+    const uint64_t tt = batched_table_tile_elems(dtype);
+    uint64_t total_tiles = 0, table_tiles = 0, total_ptrs = 0;
     for (int k = 0; k < nitems; ++k) {
         const xred_item &it = items[k];
         if (it.reserved != 0) return fail(XRED_INVALID_ARGUMENT, "items[%d].reserved != 0", k);
@@ -155,6 +156,7 @@ xred_status batched_host(const xred_item *items, int nitems, xred_dtype dtype, x
                 return fail(XRED_ALIAS, "items[%d].dst partially overlaps source %u", k, p);
         }
         total_tiles += (it.count + te - 1) / te;
+        table_tiles += (it.count + tt - 1) / tt;
         total_ptrs += it.nsrc;
     }
     if (total_tiles == 0) return XRED_SUCCESS;
@@ -170,16 +172,25 @@ xred_status batched_host(const xred_item *items, int nitems, xred_dtype dtype, x
         return fail(XRED_UNSUPPORTED, "host-side descriptors cannot be captured in a graph "
                                       "(their staging is reused); use XRED_ITEMS_ON_DEVICE");
 
-    // Round-robin layout (batches up to batched_rr_max_items() items):
+    // Tile-table layout (one workgroup per tile; the table adds 4 bytes per
+    // tile to the descriptor copy, so batches of very large items, whose table
+    // would pass kMaxTableTiles entries (2 MiB), use the layouts after it):
+    //     items (reserved = the item's first tile) | item of every tile (u32,
+    //     padded to 8 B) | source pointers
+    // Round-robin layout (up to batched_rr_max_items() items):
     //     items | tile-start prefix (nitems + 1 u32, padded to 8 B) | source pointers
-    // Range layout (larger batches):
+    // Range layout (more items):
     //     items | per-workgroup starts | source pointers
-    const bool rr = nitems <= batched_rr_max_items();
-    const unsigned grid =
-        rr ? 0u : (unsigned)std::min<uint64_t>(total_tiles, batched_device_grid());
+    constexpr uint64_t kMaxTableTiles = 1u << 19;
+    const bool table = table_tiles <= kMaxTableTiles;
+    const bool rr = !table && nitems <= batched_rr_max_items();
+    const unsigned grid = table || rr
+                              ? 0u
+                              : (unsigned)std::min<uint64_t>(total_tiles, batched_device_grid());
     const size_t items_bytes = sizeof(xred_item) * (size_t)nitems;
-    const size_t plan_bytes = rr ? (4 * ((size_t)nitems + 1) + 7) / 8 * 8
-                                 : sizeof(WgStart) * (size_t)grid;
+    const size_t plan_bytes = table ? (4 * (size_t)table_tiles + 7) / 8 * 8
+                              : rr  ? (4 * ((size_t)nitems + 1) + 7) / 8 * 8
+                                    : sizeof(WgStart) * (size_t)grid;
     const size_t need = items_bytes + plan_bytes + 8 * (size_t)total_ptrs;
 
     int dev = 0;
@@ -231,7 +242,15 @@ xred_status batched_host(const xred_item *items, int nitems, xred_dtype dtype, x
         for (uint32_t p = 0; p < it.nsrc; ++p) h_ptrs[pos + p] = it.srcs[p];
         pos += it.nsrc;
     }
-    if (rr) {
+    if (table) {
+        uint32_t *h_tab = (uint32_t *)(h + items_bytes);
+        uint32_t w = 0;
+        for (int k = 0; k < nitems; ++k) {
+            const uint32_t nt = (uint32_t)((items[k].count + tt - 1) / tt);
+            h_items[k].reserved = w;
+            for (uint32_t t = 0; t < nt; ++t) h_tab[w++] = (uint32_t)k;
+        }
+    } else if (rr) {
         uint32_t *h_pre = (uint32_t *)(h + items_bytes);
         uint64_t acc = 0;
         for (int k = 0; k < nitems; ++k) {
@@ -260,7 +279,10 @@ xred_status batched_host(const xred_item *items, int nitems, xred_dtype dtype, x
     e = hipMemcpyAsync(s.dev, s.host, need, hipMemcpyHostToDevice, stream);
     if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync(descriptors)");
     hipError_t le;
-    if (rr)
+    if (table)
+        le = launch_batched_table(dtype, op, (const xred_item *)d,
+                                  (const uint32_t *)(d + items_bytes), table_tiles, stream);
+    else if (rr)
         le = launch_batched_rr(dtype, op, (const xred_item *)d, nitems,
                                (const uint32_t *)(d + items_bytes), stream);
     else

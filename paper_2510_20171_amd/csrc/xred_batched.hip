@@ -45,6 +45,29 @@ hipError_t launch_batched_device(xred_dtype dtype, xred_op op, const xred_item *
     return range_dispatch(dtype, op, false, d_items, nitems, nullptr, grid, stream);
 }
 
+uint64_t batched_table_tile_elems(xred_dtype dtype)
+{
+    uint64_t n = 0;
+    (void)with_dtype(dtype, [&](auto t) {
+        n = table_tile_elems<decltype(t)>();
+        return hipSuccess;
+    });
+    return n;
+}
+
+hipError_t launch_batched_table(xred_dtype dtype, xred_op op, const xred_item *d_items,
+                                const uint32_t *d_table, uint64_t ntiles, hipStream_t stream)
+{
+    switch (group_of(dtype)) {
+    case TypeGroup::kFloat:
+        return launch_batched_table_float(dtype, op, d_items, d_table, ntiles, stream);
+    case TypeGroup::kFp8:
+        return launch_batched_table_fp8(dtype, op, d_items, d_table, ntiles, stream);
+    default:
+        return launch_batched_table_int(dtype, op, d_items, d_table, ntiles, stream);
+    }
+}
+
 int batched_rr_max_items() { return kRrMaxItems; }
 
 hipError_t launch_batched_rr(xred_dtype dtype, xred_op op, const xred_item *d_items, int nitems,

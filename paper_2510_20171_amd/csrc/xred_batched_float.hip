@@ -16,4 +16,10 @@ hipError_t launch_batched_rr_float(xred_dtype dtype, xred_op op, const xred_item
     return batched_rr_group<TF32, TBF16, TF16>(dtype, op, d_items, nitems, d_tile_start, stream);
 }
 
+hipError_t launch_batched_table_float(xred_dtype dtype, xred_op op, const xred_item *d_items,
+                                 const uint32_t *d_table, uint64_t ntiles, hipStream_t stream)
+{
+    return batched_table_group<TF32, TBF16, TF16>(dtype, op, d_items, d_table, ntiles, stream);
+}
+
 }  // namespace xred

@@ -16,4 +16,10 @@ hipError_t launch_batched_rr_int(xred_dtype dtype, xred_op op, const xred_item *
     return batched_rr_group<TI32, TU32, TI64, TU64>(dtype, op, d_items, nitems, d_tile_start, stream);
 }
 
+hipError_t launch_batched_table_int(xred_dtype dtype, xred_op op, const xred_item *d_items,
+                                 const uint32_t *d_table, uint64_t ntiles, hipStream_t stream)
+{
+    return batched_table_group<TI32, TU32, TI64, TU64>(dtype, op, d_items, d_table, ntiles, stream);
+}
+
 }  // namespace xred

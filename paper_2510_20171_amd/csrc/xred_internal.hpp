@@ -50,6 +50,13 @@ static_assert(sizeof(xred_item) == 32, "xred_item layout");
 
 uint64_t batched_tile_elems(xred_dtype dtype);
 
+// Host descriptors, one workgroup per tile: tile w of the batch (of
+// batched_table_tile_elems(dtype) elements) belongs to item table[w], whose
+// staged descriptor holds the index of its first tile in `reserved`.
+uint64_t batched_table_tile_elems(xred_dtype dtype);
+hipError_t launch_batched_table(xred_dtype dtype, xred_op op, const xred_item *d_items,
+                                const uint32_t *d_table, uint64_t ntiles, hipStream_t stream);
+
 // Host-planned: d_items (device copy, srcs pointing to device arrays) and one
 // WgStart per workgroup.
 hipError_t launch_batched_planned(xred_dtype dtype, xred_op op, const xred_item *d_items,
@@ -78,7 +85,9 @@ hipError_t launch_batched_rr(xred_dtype dtype, xred_op op, const xred_item *d_it
                                         const xred_item *d_items, int nitems,                  \
                                         const WgStart *d_wg, unsigned grid, hipStream_t s);    \
     hipError_t launch_batched_rr_##G(xred_dtype dtype, xred_op op, const xred_item *d_items,   \
-                                     int nitems, const uint32_t *d_tile_start, hipStream_t s);
+                                     int nitems, const uint32_t *d_tile_start, hipStream_t s); \
+    hipError_t launch_batched_table_##G(xred_dtype dtype, xred_op op, const xred_item *d_items, \
+                                        const uint32_t *d_table, uint64_t ntiles, hipStream_t s);
 XRED_BATCHED_GROUP(float)
 XRED_BATCHED_GROUP(fp8)
 XRED_BATCHED_GROUP(int)

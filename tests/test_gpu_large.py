@@ -89,3 +89,23 @@ def test_fused_eight_large_sources(xr, orc, mib):
     gu.assert_parity(out[idx], exp, "bf16", "sum", f"P=8 x {mib} MiB (sampled)")
     del srcs, out
     torch.cuda.empty_cache()
+
+
+def test_batched_beyond_table_and_round_robin_limits(xr, orc):
+    """A host batch whose tile table would pass its size limit (2^19 tiles of
+    4096 bf16) and whose item count passes the round-robin plan's (8192): the
+    range-walking kernel runs it.  8200 items of 65 tiles each, one source;
+    sampled items checked whole."""
+    n, K = 65 * 4096, 8200
+    src = _random_bits(n * K, 2, 1500)
+    dst = torch.zeros(n * K, dtype=torch.int16, device="cuda")
+    items = [([src[k * n:(k + 1) * n]], dst[k * n:(k + 1) * n]) for k in range(K)]
+    xr.batched_reduce(items, "sum", dtype="bf16")
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(15)
+    for k in sorted({0, K - 1} | set(rng.integers(0, K, 32).tolist())):
+        col = gu.bits(src[k * n:(k + 1) * n], "bf16").copy()
+        gu.assert_parity(dst[k * n:(k + 1) * n], orc.allreduce_local([col], "bf16", "sum"),
+                         "bf16", "sum", f"item {k}")
+    del src, dst, items
+    torch.cuda.empty_cache()
