@@ -109,3 +109,20 @@ def test_batched_beyond_table_and_round_robin_limits(xr, orc):
                          "bf16", "sum", f"item {k}")
     del src, dst, items
     torch.cuda.empty_cache()
+
+
+def test_batched_table_at_its_limit(xr, orc):
+    """Exactly 2^19 tiles (two items of 2^30 bf16, one source each): the
+    largest batch the tile list takes; sampled columns of both items."""
+    n = 1 << 30
+    srcs = [_random_bits(n, 2, 1600 + k) for k in range(2)]
+    outs = [torch.empty(n, dtype=torch.int16, device="cuda") for _ in range(2)]
+    xr.batched_reduce([([s], o) for s, o in zip(srcs, outs)], "sum", dtype="bf16")
+    torch.cuda.synchronize()
+    for k in range(2):
+        idx = _samples(n, 2, np.random.default_rng(20 + k))
+        col = gu.bits(srcs[k][idx], "bf16").copy()
+        gu.assert_parity(outs[k][idx], orc.allreduce_local([col], "bf16", "sum"), "bf16", "sum",
+                         f"item {k} (sampled)")
+    del srcs, outs
+    torch.cuda.empty_cache()
