@@ -4,19 +4,20 @@
 //
 // Small messages are dominated by per-call overhead (the T_c term of the
 // LogP model in Section 6.2), so a batch of K reductions is run as one
-// kernel.  Work is cut into tiles of kB*kU 16-byte vectors of one item;
-// the global tile sequence (item 0's tiles, then item 1's, ...) is split
-// into one contiguous range per workgroup, so each workgroup walks forward
-// through consecutive items and reads each descriptor once.
-//
-// Two ways to find a workgroup's range:
-//   planned  (host descriptors): the host computes each workgroup's first
-//            item, first tile and tile count and stages them with the items;
-//   device   (XRED_ITEMS_ON_DEVICE): descriptors are read only when the
-//            kernel runs (metadata by reference, Section 6.1), so every
-//            workgroup sums the tile counts itself (an LDS scan over the
-//            descriptors), then locates its first tile.  No state is kept
-//            between calls, so the kernel can be captured in a graph.
+// kernel.  Work is cut into tiles of 16-byte vectors of one item, in the
+// global order item 0's tiles, then item 1's, ...  Three kernels:
+//   table        (host descriptors, the usual case): the host stages the
+//                item of every tile and one workgroup runs each tile, so the
+//                hardware dispatches tiles in order, as for the fused kernel;
+//   round-robin  (device descriptors, or host batches past the table's size):
+//                a persistent grid, tile g on workgroup g mod G, the
+//                tile-start prefix in LDS (staged, or scanned from the
+//                descriptors when they are read in the kernel: metadata by
+//                reference, Section 6.1; no state is kept between calls, so
+//                the kernel can be captured in a graph);
+//   range        (more than the round-robin plan's items): contiguous tile
+//                ranges per workgroup, planned on the host or found by each
+//                workgroup with an LDS scan.
 
 #pragma once
 
