@@ -477,6 +477,57 @@ def secondary(torch, xr, L, timer, wl, flush):
         del d, out
         torch.cuda.empty_cache()
     res["large_p8_bf16"] = big
+
+    # co-scheduling: P=8 bf16 x 8 MiB reduces on one stream while bf16 8192^3
+    # matrix products run on another (both default priority), per CU budget;
+    # the reduce loop alone lasts about as long as the products
+    sg, sr = torch.cuda.Stream(), torch.cuda.Stream()
+    n = 4 << 20
+    d = [torch.randn(n, device="cuda").to(torch.bfloat16) for _ in range(8)]
+    out = torch.empty_like(d[0])
+    arr = xr._lib.ptr_array([x.data_ptr() for x in d])
+    ga = torch.randn(8192, 8192, device="cuda").to(torch.bfloat16)
+    gb = torch.randn(8192, 8192, device="cuda").to(torch.bfloat16)
+    gc = torch.empty_like(ga)
+    reps_g = 20
+
+    def run(g, reps_r):
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+        torch.cuda.synchronize()
+        ev[0].record(sg)
+        ev[2].record(sr)
+        if g:
+            with torch.cuda.stream(sg):
+                for _ in range(reps_g):
+                    torch.mm(ga, gb, out=gc)
+        st = ctypes.c_void_p(sr.cuda_stream)
+        for _ in range(reps_r):
+            L.xred_allreduce_local(arr, 8, ctypes.c_void_p(out.data_ptr()), n, 1, 0, st)
+        ev[1].record(sg)
+        ev[3].record(sr)
+        torch.cuda.synchronize()
+        return ev[0].elapsed_time(ev[1]), ev[2].elapsed_time(ev[3])
+
+    run(True, 10)
+    g_alone, _ = run(True, 0)
+    co = {"gemm_alone_ms": round(g_alone / reps_g, 3),
+          "gemm_TFLOPs": round(2 * 8192 ** 3 * reps_g / g_alone / 1e9, 0)}
+    prev = xr.set_max_workgroups(0)
+    try:
+        for budget in (16, 64, 0):
+            xr.set_max_workgroups(budget)
+            _, r1 = run(False, 100)
+            reps = max(10, int(g_alone / (r1 / 100)))
+            _, r_alone = run(False, reps)
+            g_with, r_with = run(True, reps)
+            co[f"budget_{budget or 'none'}"] = {
+                "reduce_us_alone": round(r_alone / reps * 1e3, 1),
+                "reduce_us_with_gemm": round(r_with / reps * 1e3, 1),
+                "gemm_slowdown_pct": round(100 * (g_with / g_alone - 1), 1)}
+    finally:
+        xr.set_max_workgroups(prev)
+    res["coschedule_gemm_bf16"] = co
+    del d, out, ga, gb, gc
     return res
 
 
