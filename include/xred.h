@@ -295,6 +295,11 @@ XRED_API size_t xred_sim_chunk(size_t count, int nranks);
  * behind the network (Section 5).  Results do not depend on it.  Process-wide;
  * returns the previous value.  xred_ring_reduce applies it too, but never goes
  * below the workgroups its on-chip accumulators need (one per 4 tiles).
+ * The budget bounds the CUs a launch may occupy; it does not lower the
+ * interference with a kernel running beside it: next to a bf16 matrix
+ * product, a reduce capped at 16 or 64 workgroups slowed the product more
+ * (11-13 %, 7-9 %) than an uncapped one (2-5 %), whose short workgroups the
+ * hardware interleaves with the product's.
  */
 XRED_API unsigned xred_set_max_workgroups(unsigned max_workgroups);
 
