@@ -64,6 +64,12 @@ def load(path: Path = LIB_PATH) -> ctypes.CDLL:
     if not Path(path).exists():
         raise ImportError(f"{path} is not built: run `python -m paper_2510_20171_amd.build` "
                           "(there is no CPU fallback)")
+    # The binding hands over torch's device pointers and streams, so the
+    # library must resolve libamdhip64 to the runtime torch already holds.
+    # Loaded first, it would map the system ROCm runtime as a second HIP
+    # runtime in the process, one that knows none of torch's allocations or
+    # streams (and may fail to open the device torch has open).
+    import torch  # noqa: F401
     L = ctypes.CDLL(str(path))
     vp, i32, sz, u32 = ctypes.c_void_p, ctypes.c_int, ctypes.c_size_t, ctypes.c_uint
     L.xred_allreduce_local.argtypes = [vp, i32, vp, sz, i32, i32, vp]

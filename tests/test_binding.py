@@ -94,3 +94,22 @@ def test_sim_buffers_are_checked():
     _invalid(lambda: xr.allreduce_sim(sends, [FakeGpuTensor(50)] * 3), "one recv buffer")
     _invalid(lambda: xr.allreduce_sim(sends, [FakeGpuTensor(50)] * 3 + [FakeGpuTensor(51)]),
              "recvs[3] has 51")
+
+
+def test_library_shares_torchs_hip_runtime():
+    """Loading the library with nothing else imported first must not map a
+    second HIP runtime beside torch's: torch's device pointers and streams are
+    only valid in the runtime that made them."""
+    import ast
+    import subprocess
+    import sys
+    from pathlib import Path
+    root = Path(__file__).resolve().parents[1]
+    code = ("import paper_2510_20171_amd as xr\n"
+            "xr.load()\n"
+            "import torch\n"
+            "print(sorted({l.split()[-1] for l in open('/proc/self/maps') if 'libamdhip64' in l}))\n")
+    out = subprocess.run([sys.executable, "-c", code], cwd=root, capture_output=True, text=True,
+                         timeout=300, check=True).stdout
+    runtimes = ast.literal_eval(out.strip().splitlines()[-1])
+    assert len(runtimes) == 1, runtimes
