@@ -15,34 +15,18 @@ uint64_t batched_tile_elems(xred_dtype dtype)
     return n;
 }
 
-namespace {
-
-hipError_t range_dispatch(xred_dtype dtype, xred_op op, bool planned, const xred_item *d_items,
-                          int nitems, const WgStart *d_wg, unsigned grid, hipStream_t s)
-{
-    switch (group_of(dtype)) {
-    case TypeGroup::kFloat:
-        return launch_batched_range_float(dtype, op, planned, d_items, nitems, d_wg, grid, s);
-    case TypeGroup::kFp8:
-        return launch_batched_range_fp8(dtype, op, planned, d_items, nitems, d_wg, grid, s);
-    default:
-        return launch_batched_range_int(dtype, op, planned, d_items, nitems, d_wg, grid, s);
-    }
-}
-
-}  // namespace
-
 hipError_t launch_batched_planned(xred_dtype dtype, xred_op op, const xred_item *d_items,
                                   int nitems, const WgStart *d_wg, unsigned grid,
                                   hipStream_t stream)
 {
-    return range_dispatch(dtype, op, true, d_items, nitems, d_wg, grid, stream);
-}
-
-hipError_t launch_batched_device(xred_dtype dtype, xred_op op, const xred_item *d_items,
-                                 int nitems, unsigned grid, hipStream_t stream)
-{
-    return range_dispatch(dtype, op, false, d_items, nitems, nullptr, grid, stream);
+    switch (group_of(dtype)) {
+    case TypeGroup::kFloat:
+        return launch_batched_range_float(dtype, op, d_items, nitems, d_wg, grid, stream);
+    case TypeGroup::kFp8:
+        return launch_batched_range_fp8(dtype, op, d_items, nitems, d_wg, grid, stream);
+    default:
+        return launch_batched_range_int(dtype, op, d_items, nitems, d_wg, grid, stream);
+    }
 }
 
 uint64_t batched_table_tile_elems(xred_dtype dtype)
@@ -69,6 +53,25 @@ hipError_t launch_batched_table(xred_dtype dtype, xred_op op, const xred_item *d
 }
 
 int batched_rr_max_items() { return kRrMaxItems; }
+
+int batched_grouped_max_items() { return kGrpMaxItems; }
+
+hipError_t launch_batched_grouped(xred_dtype dtype, xred_op op, const xred_item *d_items,
+                                  int nitems, uint32_t ngroups, uint32_t m, unsigned grid,
+                                  int wgs_per_cu, hipStream_t stream)
+{
+    switch (group_of(dtype)) {
+    case TypeGroup::kFloat:
+        return launch_batched_grouped_float(dtype, op, d_items, nitems, ngroups, m, grid,
+                                            wgs_per_cu, stream);
+    case TypeGroup::kFp8:
+        return launch_batched_grouped_fp8(dtype, op, d_items, nitems, ngroups, m, grid,
+                                          wgs_per_cu, stream);
+    default:
+        return launch_batched_grouped_int(dtype, op, d_items, nitems, ngroups, m, grid,
+                                          wgs_per_cu, stream);
+    }
+}
 
 hipError_t launch_batched_rr(xred_dtype dtype, xred_op op, const xred_item *d_items, int nitems,
                              const uint32_t *d_tile_start, hipStream_t stream)

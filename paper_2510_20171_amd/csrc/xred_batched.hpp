@@ -5,19 +5,23 @@
 // Small messages are dominated by per-call overhead (the T_c term of the
 // LogP model in Section 6.2), so a batch of K reductions is run as one
 // kernel.  Work is cut into tiles of 16-byte vectors of one item, in the
-// global order item 0's tiles, then item 1's, ...  Three kernels:
+// global order item 0's tiles, then item 1's, ...  Four kernels:
 //   table        (host descriptors, the usual case): the host stages the
 //                item of every tile and one workgroup runs each tile, so the
 //                hardware dispatches tiles in order, as for the fused kernel;
-//   round-robin  (device descriptors, or host batches past the table's size):
-//                a persistent grid, tile g on workgroup g mod G, the
-//                tile-start prefix in LDS (staged, or scanned from the
-//                descriptors when they are read in the kernel: metadata by
-//                reference, Section 6.1; no state is kept between calls, so
-//                the kernel can be captured in a graph);
-//   range        (more than the round-robin plan's items): contiguous tile
-//                ranges per workgroup, planned on the host or found by each
-//                workgroup with an LDS scan.
+//   grouped      (device descriptors, more than one run of items): runs of
+//                consecutive items, each dealt tile by tile to its own set of
+//                workgroups, which plan their tiles from the descriptors in the
+//                kernel (metadata by reference, Section 6.1); the sets are
+//                dispatched in order, so the runs balance over the chip;
+//   round-robin  (device descriptors of one run, or host batches past the
+//                table's size): a persistent grid, tile g on workgroup g mod G,
+//                the tile-start prefix in LDS (staged, or scanned from the
+//                descriptors in the kernel);
+//   range        (host batches past the round-robin plan's items): contiguous
+//                tile ranges per workgroup, planned on the host.
+// Device-descriptor kernels keep no state between calls, so they can be
+// captured in a graph.
 
 #pragma once
 
@@ -142,58 +146,21 @@ __device__ void batched_tile(const xred_item &it, uint64_t lt)
     }
 }
 
-template <class T, class Op, bool PLANNED>
+template <class T, class Op>
 __global__ __launch_bounds__(kB) void batched_kernel(const xred_item *items, int nitems,
-                                                         const WgStart *wg)
+                                                     const WgStart *wg)
 {
-    __shared__ uint64_t s_scan[kB];
-    __shared__ uint64_t s_start[2];
-    uint64_t k, lt, left;
-    if constexpr (PLANNED) {
-        const WgStart *w = wg + blockIdx.x;
-        k = sload(&w->item);
-        lt = sload(&w->local_tile);
-        left = sload(&w->ntiles);
-    } else {
-        uint64_t mine = 0;
-        for (int i = threadIdx.x; i < nitems; i += kB) mine += item_tiles<T, true>(items[i]);
-        block_inclusive_scan(mine, s_scan);
-        const uint64_t total = s_scan[kB - 1];
-        const uint64_t g0 = total * blockIdx.x / gridDim.x;
-        const uint64_t g1 = total * (blockIdx.x + 1) / gridDim.x;
-        if (g0 == g1) return;
-        left = g1 - g0;
-        // find the item holding global tile g0 (if none is found the walk
-        // below starts past the last item and does nothing)
-        if (threadIdx.x == 0) {
-            s_start[0] = (uint64_t)nitems;
-            s_start[1] = 0;
-        }
-        uint64_t base = 0;
-        for (int w0 = 0; w0 < nitems; w0 += kB) {
-            const int i = w0 + (int)threadIdx.x;
-            const uint64_t c = i < nitems ? item_tiles<T, true>(items[i]) : 0;
-            const uint64_t incl = block_inclusive_scan(c, s_scan);
-            const uint64_t excl = incl - c;
-            if (c > 0 && base + excl <= g0 && g0 < base + incl) {
-                s_start[0] = (uint64_t)i;
-                s_start[1] = g0 - base - excl;
-            }
-            const uint64_t wtot = s_scan[kB - 1];
-            __syncthreads();
-            if (base + wtot > g0) break;
-            base += wtot;
-        }
-        k = s_start[0];
-        lt = s_start[1];
-    }
+    const WgStart *w = wg + blockIdx.x;
+    uint64_t k = sload(&w->item);
+    uint64_t lt = sload(&w->local_tile);
+    uint64_t left = sload(&w->ntiles);
     k = uniform64(k);
     lt = uniform64(lt);
     left = uniform64(left);
     while (left > 0 && k < (uint64_t)nitems) {
         k = uniform64(k);
         const xred_item it = load_item(items, k);
-        const uint64_t nt = item_tiles<T, !PLANNED>(it);
+        const uint64_t nt = item_tiles<T, false>(it);
         if (lt >= nt) {
             ++k;
             lt = 0;
@@ -228,11 +195,9 @@ struct TileDesc {
     bool fast;                // nsrc <= 8, no NULL source, all pointers 16-byte aligned
 };
 
-__device__ __forceinline__ void fetch_desc(TileDesc &d, const xred_item *items, const uint2 *s_list,
-                                           int j)
+__device__ __forceinline__ void fetch_desc(TileDesc &d, const xred_item *items, uint32_t k,
+                                           uint64_t lt)
 {
-    const uint32_t k = __builtin_amdgcn_readfirstlane(s_list[j].x);
-    const uint32_t lt = __builtin_amdgcn_readfirstlane(s_list[j].y);
     const xred_item *it = items + k;
     d.k = k;
     d.lt = lt;
@@ -291,7 +256,8 @@ __global__ __launch_bounds__(kB) void batched_rr_kernel(const xred_item *items, 
         }
         __syncthreads();
         TileDesc cur, nxt;
-        fetch_desc(cur, items, s_list, 0);
+        fetch_desc(cur, items, __builtin_amdgcn_readfirstlane(s_list[0].x),
+                   __builtin_amdgcn_readfirstlane(s_list[0].y));
         for (int j = 0; j < n; ++j) {
             // Issue the current tile's loads.  Straight-line code: sources
             // beyond nsrc, and tiles not on the fast path, get a zero-length
@@ -310,7 +276,9 @@ __global__ __launch_bounds__(kB) void batched_rr_kernel(const xred_item *items, 
                     in[q][h] = bload<kLoadStream>(r, (uint32_t)(h * kB + threadIdx.x) * 16u);
             }
             // fetch the next tile's descriptor while those loads are in flight
-            if (j + 1 < n) fetch_desc(nxt, items, s_list, j + 1);
+            if (j + 1 < n)
+                fetch_desc(nxt, items, __builtin_amdgcn_readfirstlane(s_list[j + 1].x),
+                           __builtin_amdgcn_readfirstlane(s_list[j + 1].y));
             // fold (unused sources skipped by a uniform select) and store
             const rsrc_t w = make_rsrc(cur.dst + toff, nrec);
 #pragma unroll
@@ -367,6 +335,100 @@ constexpr int kTableWgsPerCu = 2;
 template <class T>
 constexpr uint64_t table_tile_elems() { return (uint64_t)kTB * T::kVec; }
 
+// The fields of a descriptor a tile needs, loaded with scalar loads.
+struct ItemHead {
+    const char *const *srcs;
+    char *dst;
+    uint64_t count;
+    int nsrc;
+};
+
+__device__ __forceinline__ ItemHead load_head(const xred_item *it)
+{
+    return ItemHead{(const char *const *)sload(&it->srcs), (char *)sload(&it->dst),
+                    sload(&it->count), (int)sload(&it->nsrc)};
+}
+
+// Tile lt (of kTB vectors) of the item with header h.  CHECK: the descriptor is the
+// caller's device memory, so an item with a NULL source pointer is skipped
+// (the host validates its own descriptors before staging them).
+template <class T, class Op, bool CHECK>
+__device__ __forceinline__ void table_tile(const ItemHead &h, uint64_t lt)
+{
+    constexpr uint32_t kBytes = (uint32_t)kTB * 16u;
+    const char *const *srcs = h.srcs;
+    char *dst = h.dst;
+    const uint64_t count = h.count;
+    const int nsrc = h.nsrc;
+    const GlobalSrc src{srcs};
+    const size_t nvec = count / T::kVec, vbytes = nvec * 16, toff = lt * kBytes;
+    const char *p[8];
+    uintptr_t bits = (uintptr_t)dst;
+    bool null_src = false;
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+        p[q] = q < nsrc ? sload(srcs + q) : nullptr;
+        bits |= (uintptr_t)p[q];
+        null_src |= q < nsrc && p[q] == nullptr;
+    }
+    if (nsrc > 8 || (bits & 15u) != 0) {
+        // the general tile: any source count, element-aligned buffers
+        uintptr_t all = (uintptr_t)dst;
+        for (int q = 0; q < nsrc; ++q) {
+            const uintptr_t x = (uintptr_t)sload(srcs + q);
+            all |= x;
+            null_src |= x == 0;
+        }
+        if (CHECK && null_src) return;
+        if ((all & 15u) == 0) {
+            if (toff < vbytes)
+                reduce_tile<T, Op, 0, 1, kTB>(src, nsrc, dst,
+                                              Tile{toff, tile_nrec(vbytes, toff, kBytes)});
+        } else {
+            const uint64_t e0 = lt * table_tile_elems<T>();
+            const uint64_t e1 =
+                count < e0 + table_tile_elems<T>() ? count : e0 + table_tile_elems<T>();
+            for (uint64_t i = e0 + threadIdx.x; i < e1; i += kTB)
+                reduce_elem<T, Op>(src, nsrc, dst, i);
+            return;
+        }
+    } else {
+        if (CHECK && null_src) return;
+        // straight-line tile: sources beyond nsrc get a zero-length range
+        const uint32_t nrec = toff < vbytes ? tile_nrec(vbytes, toff, kBytes) : 0u;
+        u32x4 in[8];
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+            const bool on = q < nsrc;
+            in[q] = bload<kLoadStream>(make_rsrc((on ? p[q] : dst) + toff, on ? nrec : 0u),
+                                       threadIdx.x * 16u);
+        }
+        typename T::Acc acc[T::kVec];
+        up_vec<T>(in[0], acc);
+#pragma unroll
+        for (int q = 1; q < 8; ++q) {
+            const bool on = q < nsrc;
+            typename T::Acc b[T::kVec];
+            up_vec<T>(in[q], b);
+#pragma unroll
+            for (int e = 0; e < T::kVec; ++e) {
+                const typename T::Acc c = combine<T, Op>(acc[e], b[e]);
+                acc[e] = on ? c : acc[e];
+            }
+        }
+        if constexpr (__is_same(Op, OpAvg)) {
+#pragma unroll
+            for (int e = 0; e < T::kVec; ++e) acc[e] = avg_scale<T, Op>(acc[e], nsrc);
+        }
+        bstore<kStoreOut>(down_vec<T, Op>(acc), make_rsrc(dst + toff, nrec), threadIdx.x * 16u);
+    }
+    // the item's last tile also takes the elements after its last full vector
+    if ((lt + 1) * table_tile_elems<T>() >= count) {
+        const uint32_t tail = (uint32_t)(count % T::kVec);
+        if (threadIdx.x < tail) reduce_elem<T, Op>(src, nsrc, dst, nvec * T::kVec + threadIdx.x);
+    }
+}
+
 template <class T, class Op>
 __global__ __launch_bounds__(kTB) void batched_table_kernel(const xred_item *items,
                                                             const uint32_t *table,
@@ -374,74 +436,10 @@ __global__ __launch_bounds__(kTB) void batched_table_kernel(const xred_item *ite
 {
     extern __shared__ char occupancy_reservation[];
     (void)occupancy_reservation;
-    constexpr uint32_t kBytes = (uint32_t)kTB * 16u;
     for (uint64_t g = blockIdx.x; g < ntiles; g += gridDim.x) {
         const uint32_t k = sload(&table[g]);
         const xred_item *it = items + k;
-        const uint64_t lt = g - sload(&it->reserved);
-        const char *const *srcs = (const char *const *)sload(&it->srcs);
-        char *dst = (char *)sload(&it->dst);
-        const uint64_t count = sload(&it->count);
-        const int nsrc = (int)sload(&it->nsrc);
-        const GlobalSrc src{srcs};
-        const size_t nvec = count / T::kVec, vbytes = nvec * 16, toff = lt * kBytes;
-        const char *p[8];
-        uintptr_t bits = (uintptr_t)dst;
-#pragma unroll
-        for (int q = 0; q < 8; ++q) {
-            p[q] = q < nsrc ? sload(srcs + q) : nullptr;
-            bits |= (uintptr_t)p[q];
-        }
-        if (nsrc > 8 || (bits & 15u) != 0) {
-            // the general tile: any source count, element-aligned buffers
-            uintptr_t all = (uintptr_t)dst;
-            for (int q = 0; q < nsrc; ++q) all |= (uintptr_t)sload(srcs + q);
-            if ((all & 15u) == 0) {
-                if (toff < vbytes)
-                    reduce_tile<T, Op, 0, 1, kTB>(src, nsrc, dst,
-                                                  Tile{toff, tile_nrec(vbytes, toff, kBytes)});
-            } else {
-                const uint64_t e0 = lt * table_tile_elems<T>();
-                const uint64_t e1 =
-                    count < e0 + table_tile_elems<T>() ? count : e0 + table_tile_elems<T>();
-                for (uint64_t i = e0 + threadIdx.x; i < e1; i += kTB)
-                    reduce_elem<T, Op>(src, nsrc, dst, i);
-                continue;
-            }
-        } else {
-            // straight-line tile: sources beyond nsrc get a zero-length range
-            const uint32_t nrec = toff < vbytes ? tile_nrec(vbytes, toff, kBytes) : 0u;
-            u32x4 in[8];
-#pragma unroll
-            for (int q = 0; q < 8; ++q) {
-                const bool on = q < nsrc;
-                in[q] = bload<kLoadStream>(make_rsrc((on ? p[q] : dst) + toff, on ? nrec : 0u),
-                                           threadIdx.x * 16u);
-            }
-            typename T::Acc acc[T::kVec];
-            up_vec<T>(in[0], acc);
-#pragma unroll
-            for (int q = 1; q < 8; ++q) {
-                const bool on = q < nsrc;
-                typename T::Acc b[T::kVec];
-                up_vec<T>(in[q], b);
-#pragma unroll
-                for (int e = 0; e < T::kVec; ++e) {
-                    const typename T::Acc c = combine<T, Op>(acc[e], b[e]);
-                    acc[e] = on ? c : acc[e];
-                }
-            }
-            if constexpr (__is_same(Op, OpAvg)) {
-#pragma unroll
-                for (int e = 0; e < T::kVec; ++e) acc[e] = avg_scale<T, Op>(acc[e], nsrc);
-            }
-            bstore<kStoreOut>(down_vec<T, Op>(acc), make_rsrc(dst + toff, nrec), threadIdx.x * 16u);
-        }
-        // the item's last tile also takes the elements after its last full vector
-        if ((lt + 1) * table_tile_elems<T>() >= count) {
-            const uint32_t tail = (uint32_t)(count % T::kVec);
-            if (threadIdx.x < tail) reduce_elem<T, Op>(src, nsrc, dst, nvec * T::kVec + threadIdx.x);
-        }
+        table_tile<T, Op, false>(load_head(it), g - sload(&it->reserved));
     }
 }
 
@@ -476,6 +474,145 @@ hipError_t batched_table_group(xred_dtype dtype, xred_op op, const xred_item *d_
     });
 }
 
+// ---------------------------------------------------------- grouped variant --
+// Device descriptors (the host cannot see the sizes, so it cannot list the
+// tiles): the batch is cut into `ngroups` runs of consecutive items, run q
+// gets its own `m` workgroups (blockIdx m*q .. m*q+m-1), and tile j of the
+// run goes to the run's workgroup j mod m.  The m workgroups of a run walk
+// its tiles side by side, so the tiles in flight stay one compact window, as
+// in the tile-table kernel; and since the workgroups of later runs are
+// dispatched in order as earlier ones retire, no workgroup keeps a fixed
+// share of the whole batch (a persistent grid ends with its slowest
+// workgroup).  Each workgroup scans its run's descriptors into an LDS
+// tile-start prefix, lists its own tiles (item, tile) by binary search, and
+// runs the tile-table kernel's tile on each.  No state is kept between calls,
+// so the launch can be captured in a graph.  With fewer workgroups than
+// m * ngroups (a CU budget), each set of m workgroups strides over the runs.
+constexpr int kGrpMaxItems = 2048;          // items per run (LDS prefix)
+constexpr int kGrpPerThread = kGrpMaxItems / kTB;
+constexpr size_t kGrpLdsBytes =
+    sizeof(uint64_t) * (kGrpMaxItems + 1 + kTB + kTB / 64) + sizeof(uint32_t) * kTB;
+
+template <class T>
+__device__ __forceinline__ uint64_t table_item_tiles(const xred_item &it)
+{
+    if (!item_runnable(it)) return 0;
+    return (it.count + table_tile_elems<T>() - 1) / table_tile_elems<T>();
+}
+
+// Exclusive prefix sum over the workgroup (kTB threads); *total gets the sum.
+__device__ __forceinline__ uint64_t block_exclusive_scan(uint64_t v, uint64_t *s_wave,
+                                                         uint64_t *total)
+{
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    uint64_t incl = v;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+        const uint64_t t = __shfl_up(incl, (unsigned)off, 64);
+        if (lane >= off) incl += t;
+    }
+    if (lane == 63) s_wave[wave] = incl;
+    __syncthreads();
+    uint64_t before = 0, sum = 0;
+#pragma unroll
+    for (int w = 0; w < kTB / 64; ++w) {
+        const uint64_t x = s_wave[w];
+        before += w < wave ? x : 0;
+        sum += x;
+    }
+    *total = sum;
+    return before + incl - v;
+}
+
+template <class T, class Op>
+__global__ __launch_bounds__(kTB) void batched_grouped_kernel(const xred_item *items, int nitems,
+                                                              uint32_t ngroups, uint32_t m)
+{
+    extern __shared__ uint64_t s_grp[];          // the occupancy reservation, partly used
+    uint64_t *s_pre = s_grp;                     // kGrpMaxItems + 1 tile starts
+    uint64_t *s_lt = s_pre + kGrpMaxItems + 1;   // kTB tiles within their item
+    uint64_t *s_wave = s_lt + kTB;               // kTB / 64 wave sums
+    uint32_t *s_item = (uint32_t *)(s_wave + kTB / 64);   // kTB items within the run
+    const uint32_t w = blockIdx.x % m;
+    const uint32_t sets = gridDim.x / m;
+    for (uint32_t q = blockIdx.x / m; q < ngroups; q += sets) {
+        const int i0 = (int)((uint64_t)nitems * q / ngroups);
+        const int n = (int)((uint64_t)nitems * (q + 1) / ngroups) - i0;   // <= kGrpMaxItems
+        // tile counts of the run's items, kGrpPerThread consecutive items per thread
+        uint64_t c[kGrpPerThread], mine = 0;
+#pragma unroll
+        for (int j = 0; j < kGrpPerThread; ++j) {
+            const int i = (int)threadIdx.x * kGrpPerThread + j;
+            c[j] = i < n ? table_item_tiles<T>(items[i0 + i]) : 0;
+            mine += c[j];
+        }
+        uint64_t total = 0;
+        uint64_t run = block_exclusive_scan(mine, s_wave, &total);
+#pragma unroll
+        for (int j = 0; j < kGrpPerThread; ++j) {
+            const int i = (int)threadIdx.x * kGrpPerThread + j;
+            if (i < n) s_pre[i] = run;
+            run += c[j];
+        }
+        if (threadIdx.x == 0) s_pre[n] = total;
+        __syncthreads();
+        // this workgroup's tiles are w, w + m, w + 2m, ... below total
+        for (uint64_t g0 = w; g0 < total; g0 += (uint64_t)kTB * m) {
+            const uint64_t left = (total - g0 + m - 1) / m;
+            const int cnt = left < (uint64_t)kTB ? (int)left : kTB;
+            if ((int)threadIdx.x < cnt) {
+                const uint64_t g = g0 + (uint64_t)threadIdx.x * m;
+                int lo = 0, hi = n;   // s_pre[lo] <= g < s_pre[hi]
+                while (hi - lo > 1) {
+                    const int mid = (lo + hi) >> 1;
+                    if (s_pre[mid] <= g) lo = mid;
+                    else hi = mid;
+                }
+                s_item[threadIdx.x] = (uint32_t)lo;
+                s_lt[threadIdx.x] = g - s_pre[lo];
+            }
+            __syncthreads();
+            for (int j = 0; j < cnt; ++j) {
+                const uint32_t k = __builtin_amdgcn_readfirstlane(s_item[j]);
+                table_tile<T, Op, true>(load_head(items + i0 + k), uniform64(s_lt[j]));
+            }
+            __syncthreads();   // the list is rewritten next
+        }
+        __syncthreads();       // the prefix is rewritten next
+    }
+}
+
+template <class T, class Op>
+hipError_t go_grouped(const xred_item *d_items, int nitems, uint32_t ngroups, uint32_t m,
+                      unsigned grid, int wgs_per_cu, hipStream_t s)
+{
+    int dev = 0, v = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&v, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor, dev) !=
+            hipSuccess ||
+        v <= 0)
+        v = 160 * 1024;
+    size_t lds = (size_t)(v / wgs_per_cu) / 512 * 512 - 512;
+    if (lds < kGrpLdsBytes) lds = kGrpLdsBytes;
+    hipLaunchKernelGGL((batched_grouped_kernel<T, Op>), dim3(grid), dim3(kTB), lds, s, d_items,
+                       nitems, ngroups, m);
+    return hipGetLastError();
+}
+
+// Grouped launcher for the element types Ts.
+template <class... Ts>
+hipError_t batched_grouped_group(xred_dtype dtype, xred_op op, const xred_item *d_items,
+                                 int nitems, uint32_t ngroups, uint32_t m, unsigned grid,
+                                 int wgs_per_cu, hipStream_t s)
+{
+    return with_dtype_among<Ts...>(dtype, [&](auto t) {
+        using T = decltype(t);
+        return with_op<T, true>(op, [&](auto o) {
+            return go_grouped<T, decltype(o)>(d_items, nitems, ngroups, m, grid, wgs_per_cu, s);
+        });
+    });
+}
+
 constexpr size_t rr_lds_bytes(int nitems)
 {
     return sizeof(uint2) * kListMax + sizeof(uint32_t) * ((size_t)nitems + 1);
@@ -502,27 +639,22 @@ hipError_t go_rr(bool planned, const xred_item *d_items, int nitems, const uint3
 }
 
 template <class T, class Op>
-hipError_t go(bool planned, const xred_item *d_items, int nitems, const WgStart *d_wg,
-              unsigned grid, hipStream_t s)
+hipError_t go(const xred_item *d_items, int nitems, const WgStart *d_wg, unsigned grid,
+              hipStream_t s)
 {
-    if (planned)
-        hipLaunchKernelGGL((batched_kernel<T, Op, true>), dim3(grid), dim3(kB), 0, s, d_items,
-                           nitems, d_wg);
-    else
-        hipLaunchKernelGGL((batched_kernel<T, Op, false>), dim3(grid), dim3(kB), 0, s,
-                           d_items, nitems, d_wg);
+    hipLaunchKernelGGL((batched_kernel<T, Op>), dim3(grid), dim3(kB), 0, s, d_items, nitems, d_wg);
     return hipGetLastError();
 }
 
 // Range-walking launcher for the element types Ts.
 template <class... Ts>
-hipError_t batched_group(xred_dtype dtype, xred_op op, bool planned, const xred_item *d_items,
-                         int nitems, const WgStart *d_wg, unsigned grid, hipStream_t s)
+hipError_t batched_group(xred_dtype dtype, xred_op op, const xred_item *d_items, int nitems,
+                         const WgStart *d_wg, unsigned grid, hipStream_t s)
 {
     return with_dtype_among<Ts...>(dtype, [&](auto t) {
         using T = decltype(t);
         return with_op<T, true>(op, [&](auto o) {
-            return go<T, decltype(o)>(planned, d_items, nitems, d_wg, grid, s);
+            return go<T, decltype(o)>(d_items, nitems, d_wg, grid, s);
         });
     });
 }

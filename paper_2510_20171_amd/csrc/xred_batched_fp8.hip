@@ -3,11 +3,10 @@
 
 namespace xred {
 
-hipError_t launch_batched_range_fp8(xred_dtype dtype, xred_op op, bool planned,
-                                 const xred_item *d_items, int nitems, const WgStart *d_wg,
-                                 unsigned grid, hipStream_t stream)
+hipError_t launch_batched_range_fp8(xred_dtype dtype, xred_op op, const xred_item *d_items,
+                                    int nitems, const WgStart *d_wg, unsigned grid, hipStream_t stream)
 {
-    return batched_group<TE4M3, TE5M2>(dtype, op, planned, d_items, nitems, d_wg, grid, stream);
+    return batched_group<TE4M3, TE5M2>(dtype, op, d_items, nitems, d_wg, grid, stream);
 }
 
 hipError_t launch_batched_rr_fp8(xred_dtype dtype, xred_op op, const xred_item *d_items,
@@ -20,6 +19,14 @@ hipError_t launch_batched_table_fp8(xred_dtype dtype, xred_op op, const xred_ite
                                  const uint32_t *d_table, uint64_t ntiles, hipStream_t stream)
 {
     return batched_table_group<TE4M3, TE5M2>(dtype, op, d_items, d_table, ntiles, stream);
+}
+
+hipError_t launch_batched_grouped_fp8(xred_dtype dtype, xred_op op, const xred_item *d_items,
+                                 int nitems, uint32_t ngroups, uint32_t m, unsigned grid,
+                                 int wgs_per_cu, hipStream_t stream)
+{
+    return batched_grouped_group<TE4M3, TE5M2>(dtype, op, d_items, nitems, ngroups, m, grid,
+                                          wgs_per_cu, stream);
 }
 
 }  // namespace xred

@@ -63,11 +63,7 @@ hipError_t launch_batched_planned(xred_dtype dtype, xred_op op, const xred_item 
                                   int nitems, const WgStart *d_wg, unsigned grid,
                                   hipStream_t stream);
 
-// Device-resident descriptors: every workgroup derives its share itself.
-hipError_t launch_batched_device(xred_dtype dtype, xred_op op, const xred_item *d_items,
-                                 int nitems, unsigned grid, hipStream_t stream);
-
-// Grid used for device-resident batches (fixed: the host cannot see sizes).
+// Grid of the host-planned range layout.
 unsigned batched_device_grid();
 
 // Round-robin batched kernel (batches of at most batched_rr_max_items()
@@ -78,16 +74,31 @@ int batched_rr_max_items();
 hipError_t launch_batched_rr(xred_dtype dtype, xred_op op, const xred_item *d_items, int nitems,
                              const uint32_t *d_tile_start, hipStream_t stream);
 
+// Device-resident descriptors, grouped: the batch is cut into ngroups runs of
+// at most batched_grouped_max_items() consecutive items, each run is dealt to
+// m workgroups tile by tile, and grid (a multiple of m, at least m) is
+// m * ngroups or fewer under a CU budget.  wgs_per_cu: workgroups allowed to
+// share one CU (the kernel's LDS reservation enforces it; m should be the
+// device's CUs times it).
+int batched_grouped_max_items();
+hipError_t launch_batched_grouped(xred_dtype dtype, xred_op op, const xred_item *d_items,
+                                  int nitems, uint32_t ngroups, uint32_t m, unsigned grid,
+                                  int wgs_per_cu, hipStream_t stream);
+
 // The batched launchers per group of element types (each in its own
 // translation unit).
 #define XRED_BATCHED_GROUP(G)                                                                  \
-    hipError_t launch_batched_range_##G(xred_dtype dtype, xred_op op, bool planned,            \
+    hipError_t launch_batched_range_##G(xred_dtype dtype, xred_op op,                          \
                                         const xred_item *d_items, int nitems,                  \
                                         const WgStart *d_wg, unsigned grid, hipStream_t s);    \
     hipError_t launch_batched_rr_##G(xred_dtype dtype, xred_op op, const xred_item *d_items,   \
                                      int nitems, const uint32_t *d_tile_start, hipStream_t s); \
     hipError_t launch_batched_table_##G(xred_dtype dtype, xred_op op, const xred_item *d_items, \
-                                        const uint32_t *d_table, uint64_t ntiles, hipStream_t s);
+                                        const uint32_t *d_table, uint64_t ntiles, hipStream_t s); \
+    hipError_t launch_batched_grouped_##G(xred_dtype dtype, xred_op op,                        \
+                                          const xred_item *d_items, int nitems,                \
+                                          uint32_t ngroups, uint32_t m, unsigned grid,         \
+                                          int wgs_per_cu, hipStream_t s);
 XRED_BATCHED_GROUP(float)
 XRED_BATCHED_GROUP(fp8)
 XRED_BATCHED_GROUP(int)
