@@ -538,7 +538,7 @@ def build_workload(name, torch, xr, L, wl):
     dominant kernel, its source family and committed profile, a config
     description, and a callable timing the CPU oracle on a bounded sample."""
     import numpy as np
-    w = wl.WORKLOADS["c3" if name == "c3ring" else name]
+    w = wl.WORKLOADS[{"c3ring": "c3", "c4dev": "c4"}.get(name, name)]
     stream = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
     if name == "c3ring":
         log(f"generating c3 inputs for the one-launch ring (16 chunks x {w.count} bf16)")
@@ -665,16 +665,34 @@ def build_workload(name, torch, xr, L, wl):
     items = xr.pack_items([(ctypes.addressof(rows[k]), outs.data_ptr() + int(opos[k]) * 2,
                             int(sizes[k]), P) for k in range(K)])
 
-    def step():
-        st = L.xred_batched_reduce(items, K, 1, 0, 0, stream)
-        if st:
-            xr._lib.check(st)
-    step._keep_inputs = (arena_d, outs, rows, items)
-    res = dict(step=step, alg_bytes=w.alg_bytes(sizes), family="batched",
-               kernel="batched_rr_kernel<bf16, sum, planned>",
+    if name == "c4dev":
+        # the same items with descriptors and source-pointer arrays in device memory
+        ptrs_d = torch.tensor((base + offs * 2).reshape(-1).astype(np.int64), device="cuda")
+        arr = np.zeros(K, xr.ITEM_DTYPE)
+        arr["srcs"] = ptrs_d.data_ptr() + 8 * P * np.arange(K, dtype=np.uint64)
+        arr["dst"] = outs.data_ptr() + opos.astype(np.uint64) * 2
+        arr["count"] = sizes
+        arr["nsrc"] = P
+        items_d = torch.from_numpy(arr.view(np.uint8).copy()).to("cuda")
+        items_ptr = ctypes.c_void_p(items_d.data_ptr())
+
+        def step():
+            st = L.xred_batched_reduce(items_ptr, K, 1, 0, 1, stream)
+            if st:
+                xr._lib.check(st)
+        step._keep_inputs = (arena_d, outs, ptrs_d, items_d)
+        kernel, where = "batched_grouped_kernel<bf16, sum>", "device descriptors"
+    else:
+        def step():
+            st = L.xred_batched_reduce(items, K, 1, 0, 0, stream)
+            if st:
+                xr._lib.check(st)
+        step._keep_inputs = (arena_d, outs, rows, items)
+        kernel, where = "batched_table_kernel<bf16, sum>", "host descriptors"
+    res = dict(step=step, alg_bytes=w.alg_bytes(sizes), family="batched", kernel=kernel,
                profile=ROOT / "profiles" / f"batched_bf16_{name}.md",
                config={"workload": f"{name}: batched_reduce of {K} items, P={P} bf16, sizes "
-                                   "log-uniform 8 KiB-1 MiB per source, host descriptors",
+                                   f"log-uniform 8 KiB-1 MiB per source, {where}",
                        "items": K, "P": P, "io_dtype": "bf16"})
     sample = [[arena[o:o + int(sizes[k])] for o in offs[k]] for k in range(64)]
 
@@ -701,7 +719,8 @@ def main() -> int:
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="c2",
-                    choices=["c1", "c2", "c3", "c3ring", "c4", "c5a", "c5b", "c2fp8", "sim", "sim1"],
+                    choices=["c1", "c2", "c3", "c3ring", "c4", "c4dev", "c5a", "c5b", "c2fp8", "sim",
+                             "sim1"],
                     help="which workload one step runs (default: the c2 gradient bucket)")
     ap.add_argument("--no-secondary", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
