@@ -54,6 +54,13 @@
  *     next synchronisation of the stream, as for any HIP kernel.
  *   - Element pointers must be aligned to the element size; 16-byte aligned
  *     buffers take the fast vector path, other alignments a slower scalar one.
+ *
+ * Environment (read once, when first needed; results never depend on them):
+ *   XRED_MAX_WORKGROUPS      initial CU budget (see xred_set_max_workgroups)
+ *   XRED_FUSED_WAVES_PER_CU  overrides the fused kernel's resident-wave cap
+ *   XRED_RR_WG_PER_CU        workgroups per CU of the round-robin batched kernel
+ *   XRED_BATCH_WG_PER_CU     workgroups per CU of host-planned range batches
+ * The last three are tuning overrides for measurement; leave them unset.
  */
 #ifndef XRED_H
 #define XRED_H

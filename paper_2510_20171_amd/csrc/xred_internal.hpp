@@ -7,9 +7,35 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include <tuple>
+#include <utility>
+
 #include "../../include/xred.h"
 
 namespace xred {
+
+// Enqueue kernel<<<grid, block, lds, stream>>>(args...) and return the launch
+// status.  hipLaunchKernel takes one pointer per argument; each argument is
+// first converted to the kernel's own parameter type.  (The <<<>>> form makes
+// two more runtime calls per launch and needs hipGetLastError afterwards,
+// about 0.15 us of host time on a launch-bound small call.)
+template <class... P, class... A, size_t... I>
+hipError_t launch_kernel_impl(void (*kernel)(P...), dim3 grid, dim3 block, size_t lds,
+                              hipStream_t stream, std::index_sequence<I...>, A &&...args)
+{
+    std::tuple<P...> packed(std::forward<A>(args)...);
+    void *ptrs[sizeof...(P) > 0 ? sizeof...(P) : 1] = {(void *)&std::get<I>(packed)...};
+    return hipLaunchKernel((const void *)kernel, grid, block, ptrs, lds, stream);
+}
+
+template <class... P, class... A>
+hipError_t launch_kernel(void (*kernel)(P...), dim3 grid, dim3 block, size_t lds,
+                         hipStream_t stream, A &&...args)
+{
+    static_assert(sizeof...(P) == sizeof...(A), "argument count differs from the kernel's");
+    return launch_kernel_impl(kernel, grid, block, lds, stream,
+                              std::index_sequence_for<P...>{}, std::forward<A>(args)...);
+}
 
 // Workgroup budget for one launch on the current device: the number of tiles,
 // capped by XRED_MAX_WORKGROUPS when set (a CU-budget knob: it never changes

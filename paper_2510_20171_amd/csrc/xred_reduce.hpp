@@ -99,18 +99,15 @@ hipError_t go_vec(const char *const *srcs, int nsrc, char *dst, size_t count, hi
     const uint32_t tail = (uint32_t)(count % T::kVec);
     constexpr size_t kTileWide = (size_t)kBWide * kU;
     const uint64_t tiles_wide = (nvec + kTileWide - 1) / kTileWide + (tail ? 1 : 0);
-    if (tiles_wide <= (uint64_t)device_cus() * kWideWgsPerCu) {
-        hipLaunchKernelGGL((reduce_vec_kernel<T, Op, NP, MAXP, kU, kBWide>),
-                           dim3(grid_for(tiles_wide)), dim3(kBWide), 0, s, ks, nsrc, dst, nvec,
-                           tail);
-        return hipGetLastError();
-    }
+    if (tiles_wide <= (uint64_t)device_cus() * kWideWgsPerCu)
+        return launch_kernel(reduce_vec_kernel<T, Op, NP, MAXP, kU, kBWide>,
+                             dim3(grid_for(tiles_wide)), dim3(kBWide), 0, s, ks, nsrc, dst, nvec,
+                             tail);
     constexpr size_t kTile = (size_t)kB * kU;
     const uint64_t tiles = (nvec + kTile - 1) / kTile + (tail ? 1 : 0);
-    hipLaunchKernelGGL((reduce_vec_kernel<T, Op, NP, MAXP, kU, kB>), dim3(grid_for(tiles)),
-                       dim3(kB), lds_for_waves(waves_for<NP>(count * T::kSize)), s, ks, nsrc, dst,
-                       nvec, tail);
-    return hipGetLastError();
+    return launch_kernel(reduce_vec_kernel<T, Op, NP, MAXP, kU, kB>, dim3(grid_for(tiles)),
+                         dim3(kB), lds_for_waves(waves_for<NP>(count * T::kSize)), s, ks, nsrc,
+                         dst, nvec, tail);
 }
 
 template <class T, class Op>
@@ -122,9 +119,9 @@ hipError_t go(const char *const *srcs, int nsrc, char *dst, size_t count, hipStr
         KernargSrc<XRED_MAX_SRC> ks;
         for (int p = 0; p < nsrc; ++p) ks.p[p] = srcs[p];
         for (int p = nsrc; p < XRED_MAX_SRC; ++p) ks.p[p] = nullptr;
-        hipLaunchKernelGGL((reduce_scalar_kernel<T, Op, kB>), dim3(grid_for((count + kB - 1) / kB)),
-                           dim3(kB), 0, s, ks, nsrc, dst, count);
-        return hipGetLastError();
+        return launch_kernel(reduce_scalar_kernel<T, Op, kB>,
+                             dim3(grid_for((count + kB - 1) / kB)), dim3(kB), 0, s, ks, nsrc, dst,
+                             count);
     }
     constexpr bool kWide = is_core_type<T>() && !__is_same(Op, OpAvg);
     switch (nsrc) {
