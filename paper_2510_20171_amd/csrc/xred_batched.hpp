@@ -485,7 +485,9 @@ hipError_t batched_table_group(xred_dtype dtype, xred_op op, const xred_item *d_
 // share of the whole batch (a persistent grid ends with its slowest
 // workgroup).  Each workgroup scans its run's descriptors into an LDS
 // tile-start prefix, lists its own tiles (item, tile) by binary search, and
-// runs the tile-table kernel's tile on each.  No state is kept between calls,
+// runs the tile-table kernel's tile on each, with a barrier after every tile
+// so the workgroup's waves read one tile together (c4: 5.7 against 5.45 TB/s
+// with the waves left to drift apart).  No state is kept between calls,
 // so the launch can be captured in a graph.  With fewer workgroups than
 // m * ngroups (a CU budget), each set of m workgroups strides over the runs.
 constexpr int kGrpMaxItems = 2048;          // items per run (LDS prefix)
@@ -575,6 +577,7 @@ __global__ __launch_bounds__(kTB) void batched_grouped_kernel(const xred_item *i
             for (int j = 0; j < cnt; ++j) {
                 const uint32_t k = __builtin_amdgcn_readfirstlane(s_item[j]);
                 table_tile<T, Op, true>(load_head(items + i0 + k), uniform64(s_lt[j]));
+                __syncthreads();   // the waves start every tile together
             }
             __syncthreads();   // the list is rewritten next
         }
