@@ -313,6 +313,9 @@ __global__ __launch_bounds__(kB) void batched_rr_kernel(const xred_item *items, 
                 batched_tile<T, Op>(load_item(items, cur.k), cur.lt);
             }
             cur = nxt;
+            // the waves start every tile together (8 items of 32M bf16 per
+            // source: 5.18 against 4.99 TB/s; 64 items of 4M: 4.90 against 4.98)
+            __syncthreads();
         }
         __syncthreads();
     }
