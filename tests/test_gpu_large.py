@@ -126,3 +126,39 @@ def test_batched_table_at_its_limit(xr, orc):
                          f"item {k} (sampled)")
     del srcs, outs
     torch.cuda.empty_cache()
+
+
+def test_device_batch_with_an_item_past_4gib(xr, orc):
+    """Device descriptors, 70 items (two runs of the grouped kernel): item 0
+    holds 2^31 + 5 bf16 elements per source (past 4 GiB, over 2^19 tiles), the
+    others up to 9000; sampled columns of item 0, every other item whole."""
+    n0 = (1 << 31) + 5
+    big = [_random_bits(n0, 2, 1700 + p) for p in range(2)]
+    out0 = torch.empty(n0, dtype=torch.int16, device="cuda")
+    rng = np.random.default_rng(31)
+    small = []
+    for k in range(69):
+        n = int(rng.integers(1, 9000))
+        small.append(([_random_bits(n, 2, 1800 + 2 * k + p) for p in range(2)],
+                      torch.zeros(n, dtype=torch.int16, device="cuda")))
+    keep, rows = [], []
+    for srcs, out in [(big, out0)] + small:
+        pa = torch.tensor([s.data_ptr() for s in srcs], dtype=torch.int64, device="cuda")
+        keep.append(pa)
+        rows.append((pa.data_ptr(), out.data_ptr(), out.numel(), len(srcs), 0))
+    arr = np.zeros(len(rows), xr.ITEM_DTYPE)
+    for k, r in enumerate(rows):
+        arr[k] = r
+    xr.batched_reduce(torch.from_numpy(arr.view(np.uint8).copy()).to("cuda"), "sum",
+                      dtype="bf16")
+    torch.cuda.synchronize()
+    idx = _samples(n0, 2, np.random.default_rng(32))
+    cols = [gu.bits(s[idx], "bf16").copy() for s in big]
+    gu.assert_parity(out0[idx], orc.allreduce_local(cols, "bf16", "sum"), "bf16", "sum",
+                     "item 0")
+    for k, (srcs, out) in enumerate(small):
+        cols = [gu.bits(s, "bf16").copy() for s in srcs]
+        gu.assert_parity(out, orc.allreduce_local(cols, "bf16", "sum"), "bf16", "sum",
+                         f"item {k + 1}")
+    del big, out0, small, keep
+    torch.cuda.empty_cache()

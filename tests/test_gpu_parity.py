@@ -441,8 +441,10 @@ def test_specials_exact(xr):
 
 @pytest.mark.parametrize("on_device", [False, True])
 def test_batched_beyond_round_robin_limit(xr, orc, on_device):
-    """More items than the round-robin plan holds (8192): the range-walking
-    kernels take over; every item against the oracle."""
+    """More items than the round-robin plan holds (8192): host descriptors
+    take the tile table (or, past its size, the host-planned range kernel),
+    device descriptors the grouped kernel (141 runs of 64 items); every item
+    against the oracle."""
     rng = np.random.default_rng(77)
     K = 9000
     sizes = rng.integers(1, 600, size=K)
