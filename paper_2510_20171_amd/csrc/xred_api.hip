@@ -322,8 +322,9 @@ int device_cus()
 std::atomic<unsigned> g_max_workgroups{(unsigned)env_long("XRED_MAX_WORKGROUPS", 0)};
 
 // Device-descriptor batches: items per run and workgroups per CU of the
-// grouped kernel (measured on the 4096-item log-uniform batch: 32 / 64 / 128 /
-// 256 items per run 5.47 / 5.45 / 5.19 / 5.12 TB/s, 64 best on equal items).
+// grouped kernel (measured on the 4096-item log-uniform batch: 32 / 64 / 96 /
+// 128 items per run 5.44-5.50 / 5.69-5.70 / 5.49-5.51 / 5.36-5.38 TB/s; 64
+// also best on equal items).
 constexpr int kGroupedRunItems = 64;
 constexpr int kGroupedWgsPerCu = 2;
 
@@ -350,7 +351,9 @@ unsigned batched_device_grid()
 hipError_t batched_device(const xred_item *items, int nitems, xred_dtype dtype, xred_op op,
                           hipStream_t stream)
 {
-    const uint64_t ngroups = ((uint64_t)nitems + kGroupedRunItems - 1) / kGroupedRunItems;
+    const uint64_t per_run =
+        (uint64_t)std::min(kGroupedRunItems, batched_grouped_max_items());   // LDS prefix size
+    const uint64_t ngroups = ((uint64_t)nitems + per_run - 1) / per_run;
     const unsigned cap = g_max_workgroups.load(std::memory_order_relaxed);
     uint64_t m = (uint64_t)device_cus() * kGroupedWgsPerCu;
     if (cap != 0 && m > cap) m = cap;
