@@ -34,6 +34,9 @@ sys.path.insert(0, str(ROOT))
 
 METRIC = "reduce-copy GB/s (read+write) and % HBM peak at 1 GPU; small-msg µs/call"
 HBM_PEAK_GBS = 8000.0     # MI355X HBM3E, published
+# workloads --workload can time; the variants reuse another workload's inputs
+WORKLOAD_NAMES = ("c1", "c2", "c3", "c3ring", "c4", "c4dev", "c5a", "c5b", "c2fp8", "sim", "sim1")
+WORKLOAD_OF = {"c3ring": "c3", "c4dev": "c4"}
 CSRC = "paper_2510_20171_amd/csrc/"
 _COMMON = [CSRC + "xred_device.hpp", CSRC + "xred_kernels.hpp", CSRC + "xred_dispatch.hpp"]
 KERNEL_SOURCES = {
@@ -552,7 +555,7 @@ def build_workload(name, torch, xr, L, wl):
     dominant kernel, its source family and committed profile, a config
     description, and a callable timing the CPU oracle on a bounded sample."""
     import numpy as np
-    w = wl.WORKLOADS[{"c3ring": "c3", "c4dev": "c4"}.get(name, name)]
+    w = wl.WORKLOADS[WORKLOAD_OF.get(name, name)]
     stream = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
     if name == "c3ring":
         log(f"generating c3 inputs for the one-launch ring (16 chunks x {w.count} bf16)")
@@ -733,8 +736,7 @@ def main() -> int:
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="c2",
-                    choices=["c1", "c2", "c3", "c3ring", "c4", "c4dev", "c5a", "c5b", "c2fp8", "sim",
-                             "sim1"],
+                    choices=WORKLOAD_NAMES,
                     help="which workload one step runs (default: the c2 gradient bucket)")
     ap.add_argument("--no-secondary", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")

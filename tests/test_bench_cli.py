@@ -29,3 +29,21 @@ def test_algorithmic_bytes():
     assert wl.WORKLOADS["sim1"].alg_bytes() == 2 * 8 * 64 * M * 2
     # batched: (P_k + 1) n_k sizeof summed over the items
     assert wl.WORKLOADS["c4"].alg_bytes([10, 20]) == 9 * 30 * 2
+
+
+def test_c4_batch_bytes_match_the_quoted_figure():
+    # the seeded 4096-item batch (host and device descriptors alike) moves the
+    # algorithmic byte count the committed profiles and results quote
+    w = wl.WORKLOADS["c4"]
+    sizes = wl.batched_sizes(w)
+    assert len(sizes) == 4096
+    assert 4096 <= int(sizes.min()) and int(sizes.max()) <= (1 << 20) // 2
+    assert w.alg_bytes(sizes) == 7_801_271_568
+
+
+def test_every_bench_workload_has_a_definition():
+    sys.path.insert(0, str(ROOT))
+    import bench
+    assert "c4dev" in bench.WORKLOAD_NAMES and "c2" in bench.WORKLOAD_NAMES
+    for n in bench.WORKLOAD_NAMES:
+        assert bench.WORKLOAD_OF.get(n, n) in wl.WORKLOADS, n
