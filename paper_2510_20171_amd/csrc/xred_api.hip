@@ -172,11 +172,11 @@ xred_status batched_host(const xred_item *items, int nitems, xred_dtype dtype, x
         return fail(XRED_UNSUPPORTED, "host-side descriptors cannot be captured in a graph "
                                       "(their staging is reused); use XRED_ITEMS_ON_DEVICE");
 
-    // Tile-table layout (one workgroup per tile; the table adds 4 bytes per
-    // tile to the descriptor copy, so batches of very large items, whose table
-    // would pass kMaxTableTiles entries (2 MiB), use the layouts after it):
-    //     items (reserved = the item's first tile) | item of every tile (u32,
-    //     padded to 8 B) | source pointers
+    // Tile-table layout (one workgroup per tile; the table adds 2 or 4 bytes
+    // per tile to the descriptor copy, so batches of very large items, whose
+    // table would pass kMaxTableTiles entries (2 MiB), use the layouts after it):
+    //     items (reserved = the item's first tile) | item of every tile (u16 up
+    //     to 65536 items, else u32; padded to 8 B) | source pointers
     // Round-robin layout (up to batched_rr_max_items() items):
     //     items | tile-start prefix (nitems + 1 u32, padded to 8 B) | source pointers
     // Range layout (more items):
@@ -184,11 +184,14 @@ xred_status batched_host(const xred_item *items, int nitems, xred_dtype dtype, x
     constexpr uint64_t kMaxTableTiles = 1u << 19;
     const bool table = table_tiles <= kMaxTableTiles;
     const bool rr = !table && nitems <= batched_rr_max_items();
+    // 16-bit tile-list entries while item indices fit (halves the largest part
+    // of the staged copy; c4: 830 -> 616 KB)
+    const bool narrow = table && nitems <= 65536;
     const unsigned grid = table || rr
                               ? 0u
                               : (unsigned)std::min<uint64_t>(total_tiles, batched_device_grid());
     const size_t items_bytes = sizeof(xred_item) * (size_t)nitems;
-    const size_t plan_bytes = table ? (4 * (size_t)table_tiles + 7) / 8 * 8
+    const size_t plan_bytes = table ? ((narrow ? 2 : 4) * (size_t)table_tiles + 7) / 8 * 8
                               : rr  ? (4 * ((size_t)nitems + 1) + 7) / 8 * 8
                                     : sizeof(WgStart) * (size_t)grid;
     const size_t need = items_bytes + plan_bytes + 8 * (size_t)total_ptrs;
@@ -242,7 +245,16 @@ xred_status batched_host(const xred_item *items, int nitems, xred_dtype dtype, x
         for (uint32_t p = 0; p < it.nsrc; ++p) h_ptrs[pos + p] = it.srcs[p];
         pos += it.nsrc;
     }
-    if (table) {
+    if (table && narrow) {
+        uint16_t *h_tab = (uint16_t *)(h + items_bytes);
+        uint32_t w = 0;
+        for (int k = 0; k < nitems; ++k) {
+            const uint32_t nt = (uint32_t)((items[k].count + tt - 1) / tt);
+            h_items[k].reserved = w;
+            for (uint32_t t = 0; t < nt; ++t) h_tab[w++] = (uint16_t)k;
+        }
+        if (w & 1) h_tab[w] = 0;   // the padding half of the last word
+    } else if (table) {
         uint32_t *h_tab = (uint32_t *)(h + items_bytes);
         uint32_t w = 0;
         for (int k = 0; k < nitems; ++k) {
@@ -281,7 +293,8 @@ xred_status batched_host(const xred_item *items, int nitems, xred_dtype dtype, x
     hipError_t le;
     if (table)
         le = launch_batched_table(dtype, op, (const xred_item *)d,
-                                  (const uint32_t *)(d + items_bytes), table_tiles, stream);
+                                  (const uint32_t *)(d + items_bytes), narrow, table_tiles,
+                                  stream);
     else if (rr)
         le = launch_batched_rr(dtype, op, (const xred_item *)d, nitems,
                                (const uint32_t *)(d + items_bytes), stream);

@@ -40,15 +40,16 @@ uint64_t batched_table_tile_elems(xred_dtype dtype)
 }
 
 hipError_t launch_batched_table(xred_dtype dtype, xred_op op, const xred_item *d_items,
-                                const uint32_t *d_table, uint64_t ntiles, hipStream_t stream)
+                                const uint32_t *d_table, bool narrow, uint64_t ntiles,
+                                hipStream_t stream)
 {
     switch (group_of(dtype)) {
     case TypeGroup::kFloat:
-        return launch_batched_table_float(dtype, op, d_items, d_table, ntiles, stream);
+        return launch_batched_table_float(dtype, op, d_items, d_table, narrow, ntiles, stream);
     case TypeGroup::kFp8:
-        return launch_batched_table_fp8(dtype, op, d_items, d_table, ntiles, stream);
+        return launch_batched_table_fp8(dtype, op, d_items, d_table, narrow, ntiles, stream);
     default:
-        return launch_batched_table_int(dtype, op, d_items, d_table, ntiles, stream);
+        return launch_batched_table_int(dtype, op, d_items, d_table, narrow, ntiles, stream);
     }
 }
 

@@ -432,7 +432,10 @@ __device__ __forceinline__ void table_tile(const ItemHead &h, uint64_t lt)
     }
 }
 
-template <class T, class Op>
+// NARROW: the table holds 16-bit item indices (batches of at most 65536
+// items), two per 32-bit word, little-endian; the word is loaded whole (the
+// table is padded to 8 bytes) so every scalar load stays dword-aligned.
+template <class T, class Op, bool NARROW>
 __global__ __launch_bounds__(kTB) void batched_table_kernel(const xred_item *items,
                                                             const uint32_t *table,
                                                             uint64_t ntiles)
@@ -440,15 +443,21 @@ __global__ __launch_bounds__(kTB) void batched_table_kernel(const xred_item *ite
     extern __shared__ char occupancy_reservation[];
     (void)occupancy_reservation;
     for (uint64_t g = blockIdx.x; g < ntiles; g += gridDim.x) {
-        const uint32_t k = sload(&table[g]);
+        uint32_t k;
+        if constexpr (NARROW) {
+            const uint32_t pair = sload(&table[g >> 1]);
+            k = (g & 1) ? pair >> 16 : pair & 0xFFFFu;
+        } else {
+            k = sload(&table[g]);
+        }
         const xred_item *it = items + k;
         table_tile<T, Op, false>(load_head(it), g - sload(&it->reserved));
     }
 }
 
 template <class T, class Op>
-hipError_t go_table(const xred_item *d_items, const uint32_t *d_table, uint64_t ntiles,
-                    hipStream_t s)
+hipError_t go_table(const xred_item *d_items, const uint32_t *d_table, bool narrow,
+                    uint64_t ntiles, hipStream_t s)
 {
     static const size_t lds = [] {
         int dev = 0, v = 0;
@@ -459,20 +468,23 @@ hipError_t go_table(const xred_item *d_items, const uint32_t *d_table, uint64_t 
             v = 160 * 1024;
         return (size_t)(v / kTableWgsPerCu) / 512 * 512 - 512;
     }();
-    hipLaunchKernelGGL((batched_table_kernel<T, Op>), dim3(grid_for(ntiles)), dim3(kTB), lds, s,
-                       d_items, d_table, ntiles);
-    return hipGetLastError();
+    if (narrow)
+        return launch_kernel(batched_table_kernel<T, Op, true>, dim3(grid_for(ntiles)), dim3(kTB),
+                             lds, s, d_items, d_table, ntiles);
+    return launch_kernel(batched_table_kernel<T, Op, false>, dim3(grid_for(ntiles)), dim3(kTB),
+                         lds, s, d_items, d_table, ntiles);
 }
 
 // Tile-table launcher for the element types Ts.
 template <class... Ts>
 hipError_t batched_table_group(xred_dtype dtype, xred_op op, const xred_item *d_items,
-                               const uint32_t *d_table, uint64_t ntiles, hipStream_t s)
+                               const uint32_t *d_table, bool narrow, uint64_t ntiles,
+                               hipStream_t s)
 {
     return with_dtype_among<Ts...>(dtype, [&](auto t) {
         using T = decltype(t);
         return with_op<T, true>(op, [&](auto o) {
-            return go_table<T, decltype(o)>(d_items, d_table, ntiles, s);
+            return go_table<T, decltype(o)>(d_items, d_table, narrow, ntiles, s);
         });
     });
 }

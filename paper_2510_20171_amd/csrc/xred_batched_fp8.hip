@@ -16,9 +16,11 @@ hipError_t launch_batched_rr_fp8(xred_dtype dtype, xred_op op, const xred_item *
 }
 
 hipError_t launch_batched_table_fp8(xred_dtype dtype, xred_op op, const xred_item *d_items,
-                                 const uint32_t *d_table, uint64_t ntiles, hipStream_t stream)
+                                    const uint32_t *d_table, bool narrow, uint64_t ntiles,
+                                    hipStream_t stream)
 {
-    return batched_table_group<TE4M3, TE5M2>(dtype, op, d_items, d_table, ntiles, stream);
+    return batched_table_group<TE4M3, TE5M2>(dtype, op, d_items, d_table, narrow,
+                                                  ntiles, stream);
 }
 
 hipError_t launch_batched_grouped_fp8(xred_dtype dtype, xred_op op, const xred_item *d_items,

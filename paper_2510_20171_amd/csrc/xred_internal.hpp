@@ -78,10 +78,13 @@ uint64_t batched_tile_elems(xred_dtype dtype);
 
 // Host descriptors, one workgroup per tile: tile w of the batch (of
 // batched_table_tile_elems(dtype) elements) belongs to item table[w], whose
-// staged descriptor holds the index of its first tile in `reserved`.
+// staged descriptor holds the index of its first tile in `reserved`.  narrow:
+// the entries are 16-bit (two per 32-bit word, little-endian; the table is
+// padded to 8 bytes), for batches of at most 65536 items.
 uint64_t batched_table_tile_elems(xred_dtype dtype);
 hipError_t launch_batched_table(xred_dtype dtype, xred_op op, const xred_item *d_items,
-                                const uint32_t *d_table, uint64_t ntiles, hipStream_t stream);
+                                const uint32_t *d_table, bool narrow, uint64_t ntiles,
+                                hipStream_t stream);
 
 // Host-planned: d_items (device copy, srcs pointing to device arrays) and one
 // WgStart per workgroup.
@@ -120,7 +123,8 @@ hipError_t launch_batched_grouped(xred_dtype dtype, xred_op op, const xred_item 
     hipError_t launch_batched_rr_##G(xred_dtype dtype, xred_op op, const xred_item *d_items,   \
                                      int nitems, const uint32_t *d_tile_start, hipStream_t s); \
     hipError_t launch_batched_table_##G(xred_dtype dtype, xred_op op, const xred_item *d_items, \
-                                        const uint32_t *d_table, uint64_t ntiles, hipStream_t s); \
+                                        const uint32_t *d_table, bool narrow, uint64_t ntiles, \
+                                        hipStream_t s);                                        \
     hipError_t launch_batched_grouped_##G(xred_dtype dtype, xred_op op,                        \
                                           const xred_item *d_items, int nitems,                \
                                           uint32_t ngroups, uint32_t m, unsigned grid,         \

@@ -481,3 +481,25 @@ def test_batched_beyond_round_robin_limit(xr, orc, on_device):
     got = gu.bits(out_dev, "bf16")
     exp = np.concatenate([orc.allreduce_local(s, "bf16", "sum") for s in host_srcs])
     gu.assert_parity(got, exp, "bf16", "sum", f"{K} items, device={on_device}")
+
+
+@pytest.mark.parametrize("K", [65536, 65537])
+def test_batched_tile_list_entry_width(xr, orc, K):
+    """Host descriptors on both sides of the tile list's 16-bit entries (at
+    most 65536 items) and its 32-bit ones: K int32 items of 1..40 elements
+    over two sources, laid end to end, so the concatenated outputs equal one
+    oracle reduction of the concatenated sources."""
+    rng = np.random.default_rng(K)
+    sizes = rng.integers(1, 41, size=K)
+    sizes[-1] = 4097                        # the last item spans two tiles
+    total = int(sizes.sum())
+    srcs_np = [pins.random_column_values(rng, "i32", total) for _ in range(2)]
+    d = [gu.to_dev(s, "i32") for s in srcs_np]
+    out = torch.zeros(total, dtype=torch.int32, device="cuda")
+    items, pos = [], 0
+    for n in sizes.tolist():
+        items.append(([x[pos:pos + n] for x in d], out[pos:pos + n]))
+        pos += n
+    xr.batched_reduce(items, "sum", dtype="i32")
+    torch.cuda.synchronize()
+    gu.assert_parity(out, orc.allreduce_local(srcs_np, "i32", "sum"), "i32", "sum", f"K={K}")
