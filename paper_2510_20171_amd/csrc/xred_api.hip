@@ -109,6 +109,7 @@ struct Slot {
     void *dev = nullptr;
     size_t cap = 0;
     hipEvent_t done = nullptr;
+    hipEvent_t copied = nullptr;   // the slot's copy on the side stream has completed
     bool pending = false;
 };
 constexpr int kSlots = 4;
@@ -116,7 +117,13 @@ struct Pool {
     std::mutex mu;
     Slot slot[kSlots];
     unsigned next = 0;
+    hipStream_t copy = nullptr;    // side stream for the copies of large batches
 };
+// Staged batches at least this large are copied on the pool's side stream, so
+// the copy overlaps the kernel already running on the caller's stream; smaller
+// ones stay on the caller's stream, where the cross-stream wait would cost
+// more than the copy.
+constexpr size_t kSideCopyBytes = 256 << 10;
 Pool g_pool[kMaxDevices];
 
 void free_slot(Slot &s)
@@ -225,6 +232,15 @@ xred_status batched_host(const xred_item *items, int nitems, xred_dtype dtype, x
     }
     if (!s.done && (e = hipEventCreateWithFlags(&s.done, hipEventDisableTiming)) != hipSuccess)
         return hip_fail(e, "hipEventCreate");
+    const bool side = need >= kSideCopyBytes;
+    if (side && !s.copied &&
+        (e = hipEventCreateWithFlags(&s.copied, hipEventDisableTiming)) != hipSuccess)
+        return hip_fail(e, "hipEventCreate");
+    if (side && !pool.copy &&
+        (e = hipStreamCreateWithFlags(&pool.copy, hipStreamNonBlocking)) != hipSuccess) {
+        pool.copy = nullptr;
+        return hip_fail(e, "hipStreamCreate(copy stream)");
+    }
 
     char *h = (char *)s.host;
     char *d = (char *)s.dev;
@@ -288,8 +304,19 @@ xred_status batched_host(const xred_item *items, int nitems, xred_dtype dtype, x
             h_wg[b].local_tile = g0 - k_first;
         }
     }
-    e = hipMemcpyAsync(s.dev, s.host, need, hipMemcpyHostToDevice, stream);
-    if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync(descriptors)");
+    if (side) {
+        // the slot's device half is free (its last kernel completed above)
+        e = hipMemcpyAsync(s.dev, s.host, need, hipMemcpyHostToDevice, pool.copy);
+        if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync(descriptors)");
+        if ((e = hipEventRecord(s.copied, pool.copy)) != hipSuccess ||
+            (e = hipStreamWaitEvent(stream, s.copied, 0)) != hipSuccess) {
+            (void)hipStreamSynchronize(pool.copy);
+            return hip_fail(e, "copy-stream event");
+        }
+    } else {
+        e = hipMemcpyAsync(s.dev, s.host, need, hipMemcpyHostToDevice, stream);
+        if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync(descriptors)");
+    }
     hipError_t le;
     if (table)
         le = launch_batched_table(dtype, op, (const xred_item *)d,
@@ -675,13 +702,17 @@ XRED_API void xred_release(void)
         std::lock_guard<std::mutex> lock(pool.mu);
         bool any = false;
         for (Slot &s : pool.slot) any |= s.host != nullptr || s.done != nullptr;
+        any |= pool.copy != nullptr;
         if (!any) continue;
         (void)hipSetDevice(d);
         for (Slot &s : pool.slot) {
             free_slot(s);
             if (s.done) (void)hipEventDestroy(s.done);
-            s.done = nullptr;
+            if (s.copied) (void)hipEventDestroy(s.copied);
+            s.done = s.copied = nullptr;
         }
+        if (pool.copy) (void)hipStreamDestroy(pool.copy);
+        pool.copy = nullptr;
     }
     if (have_dev) (void)hipSetDevice(cur);
 }
