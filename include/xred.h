@@ -185,7 +185,11 @@ XRED_API xred_status xred_acc_cast(const void *acc, void *dst, size_t count, xre
  *            xred_allreduce_local; the library stages the descriptors, with
  *            a list of every tile's item, into device memory it owns (pinned
  *            staging slots reused once the launch that read them has
- *            completed) and runs one workgroup per tile.  Not capturable: on a
+ *            completed) and runs one workgroup per tile.  Batches of 256 KiB
+ *            of staged data or more are copied on a stream the library owns
+ *            (one per device, default priority), which the caller's stream
+ *            then waits for through an event, so the copy overlaps earlier
+ *            work on the caller's stream.  Not capturable: on a
  *            stream under graph capture the call returns XRED_UNSUPPORTED
  *            (a replay would copy whatever a later call left in the slot).
  *   XRED_ITEMS_ON_DEVICE: `items` and every items[k].srcs are DEVICE memory,

@@ -503,3 +503,33 @@ def test_batched_tile_list_entry_width(xr, orc, K):
     xr.batched_reduce(items, "sum", dtype="i32")
     torch.cuda.synchronize()
     gu.assert_parity(out, orc.allreduce_local(srcs_np, "i32", "sum"), "i32", "sum", f"K={K}")
+
+
+def test_batched_large_host_batches_back_to_back(xr, orc):
+    """Six host batches whose staged descriptors pass 256 KiB (copied on the
+    library's own stream), enqueued back to back on two alternating caller
+    streams with no synchronisation in between: the staging slots are reused
+    and every batch must still see its own descriptors."""
+    rng = np.random.default_rng(61)
+    K = 3000
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    runs = []
+    for r in range(6):
+        sizes = rng.integers(1, 300, size=K)
+        total = int(sizes.sum())
+        srcs_np = [pins.random_column_values(rng, "bf16", total) for _ in range(3)]
+        d = [gu.to_dev(s, "bf16") for s in srcs_np]
+        out = torch.zeros(total, dtype=torch.bfloat16, device="cuda")
+        items, pos = [], 0
+        for n in sizes.tolist():
+            items.append(([x[pos:pos + n] for x in d], out[pos:pos + n]))
+            pos += n
+        runs.append((srcs_np, d, out, items))
+    torch.cuda.synchronize()
+    for r, (_, _, _, items) in enumerate(runs):
+        with torch.cuda.stream(streams[r % 2]):
+            xr.batched_reduce(items, "sum", dtype="bf16")
+    torch.cuda.synchronize()
+    for r, (srcs_np, _, out, _) in enumerate(runs):
+        gu.assert_parity(out, orc.allreduce_local(srcs_np, "bf16", "sum"), "bf16", "sum",
+                         f"batch {r}")
