@@ -185,7 +185,9 @@ XRED_API xred_status xred_acc_cast(const void *acc, void *dst, size_t count, xre
  *            xred_allreduce_local; the library stages the descriptors, with
  *            a list of every tile's item, into device memory it owns (pinned
  *            staging slots reused once the launch that read them has
- *            completed) and runs one workgroup per tile.  Batches of 256 KiB
+ *            completed) and runs one workgroup per tile.  A batch of at most
+ *            two tiles per CU and 64 KiB of staged data is read by the kernel
+ *            straight from the pinned slot (no copy); batches of 256 KiB
  *            of staged data or more are copied on a stream the library owns
  *            (one per device, default priority), which the caller's stream
  *            then waits for through an event, so the copy overlaps earlier

@@ -107,6 +107,7 @@ long env_long(const char *name, long dflt)
 struct Slot {
     void *host = nullptr;
     void *dev = nullptr;
+    void *host_dev = nullptr;      // the device's address of `host`
     size_t cap = 0;
     hipEvent_t done = nullptr;
     hipEvent_t copied = nullptr;   // the slot's copy on the side stream has completed
@@ -124,6 +125,8 @@ struct Pool {
 // ones stay on the caller's stream, where the cross-stream wait would cost
 // more than the copy.
 constexpr size_t kSideCopyBytes = 256 << 10;
+// At most this much staged data is read by the kernel from pinned memory.
+constexpr size_t kDirectBytes = 64 << 10;
 Pool g_pool[kMaxDevices];
 
 void free_slot(Slot &s)
@@ -131,7 +134,7 @@ void free_slot(Slot &s)
     if (s.pending && s.done) (void)hipEventSynchronize(s.done);
     if (s.host) (void)hipHostFree(s.host);
     if (s.dev) (void)hipFree(s.dev);
-    s.host = s.dev = nullptr;
+    s.host = s.dev = s.host_dev = nullptr;
     s.cap = 0;
     s.pending = false;
 }
@@ -228,11 +231,20 @@ xred_status batched_host(const xred_item *items, int nitems, xred_dtype dtype, x
             s.host = s.dev = nullptr;
             return fail(XRED_OUT_OF_MEMORY, "device staging of %zu bytes", cap);
         }
+        if ((e = hipHostGetDevicePointer(&s.host_dev, s.host, 0)) != hipSuccess) {
+            free_slot(s);
+            return hip_fail(e, "hipHostGetDevicePointer(staging)");
+        }
         s.cap = cap;
     }
     if (!s.done && (e = hipEventCreateWithFlags(&s.done, hipEventDisableTiming)) != hipSuccess)
         return hip_fail(e, "hipEventCreate");
-    const bool side = need >= kSideCopyBytes;
+    // A batch of one round of table workgroups (two per CU) and little staged
+    // data is read by the kernel straight from the pinned slot: a few host
+    // reads per workgroup, paid once in parallel, instead of a copy on the
+    // stream before the launch.
+    const bool direct = table && table_tiles <= 2 * (uint64_t)device_cus() && need <= kDirectBytes;
+    const bool side = !direct && need >= kSideCopyBytes;
     if (side && !s.copied &&
         (e = hipEventCreateWithFlags(&s.copied, hipEventDisableTiming)) != hipSuccess)
         return hip_fail(e, "hipEventCreate");
@@ -243,7 +255,7 @@ xred_status batched_host(const xred_item *items, int nitems, xred_dtype dtype, x
     }
 
     char *h = (char *)s.host;
-    char *d = (char *)s.dev;
+    char *d = (char *)(direct ? s.host_dev : s.dev);
     xred_item *h_items = (xred_item *)h;
     const void **h_ptrs = (const void **)(h + items_bytes + plan_bytes);
     const char *d_ptrs = d + items_bytes + plan_bytes;
@@ -313,7 +325,7 @@ xred_status batched_host(const xred_item *items, int nitems, xred_dtype dtype, x
             (void)hipStreamSynchronize(pool.copy);
             return hip_fail(e, "copy-stream event");
         }
-    } else {
+    } else if (!direct) {
         e = hipMemcpyAsync(s.dev, s.host, need, hipMemcpyHostToDevice, stream);
         if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync(descriptors)");
     }

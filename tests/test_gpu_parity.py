@@ -505,17 +505,18 @@ def test_batched_tile_list_entry_width(xr, orc, K):
     gu.assert_parity(out, orc.allreduce_local(srcs_np, "i32", "sum"), "i32", "sum", f"K={K}")
 
 
-def test_batched_large_host_batches_back_to_back(xr, orc):
-    """Six host batches whose staged descriptors pass 256 KiB (copied on the
-    library's own stream), enqueued back to back on two alternating caller
-    streams with no synchronisation in between: the staging slots are reused
-    and every batch must still see its own descriptors."""
-    rng = np.random.default_rng(61)
-    K = 3000
+@pytest.mark.parametrize("K,nruns,maxn", [(3000, 6, 300), (40, 12, 300)])
+def test_batched_host_batches_back_to_back(xr, orc, K, nruns, maxn):
+    """Host batches enqueued back to back on two alternating caller streams
+    with no synchronisation in between, so the staging slots are reused while
+    earlier batches may still run: 3000 items (staged data past 256 KiB,
+    copied on the library's own stream) and 40 items (read by the kernel from
+    the pinned slot itself).  Every batch must still see its own descriptors."""
+    rng = np.random.default_rng(61 + K)
     streams = [torch.cuda.Stream(), torch.cuda.Stream()]
     runs = []
-    for r in range(6):
-        sizes = rng.integers(1, 300, size=K)
+    for r in range(nruns):
+        sizes = rng.integers(1, maxn, size=K)
         total = int(sizes.sum())
         srcs_np = [pins.random_column_values(rng, "bf16", total) for _ in range(3)]
         d = [gu.to_dev(s, "bf16") for s in srcs_np]
