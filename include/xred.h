@@ -167,9 +167,14 @@ XRED_API xred_status xred_reduce_copy_step(const void *in, void *acc, void *dst,
                                            void *hip_stream);
 
 /*
- * Closing cast of a step-wise sequence: dst[i] = down(acc[i]), i < count.
+ * Closing cast of a step-wise sequence: dst[i] = down(acc[i]), i < count --
+ * the rounding to the I/O type that ends the ring's ReduceScatter phase once
+ * the last incoming chunk has been folded into the accumulator (the Reduce of
+ * the FTAR pipeline, Section 5, when the last step is not run as FINAL).
  *   acc      count accumulator elements (see xred_reduce_copy_step)
  *   dst      count elements of dtype; must not overlap acc
+ * Errors: XRED_INVALID_ARGUMENT (NULL or misaligned pointer, overflow),
+ * XRED_UNSUPPORTED (unknown dtype), XRED_ALIAS, XRED_HIP_ERROR.
  */
 XRED_API xred_status xred_acc_cast(const void *acc, void *dst, size_t count, xred_dtype dtype,
                                    void *hip_stream);
@@ -226,12 +231,20 @@ XRED_API xred_status xred_batched_reduce(const xred_item *items, int nitems, xre
  *   ready      NULL: every chunk is ready at launch.  Otherwise nchunks
  *              uint32 words the GPU can read coherently (hipHostMalloc'd or
  *              device memory); chunk s is read only once
- *              (int32_t)(ready[s] - epoch) >= 0, observed with a system-scope
- *              acquire, so data written before the flag is seen.
+ *              (int32_t)(ready[s] - epoch) >= 0 has been observed, and then
+ *              with system-coherent loads, so data written before the flag
+ *              is seen.  One wave of the launch polls the flags and relays
+ *              their progress to the other workgroups through a word in
+ *              device memory the library binds to the calling stream (up to
+ *              64 streams per device, until xred_release); under graph
+ *              capture, on hipStreamPerThread or past 64 streams, every
+ *              workgroup polls the flags itself, which costs more with host
+ *              flags.
  *   timeout_us bound on each wait (0: one second; capped at 60 s).  A
- *              workgroup whose wait times out writes 1 to *status (if status
- *              is not NULL) and stops; dst is then unspecified.  The caller
- *              zeroes *status before the call if it wants to check it.
+ *              workgroup whose wait makes no progress for that long writes 1
+ *              to *status (if status is not NULL) and stops; dst is then
+ *              unspecified.  The caller zeroes *status before the call if it
+ *              wants to check it.
  * Errors: as xred_allreduce_local; XRED_UNSUPPORTED for misaligned buffers or
  * counts beyond the capacity.
  */
@@ -329,8 +342,9 @@ XRED_API const char *xred_last_error(void);
 /* Library version: major*10000 + minor*100 + patch. */
 XRED_API int xred_version(void);
 
-/* Frees the library's host-mode batch staging buffers on every device after
- * synchronising the device work that uses them.  Optional; later calls
+/* Frees the library's host-mode batch staging buffers and the ring's relay
+ * words on every device after synchronising the device work that uses them,
+ * and unbinds the relay words from their streams.  Optional; later calls
  * re-create what they need. */
 XRED_API void xred_release(void);
 

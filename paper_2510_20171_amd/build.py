@@ -9,6 +9,11 @@ into paper_2510_20171_amd/libxred.so.  Flags:
   -fno-gpu-flush-denormals-to-zero   binary32 subnormals are kept
   -packed-fp32-ops (off)     no v_pk_{add,mul,fma}_f32 generated
   -fvisibility=hidden        only the xred_* C ABI is exported
+  -mllvm -amdgpu-atomic-optimizer-strategy=None
+                             single-lane atomics stay single-lane: the
+                             optimizer turns them into wave-wide sequences
+                             that wait for the atomic's result at once
+                             (the batched queue claims tiles ahead)
 """
 from __future__ import annotations
 
@@ -28,6 +33,7 @@ HIPFLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-fvisibility=hidden",
     "-ffp-contract=off", "-fno-gpu-flush-denormals-to-zero",
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    "-mllvm", "-amdgpu-atomic-optimizer-strategy=None",
     "-Wall", "-Wno-unused-function",
 ]
 

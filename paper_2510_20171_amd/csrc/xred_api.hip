@@ -88,6 +88,7 @@ bool bad_overlap(const void *a, size_t na, const void *b, size_t nb, bool exact_
 bool mul_overflows(size_t a, size_t b) { return b != 0 && a > SIZE_MAX / b; }
 
 int cached_cus[kMaxDevices];
+int cached_lds[kMaxDevices];
 int cached_ticks[kMaxDevices];
 
 long env_long(const char *name, long dflt)
@@ -354,6 +355,93 @@ xred_status batched_host(const xred_item *items, int nitems, xred_dtype dtype, x
 
 }  // namespace
 
+// ------------------------------------------------------------ stream slots --
+namespace {
+struct SlotPool {
+    std::mutex mu;
+    uint32_t *words = nullptr;                  // kStreamSlots x 64 bytes
+    hipStream_t stream[kStreamSlots] = {};
+    uint64_t launches[kStreamSlots] = {};
+    int bound = 0;
+    bool unavailable = false;                   // allocation failed on this device
+};
+SlotPool g_slots[kMaxDevices][kSlotUsers];
+}  // namespace
+
+bool StreamSlot::acquire(StreamSlotUser user, hipStream_t stream)
+{
+    hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+    int dev = 0;
+    if (stream == hipStreamPerThread || hipStreamIsCapturing(stream, &cs) != hipSuccess ||
+        cs != hipStreamCaptureStatusNone || hipGetDevice(&dev) != hipSuccess || dev < 0 ||
+        dev >= kMaxDevices)
+        return false;
+    SlotPool &p = g_slots[dev][user];
+    p.mu.lock();
+    int i = 0;
+    while (i < p.bound && p.stream[i] != stream) ++i;
+    if (i == p.bound) {
+        bool ok = i < kStreamSlots && !p.unavailable;
+        if (ok && !p.words) {
+            // zeroed on the stream that first needs a slot, and waited for, so
+            // the launches of every stream find their slot zeroed
+            void *w = nullptr;
+            ok = hipMalloc(&w, (size_t)kStreamSlots * 64) == hipSuccess;
+            if (ok && (hipMemsetAsync(w, 0, (size_t)kStreamSlots * 64, stream) != hipSuccess ||
+                       hipStreamSynchronize(stream) != hipSuccess)) {
+                (void)hipFree(w);
+                ok = false;
+            }
+            if (ok) p.words = (uint32_t *)w;
+            else p.unavailable = true;
+        }
+        if (!ok) {
+            p.mu.unlock();
+            return false;
+        }
+        p.stream[i] = stream;
+        ++p.bound;
+    }
+    pool_ = &p;
+    index_ = i;
+    words = p.words + 16 * i;
+    launches = p.launches[i];
+    return true;
+}
+
+void StreamSlot::commit()
+{
+    if (pool_) ((SlotPool *)pool_)->launches[index_] = ++launches;
+}
+
+StreamSlot::~StreamSlot()
+{
+    if (pool_) ((SlotPool *)pool_)->mu.unlock();
+}
+
+void release_stream_slots()
+{
+    int cur = 0;
+    const bool have_dev = hipGetDevice(&cur) == hipSuccess;
+    for (int d = 0; d < kMaxDevices; ++d) {
+        for (int u = 0; u < kSlotUsers; ++u) {
+            SlotPool &p = g_slots[d][u];
+            std::lock_guard<std::mutex> lock(p.mu);
+            if (!p.words) continue;
+            (void)hipSetDevice(d);
+            (void)hipDeviceSynchronize();
+            (void)hipFree(p.words);
+            p.words = nullptr;
+            for (int i = 0; i < kStreamSlots; ++i) {
+                p.stream[i] = nullptr;
+                p.launches[i] = 0;
+            }
+            p.bound = 0;
+        }
+    }
+    if (have_dev) (void)hipSetDevice(cur);
+}
+
 // ------------------------------------------------------- internal helpers --
 int device_cus()
 {
@@ -369,6 +457,28 @@ int device_cus()
     return c;
 }
 
+int lds_per_cu()
+{
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return 160 * 1024;
+    int v = __atomic_load_n(&cached_lds[dev], __ATOMIC_RELAXED);
+    if (v <= 0) {
+        if (hipDeviceGetAttribute(&v, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor, dev) !=
+                hipSuccess ||
+            v <= 0)
+            v = 160 * 1024;
+        __atomic_store_n(&cached_lds[dev], v, __ATOMIC_RELAXED);
+    }
+    return v;
+}
+
+int current_device_index()
+{
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevicesCached) return 0;
+    return dev;
+}
+
 // Workgroup budget: 0 = none.  Set by xred_set_max_workgroups (or the
 // XRED_MAX_WORKGROUPS environment variable at load); read on every launch.
 std::atomic<unsigned> g_max_workgroups{(unsigned)env_long("XRED_MAX_WORKGROUPS", 0)};
@@ -376,9 +486,11 @@ std::atomic<unsigned> g_max_workgroups{(unsigned)env_long("XRED_MAX_WORKGROUPS",
 // Device-descriptor batches: items per run and workgroups per CU of the
 // grouped kernel (measured on the 4096-item log-uniform batch: 32 / 64 / 96 /
 // 128 items per run 5.44-5.50 / 5.69-5.70 / 5.49-5.51 / 5.36-5.38 TB/s; 64
-// also best on equal items).
+// also best on equal items), and workgroups per CU of the queue kernel (one:
+// a second widens the window of tiles being read, 1265 against 1301 us).
 constexpr int kGroupedRunItems = 64;
 constexpr int kGroupedWgsPerCu = 2;
+constexpr int kQueueWgsPerCu = 1;
 
 unsigned grid_for(uint64_t tiles)
 {
@@ -394,15 +506,35 @@ unsigned batched_device_grid()
     return grid_for((uint64_t)device_cus() * (uint64_t)per_cu);
 }
 
-// Device-resident descriptors, more than one run of items: runs of
+// Device-resident descriptors, more than one run of items.  Batches of one
+// run keep the round-robin kernel: within a run the split is fixed, and the
+// round-robin kernel's larger tiles stream large items faster (64 items of
+// 8 MiB per source: 5.0 against 4.8 TB/s).  Grouped kernel: runs of
 // kGroupedRunItems consecutive items, each dealt to the workgroups that fit on
 // the chip at once; under a CU budget, fewer workgroups per run and fewer runs
-// at a time.  Batches of one run keep the round-robin kernel: within a run the
-// split is fixed, and the round-robin kernel's larger tiles stream large
-// items faster (64 items of 8 MiB per source: 5.0 against 4.8 TB/s).
+// at a time.
 hipError_t batched_device(const xred_item *items, int nitems, xred_dtype dtype, xred_op op,
                           hipStream_t stream)
 {
+    // The queue kernel, with the two tile counters of the stream's slot: the
+    // launch takes tiles from counter (launches % 2), zeroed by the launch
+    // before it on the stream (or when the slot was created), and zeroes the
+    // other one for the launch after it.
+    if (nitems <= batched_queue_max_items()) {
+        StreamSlot slot;
+        if (slot.acquire(kSlotQueue, stream)) {
+            uint64_t *c = (uint64_t *)slot.words;
+            const int par = (int)(slot.launches & 1);
+            const unsigned grid = grid_for((uint64_t)device_cus() * kQueueWgsPerCu);
+            const hipError_t e = launch_batched_queue(dtype, op, items, nitems, c + par,
+                                                      c + (par ^ 1), nullptr, grid,
+                                                      kQueueWgsPerCu, stream);
+            if (e == hipSuccess) slot.commit();
+            return e;
+        }
+    }
+    // Under graph capture (a replay would repeat the captured counter), past
+    // the queue's item limit, or without a slot: the stateless grouped kernel.
     const uint64_t per_run =
         (uint64_t)std::min(kGroupedRunItems, batched_grouped_max_items());   // LDS prefix size
     const uint64_t ngroups = ((uint64_t)nitems + per_run - 1) / per_run;
@@ -707,6 +839,7 @@ XRED_API int xred_version(void) { return 20000; }
 
 XRED_API void xred_release(void)
 {
+    release_stream_slots();
     int cur = 0;
     const bool have_dev = hipGetDevice(&cur) == hipSuccess;
     for (int d = 0; d < kMaxDevices; ++d) {

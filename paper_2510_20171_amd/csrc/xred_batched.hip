@@ -74,6 +74,25 @@ hipError_t launch_batched_grouped(xred_dtype dtype, xred_op op, const xred_item 
     }
 }
 
+int batched_queue_max_items() { return kQMaxItems; }
+
+hipError_t launch_batched_queue(xred_dtype dtype, xred_op op, const xred_item *d_items,
+                                int nitems, uint64_t *next, uint64_t *clear, uint64_t *finished,
+                                unsigned grid, int wgs_per_cu, hipStream_t stream)
+{
+    switch (group_of(dtype)) {
+    case TypeGroup::kFloat:
+        return launch_batched_queue_float(dtype, op, d_items, nitems, next, clear, finished, grid,
+                                          wgs_per_cu, stream);
+    case TypeGroup::kFp8:
+        return launch_batched_queue_fp8(dtype, op, d_items, nitems, next, clear, finished, grid,
+                                        wgs_per_cu, stream);
+    default:
+        return launch_batched_queue_int(dtype, op, d_items, nitems, next, clear, finished, grid,
+                                        wgs_per_cu, stream);
+    }
+}
+
 hipError_t launch_batched_rr(xred_dtype dtype, xred_op op, const xred_item *d_items, int nitems,
                              const uint32_t *d_tile_start, hipStream_t stream)
 {

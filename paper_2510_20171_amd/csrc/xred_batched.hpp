@@ -95,10 +95,36 @@ __device__ uint64_t block_inclusive_scan(uint64_t v, uint64_t *s)
     return s[threadIdx.x];
 }
 
-// Tile lt of one item.
-template <class T, class Op>
+// Exclusive prefix sum over the workgroup (kB threads); *total gets the sum.
+__device__ __forceinline__ uint64_t block_exclusive_scan(uint64_t v, uint64_t *s_wave,
+                                                         uint64_t *total)
+{
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    uint64_t incl = v;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+        const uint64_t t = __shfl_up(incl, (unsigned)off, 64);
+        if (lane >= off) incl += t;
+    }
+    if (lane == 63) s_wave[wave] = incl;
+    __syncthreads();
+    uint64_t before = 0, sum = 0;
+#pragma unroll
+    for (int w = 0; w < kB / 64; ++w) {
+        const uint64_t x = s_wave[w];
+        before += w < wave ? x : 0;
+        sum += x;
+    }
+    *total = sum;
+    return before + incl - v;
+}
+
+// Tile lt (of SUB sub-tiles of kB*kU vectors) of one item.
+template <class T, class Op, int SUB = kSub>
 __device__ void batched_tile(const xred_item &it, uint64_t lt)
 {
+    constexpr uint32_t kTileBytes = (uint32_t)kB * kU * SUB * 16u;
+    constexpr uint64_t kTileElems = (uint64_t)kB * kU * SUB * T::kVec;
     const char *const *sp = (const char *const *)it.srcs;
     const int nsrc = (int)it.nsrc;
     uintptr_t bits = (uintptr_t)it.dst;
@@ -115,7 +141,7 @@ __device__ void batched_tile(const xred_item &it, uint64_t lt)
     if ((bits & 15u) == 0) {
         const size_t nvec = count / T::kVec;
         const size_t vbytes = nvec * 16;
-        for (int h = 0; h < kSub; ++h) {
+        for (int h = 0; h < SUB; ++h) {
             const size_t off = lt * kTileBytes + (size_t)h * kSubBytes;
             if (off >= vbytes) break;
             const Tile tl{off, tile_nrec(vbytes, off, kSubBytes)};
@@ -135,13 +161,13 @@ __device__ void batched_tile(const xred_item &it, uint64_t lt)
             }
         }
         // the item's last tile also takes the elements after its last full vector
-        if ((lt + 1) * tile_elems<T>() >= count) {
+        if ((lt + 1) * kTileElems >= count) {
             const uint32_t tail = (uint32_t)(count % T::kVec);
             if (threadIdx.x < tail) reduce_elem<T, Op>(src, nsrc, dst, nvec * T::kVec + threadIdx.x);
         }
     } else {
-        const uint64_t e0 = lt * tile_elems<T>();
-        const uint64_t e1 = count < e0 + tile_elems<T>() ? count : e0 + tile_elems<T>();
+        const uint64_t e0 = lt * kTileElems;
+        const uint64_t e1 = count < e0 + kTileElems ? count : e0 + kTileElems;
         for (uint64_t i = e0 + threadIdx.x; i < e1; i += kB) reduce_elem<T, Op>(src, nsrc, dst, i);
     }
 }
@@ -321,6 +347,197 @@ __global__ __launch_bounds__(kB) void batched_rr_kernel(const xred_item *items, 
     }
 }
 
+// ------------------------------------------------------------ queue variant --
+// Device descriptors (the host never sees the sizes): a persistent grid takes
+// the batch's tiles in order from a counter in device memory, one tile per
+// claim, so the tiles in flight stay one compact window over the batch, as
+// when the hardware dispatches one workgroup per tile of a host-built table,
+// and no workgroup keeps a fixed share of the batch.  Each workgroup first
+// scans the tile counts of all items into an LDS tile-start prefix (its first
+// claim in flight meanwhile).  Per tile it finds the tile's item (a 64-ary
+// search of the prefix, in every wave), fetches the descriptor and source
+// pointers, claims the next tile, and reduces this one; the claim's answer is
+// handed to all waves through LDS at the tile's end.
+//
+// What was measured on the 4096-item log-uniform batch (MI355X, same box):
+// one workgroup of 512 threads per CU and tiles of two 512-vector sub-tiles
+// (16 KiB per source) 1265 us; two workgroups per CU 1301-1304 us; 8 KiB
+// tiles 1533-1610 us; 32 KiB tiles 1294 us; claiming two tiles ahead with
+// the next descriptor prefetched 1445 us, and double-buffered loads 1262 us
+// (every claim ahead widens the window of tiles being read, which costs
+// more than the latency it hides); eight interleaved counters 1339 us.
+//
+// The counter: *next is zero when the launch starts.  clear (if set) is
+// another counter the launch zeroes for the next launch on the stream;
+// finished (if set) counts workgroups out, and the last one returns *next and
+// *finished to zero, so the counters are zero again when the launch ends.
+struct QueueCtl {
+    uint64_t *next;
+    uint64_t *clear;
+    uint64_t *finished;
+};
+constexpr int kQMaxItems = 16384;   // items whose 32-bit tile-start prefix fits in LDS
+constexpr int kQSub = 2;            // 512-vector sub-tiles per claimed tile
+
+// The item k < n holding tile g: the last k with pre[k] <= g (pre[0] = 0 <= g,
+// pre non-decreasing).  Each level reads one prefix entry per lane and keeps
+// the run of lanes at or below g: 64^levels entries in `levels` LDS reads.
+__device__ __forceinline__ int find_item(const uint32_t *pre, int n, uint32_t g)
+{
+    const int lane = (int)(threadIdx.x & 63);
+    int step = 1;
+    while (step * 64 < n) step *= 64;
+    int lo = 0;
+    for (;;) {
+        const int i = lo + lane * step;
+        const bool ok = i < n && pre[i] <= g;
+        lo += (__popcll(__ballot(ok)) - 1) * step;
+        if (step == 1) break;
+        step /= 64;
+    }
+    return __builtin_amdgcn_readfirstlane(lo);
+}
+
+// A workgroup barrier that orders LDS only: __syncthreads() also waits for
+// every outstanding global store and atomic of the wave (its release fence
+// covers global memory), which would drain each tile's stores before the
+// next tile's loads could be issued.
+__device__ __forceinline__ void lds_barrier()
+{
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
+template <class T, class Op, int SUB>
+__global__ __launch_bounds__(kB) void batched_queue_kernel(const xred_item *items, int nitems,
+                                                           QueueCtl q)
+{
+    constexpr uint32_t kTileBytes = (uint32_t)kB * SUB * 16u;
+    constexpr uint64_t kTileElems = (uint64_t)kB * SUB * T::kVec;
+    auto tiles_of = [](const xred_item &it) -> uint64_t {
+        return item_runnable(it) ? (it.count + kTileElems - 1) / kTileElems : 0;
+    };
+    auto claim = [&q]() -> uint64_t {
+        return __hip_atomic_fetch_add(q.next, (uint64_t)1, __ATOMIC_RELAXED,
+                                      __HIP_MEMORY_SCOPE_AGENT);
+    };
+    extern __shared__ uint32_t s_pre[];   // nitems + 1 tile starts, in the occupancy reservation
+    __shared__ uint64_t s_wave[kB / 64];
+    // The claim made during tile b is written to s_claim[b % 2] at the
+    // tile's end and read after its barrier; the slot's previous claim was
+    // read before the barrier that precedes the write.
+    __shared__ uint64_t s_claim[2];
+    if (q.clear != nullptr && blockIdx.x == 0 && threadIdx.x == 0)
+        __hip_atomic_store(q.clear, (uint64_t)0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    uint64_t c0 = 0;
+    if (threadIdx.x == 0) c0 = claim();   // in flight while the workgroup scans
+    // tile counts of this thread's consecutive items (four descriptor loads
+    // in flight at a time), kept in the prefix's place; then the
+    // workgroup's exclusive scan turns them into tile starts
+    const int per = (nitems + kB - 1) / kB;
+    const int i0 = min(nitems, (int)threadIdx.x * per), i1 = min(nitems, i0 + per);
+    uint64_t mine = 0;
+    for (int j = i0; j < i1; j += 4) {
+        xred_item it[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+            if (j + u < i1) it[u] = items[j + u];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+            if (j + u < i1) {
+                const uint64_t t = tiles_of(it[u]);
+                mine += t;
+                s_pre[j + u] = t < 0xFFFFFFFFull ? (uint32_t)t : 0xFFFFFFFFu;
+            }
+        }
+    }
+    uint64_t total = 0;
+    uint64_t run = block_exclusive_scan(mine, s_wave, &total);
+    for (int i = i0; i < i1; ++i) {
+        const uint32_t t = s_pre[i];
+        s_pre[i] = (uint32_t)run;
+        run += t;
+    }
+    total = uniform64(total);
+    if (total > 0xFFFFFFFFull) total = 0;   // more tiles than the prefix indexes: run nothing
+    if (threadIdx.x == 0) {
+        s_pre[nitems] = (uint32_t)total;
+        s_claim[1] = c0;
+    }
+    __syncthreads();
+    uint64_t g = uniform64(s_claim[1]);
+    for (int b = 0; g < total; ++b) {
+        TileDesc cur;
+        {
+            const int k = find_item(s_pre, nitems, (uint32_t)g);
+            fetch_desc(cur, items, (uint32_t)k, uniform64(g - s_pre[k]));
+        }
+        uint64_t c = 0;
+        if (threadIdx.x == 0) c = claim();   // answered while this tile streams
+        // straight-line tile: sources beyond nsrc, and tiles off the fast
+        // path, get a zero-length buffer range
+        const size_t nvec = cur.count / T::kVec;
+        const size_t vbytes = nvec * 16, toff = cur.lt * kTileBytes;
+        const uint32_t nrec = cur.fast && toff < vbytes ? tile_nrec(vbytes, toff, kTileBytes) : 0u;
+        u32x4 in[8][SUB];
+#pragma unroll
+        for (int p = 0; p < 8; ++p) {
+            const bool on = p < cur.nsrc;
+            const rsrc_t r = make_rsrc((on ? cur.p[p] : cur.dst) + toff, on ? nrec : 0u);
+#pragma unroll
+            for (int h = 0; h < SUB; ++h)
+                in[p][h] = bload<kLoadStream>(r, (uint32_t)(h * kB + threadIdx.x) * 16u);
+        }
+        const rsrc_t w = make_rsrc(cur.dst + toff, nrec);
+#pragma unroll
+        for (int h = 0; h < SUB; ++h) {
+            typename T::Acc acc[T::kVec];
+            up_vec<T>(in[0][h], acc);
+#pragma unroll
+            for (int p = 1; p < 8; ++p) {
+                const bool on = p < cur.nsrc;
+                typename T::Acc x[T::kVec];
+                up_vec<T>(in[p][h], x);
+#pragma unroll
+                for (int e = 0; e < T::kVec; ++e) {
+                    const typename T::Acc cmb = combine<T, Op>(acc[e], x[e]);
+                    acc[e] = on ? cmb : acc[e];
+                }
+            }
+            if constexpr (__is_same(Op, OpAvg)) {
+#pragma unroll
+                for (int e = 0; e < T::kVec; ++e) acc[e] = avg_scale<T, Op>(acc[e], cur.nsrc);
+            }
+            bstore<kStoreOut>(down_vec<T, Op>(acc), w, (uint32_t)(h * kB + threadIdx.x) * 16u);
+        }
+        if (cur.fast) {
+            if ((cur.lt + 1) * kTileElems >= cur.count) {
+                const uint32_t tail = (uint32_t)(cur.count % T::kVec);
+                if (threadIdx.x < tail)
+                    reduce_elem<T, Op>(GlobalSrc{cur.srcs}, cur.nsrc, cur.dst,
+                                       nvec * T::kVec + threadIdx.x);
+            }
+        } else {
+            batched_tile<T, Op, SUB>(load_item(items, cur.k), cur.lt);
+        }
+        if (threadIdx.x == 0) s_claim[b & 1] = c;
+        lds_barrier();   // the waves start every tile together
+        g = uniform64(s_claim[b & 1]);
+    }
+    // every claim of this workgroup has been answered (each was read back
+    // above), so the last workgroup's reset is the counter's last write
+    if (q.finished != nullptr && threadIdx.x == 0) {
+        const uint64_t n = __hip_atomic_fetch_add(q.finished, (uint64_t)1, __ATOMIC_RELAXED,
+                                                  __HIP_MEMORY_SCOPE_AGENT);
+        if (n + 1 == gridDim.x) {
+            __hip_atomic_store(q.next, (uint64_t)0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            __hip_atomic_store(q.finished, (uint64_t)0, __ATOMIC_RELAXED,
+                               __HIP_MEMORY_SCOPE_AGENT);
+        }
+    }
+}
+
 // ------------------------------------------------------- tile-table variant --
 // Host descriptors: the host lists the item of every tile, and stages each
 // item with the index of its first tile in the descriptor's reserved field;
@@ -459,15 +676,7 @@ template <class T, class Op>
 hipError_t go_table(const xred_item *d_items, const uint32_t *d_table, bool narrow,
                     uint64_t ntiles, hipStream_t s)
 {
-    static const size_t lds = [] {
-        int dev = 0, v = 0;
-        if (hipGetDevice(&dev) != hipSuccess ||
-            hipDeviceGetAttribute(&v, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor, dev) !=
-                hipSuccess ||
-            v <= 0)
-            v = 160 * 1024;
-        return (size_t)(v / kTableWgsPerCu) / 512 * 512 - 512;
-    }();
+    const size_t lds = (size_t)(lds_per_cu() / kTableWgsPerCu) / 512 * 512 - 512;
     if (narrow)
         return launch_kernel(batched_table_kernel<T, Op, true>, dim3(grid_for(ntiles)), dim3(kTB),
                              lds, s, d_items, d_table, ntiles);
@@ -515,30 +724,6 @@ __device__ __forceinline__ uint64_t table_item_tiles(const xred_item &it)
 {
     if (!item_runnable(it)) return 0;
     return (it.count + table_tile_elems<T>() - 1) / table_tile_elems<T>();
-}
-
-// Exclusive prefix sum over the workgroup (kTB threads); *total gets the sum.
-__device__ __forceinline__ uint64_t block_exclusive_scan(uint64_t v, uint64_t *s_wave,
-                                                         uint64_t *total)
-{
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    uint64_t incl = v;
-#pragma unroll
-    for (int off = 1; off < 64; off <<= 1) {
-        const uint64_t t = __shfl_up(incl, (unsigned)off, 64);
-        if (lane >= off) incl += t;
-    }
-    if (lane == 63) s_wave[wave] = incl;
-    __syncthreads();
-    uint64_t before = 0, sum = 0;
-#pragma unroll
-    for (int w = 0; w < kTB / 64; ++w) {
-        const uint64_t x = s_wave[w];
-        before += w < wave ? x : 0;
-        sum += x;
-    }
-    *total = sum;
-    return before + incl - v;
 }
 
 template <class T, class Op>
@@ -604,13 +789,7 @@ template <class T, class Op>
 hipError_t go_grouped(const xred_item *d_items, int nitems, uint32_t ngroups, uint32_t m,
                       unsigned grid, int wgs_per_cu, hipStream_t s)
 {
-    int dev = 0, v = 0;
-    if (hipGetDevice(&dev) != hipSuccess ||
-        hipDeviceGetAttribute(&v, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor, dev) !=
-            hipSuccess ||
-        v <= 0)
-        v = 160 * 1024;
-    size_t lds = (size_t)(v / wgs_per_cu) / 512 * 512 - 512;
+    size_t lds = (size_t)(lds_per_cu() / wgs_per_cu) / 512 * 512 - 512;
     if (lds < kGrpLdsBytes) lds = kGrpLdsBytes;
     hipLaunchKernelGGL((batched_grouped_kernel<T, Op>), dim3(grid), dim3(kTB), lds, s, d_items,
                        nitems, ngroups, m);
@@ -631,22 +810,66 @@ hipError_t batched_grouped_group(xred_dtype dtype, xred_op op, const xred_item *
     });
 }
 
+template <class T, class Op>
+hipError_t go_queue(const xred_item *d_items, int nitems, QueueCtl q, unsigned grid,
+                    int wgs_per_cu, hipStream_t s)
+{
+    size_t lds = (size_t)(lds_per_cu() / wgs_per_cu) / 512 * 512 - 512;
+    const size_t need = sizeof(uint32_t) * ((size_t)nitems + 1);
+    if (lds < need) lds = need;
+    return launch_kernel(batched_queue_kernel<T, Op, kQSub>, dim3(grid), dim3(kB), lds, s,
+                         d_items, nitems, q);
+}
+
+// Queue launcher for the element types Ts.
+template <class... Ts>
+hipError_t batched_queue_group(xred_dtype dtype, xred_op op, const xred_item *d_items,
+                               int nitems, QueueCtl q, unsigned grid, int wgs_per_cu,
+                               hipStream_t s)
+{
+    return with_dtype_among<Ts...>(dtype, [&](auto t) {
+        using T = decltype(t);
+        return with_op<T, true>(op, [&](auto o) {
+            return go_queue<T, decltype(o)>(d_items, nitems, q, grid, wgs_per_cu, s);
+        });
+    });
+}
+
 constexpr size_t rr_lds_bytes(int nitems)
 {
     return sizeof(uint2) * kListMax + sizeof(uint32_t) * ((size_t)nitems + 1);
+}
+
+// The round-robin kernel's LDS is rounded up to whole kRrLdsStep blocks, so
+// its occupancy is known per block count and cached per device.
+constexpr size_t kRrLdsStep = 4096;
+constexpr int kRrLdsSteps = (int)((rr_lds_bytes(kRrMaxItems) + kRrLdsStep - 1) / kRrLdsStep);
+
+template <class T, class Op, bool PLANNED>
+int rr_per_cu(int steps)
+{
+    static int cache[kMaxDevicesCached][kRrLdsSteps + 1];
+    const int dev = current_device_index();
+    int v = __atomic_load_n(&cache[dev][steps], __ATOMIC_RELAXED);
+    if (v <= 0) {
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(
+                &v, (const void *)batched_rr_kernel<T, Op, PLANNED>, kB,
+                (size_t)steps * kRrLdsStep) != hipSuccess ||
+            v <= 0)
+            v = 1;
+        __atomic_store_n(&cache[dev][steps], v, __ATOMIC_RELAXED);
+    }
+    return v;
 }
 
 template <class T, class Op>
 hipError_t go_rr(bool planned, const xred_item *d_items, int nitems, const uint32_t *d_tile_start,
                  hipStream_t s)
 {
-    const void *fn = planned ? (const void *)batched_rr_kernel<T, Op, true>
-                             : (const void *)batched_rr_kernel<T, Op, false>;
-    const size_t lds = rr_lds_bytes(nitems);
-    int per_cu = 0;
-    hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, fn, kB, lds);
-    if (e != hipSuccess) return e;
-    const unsigned grid = batched_rr_grid(per_cu > 0 ? per_cu : 1);
+    const int steps = (int)((rr_lds_bytes(nitems) + kRrLdsStep - 1) / kRrLdsStep);
+    const size_t lds = (size_t)steps * kRrLdsStep;
+    const int per_cu = planned ? rr_per_cu<T, Op, true>(steps) : rr_per_cu<T, Op, false>(steps);
+    const unsigned grid = batched_rr_grid(per_cu);
     if (planned)
         hipLaunchKernelGGL((batched_rr_kernel<T, Op, true>), dim3(grid), dim3(kB), lds, s,
                            d_items, nitems, d_tile_start);

@@ -31,4 +31,13 @@ hipError_t launch_batched_grouped_float(xred_dtype dtype, xred_op op, const xred
                                           wgs_per_cu, stream);
 }
 
+hipError_t launch_batched_queue_float(xred_dtype dtype, xred_op op, const xred_item *d_items,
+                                  int nitems, uint64_t *next, uint64_t *clear, uint64_t *finished,
+                                  unsigned grid, int wgs_per_cu, hipStream_t stream)
+{
+    return batched_queue_group<TF32, TBF16, TF16>(dtype, op, d_items, nitems,
+                                        QueueCtl{next, clear, finished}, grid, wgs_per_cu,
+                                        stream);
+}
+
 }  // namespace xred

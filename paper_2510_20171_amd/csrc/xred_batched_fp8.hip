@@ -31,4 +31,13 @@ hipError_t launch_batched_grouped_fp8(xred_dtype dtype, xred_op op, const xred_i
                                           wgs_per_cu, stream);
 }
 
+hipError_t launch_batched_queue_fp8(xred_dtype dtype, xred_op op, const xred_item *d_items,
+                                  int nitems, uint64_t *next, uint64_t *clear, uint64_t *finished,
+                                  unsigned grid, int wgs_per_cu, hipStream_t stream)
+{
+    return batched_queue_group<TE4M3, TE5M2>(dtype, op, d_items, nitems,
+                                        QueueCtl{next, clear, finished}, grid, wgs_per_cu,
+                                        stream);
+}
+
 }  // namespace xred

@@ -42,8 +42,14 @@ hipError_t launch_kernel(void (*kernel)(P...), dim3 grid, dim3 block, size_t lds
 // results, only how many workgroups share the work).
 unsigned grid_for(uint64_t tiles);
 
-// Compute units of the current device (cached per device).
+// Compute units and LDS bytes per CU of the current device (cached per device).
 int device_cus();
+int lds_per_cu();
+
+// Index of the current device for per-device caches of kMaxDevicesCached
+// entries (0 if the query fails or the index is out of range).
+constexpr int kMaxDevicesCached = 64;
+int current_device_index();
 
 bool supported(xred_dtype dtype, xred_op op);
 size_t elem_size(xred_dtype dtype);
@@ -128,11 +134,26 @@ hipError_t launch_batched_grouped(xred_dtype dtype, xred_op op, const xred_item 
     hipError_t launch_batched_grouped_##G(xred_dtype dtype, xred_op op,                        \
                                           const xred_item *d_items, int nitems,                \
                                           uint32_t ngroups, uint32_t m, unsigned grid,         \
-                                          int wgs_per_cu, hipStream_t s);
+                                          int wgs_per_cu, hipStream_t s);                      \
+    hipError_t launch_batched_queue_##G(xred_dtype dtype, xred_op op,                          \
+                                        const xred_item *d_items, int nitems, uint64_t *next,  \
+                                        uint64_t *clear, uint64_t *finished, unsigned grid,    \
+                                        int wgs_per_cu, hipStream_t s);
 XRED_BATCHED_GROUP(float)
 XRED_BATCHED_GROUP(fp8)
 XRED_BATCHED_GROUP(int)
 #undef XRED_BATCHED_GROUP
+
+// Device-resident descriptors, queued: a persistent grid takes tiles in
+// order from a counter in device memory (see QueueCtl in xred_batched.hpp:
+// `next` must be zero at launch; the launch zeroes `clear` if set; with
+// `finished` set the launch leaves both counters at zero).  At most
+// batched_queue_max_items() items; wgs_per_cu workgroups share one CU (the
+// kernel's LDS reservation enforces it).
+int batched_queue_max_items();
+hipError_t launch_batched_queue(xred_dtype dtype, xred_op op, const xred_item *d_items,
+                                int nitems, uint64_t *next, uint64_t *clear, uint64_t *finished,
+                                unsigned grid, int wgs_per_cu, hipStream_t stream);
 
 // Workgroups for the round-robin kernel given how many fit on one CU.
 unsigned batched_rr_grid(int fit_per_cu);
@@ -142,6 +163,38 @@ uint64_t ring_max_count(xred_dtype dtype);
 hipError_t launch_ring(xred_dtype dtype, xred_op op, const char *const *chunks, int nchunks,
                        char *dst, size_t count, const uint32_t *ready, uint32_t epoch,
                        uint64_t timeout_ticks, uint32_t *status, hipStream_t stream);
+
+// 64 bytes of device memory bound to a stream, for kernels whose state
+// carries from one launch to the next launch on the same stream (launches on
+// one stream run in order, so they may share it): the ring's relay word and
+// the batched queue's tile counters.  Each user has kStreamSlots slots per
+// device, bound to the first streams that ask, for good (until
+// xred_release), and zeroed when first allocated.  acquire() holds the
+// user's lock until the object is destroyed, so the caller launches and
+// commits under it and the launch count follows the order of the launches.
+constexpr int kStreamSlots = 64;
+enum StreamSlotUser { kSlotRing = 0, kSlotQueue = 1, kSlotUsers = 2 };
+class StreamSlot {
+public:
+    StreamSlot() = default;
+    StreamSlot(const StreamSlot &) = delete;
+    StreamSlot &operator=(const StreamSlot &) = delete;
+    ~StreamSlot();
+    // The slot of `stream` on the current device; false under graph capture
+    // (a replay would repeat the captured launch's state), on
+    // hipStreamPerThread (one handle for a different stream in every thread),
+    // once all slots are bound to other streams, or if allocation failed.
+    bool acquire(StreamSlotUser user, hipStream_t stream);
+    uint32_t *words = nullptr;   // 16 words of device memory
+    uint64_t launches = 0;       // launches committed on the slot before this one
+    void commit();               // the launch was enqueued
+private:
+    void *pool_ = nullptr;
+    int index_ = -1;
+};
+
+// Frees every user's stream slots on every device (xred_release).
+void release_stream_slots();
 
 // A whole AllReduce over nranks simulated ranks on this GPU, one launch per
 // step of the ring or halving-doubling schedule (xred_allreduce_sim).

@@ -4,20 +4,41 @@
 // the network has delivered it, and kernel and host thread hand chunks over
 // through producer/consumer flags in host-pinned memory (the host-kernel
 // coordinated mode of Section 4).  Here one launch folds nchunks chunks, in
-// order, into an accumulator that never leaves the chip: each workgroup owns
-// up to kMaxTilesPerWg tiles whose binary32 / uint32 accumulators live in
-// LDS between steps, so the only HBM traffic is the chunks read once and the
+// order, into an accumulator that never leaves the chip: each tile workgroup
+// owns up to kMaxTilesPerWg tiles whose binary32 / uint32 accumulators live in
+// LDS between rounds, so the only HBM traffic is the chunks read once and the
 // result written once (the per-step launches of xred_reduce_copy_step move
 // the accumulator to memory and back on every step).
 //
 // Chunk s is read only after ready[s] has reached `epoch` (serial-number
-// comparison, so a producer may run ahead).  The first wave of each
-// workgroup polls the next kDepth flags at once, one lane per flag, with
-// relaxed system-scope loads; once chunk `next` is ready, the run of
-// consecutive ready chunks after it is folded in one round, after a single
-// acquire fence (an acquire per poll would invalidate L2 on every poll).
-// Every wait is bounded: after `timeout` device-clock ticks the workgroup
-// records 1 in *status (if given) and stops; dst is then unspecified.
+// comparison, so a producer may run ahead).  Reading host memory is what
+// costs: every wave polling pinned host flags from hundreds of workgroups at
+// once took 8-15 us per poll on MI355X, against about 2 us for one wave.  So a
+// flagged launch has one extra workgroup (blockIdx 0) whose first wave alone
+// polls the flags, 64 at a time (one lane per flag), and publishes the number
+// of consecutive ready chunks in a relay word in device memory; the tile
+// workgroups wait on that word (agent-scope loads, served on chip).  Chunks of
+// a flagged launch are read with system-coherent loads (sc0 sc1): they are
+// issued only after the wave has seen the flag, and are served at the point
+// of coherence rather than from a cache that could hold stale lines -- what
+// an acquire fence's cache invalidation would otherwise provide, without an
+// L2 invalidation per workgroup.
+//
+// The relay word belongs to a slot bound to the caller's stream (see
+// StreamSlot): launches on one stream run in order, so they share it, and each
+// launch's values carry its ticket, so a value an earlier launch left is
+// never taken for this one's.  Nothing has to be reset or tracked on the GPU.
+// Under graph capture (a replay would repeat the captured ticket), on the
+// per-thread default stream, or once every slot is bound, there is no relay:
+// each tile workgroup polls the flags itself (and the grid is capped at
+// kFlagPollers).
+//
+// Every wait is bounded: after `timeout` device-clock ticks without progress
+// the waiting workgroup records 1 in *status (if given) and stops; the poller
+// also marks the relay word as failed, which stops the tile workgroups at
+// once; dst is then unspecified.
+#include <algorithm>
+
 #include "xred_dispatch.hpp"
 #include "xred_internal.hpp"
 #include "xred_kernels.hpp"
@@ -26,9 +47,18 @@ namespace xred {
 namespace {
 
 constexpr int kB = 512;
-constexpr int kDepth = 8;            // chunks in flight per round
-constexpr int kMaxTilesPerWg = 4;    // tiles whose accumulators one workgroup holds
-constexpr uint64_t kFlagPollers = 128;   // workgroups of a launch with ready flags
+constexpr int kGroup = 8;                // chunks loaded together before folding
+constexpr int kMaxTilesPerWg = 4;        // tiles whose accumulators one workgroup holds
+constexpr uint64_t kFlagPollers = 128;   // tile workgroups when each polls the flags
+constexpr int kMaxDevices = 64;
+// Relay value: bits 0-6 chunks known ready (at most 64), bit 7 a failed
+// wait, bits 8-31 the low bits of the launch's ticket.
+constexpr uint32_t kRelayCount = 0x7Fu;
+constexpr uint32_t kRelayFailed = 0x80u;
+// Cache policy of the chunk loads of a flagged launch: system-coherent
+// (sc0 | sc1) and nontemporal.
+constexpr int kLoadCoherent = 1 | 2 | 16;
+
 // LDS bytes of one tile's accumulators for element type T.
 template <class T>
 constexpr size_t lds_tile_bytes() { return (size_t)kB * acc_vecs<T>() * 16; }
@@ -41,105 +71,240 @@ __device__ __forceinline__ u32x4 *acc_slot(u32x4 *s_acc, int j, int h)
     return s_acc + ((size_t)j * acc_vecs<T>() + h) * kB + threadIdx.x;
 }
 
+// One flagged launch's relay.  word == NULL: no relay.
+struct Relay {
+    uint32_t *word;         // the relay value (device memory)
+    uint32_t ticket;        // this launch's number on the slot (from 1)
+};
+
+__device__ __forceinline__ uint32_t relay_tag(const Relay &r) { return r.ticket << 8; }
+
+// Run of consecutive ready chunks from `base` in a ballot (bit q: chunk base+q).
+__device__ __forceinline__ int ready_run(uint64_t got)
+{
+    return ~got == 0 ? 64 : (int)__builtin_ctzll(~got);
+}
+
+__device__ __forceinline__ bool flag_set(const uint32_t *ready, int idx, bool mine, uint32_t epoch)
+{
+    const uint32_t v =
+        __hip_atomic_load(ready + (mine ? idx : 0), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+    return mine && (int32_t)(v - epoch) >= 0;
+}
+
+__device__ __forceinline__ void report_timeout(uint32_t *status)
+{
+    if (status) __hip_atomic_store(status, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+}
+
+// The poller (first wave of workgroup 0): publish the ready prefix of the
+// flags as it grows, until every chunk is published or a wait times out.
+__device__ void poll_and_publish(const uint32_t *ready, uint32_t epoch, int nchunks,
+                                 uint64_t timeout, uint32_t *status, const Relay &r)
+{
+    uint32_t *word = r.word;
+    const uint32_t tag = relay_tag(r);
+    const int lane = (int)threadIdx.x;
+    int published = 0;
+    uint64_t t0 = wall_clock64();
+    while (published < nchunks) {
+        const int idx = published + lane;
+        const uint64_t got = __ballot(flag_set(ready, idx, idx < nchunks, epoch));
+        const int run = ready_run(got);
+        if (run > 0) {
+            published += run;
+            if (lane == 0)
+                __hip_atomic_store(word, tag | (uint32_t)published, __ATOMIC_RELAXED,
+                                   __HIP_MEMORY_SCOPE_AGENT);
+            t0 = wall_clock64();
+            continue;
+        }
+        if (wall_clock64() - t0 > timeout) {
+            if (lane == 0) {
+                report_timeout(status);
+                __hip_atomic_store(word, tag | kRelayFailed | (uint32_t)published,
+                                   __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            }
+            return;
+        }
+        __builtin_amdgcn_s_sleep(2);
+    }
+}
+
+// A tile workgroup's wait on the relay (thread 0): chunks ready beyond
+// `next`, or -1 after a failure or a timeout.  Values without this launch's
+// tag are an earlier launch's.
+__device__ int wait_relay(const Relay &r, int next, uint64_t timeout, uint32_t *status)
+{
+    const uint32_t tag = relay_tag(r);
+    const uint64_t t0 = wall_clock64();
+    for (;;) {
+        const uint32_t v = __hip_atomic_load(r.word, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if ((v & ~(kRelayCount | kRelayFailed)) == tag) {
+            if (v & kRelayFailed) return -1;
+            if ((int)(v & kRelayCount) > next) return (int)(v & kRelayCount);
+        }
+        if (wall_clock64() - t0 > timeout) {
+            report_timeout(status);
+            return -1;
+        }
+        __builtin_amdgcn_s_sleep(1);
+    }
+}
+
+// A tile workgroup polling the flags itself (first wave, all lanes): chunks
+// ready from `next` on, or -1 after a timeout.
+__device__ int poll_own(const uint32_t *ready, uint32_t epoch, int next, int nchunks,
+                        uint64_t timeout, uint32_t *status)
+{
+    const int idx = next + (int)threadIdx.x;
+    const uint64_t t0 = wall_clock64();
+    for (;;) {
+        const uint64_t got = __ballot(flag_set(ready, idx, idx < nchunks, epoch));
+        if (got & 1u) return next + ready_run(got);
+        if (wall_clock64() - t0 > timeout) {
+            if (threadIdx.x == 0) report_timeout(status);
+            return -1;
+        }
+        __builtin_amdgcn_s_sleep(2);
+    }
+}
+
+// Chunks [next, upto) of tile j (byte offset off, nrec bytes exist), in groups
+// of kGroup loaded before folding; the accumulator comes from the first chunk
+// or LDS and goes to dst (last round) or LDS.
+template <class T, class Op, int POL>
+__device__ __forceinline__ void fold_round(const KernargSrc<XRED_MAX_SRC> &chunks, int nchunks,
+                                           char *dst, u32x4 *s_acc, int j, size_t off,
+                                           uint32_t nrec, int next, int upto)
+{
+    constexpr int H = acc_vecs<T>();
+    constexpr int PV = acc_per_vec<T>();
+    typename T::Acc a[T::kVec];
+    if (next > 0) {
+#pragma unroll
+        for (int h = 0; h < H; ++h) unpack_acc<T>(*acc_slot<T>(s_acc, j, h), &a[PV * h]);
+    }
+    for (int g0 = next; g0 < upto; g0 += kGroup) {
+        u32x4 in[kGroup];
+#pragma unroll
+        for (int q = 0; q < kGroup; ++q) {
+            const bool on = g0 + q < upto;
+            in[q] = __builtin_amdgcn_raw_buffer_load_b128(
+                make_rsrc((on ? chunks.p[g0 + q] : dst) + off, on ? nrec : 0u),
+                (uint32_t)threadIdx.x * 16u, 0, POL);
+        }
+        if (g0 == 0) up_vec<T>(in[0], a);
+#pragma unroll
+        for (int q = 0; q < kGroup; ++q) {
+            const bool on = g0 + q < upto && g0 + q > 0;
+            typename T::Acc b[T::kVec];
+            up_vec<T>(in[q], b);
+#pragma unroll
+            for (int e = 0; e < T::kVec; ++e) {
+                const typename T::Acc c = combine<T, Op>(a[e], b[e]);
+                a[e] = on ? c : a[e];
+            }
+        }
+    }
+    if (upto == nchunks) {
+        bstore<kStoreOut>(down_vec<T, Op>(a), make_rsrc(dst + off, nrec),
+                          (uint32_t)threadIdx.x * 16u);
+    } else {
+#pragma unroll
+        for (int h = 0; h < H; ++h) *acc_slot<T>(s_acc, j, h) = pack_acc<T>(&a[PV * h]);
+    }
+}
+
 template <class T, class Op>
 __global__ __launch_bounds__(kB) void ring_kernel(KernargSrc<XRED_MAX_SRC> chunks, int nchunks,
                                                   char *dst, size_t nvec, uint32_t tail,
                                                   int tiles_per_wg, const uint32_t *ready,
                                                   uint32_t epoch, uint64_t timeout,
-                                                  uint32_t *status)
+                                                  uint32_t *status, Relay relay)
 {
     extern __shared__ u32x4 s_acc[];
     __shared__ int s_upto;
     constexpr uint32_t kTileBytes = (uint32_t)kB * 16u;
-    constexpr int H = acc_vecs<T>();
-    constexpr int PV = acc_per_vec<T>();
+    const bool flagged = ready != nullptr;
+    const bool relayed = flagged && relay.word != nullptr;
+    if (relayed && blockIdx.x == 0) {
+        // the poller: one wave; the others end at once
+        if (threadIdx.x < 64) poll_and_publish(ready, epoch, nchunks, timeout, status, relay);
+        return;
+    }
+    const size_t wg = blockIdx.x - (relayed ? 1u : 0u);
+    const size_t nwg = gridDim.x - (relayed ? 1u : 0u);
     const size_t vbytes = nvec * 16;
     const size_t ntiles = (nvec + kB - 1) / kB;
     int next = 0;
     while (next < nchunks) {
-        if (threadIdx.x < 64) {
-            // Wave 0 polls: lane q watches chunk next+q (q < kDepth) with
-            // relaxed system-scope loads (no cache invalidation per poll);
-            // a ballot gives the run of consecutive ready chunks from `next`.
-            const int last = next + kDepth < nchunks ? next + kDepth : nchunks;
-            int upto = last;
-            if (ready != nullptr) {
-                const int idx = next + (int)threadIdx.x;
-                const bool mine = idx < last;
-                const uint64_t t0 = wall_clock64();
-                uint64_t got = 0;
-                for (;;) {
-                    const bool r = mine && (int32_t)(__hip_atomic_load(ready + (mine ? idx : 0),
-                                                                       __ATOMIC_RELAXED,
-                                                                       __HIP_MEMORY_SCOPE_SYSTEM) -
-                                                     epoch) >= 0;
-                    got = __ballot(r);
-                    if (got & 1u) break;
-                    if (wall_clock64() - t0 > timeout) break;
-                    __builtin_amdgcn_s_sleep(2);
-                }
-                if (got & 1u) {
-                    // acquire once for the whole run: data written before the
-                    // flags is visible to the loads that follow
-                    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "");
-                    upto = next + (int)__builtin_ctzll(~got);
-                } else {
-                    if (threadIdx.x == 0 && status)
-                        __hip_atomic_store(status, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
-                    upto = -1;
-                }
+        if (relayed) {
+            if (threadIdx.x == 0) s_upto = wait_relay(relay, next, timeout, status);
+        } else if (flagged) {
+            if (threadIdx.x < 64) {
+                const int upto = poll_own(ready, epoch, next, nchunks, timeout, status);
+                if (threadIdx.x == 0) s_upto = upto;
             }
-            if (threadIdx.x == 0) s_upto = upto;
+        } else if (threadIdx.x == 0) {
+            s_upto = nchunks;
         }
         __syncthreads();
         const int upto = s_upto;
-        if (upto < 0) return;   // timed out: the whole workgroup stops
+        if (upto < 0) break;   // failed or timed out: the whole workgroup stops
         for (int j = 0; j < tiles_per_wg; ++j) {
-            const size_t t = blockIdx.x + (size_t)j * gridDim.x;
+            const size_t t = wg + (size_t)j * nwg;
             if (t >= ntiles) break;
             const size_t off = t * kTileBytes;
             const uint32_t nrec = tile_nrec(vbytes, off, kTileBytes);
-            u32x4 in[kDepth];
-#pragma unroll
-            for (int q = 0; q < kDepth; ++q) {
-                const bool on = next + q < upto;
-                in[q] = bload<kLoadStream>(
-                    make_rsrc((on ? chunks.p[next + q] : dst) + off, on ? nrec : 0u),
-                    (uint32_t)threadIdx.x * 16u);
-            }
-            typename T::Acc a[T::kVec];
-            if (next == 0) {
-                up_vec<T>(in[0], a);
-            } else {
-#pragma unroll
-                for (int h = 0; h < H; ++h) unpack_acc<T>(*acc_slot<T>(s_acc, j, h), &a[PV * h]);
-            }
-#pragma unroll
-            for (int q = 0; q < kDepth; ++q) {
-                const bool on = next + q < upto && !(next == 0 && q == 0);
-                typename T::Acc b[T::kVec];
-                up_vec<T>(in[q], b);
-#pragma unroll
-                for (int e = 0; e < T::kVec; ++e) {
-                    const typename T::Acc c = combine<T, Op>(a[e], b[e]);
-                    a[e] = on ? c : a[e];
-                }
-            }
-            if (upto == nchunks) {
-                bstore<kStoreOut>(down_vec<T, Op>(a), make_rsrc(dst + off, nrec),
-                                  (uint32_t)threadIdx.x * 16u);
-            } else {
-#pragma unroll
-                for (int h = 0; h < H; ++h) *acc_slot<T>(s_acc, j, h) = pack_acc<T>(&a[PV * h]);
-            }
+            if (flagged)
+                fold_round<T, Op, kLoadCoherent>(chunks, nchunks, dst, s_acc, j, off, nrec, next,
+                                                 upto);
+            else
+                fold_round<T, Op, kLoadStream>(chunks, nchunks, dst, s_acc, j, off, nrec, next,
+                                               upto);
         }
         next = upto;
         __syncthreads();   // s_upto is rewritten by the next round
     }
-    // Elements after the last full vector: one workgroup, after all chunks
-    // were seen ready.
-    if (tail != 0 && blockIdx.x == ntiles % gridDim.x && threadIdx.x < tail)
+    // Elements after the last full vector: one workgroup, once every chunk was
+    // seen ready (its plain loads need the acquire the vector loads avoid).
+    if (next == nchunks && tail != 0 && wg == ntiles % nwg && threadIdx.x < tail) {
+        if (flagged) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "");
         reduce_elem<T, Op>(chunks, nchunks, dst, nvec * T::kVec + threadIdx.x);
+    }
+}
+
+// Resident workgroups per CU of ring_kernel<T, Op> with the LDS of
+// kMaxTilesPerWg tiles (cached per device: the host path stays free of
+// runtime queries after the first launch).
+template <class T, class Op>
+int ring_per_cu()
+{
+    static int cache[kMaxDevices];
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) dev = 0;
+    int v = __atomic_load_n(&cache[dev], __ATOMIC_RELAXED);
+    if (v <= 0) {
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&v, (const void *)ring_kernel<T, Op>, kB,
+                                                         lds_tile_bytes<T>() * kMaxTilesPerWg) !=
+                hipSuccess ||
+            v <= 0)
+            v = 1;
+        __atomic_store_n(&cache[dev], v, __ATOMIC_RELAXED);
+    }
+    return v;
+}
+
+// Workgroups that fit on the chip at once for every operator of T.
+template <class T>
+uint64_t ring_fit()
+{
+    int v = ring_per_cu<T, OpSum>();
+    v = std::min(v, ring_per_cu<T, OpProd>());
+    v = std::min(v, ring_per_cu<T, OpMax>());
+    v = std::min(v, ring_per_cu<T, OpMin>());
+    return (uint64_t)device_cus() * (uint64_t)v;
 }
 
 template <class T, class Op>
@@ -152,43 +317,42 @@ hipError_t go(const char *const *chunks, int nchunks, char *dst, size_t count,
     const size_t nvec = count / T::kVec;
     const uint32_t tail = (uint32_t)(count % T::kVec);
     const size_t ntiles = (nvec + kB - 1) / kB;
-    const size_t lds_tile = lds_tile_bytes<T>();
-    int per_cu = 0;
-    hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(
-        &per_cu, (const void *)ring_kernel<T, Op>, kB, lds_tile * kMaxTilesPerWg);
-    if (e != hipSuccess) return e;
-    const uint64_t fit = (uint64_t)device_cus() * (uint64_t)(per_cu > 0 ? per_cu : 1);
-    uint64_t grid = ntiles < fit ? ntiles : fit;
-    // a CU budget shrinks the grid down to what kMaxTilesPerWg tiles per
-    // workgroup allow (fewer workgroups also mean fewer pollers of the flags)
+    // The relay word of the stream (tickets follow the order of the launches:
+    // the slot stays locked until the launch is committed).
+    StreamSlot slot;
+    const bool relayed = ready != nullptr && slot.acquire(kSlotRing, s);
+    // one workgroup per tile while they fit on the chip (a relayed launch
+    // keeps one place for its poller); a CU budget shrinks the grid down to
+    // what kMaxTilesPerWg tiles per workgroup allow
+    const uint64_t fit = std::max<uint64_t>(ring_fit<T>(), 2) - 1;
     const uint64_t least = (ntiles + kMaxTilesPerWg - 1) / kMaxTilesPerWg;
-    grid = grid_for(grid);
-    // With flags every workgroup polls them; host-memory polls from hundreds of
-    // workgroups cost more than the bandwidth the extra workgroups add
-    // (16 x 2^20 bf16 chunks, flags preset: 31.8 us with 256 workgroups, 19.4
-    // us with 128, 5.4 us without flags), so flagged launches use at most
-    // kFlagPollers workgroups.
-    if (ready != nullptr && grid > kFlagPollers) grid = kFlagPollers;
+    uint64_t grid = ntiles < fit ? ntiles : fit;
+    grid = relayed ? grid_for(grid + 1) - 1 : grid_for(grid);   // the budget counts the poller
+    // Without a relay every tile workgroup polls the flags: host-memory polls
+    // from hundreds of workgroups cost more than the bandwidth they add.
+    if (ready != nullptr && !relayed && grid > kFlagPollers) grid = kFlagPollers;
     if (grid < least) grid = least;
     if (grid == 0) grid = 1;
     const int tpw = (int)((ntiles + grid - 1) / grid);
     if (tpw > kMaxTilesPerWg) return hipErrorInvalidValue;   // the caller checks ring_max_count
-    hipLaunchKernelGGL((ring_kernel<T, Op>), dim3((unsigned)grid), dim3(kB),
-                       lds_tile * (tpw > 0 ? tpw : 1), s, ks, nchunks, dst, nvec, tail, tpw,
-                       ready, epoch, timeout, status);
-    return hipGetLastError();
+    // tickets run 1 .. 2^24-1 (the tag's width), so no tag is 0, the value
+    // of a fresh slot
+    const Relay relay = relayed ? Relay{slot.words, (uint32_t)(slot.launches % 0xFFFFFFu) + 1}
+                                : Relay{nullptr, 0};
+    hipLaunchKernelGGL((ring_kernel<T, Op>), dim3((unsigned)(grid + (relayed ? 1 : 0))), dim3(kB),
+                       lds_tile_bytes<T>() * (tpw > 0 ? tpw : 1), s, ks, nchunks, dst, nvec, tail,
+                       tpw, ready, epoch, timeout, status, relay);
+    const hipError_t e = hipGetLastError();
+    if (relayed && e == hipSuccess) slot.commit();
+    return e;
 }
 
 template <class T>
 uint64_t max_count()
 {
-    // the grid never exceeds what fits on the chip; each workgroup holds at
-    // most kMaxTilesPerWg tiles
-    int per_cu = 0;
-    (void)hipOccupancyMaxActiveBlocksPerMultiprocessor(
-        &per_cu, (const void *)ring_kernel<T, OpSum>, kB, lds_tile_bytes<T>() * kMaxTilesPerWg);
-    if (per_cu <= 0) per_cu = 1;
-    return (uint64_t)device_cus() * per_cu * kMaxTilesPerWg * kB * T::kVec;
+    // the tile workgroups never exceed what fits on the chip beside a poller;
+    // each holds at most kMaxTilesPerWg tiles
+    return (std::max<uint64_t>(ring_fit<T>(), 2) - 1) * kMaxTilesPerWg * kB * T::kVec;
 }
 
 }  // namespace

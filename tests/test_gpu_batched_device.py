@@ -1,9 +1,16 @@
-"""Device-resident batch descriptors past one run of items (the grouped kernel).
+"""Device-resident batch descriptors past one run of items (the queue and
+grouped kernels).
 
-A batch of more than 64 items whose descriptors live in device memory is cut
-into runs of consecutive items, each run dealt tile by tile to its own set of
-workgroups that plan their tiles from the descriptors in the kernel.  These
-tests drive that path across its boundaries against the CPU oracle:
+A batch of more than 64 items whose descriptors live in device memory runs,
+when launched eagerly, on the queue kernel: a persistent grid whose
+workgroups scan every item's tile count into an LDS prefix and take tiles in
+order from a counter that the stream's slot keeps in device memory (two
+counters used alternately by successive launches on the stream).  Under
+graph capture, or past the queue's 16384 items, the batch is cut into runs
+of consecutive items, each run dealt tile by tile to its own set of
+workgroups that plan their tiles from the descriptors in the kernel (the
+grouped kernel).  These tests drive both paths across their boundaries
+against the CPU oracle:
 
 - batch sizes on both sides of whole runs (65, 127, 128, 129 items) and many
   runs (700 items), items of 0, 1 and a few elements, items ending just
@@ -12,7 +19,10 @@ tests drive that path across its boundaries against the CPU oracle:
   that must be skipped (dst untouched);
 - workgroup budgets of 1, 3, 100 and 513 (fewer workgroups than one run's
   set, and sets striding over the runs): results bit-identical;
-- graph capture of such a batch, replayed with eager work in between.
+- graph capture of such a batch, replayed with eager work in between;
+- batches enqueued back to back on one stream and alternately on two streams
+  (the counters of each stream's slot handed from launch to launch);
+- 16384 and 16385 items (the last batch the queue takes, the first past it).
 """
 import numpy as np
 import pytest
@@ -160,3 +170,54 @@ def _upload_first_sources(b):
         if srcs[0].size:
             dev0.copy_(gu.to_dev(srcs[0], b.dtype))
         pos += len(srcs) + 1
+
+
+def test_device_batches_back_to_back(xr, orc):
+    """Eight batches of different shapes enqueued without synchronisation,
+    first all on one stream, then alternating over two: each launch must take
+    every tile of its own batch exactly once from its stream's counters."""
+    rng = np.random.default_rng(5400)
+    batches = [Batch(xr, rng, "bf16", int(K), skip_rows=(K % 2 == 0))
+               for K in (70, 300, 65, 129, 500, 66, 200, 90)]
+    exps = [b.expected(orc, "sum") for b in batches]
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    for mode in ("one stream", "two streams"):
+        for b in batches:
+            for o in b.outs:
+                o.zero_()
+        torch.cuda.synchronize()
+        for r in range(3):
+            for i, b in enumerate(batches):
+                st = streams[0] if mode == "one stream" else streams[(i + r) % 2]
+                with torch.cuda.stream(st):
+                    xr.batched_reduce(b.items, "sum", dtype="bf16")
+        torch.cuda.synchronize()
+        for i, (b, e) in enumerate(zip(batches, exps)):
+            b.check(e, "sum", f"{mode}: batch {i}")
+
+
+@pytest.mark.parametrize("K", [16384, 16385])
+def test_device_batch_queue_item_limit(xr, orc, K):
+    """K int32 items of 1..40 elements over two sources, laid end to end, so
+    the concatenated outputs equal one oracle reduction of the concatenated
+    sources: the largest batch the queue kernel plans in LDS, and one more
+    item (the grouped kernel)."""
+    rng = np.random.default_rng(5500 + K)
+    sizes = rng.integers(1, 41, size=K)
+    sizes[-1] = 3 * 512 * 4 + 1             # the last item spans several tiles
+    total = int(sizes.sum())
+    srcs_np = [pins.random_column_values(rng, "i32", total) for _ in range(2)]
+    d = [gu.to_dev(x, "i32") for x in srcs_np]
+    out = torch.zeros(total, dtype=torch.int32, device="cuda")
+    starts = np.concatenate([[0], np.cumsum(sizes)[:-1]]).astype(np.uint64)
+    ptrs = torch.tensor(np.stack([d[0].data_ptr() + 4 * starts, d[1].data_ptr() + 4 * starts],
+                                 axis=1).astype(np.int64).reshape(-1), device="cuda")
+    arr = np.zeros(K, xr.ITEM_DTYPE)
+    arr["srcs"] = ptrs.data_ptr() + 16 * np.arange(K, dtype=np.uint64)
+    arr["dst"] = out.data_ptr() + 4 * starts
+    arr["count"] = sizes
+    arr["nsrc"] = 2
+    items = torch.from_numpy(arr.view(np.uint8).copy()).to("cuda")
+    xr.batched_reduce(items, "sum", dtype="i32")
+    torch.cuda.synchronize()
+    gu.assert_parity(out, orc.allreduce_local(srcs_np, "i32", "sum"), "i32", "sum", f"K={K}")

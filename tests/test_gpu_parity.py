@@ -4,8 +4,8 @@ order is fixed, so float results are deterministic); NaN payloads of float
 sum/prod are not specified and compare by NaN-ness only.
 
 Covered: the six workloads at full size in the launch configuration the
-benchmark times (c1, c2, c3, c5a, c5b fully; c4 on a sample of items plus
-host/device-descriptor agreement on all items), and an edge matrix of sizes
+benchmark times (c1, c2, c3, c4 with host and with device descriptors, c5a,
+c5b: every output element), and an edge matrix of sizes
 (empty, ragged, several tiles), source counts 1..64, every dtype x op with
 special values (+-0, +-inf, subnormals, NaN, overflow), misaligned buffers,
 in-place calls, guard bands around outputs, and every step-wise flag.
@@ -140,7 +140,29 @@ def _c4_device_descriptors(xr, arena_dev, offs, sizes, outs, es):
     return dev_items, ptrs
 
 
+def _assert_items(got_flat, exp_flat, sizes, dtype, op, what):
+    """Every element of every item against the oracle; on a mismatch, name the
+    first item that differs."""
+    ends = np.cumsum(sizes)
+    try:
+        gu.assert_parity(got_flat, exp_flat, dtype, op, what)
+    except AssertionError:
+        g, e = gu.bits(got_flat, dtype), gu.bits(exp_flat, dtype)
+        bad = g != e
+        if dtype in gu.FLOATS and op in ("sum", "prod", "avg"):
+            bad &= ~(gu.nan_mask(g, dtype) & gu.nan_mask(e, dtype))
+        i = int(np.flatnonzero(bad)[0])
+        k = int(np.searchsorted(ends, i, side="right"))
+        raise AssertionError(f"{what}: item {k} (count {int(sizes[k])}) differs first, at "
+                             f"element {i - (int(ends[k - 1]) if k else 0)}") from None
+
+
 def test_c4_batched_full(xr, orc):
+    """The small-message batch (4096 items, P=8 bf16, 8 KiB-1 MiB per source):
+    every output element of every item, with host descriptors and with
+    device-resident descriptors, compared with the oracle's per-item
+    reduction (the oracle splits each item's elements over the host's cores,
+    which does not change any element's fold)."""
     w = wl.WORKLOADS["c4"]
     sizes = wl.batched_sizes(w)
     arena, offs = wl.batched_arena(w, sizes)
@@ -150,25 +172,20 @@ def test_c4_batched_full(xr, orc):
     items = [([arena_dev[o:o + int(n)] for o in offs[k]], outs[k])
              for k, n in enumerate(sizes)]
     xr.batched_reduce(items, w.op, dtype=w.dtype)
-    torch.cuda.synchronize()
-    # sampled items against the oracle, one by one
-    rng = np.random.default_rng(44)
-    sample = sorted(set(rng.choice(len(sizes), 64, replace=False).tolist())
-                    | {0, len(sizes) - 1, int(np.argmax(sizes)), int(np.argmin(sizes))})
-    for k in sample:
-        n = int(sizes[k])
-        srcs = [arena[o:o + n] for o in offs[k]]
-        exp = orc.allreduce_local(srcs, w.dtype, w.op)
-        gu.assert_parity(outs[k], exp, w.dtype, w.op, f"c4 item {k}")
-    # device-resident descriptors give the same bits on every item
     outs2 = [torch.full_like(o, float("nan")) for o in outs]
     dev_items, keep = _c4_device_descriptors(xr, arena_dev, offs, sizes, outs2, es)
     xr.batched_reduce(dev_items, w.op, dtype=w.dtype)
     torch.cuda.synchronize()
-    a = torch.cat(outs).view(torch.int16)
-    b = torch.cat(outs2).view(torch.int16)
-    assert torch.equal(a, b)
-    del keep
+    got_host = torch.cat(outs).cpu()
+    got_dev = torch.cat(outs2).cpu()
+    del outs, outs2, items, keep, dev_items, arena_dev
+    exp = orc.batched_reduce([[arena[o:o + int(n)] for o in offs[k]]
+                              for k, n in enumerate(sizes)],
+                             w.dtype, w.op, nthreads=CORES)
+    exp_flat = np.concatenate(exp)
+    assert exp_flat.size == int(sizes.sum()) == got_host.numel()
+    _assert_items(got_host, exp_flat, sizes, w.dtype, w.op, "c4 host descriptors")
+    _assert_items(got_dev, exp_flat, sizes, w.dtype, w.op, "c4 device descriptors")
 
 
 # ---------------------------------------------------------- edge matrix --
@@ -373,8 +390,13 @@ def test_batched_mixed(xr, orc, dtype):
     dev_items = torch.from_numpy(arr.view(np.uint8).copy()).to("cuda")
     xr.batched_reduce(dev_items, "sum", dtype=dtype)
     torch.cuda.synchronize()
-    for k, (o1, o2) in enumerate(zip(outs, outs2)):
-        assert np.array_equal(gu.bits(o1, dtype), gu.bits(o2, dtype)), k
+    # against the oracle (NaN payloads of float sums are unspecified, and the
+    # two descriptor modes run different kernels)
+    for k, (s, o2) in enumerate(zip(host_srcs, outs2)):
+        if s[0].size == 0:
+            continue
+        gu.assert_parity(o2, orc.allreduce_local(s, dtype, "sum"), dtype, "sum",
+                         f"device item {k}")
     assert torch.all(bad_out == 7)
     del keep
 
@@ -505,20 +527,37 @@ def test_batched_tile_list_entry_width(xr, orc, K):
     gu.assert_parity(out, orc.allreduce_local(srcs_np, "i32", "sum"), "i32", "sum", f"K={K}")
 
 
-@pytest.mark.parametrize("K,nruns,maxn", [(3000, 6, 300), (40, 12, 300)])
-def test_batched_host_batches_back_to_back(xr, orc, K, nruns, maxn):
+def _staged_bytes(sizes, nsrc, tile_elems):
+    """Bytes a host batch stages when it takes the tile-list layout: 32 per
+    item, the item of every tile (2 bytes each up to 65536 items, padded to
+    8 bytes) and 8 per source pointer."""
+    tiles = int(((np.asarray(sizes) + tile_elems - 1) // tile_elems).sum())
+    width = 2 if len(sizes) <= 65536 else 4
+    return 32 * len(sizes) + (width * tiles + 7) // 8 * 8 + 8 * nsrc * len(sizes)
+
+
+@pytest.mark.parametrize("K,nruns,maxn,nsrc", [(3000, 12, 300, 8), (40, 12, 300, 3)])
+def test_batched_host_batches_back_to_back(xr, orc, K, nruns, maxn, nsrc):
     """Host batches enqueued back to back on two alternating caller streams
-    with no synchronisation in between, so the staging slots are reused while
-    earlier batches may still run: 3000 items (staged data past 256 KiB,
-    copied on the library's own stream) and 40 items (read by the kernel from
-    the pinned slot itself).  Every batch must still see its own descriptors."""
+    with no synchronisation in between, so the four staging slots are reused
+    while earlier batches may still run: 3000 items of 8 sources (staged data
+    past 256 KiB, copied on the library's own stream, which the caller's
+    stream then waits for) and 40 items of 3 sources (one round of
+    workgroups and at most 64 KiB: read by the kernel from the pinned slot
+    itself).  Every batch must still see its own descriptors."""
     rng = np.random.default_rng(61 + K)
     streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
     runs = []
     for r in range(nruns):
         sizes = rng.integers(1, maxn, size=K)
+        need = _staged_bytes(sizes, nsrc, 512 * 8)
+        if K == 3000:
+            assert need >= 256 << 10, need          # the side-stream copy
+        else:
+            assert need <= 64 << 10 and K <= 2 * cus, need   # read in place
         total = int(sizes.sum())
-        srcs_np = [pins.random_column_values(rng, "bf16", total) for _ in range(3)]
+        srcs_np = [pins.random_column_values(rng, "bf16", total) for _ in range(nsrc)]
         d = [gu.to_dev(s, "bf16") for s in srcs_np]
         out = torch.zeros(total, dtype=torch.bfloat16, device="cuda")
         items, pos = [], 0

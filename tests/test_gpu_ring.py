@@ -190,3 +190,77 @@ def test_ring_timeout_exits(xr):
     finally:
         flags.free()
         status.free()
+
+
+def test_ring_flagged_launches_reuse_relay_slots(xr, orc):
+    """Flagged launches hand readiness on through a relay word bound to their
+    stream (64 per device; launches on one stream share theirs, each with its
+    own ticket).  Launches enqueued back to back on one stream, alternating
+    over two streams, and one on each of 72 streams (more than there are
+    slots: the rest poll without a relay), each with its own output: every
+    launch must fold all of its chunks, and none may take a relay value an
+    earlier launch left for its own."""
+    rng = np.random.default_rng(8)
+    nchunks, n = 6, 3 * 4096 + 16       # several tiles; whole 16-byte vectors
+    chunks = [pins.random_column_values(rng, "bf16", n) for _ in range(nchunks)]
+    exp = orc.allreduce_local(chunks, "bf16", "sum")
+    L = xr.load()
+    d = [gu.to_dev(c, "bf16") for c in chunks]
+    arr = xr._lib.ptr_array([c.data_ptr() for c in d])
+    flags = PinnedWords(nchunks)
+    status = PinnedWords(1)
+    streams = [torch.cuda.Stream() for _ in range(72)]
+    try:
+        for s in range(nchunks):
+            flags.set(s, 7)
+        outs = [torch.full_like(d[0], float("nan")) for _ in range(232)]
+        torch.cuda.synchronize()
+        for k, o in enumerate(outs):
+            st = streams[0] if k < 80 else streams[k % 2] if k < 160 else streams[k - 160]
+            xr._lib.check(L.xred_ring_reduce(arr, nchunks, ctypes.c_void_p(o.data_ptr()), n,
+                                             xr.DTYPE["bf16"], xr.OP["sum"], flags.dev, 7,
+                                             2_000_000, status.dev,
+                                             ctypes.c_void_p(st.cuda_stream)))
+        torch.cuda.synchronize()
+        assert status.get(0) == 0, "a wait timed out"
+        for k, o in enumerate(outs):
+            gu.assert_parity(o, exp, "bf16", "sum", f"flagged launch {k}")
+    finally:
+        flags.free()
+        status.free()
+
+
+def test_ring_flags_under_graph_capture(xr, orc):
+    """Under capture there is no relay (a replay would repeat the captured
+    relay ticket): each workgroup polls the flags itself.  Replays with the
+    flags set, with eager work in between, give the eager bits each time."""
+    rng = np.random.default_rng(9)
+    nchunks, n = 5, 2 * 4096 * 8
+    chunks = [pins.random_column_values(rng, "f32", n) for _ in range(nchunks)]
+    exp = orc.allreduce_local(chunks, "f32", "sum")
+    L = xr.load()
+    d = [gu.to_dev(c, "f32") for c in chunks]
+    arr = xr._lib.ptr_array([c.data_ptr() for c in d])
+    flags = PinnedWords(nchunks)
+    try:
+        for s in range(nchunks):
+            flags.set(s, 1)
+        out = torch.empty_like(d[0])
+        eager = torch.empty_like(d[0])
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            cs = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+            xr._lib.check(L.xred_ring_reduce(arr, nchunks, ctypes.c_void_p(out.data_ptr()), n,
+                                             xr.DTYPE["f32"], xr.OP["sum"], flags.dev, 1,
+                                             2_000_000, None, cs))
+        for r in range(3):
+            out.zero_()
+            g.replay()
+            torch.cuda.synchronize()
+            gu.assert_parity(out, exp, "f32", "sum", f"replay {r}")
+            _ring(xr, chunks, "f32", "sum", ready=flags, epoch=1, out=eager)
+            torch.cuda.synchronize()
+            gu.assert_parity(eager, exp, "f32", "sum", f"eager after replay {r}")
+        del g
+    finally:
+        flags.free()
