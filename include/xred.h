@@ -218,6 +218,28 @@ XRED_API xred_status xred_batched_reduce(const xred_item *items, int nitems, xre
                                          xred_op op, unsigned flags, void *hip_stream);
 
 /*
+ * For callers that cannot allocate device memory -- code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation: the
+ * device-descriptor form of xred_batched_reduce (flags XRED_ITEMS_ON_DEVICE:
+ * items and every items[k].srcs are device memory, read when the kernel runs;
+ * items that cannot be run safely are skipped; same results) with the tile
+ * counters of its kernel in a fixed 256-byte array of device memory that the
+ * library holds on each GPU it runs on until the process ends.  The call
+ * allocates nothing (no hipMalloc, hipFree or allocating library routine).
+ * The counters are zero when the library is loaded and every launch leaves
+ * them zero, so the call can be captured in a graph and replayed; calls that
+ * overlap on one GPU (other streams, other threads, replays running
+ * concurrently) share the array and race: serialise them.  The first call on
+ * a device looks up the array's device address.
+ *   nitems   0..16384 (XRED_UNSUPPORTED beyond: the kernel plans the whole
+ *            batch in on-chip memory)
+ * Errors: XRED_INVALID_ARGUMENT (nitems < 0, NULL or misaligned items),
+ * XRED_UNSUPPORTED (dtype/op, too many items), XRED_HIP_ERROR.
+ */
+XRED_API xred_status xred_batched_reduce_noalloc(const xred_item *items, int nitems,
+                                                 xred_dtype dtype, xred_op op, void *hip_stream);
+
+/*
  * All steps of a ring's ReduceCopy in one persistent launch: the FTAR
  * pipeline's in-kernel reduce (Section 5) gated by producer/consumer flags
  * in host-pinned or device memory (the host-kernel coordinated mode of

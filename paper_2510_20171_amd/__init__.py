@@ -26,6 +26,7 @@ from ._lib import (ACC_SIZE, ALIAS, DTYPE, ELEM_SIZE, EXPORTS, HIP_ERROR, INVALI
                    SUCCESS, UNSUPPORTED, XredError, XredItem, check, load, ptr_array)
 
 __all__ = ["allreduce_local", "reduce_scatter_local", "reduce_copy_step", "acc_cast",
+           "batched_reduce_noalloc",
            "batched_reduce", "ring_reduce", "ring_max_count", "allreduce_sim", "sim_chunk",
            "set_max_workgroups", "pack_items", "acc_elem_size", "version", "release",
            "XredError", "load", "EXPORTS"]
@@ -184,6 +185,20 @@ def batched_reduce(items, op: str = "sum", *, dtype: str, stream=None, device=No
     dev_t = items[0][1] if items else None
     st = _stream(dev_t, stream) if dev_t is not None else ctypes.c_void_p(0)
     check(L.xred_batched_reduce(arr, len(rows), DTYPE[dtype], OP[op], 0, st))
+
+
+def batched_reduce_noalloc(items, op: str = "sum", *, dtype: str, stream=None) -> None:
+    """Device-descriptor batch with no allocation (xred_batched_reduce_noalloc).
+
+    items: a CUDA uint8/int64 tensor of packed xred_item descriptors in device
+    memory, as for batched_reduce.  Calls that overlap on one GPU race."""
+    L = load()
+    import torch
+    if not isinstance(items, torch.Tensor) or not items.is_cuda:
+        raise XredError(INVALID_ARGUMENT, "device descriptors must be a CUDA tensor")
+    n = items.numel() * items.element_size() // ITEM_DTYPE.itemsize
+    check(L.xred_batched_reduce_noalloc(_ptr(items), n, DTYPE[dtype], OP[op],
+                                        _stream(items, stream)))
 
 
 def ring_reduce(chunks, out, op: str = "sum", *, ready=None, epoch: int = 1,

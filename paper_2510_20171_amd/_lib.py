@@ -40,7 +40,8 @@ class XredItem(ctypes.Structure):
 
 
 EXPORTS = ("xred_allreduce_local", "xred_reduce_scatter_local", "xred_reduce_copy_step",
-           "xred_acc_cast", "xred_batched_reduce", "xred_ring_reduce", "xred_ring_max_count",
+           "xred_acc_cast", "xred_batched_reduce", "xred_batched_reduce_noalloc",
+           "xred_ring_reduce", "xred_ring_max_count",
            "xred_allreduce_sim", "xred_sim_chunk", "xred_set_max_workgroups", "xred_acc_elem_size", "xred_status_string",
            "xred_last_error", "xred_version", "xred_release")
 
@@ -77,6 +78,7 @@ def load(path: Path = LIB_PATH) -> ctypes.CDLL:
     L.xred_reduce_copy_step.argtypes = [vp, vp, vp, sz, i32, i32, u32, vp]
     L.xred_acc_cast.argtypes = [vp, vp, sz, i32, vp]
     L.xred_batched_reduce.argtypes = [vp, i32, i32, i32, u32, vp]
+    L.xred_batched_reduce_noalloc.argtypes = [vp, i32, i32, i32, vp]
     L.xred_ring_reduce.argtypes = [vp, i32, vp, sz, i32, i32, vp, ctypes.c_uint32,
                                    ctypes.c_uint64, vp, vp]
     L.xred_allreduce_sim.argtypes = [vp, vp, i32, sz, i32, i32, i32, vp]
@@ -85,7 +87,8 @@ def load(path: Path = LIB_PATH) -> ctypes.CDLL:
     L.xred_ring_max_count.argtypes = [i32]
     L.xred_ring_max_count.restype = sz
     for f in ("xred_allreduce_local", "xred_reduce_scatter_local", "xred_reduce_copy_step",
-              "xred_acc_cast", "xred_batched_reduce", "xred_ring_reduce", "xred_allreduce_sim"):
+              "xred_acc_cast", "xred_batched_reduce", "xred_batched_reduce_noalloc",
+              "xred_ring_reduce", "xred_allreduce_sim"):
         getattr(L, f).restype = ctypes.c_int
     L.xred_set_max_workgroups.argtypes = [ctypes.c_uint]
     L.xred_set_max_workgroups.restype = ctypes.c_uint

@@ -355,6 +355,39 @@ xred_status batched_host(const xred_item *items, int nitems, xred_dtype dtype, x
 
 }  // namespace
 
+// ------------------------------------------------ allocation-free batches --
+// The queue kernel's tile counters for xred_batched_reduce_noalloc: words 0
+// (next tile) and 1 (workgroups finished) of a fixed array of device memory
+// that each GPU the library runs on holds until the process ends (256 bytes,
+// zero when the module is loaded; every launch leaves it zero again).  In
+// host code the name is only a stand-in for the array: the device address
+// is looked up once per device (scratch_on_device) and only that address is
+// handed to kernels.
+constexpr int kScratchWords = 32;
+static __device__ __align__(256) uint64_t scratch[kScratchWords];
+uint64_t *g_scratch_dev[kMaxDevices];
+
+// The device address of `scratch` on the current device, looked up on the
+// first call there.
+xred_status scratch_on_device(uint64_t **out)
+{
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+    if (dev < 0 || dev >= kMaxDevices) return fail(XRED_UNSUPPORTED, "device %d", dev);
+    uint64_t *p = __atomic_load_n(&g_scratch_dev[dev], __ATOMIC_ACQUIRE);
+    if (p == nullptr) {
+        void *a = nullptr;
+        e = hipGetSymbolAddress(&a, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress(scratch)");
+        if (a == nullptr) return fail(XRED_HIP_ERROR, "hipGetSymbolAddress(scratch) gave NULL");
+        p = (uint64_t *)a;
+        __atomic_store_n(&g_scratch_dev[dev], p, __ATOMIC_RELEASE);
+    }
+    *out = p;
+    return XRED_SUCCESS;
+}
+
 // ------------------------------------------------------------ stream slots --
 namespace {
 struct SlotPool {
@@ -719,6 +752,30 @@ XRED_API xred_status xred_batched_reduce(const xred_item *items, int nitems, xre
         return e == hipSuccess ? XRED_SUCCESS : hip_fail(e, "batched launch");
     }
     return batched_host(items, nitems, dtype, op, (hipStream_t)hip_stream);
+}
+
+XRED_API xred_status xred_batched_reduce_noalloc(const xred_item *items, int nitems,
+                                                 xred_dtype dtype, xred_op op, void *hip_stream)
+{
+    if (nitems < 0) return fail(XRED_INVALID_ARGUMENT, "nitems = %d", nitems);
+    xred_status st = check_types(dtype, op);
+    if (st != XRED_SUCCESS) return st;
+    if (nitems == 0) return XRED_SUCCESS;
+    if (items == nullptr) return fail(XRED_INVALID_ARGUMENT, "items is NULL");
+    if ((uintptr_t)items % alignof(xred_item))
+        return fail(XRED_INVALID_ARGUMENT, "items is not %zu-byte aligned", alignof(xred_item));
+    if (nitems > batched_queue_max_items())
+        return fail(XRED_UNSUPPORTED,
+                    "nitems = %d: xred_batched_reduce_noalloc plans at most %d items on chip",
+                    nitems, batched_queue_max_items());
+    uint64_t *sc = nullptr;
+    if ((st = scratch_on_device(&sc)) != XRED_SUCCESS) return st;
+    // counters sc[0] (next tile) and sc[1] (workgroups finished): zero at
+    // launch, returned to zero by the launch's last workgroup
+    const unsigned grid = grid_for((uint64_t)device_cus() * kQueueWgsPerCu);
+    const hipError_t e = launch_batched_queue(dtype, op, items, nitems, sc, nullptr, sc + 1, grid,
+                                              kQueueWgsPerCu, (hipStream_t)hip_stream);
+    return e == hipSuccess ? XRED_SUCCESS : hip_fail(e, "batched launch");
 }
 
 XRED_API xred_status xred_ring_reduce(const void *const *chunks, int nchunks, void *dst,
