@@ -35,8 +35,9 @@ sys.path.insert(0, str(ROOT))
 METRIC = "reduce-copy GB/s (read+write) and % HBM peak at 1 GPU; small-msg µs/call"
 HBM_PEAK_GBS = 8000.0     # MI355X HBM3E, published
 # workloads --workload can time; the variants reuse another workload's inputs
-WORKLOAD_NAMES = ("c1", "c2", "c3", "c3ring", "c4", "c4dev", "c5a", "c5b", "c2fp8", "sim", "sim1")
-WORKLOAD_OF = {"c3ring": "c3", "c4dev": "c4"}
+WORKLOAD_NAMES = ("c1", "c2", "c3", "c3ring", "c3ringflags", "c4", "c4dev", "c5a", "c5b", "c2fp8",
+                  "sim", "sim1")
+WORKLOAD_OF = {"c3ring": "c3", "c3ringflags": "c3", "c4dev": "c4"}
 CSRC = "paper_2510_20171_amd/csrc/"
 _COMMON = [CSRC + "xred_device.hpp", CSRC + "xred_kernels.hpp", CSRC + "xred_dispatch.hpp"]
 KERNEL_SOURCES = {
@@ -382,9 +383,14 @@ def secondary(torch, xr, L, timer, wl, flush):
     items_d = torch.from_numpy(arr.view(np.uint8).copy()).to("cuda")
     dev_fn = lambda: L.xred_batched_reduce(ctypes.c_void_p(items_d.data_ptr()), K, 1, 0, 1,  # noqa
                                            stream)
+    noalloc_fn = lambda: L.xred_batched_reduce_noalloc(  # noqa: E731
+        ctypes.c_void_p(items_d.data_ptr()), K, 1, 0, stream)
     ab = w.alg_bytes(sizes)
-    host_ms = timer.loop_ms(host_fn, 10)
-    dev_ms = timer.loop_ms(dev_fn, 10)
+    # 30 calls after 5: the first call's host plan, built while the GPU is
+    # idle, weighs on the average of a short loop
+    host_ms = timer.loop_ms(host_fn, 30, warm=5)
+    dev_ms = timer.loop_ms(dev_fn, 30, warm=5)
+    noalloc_ms = timer.loop_ms(noalloc_fn, 30, warm=5)
     singles = [reduce_call(L, xr, [arena_d[int(o):int(o) + int(sizes[k])] for o in offs[k]],
                            outs[int(opos[k]):int(opos[k]) + int(sizes[k])], "bf16", "sum")
                for k in range(K)]
@@ -397,10 +403,14 @@ def secondary(torch, xr, L, timer, wl, flush):
                  "host_desc_us": round(host_ms * 1e3, 1), "host_desc_GBs": round(ab / host_ms / 1e6, 1),
                  "device_desc_us": round(dev_ms * 1e3, 1),
                  "device_desc_GBs": round(ab / dev_ms / 1e6, 1),
+                 "device_desc_noalloc_us": round(noalloc_ms * 1e3, 1),
                  "us_per_item": round(host_ms * 1e3 / K, 3),
                  "separate_calls_us": round(sep_ms * 1e3, 1),
                  "separate_calls_GBs": round(ab / sep_ms / 1e6, 1)}
     del arena_d, outs, items_d, ptrs_d, singles
+
+    res["stream_mix_ceiling"] = stream_mix_ceiling(torch, xr, L, timer)
+    res["small_calls"] = small_calls(torch, xr, L)
 
     # CU budget: GB/s of the P=8 bf16 reduce on FTAR-sized 8 MiB chunks
     # (4M elements per source) as the workgroup budget grows
@@ -509,6 +519,7 @@ def secondary(torch, xr, L, timer, wl, flush):
     reps_g = 20
 
     def run(g, reps_r):
+        """(products' span, reduces' span, span of both) in ms."""
         ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
         torch.cuda.synchronize()
         ev[0].record(sg)
@@ -523,28 +534,133 @@ def secondary(torch, xr, L, timer, wl, flush):
         ev[1].record(sg)
         ev[3].record(sr)
         torch.cuda.synchronize()
-        return ev[0].elapsed_time(ev[1]), ev[2].elapsed_time(ev[3])
+        ends = (ev[0].elapsed_time(ev[1]), ev[0].elapsed_time(ev[3]))
+        both = max(ends) - min(0.0, ev[0].elapsed_time(ev[2]))
+        return ev[0].elapsed_time(ev[1]), ev[2].elapsed_time(ev[3]), both
 
     run(True, 10)
-    g_alone, _ = run(True, 0)
+    g_alone, _, _ = run(True, 0)
     co = {"gemm_alone_ms": round(g_alone / reps_g, 3),
           "gemm_TFLOPs": round(2 * 8192 ** 3 * reps_g / g_alone / 1e9, 0)}
     prev = xr.set_max_workgroups(0)
     try:
         for budget in (16, 64, 0):
             xr.set_max_workgroups(budget)
-            _, r1 = run(False, 100)
+            _, r1, _ = run(False, 100)
             reps = max(10, int(g_alone / (r1 / 100)))
-            _, r_alone = run(False, reps)
-            g_with, r_with = run(True, reps)
-            co[f"budget_{budget or 'none'}"] = {
-                "reduce_us_alone": round(r_alone / reps * 1e3, 1),
-                "reduce_us_with_gemm": round(r_with / reps * 1e3, 1),
-                "gemm_slowdown_pct": round(100 * (g_with / g_alone - 1), 1)}
+            _, r_alone, _ = run(False, reps)
+            g_with, r_with, both = run(True, reps)
+            # the two streams overlapped only if both finished well before
+            # the sum of their times alone
+            overlapped = both < 0.9 * (g_alone + r_alone)
+            entry = {"reduce_us_alone": round(r_alone / reps * 1e3, 1),
+                     "reduce_us_with_gemm": round(r_with / reps * 1e3, 1),
+                     "span_both_ms": round(both, 3),
+                     "sum_alone_ms": round(g_alone + r_alone, 3),
+                     "overlapped": overlapped}
+            if overlapped:
+                entry["gemm_slowdown_pct"] = round(100 * (g_with / g_alone - 1), 1)
+            co[f"budget_{budget or 'none'}"] = entry
     finally:
         xr.set_max_workgroups(prev)
     res["coschedule_gemm_bf16"] = co
     del d, out, ga, gb, gc
+    return res
+
+
+def stream_mix_ceiling(torch, xr, L, timer):
+    """The traffic-only ceiling of three stream mixes (libxred_ceiling.so:
+    the fused kernel's tiles reading and writing the same streams with no
+    fold), best over resident-wave caps, next to libxred on the same buffers:
+    8 reads + 1 write of 128 MiB (the bucket), 32 reads + 1 write of 32 MiB
+    (the extremum/integer configuration) and 8 reads + 8 writes of 128 MiB
+    (a simulated 8-rank AllReduce in one launch)."""
+    C = ctypes.CDLL(str(ROOT / "paper_2510_20171_amd" / "libxred_ceiling.so"))
+    C.xred_ceiling_mix.argtypes = [ctypes.c_void_p, ctypes.c_int, ctypes.c_void_p, ctypes.c_int,
+                                   ctypes.c_size_t, ctypes.c_int, ctypes.c_void_p]
+    stream = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    out = {}
+    for name, nsrc, ndst, mib in (("c2_8r1w_128MiB", 8, 1, 128), ("c5_32r1w_32MiB", 32, 1, 32),
+                                  ("sim1_8r8w_128MiB", 8, 8, 128)):
+        n = mib << 20
+        srcs = [torch.randint(-2 ** 31, 2 ** 31 - 1, (n // 4,), dtype=torch.int32, device="cuda")
+                for _ in range(nsrc)]
+        dsts = [torch.empty(n // 4, dtype=torch.int32, device="cuda") for _ in range(ndst)]
+        sa = xr._lib.ptr_array([x.data_ptr() for x in srcs])
+        da = xr._lib.ptr_array([x.data_ptr() for x in dsts])
+        ab = (nsrc + ndst) * n
+        caps = {}
+        for waves in (4, 6, 8, 12, 16, 24, 0):
+            fn = (lambda w_=waves: C.xred_ceiling_mix(sa, nsrc, da, ndst, n, w_, stream))
+            if fn() != 0:
+                raise RuntimeError("xred_ceiling_mix launch failed")
+            ms = timer.loop_ms(fn, 10)
+            caps[str(waves) if waves else "none"] = round(ab / ms / 1e6, 1)
+        best = max(caps.values())
+        if ndst == 1:
+            # the bucket's own type for its shape; the integer configuration's for P=32
+            dt, tt = ("bf16", torch.bfloat16) if nsrc == 8 else ("i32", torch.int32)
+            lib_fn = reduce_call(L, xr, [x.view(tt) for x in srcs], dsts[0].view(tt), dt, "sum")
+            what = f"xred_allreduce_local {dt} sum"
+        else:
+            lib_fn = (lambda: L.xred_allreduce_sim(sa, da, nsrc, n // 2, 1, 0,
+                                                   xr.SCHEDULE["ring1"], stream))
+            what = "xred_allreduce_sim bf16 sum ring1"
+        lib_ms = timer.loop_ms(lib_fn, 10)
+        lib = ab / lib_ms / 1e6
+        out[name] = {"ceiling_GBs": best, "ceiling_by_waves_per_cu": caps,
+                     "library": what, "library_GBs": round(lib, 1),
+                     "library_frac_of_ceiling": round(lib / best, 4)}
+        del srcs, dsts
+        torch.cuda.empty_cache()
+    return out
+
+
+def small_calls(torch, xr, L):
+    """One call and a synchronisation of its stream, wall clock (median of
+    200): latency-bound batched and ring calls."""
+    import numpy as np
+    stream = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    res = {}
+    n = 4096                                     # 8 KiB of bf16 per source
+    for K in (64, 256):
+        srcs = [torch.randn(K * n, device="cuda").to(torch.bfloat16) for _ in range(8)]
+        out = torch.empty(K * n, dtype=torch.bfloat16, device="cuda")
+        ptrs = torch.tensor([[s.data_ptr() + 2 * n * k for s in srcs] for k in range(K)],
+                            dtype=torch.int64, device="cuda")
+        arr = np.zeros(K, xr.ITEM_DTYPE)
+        arr["srcs"] = ptrs.data_ptr() + 64 * np.arange(K, dtype=np.uint64)
+        arr["dst"] = out.data_ptr() + 2 * n * np.arange(K, dtype=np.uint64)
+        arr["count"] = n
+        arr["nsrc"] = 8
+        items_d = torch.from_numpy(arr.view(np.uint8).copy()).to("cuda")
+        rows = [(ctypes.c_void_p * 8)(*[s.data_ptr() + 2 * n * k for s in srcs])
+                for k in range(K)]
+        items_h = xr.pack_items([(ctypes.addressof(rows[k]), out.data_ptr() + 2 * n * k, n, 8)
+                                 for k in range(K)])
+        dev = ctypes.c_void_p(items_d.data_ptr())
+        res[f"batch_{K}x8KiB_device_desc_us"] = round(median(call_sync_us(
+            torch, lambda: L.xred_batched_reduce(dev, K, 1, 0, 1, stream), 200)), 1)
+        res[f"batch_{K}x8KiB_noalloc_us"] = round(median(call_sync_us(
+            torch, lambda: L.xred_batched_reduce_noalloc(dev, K, 1, 0, stream), 200)), 1)
+        res[f"batch_{K}x8KiB_host_desc_us"] = round(median(call_sync_us(
+            torch, lambda: L.xred_batched_reduce(items_h, K, 1, 0, 0, stream), 200)), 1)
+        del srcs, out, ptrs, items_d
+    chunks = [torch.randn(1 << 16, device="cuda").to(torch.bfloat16) for _ in range(16)]
+    ring_out = torch.empty_like(chunks[0])
+    ca = xr._lib.ptr_array([c.data_ptr() for c in chunks])
+    ro = ctypes.c_void_p(ring_out.data_ptr())
+    flags = PinnedWords(16)
+    for i in range(16):
+        flags.words[i] = 1
+    res["ring_16x64K_bf16_us"] = round(median(call_sync_us(
+        torch, lambda: L.xred_ring_reduce(ca, 16, ro, 1 << 16, 1, 0, None, 1, 0, None, stream),
+        200)), 1)
+    res["ring_16x64K_bf16_host_flags_us"] = round(median(call_sync_us(
+        torch, lambda: L.xred_ring_reduce(ca, 16, ro, 1 << 16, 1, 0, flags.dev, 1, 0, None,
+                                          stream), 200)), 1)
+    torch.cuda.synchronize()
+    flags.free()
     return res
 
 
@@ -557,24 +673,33 @@ def build_workload(name, torch, xr, L, wl):
     import numpy as np
     w = wl.WORKLOADS[WORKLOAD_OF.get(name, name)]
     stream = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
-    if name == "c3ring":
+    if name in ("c3ring", "c3ringflags"):
         log(f"generating c3 inputs for the one-launch ring (16 chunks x {w.count} bf16)")
         chunks_np = [c.copy() for c in wl.stepwise_chunks(w)]
         chunks = [dev_bf16(torch, c) for c in chunks_np]
         out = torch.empty_like(chunks[0])
         arr = xr._lib.ptr_array([c.data_ptr() for c in chunks])
         dptr = ctypes.c_void_p(out.data_ptr())
+        flags = None
+        if name == "c3ringflags":
+            # every chunk's flag already set in pinned host memory: the launch
+            # pays the poll and the relay, not a wait
+            flags = PinnedWords(16)
+            for i in range(16):
+                flags.words[i] = 1
 
         def step():
-            st = L.xred_ring_reduce(arr, 16, dptr, w.count, 1, 0, None, 1, 0, None, stream)
+            st = L.xred_ring_reduce(arr, 16, dptr, w.count, 1, 0,
+                                    flags.dev if flags else None, 1, 0, None, stream)
             if st:
                 xr._lib.check(st)
-        step._keep_inputs = (chunks, out, arr)
+        step._keep_inputs = (chunks, out, arr, flags)
+        how = ("chunks gated by host-pinned flags, all set" if flags else "all chunks ready")
         res = dict(step=step, alg_bytes=17 * w.count * 2, family="ring",
                    kernel="ring_kernel<bf16, sum>",
-                   profile=ROOT / "profiles" / "ring_bf16_c3ring.md",
-                   config={"workload": "c3 in one launch: xred_ring_reduce of 16 chunks x "
-                                       f"{w.count} bf16, accumulator on chip",
+                   profile=ROOT / "profiles" / f"ring_bf16_{name}.md",
+                   config={"workload": f"{name}: xred_ring_reduce of 16 chunks x "
+                                       f"{w.count} bf16 in one launch, accumulator on chip, {how}",
                            "chunks": 16, "N": w.count, "io_dtype": "bf16"})
         res["cpu"] = lambda: cpu_baseline(chunks_np, "bf16", "sum", 16, 2)
         return res
@@ -698,7 +823,7 @@ def build_workload(name, torch, xr, L, wl):
             if st:
                 xr._lib.check(st)
         step._keep_inputs = (arena_d, outs, ptrs_d, items_d)
-        kernel, where = "batched_grouped_kernel<bf16, sum>", "device descriptors"
+        kernel, where = "batched_queue_kernel<bf16, sum, 2>", "device descriptors"
     else:
         def step():
             st = L.xred_batched_reduce(items, K, 1, 0, 0, stream)

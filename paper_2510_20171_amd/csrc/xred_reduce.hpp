@@ -61,20 +61,6 @@ int waves_for(size_t bytes)
     return waves_per_cu<NP>();
 }
 
-int lds_per_cu()
-{
-    static int bytes = [] {
-        int dev = 0, v = 0;
-        if (hipGetDevice(&dev) != hipSuccess ||
-            hipDeviceGetAttribute(&v, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor, dev) !=
-                hipSuccess ||
-            v <= 0)
-            v = 160 * 1024;
-        return v;
-    }();
-    return bytes;
-}
-
 // Dynamic LDS that leaves room for `waves` wavefronts per CU (0: no cap).
 size_t lds_for_waves(int waves)
 {
