@@ -54,9 +54,14 @@ KERNEL_SOURCES = {
 
 
 def kernel_source_sha(family: str = "reduce") -> str:
+    """Hash of a kernel family's sources with comments and blank space
+    removed, so that editing a comment keeps its counter profile current."""
     h = hashlib.sha256()
     for f in KERNEL_SOURCES[family]:
-        h.update((ROOT / f).read_bytes())
+        text = (ROOT / f).read_text()
+        text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+        text = re.sub(r"//[^\n]*", " ", text)
+        h.update(" ".join(text.split()).encode())
     return h.hexdigest()[:16]
 
 

@@ -16,7 +16,8 @@
 // written with device-scope (sc1) stores, which measured 2-5 % faster on
 // MI355X for this 8:1 read/write mix than ordinary write-back stores and
 // faster still than nontemporal stores; the step-wise accumulator uses
-// ordinary loads and stores so it stays in L2 / MALL between launches.
+// ordinary loads and stores, which may leave it in the MALL between
+// launches (not in L2: a launch starts with its L2 lines invalidated).
 //
 // Work is split into tiles of B*U vectors.  Tile t is processed by workgroup
 // t mod gridDim.x, so with a fixed grid a tile always lands on the same XCD

@@ -3,9 +3,12 @@
 //
 // A step moves little data (a 1M-element bf16 chunk step reads 6 MiB and
 // writes 4 MiB), so launch cost dominates; the launch path is one template
-// lookup and one kernel.  The grid is a pure function of count, so tile t of
-// the accumulator is processed by workgroup t on every step and therefore on
-// the same XCD, whose L2 may still hold it from the previous step.
+// lookup and one kernel.  The accumulator does not stay in L2 from one step
+// to the next: on this multi-XCD part each launch starts with its L2 lines
+// invalidated, and the counters show every read of a plain step missing L2
+// (6 MiB of misses per launch: the chunk and the whole accumulator), only the
+// accumulator's writes hitting the lines the same launch just read.  What can
+// carry it between launches is the 256 MB MALL, which sits beyond L2.
 #include "xred_dispatch.hpp"
 #include "xred_internal.hpp"
 #include "xred_kernels.hpp"
