@@ -223,7 +223,11 @@ xred_status batched_host(const xred_item *items, int nitems, xred_dtype dtype, x
         free_slot(s);
         size_t cap = 64 << 10;
         while (cap < need) cap <<= 1;
-        if (hipHostMalloc(&s.host, cap, hipHostMallocDefault) != hipSuccess) {
+        // coherent: small batches are read by the kernel straight from the
+        // slot, and the host rewrites a slot once its last kernel has ended,
+        // so the GPU must not serve those reads from lines it cached earlier
+        // (measured no slower than the default allocation for 8-512 items)
+        if (hipHostMalloc(&s.host, cap, hipHostMallocCoherent) != hipSuccess) {
             s.host = nullptr;
             return fail(XRED_OUT_OF_MEMORY, "pinned staging of %zu bytes", cap);
         }
