@@ -202,9 +202,14 @@ XRED_API xred_status xred_acc_cast(const void *acc, void *dst, size_t count, xre
  *   XRED_ITEMS_ON_DEVICE: `items` and every items[k].srcs are DEVICE memory,
  *            read when the kernels run, so an earlier kernel on the stream may
  *            still write them (metadata by reference, after the GPU-resident
- *            collectives of Section 6.1).  No host work per item and no
- *            allocation (each workgroup plans its share in the kernel), so
- *            the call can be captured in a HIP graph.  Items that cannot be
+ *            collectives of Section 6.1).  No host work per item: the kernel
+ *            plans the batch from the descriptors.  Batches of 65..16384
+ *            items launched eagerly take tiles in order from a counter pair
+ *            in device memory the library binds to the calling stream (64
+ *            streams per device, allocated once, until xred_release);
+ *            under graph capture, past 64 streams or past 16384 items the
+ *            batch runs on a kernel that keeps no state, so the call can be
+ *            captured in a HIP graph (same results).  Items that cannot be
  *            run safely (nsrc outside 1..64, a NULL pointer, reserved != 0)
  *            are skipped and their dst is left untouched; pointers are
  *            otherwise trusted.
@@ -343,11 +348,10 @@ XRED_API size_t xred_sim_chunk(size_t count, int nranks);
  * behind the network (Section 5).  Results do not depend on it.  Process-wide;
  * returns the previous value.  xred_ring_reduce applies it too, but never goes
  * below the workgroups its on-chip accumulators need (one per 4 tiles).
- * The budget bounds the CUs a launch may occupy; it does not lower the
- * interference with a kernel running beside it: next to a bf16 matrix
- * product, a reduce capped at 16 or 64 workgroups slowed the product more
- * (11-13 %, 7-9 %) than an uncapped one (2-5 %), whose short workgroups the
- * hardware interleaves with the product's.
+ * The budget bounds the workgroups a launch may have in flight; whether a
+ * reduce on one stream runs concurrently with a kernel on another is up to
+ * the runtime's hardware queues (on the measured box a reduce and a bf16
+ * matrix product on two streams did not overlap, capped or not).
  */
 XRED_API unsigned xred_set_max_workgroups(unsigned max_workgroups);
 
@@ -364,10 +368,10 @@ XRED_API const char *xred_last_error(void);
 /* Library version: major*10000 + minor*100 + patch. */
 XRED_API int xred_version(void);
 
-/* Frees the library's host-mode batch staging buffers and the ring's relay
- * words on every device after synchronising the device work that uses them,
- * and unbinds the relay words from their streams.  Optional; later calls
- * re-create what they need. */
+/* Frees the library's host-mode batch staging buffers, and the ring's relay
+ * words and the batch queue's counters, on every device after synchronising
+ * the device work that uses them, and unbinds those from their streams.
+ * Optional; later calls re-create what they need. */
 XRED_API void xred_release(void);
 
 #ifdef __cplusplus
