@@ -221,3 +221,96 @@ def test_device_batch_queue_item_limit(xr, orc, K):
     xr.batched_reduce(items, "sum", dtype="i32")
     torch.cuda.synchronize()
     gu.assert_parity(out, orc.allreduce_local(srcs_np, "i32", "sum"), "i32", "sum", f"K={K}")
+
+
+RAND_DTYPES = ("f32", "bf16", "f16", "e4m3", "e5m2", "i32", "u32", "i64", "u64")
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_random_queue_batches(xr, orc, seed):
+    """Seeded random device batches of 65..400 items (the queue kernel): every
+    dtype, op (AVG on float types), 1..17 sources, sizes from one element to
+    several tiles, element-aligned (not 16-byte aligned) items, under random
+    CU budgets, alternating xred_batched_reduce and
+    xred_batched_reduce_noalloc, each against the oracle."""
+    rng = np.random.default_rng(5600 + seed)
+    for case in range(6):
+        dtype = RAND_DTYPES[rng.integers(0, len(RAND_DTYPES))]
+        ops = ["sum", "prod", "max", "min"] + (["avg"] if dtype in gu.FLOATS else [])
+        op = ops[rng.integers(0, len(ops))]
+        K = int(rng.integers(65, 401))
+        tile = 2 * 512 * (16 // ES[dtype])
+        sizes = [int(rng.choice([1, 3, tile - 1, tile, tile + 1, 2 * tile + 5]))
+                 if rng.random() < 0.5 else int(rng.integers(1, 3 * tile)) for _ in range(K)]
+        nsrc = [int(rng.choice([1, 2, 3, 8, 9, 17])) for _ in range(K)]
+        budget = int(rng.choice([0, 0, 1, 7, 100]))
+        noalloc = case % 2 == 1
+        print(f"case {case}: {dtype} {op} K={K} budget={budget} noalloc={noalloc}", flush=True)
+        host, outs, keep, rows = [], [], [], []
+        for k, (n, P) in enumerate(zip(sizes, nsrc)):
+            shift = 1 if k % 4 == 3 else 0
+            srcs = [pins.random_column_values(rng, dtype, n) for _ in range(P)]
+            dev = [gu.to_dev(np.concatenate([np.zeros(shift, s.dtype), s]), dtype)[shift:]
+                   for s in srcs]
+            out = torch.zeros(n + shift, dtype=gu.torch_dtype(dtype), device="cuda")[shift:]
+            pa = torch.tensor([d.data_ptr() for d in dev], dtype=torch.int64, device="cuda")
+            keep += dev + [pa]
+            host.append(srcs)
+            outs.append(out)
+            rows.append((pa.data_ptr(), out.data_ptr(), n, P, 0))
+        arr = np.zeros(K, xr.ITEM_DTYPE)
+        for k, r in enumerate(rows):
+            arr[k] = r
+        items = torch.from_numpy(arr.view(np.uint8).copy()).to("cuda")
+        prev = xr.set_max_workgroups(budget)
+        try:
+            if noalloc:
+                xr.batched_reduce_noalloc(items, op, dtype=dtype)
+            else:
+                xr.batched_reduce(items, op, dtype=dtype)
+            torch.cuda.synchronize()
+        finally:
+            xr.set_max_workgroups(prev)
+        for k in range(K):
+            gu.assert_parity(outs[k], orc.allreduce_local(host[k], dtype, op), dtype, op,
+                             f"case {case} item {k}")
+
+
+def test_noalloc_graph_replay(xr, orc):
+    """xred_batched_reduce_noalloc captured in a HIP graph: its kernel leaves
+    the tile counters at zero, so every replay, with eager calls of both
+    device-descriptor entry points between replays, folds the whole batch."""
+    rng = np.random.default_rng(5700)
+    b = Batch(xr, rng, "f32", 180, skip_rows=False)
+    other = Batch(xr, rng, "f32", 90, skip_rows=False)
+    exp_other = other.expected(orc, "sum")
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        xr.batched_reduce_noalloc(b.items, "sum", dtype="f32")   # looks the array up eagerly
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        xr.batched_reduce_noalloc(b.items, "sum", dtype="f32")
+    torch.cuda.synchronize()
+    for r in range(3):
+        with np.errstate(over="ignore", invalid="ignore"):
+            for k in range(len(b.host)):
+                b.host[k][0] = (b.host[k][0] * np.float32(0.5 + r)).astype(np.float32)
+        _upload_first_sources(b)
+        for o in b.outs:
+            o.zero_()
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        b.check(b.expected(orc, "sum"), "sum", f"replay {r}")
+        for o in other.outs:
+            o.zero_()
+        if r % 2:
+            xr.batched_reduce_noalloc(other.items, "sum", dtype="f32")
+        else:
+            xr.batched_reduce(other.items, "sum", dtype="f32")
+        torch.cuda.synchronize()
+        other.check(exp_other, "sum", f"eager call after replay {r}")
+    del g
