@@ -354,18 +354,22 @@ __global__ __launch_bounds__(kB) void batched_rr_kernel(const xred_item *items, 
 // when the hardware dispatches one workgroup per tile of a host-built table,
 // and no workgroup keeps a fixed share of the batch.  Each workgroup first
 // scans the tile counts of all items into an LDS tile-start prefix (its first
-// claim in flight meanwhile).  Per tile it finds the tile's item (a 64-ary
-// search of the prefix, in every wave), fetches the descriptor and source
-// pointers, claims the next tile, and reduces this one; the claim's answer is
-// handed to all waves through LDS at the tile's end.
+// claim in flight meanwhile).  Per tile it claims the next tile and issues
+// this tile's loads; while they are in flight, the claim's answer is handed
+// to all waves through LDS and every wave finds the next tile's item (a
+// 64-ary search of the prefix) and fetches its descriptor and source
+// pointers, so the next tile's loads follow this tile's stores at once.
 //
 // What was measured on the 4096-item log-uniform batch (MI355X, same box):
 // one workgroup of 512 threads per CU and tiles of two 512-vector sub-tiles
-// (16 KiB per source) 1265 us; two workgroups per CU 1301-1304 us; 8 KiB
-// tiles 1533-1610 us; 32 KiB tiles 1294 us; claiming two tiles ahead with
-// the next descriptor prefetched 1445 us, and double-buffered loads 1262 us
-// (every claim ahead widens the window of tiles being read, which costs
-// more than the latency it hides); eight interleaved counters 1339 us.
+// (16 KiB per source) 1237-1240 us, against 1267 us with the next tile's
+// descriptor fetched after this tile's stores.  With the fetch overlapped:
+// 8 KiB tiles 1611 us (one or two workgroups per CU: the one counter then
+// answers twice as many claims), 24 KiB 1281 us, 32 KiB 1322 us, two
+// workgroups per CU 1393 us.  Before it: claiming two tiles ahead 1445 us
+// and double-buffered loads 1262 us (a tile claimed or loaded ahead widens
+// the window of tiles being read, which costs more than the latency it
+// hides); eight interleaved counters 1339 us.
 //
 // The counter: *next is zero when the launch starts.  clear (if set) is
 // another counter the launch zeroes for the next launch on the stream;
@@ -467,12 +471,12 @@ __global__ __launch_bounds__(kB) void batched_queue_kernel(const xred_item *item
     }
     __syncthreads();
     uint64_t g = uniform64(s_claim[1]);
+    TileDesc cur{};
+    if (g < total) {
+        const int k = find_item(s_pre, nitems, (uint32_t)g);
+        fetch_desc(cur, items, (uint32_t)k, uniform64(g - s_pre[k]));
+    }
     for (int b = 0; g < total; ++b) {
-        TileDesc cur;
-        {
-            const int k = find_item(s_pre, nitems, (uint32_t)g);
-            fetch_desc(cur, items, (uint32_t)k, uniform64(g - s_pre[k]));
-        }
         uint64_t c = 0;
         if (threadIdx.x == 0) c = claim();   // answered while this tile streams
         // straight-line tile: sources beyond nsrc, and tiles off the fast
@@ -488,6 +492,17 @@ __global__ __launch_bounds__(kB) void batched_queue_kernel(const xred_item *item
 #pragma unroll
             for (int h = 0; h < SUB; ++h)
                 in[p][h] = bload<kLoadStream>(r, (uint32_t)(h * kB + threadIdx.x) * 16u);
+        }
+        // With this tile's loads in flight, hand the claim to every wave
+        // and fetch the next tile's descriptor and source pointers, so the
+        // next tile's loads can be issued as soon as this tile is stored.
+        if (threadIdx.x == 0) s_claim[b & 1] = c;
+        lds_barrier();
+        const uint64_t gn = uniform64(s_claim[b & 1]);
+        TileDesc nxt{};
+        if (gn < total) {
+            const int k = find_item(s_pre, nitems, (uint32_t)gn);
+            fetch_desc(nxt, items, (uint32_t)k, uniform64(gn - s_pre[k]));
         }
         const rsrc_t w = make_rsrc(cur.dst + toff, nrec);
 #pragma unroll
@@ -521,9 +536,8 @@ __global__ __launch_bounds__(kB) void batched_queue_kernel(const xred_item *item
         } else {
             batched_tile<T, Op, SUB>(load_item(items, cur.k), cur.lt);
         }
-        if (threadIdx.x == 0) s_claim[b & 1] = c;
-        lds_barrier();   // the waves start every tile together
-        g = uniform64(s_claim[b & 1]);
+        cur = nxt;
+        g = gn;
     }
     // every claim of this workgroup has been answered (each was read back
     // above), so the last workgroup's reset is the counter's last write
@@ -547,13 +561,18 @@ __global__ __launch_bounds__(kB) void batched_queue_kernel(const xred_item *item
 // apart and spread the loads in flight over the batch (c4: 5.3 against
 // 6.9 TB/s for the same data).  Tiles are one 16-byte vector per thread and
 // source, two workgroups per CU (16 waves: 6.9 TB/s against 5.9 uncapped).
+// Other shapes on the 4096-item log-uniform batch (same box): 512 threads and
+// 8 KiB per source, two per CU, 1199 us; one or three per CU 1462 / 1472 us;
+// 16 KiB tiles one / two per CU 1321 / 1488 us; 1024 threads one per CU
+// 1314 us; 256 threads four per CU, 4 / 8 KiB tiles 1367 / 1489 us.
 // Under a CU budget the grid is smaller and each workgroup strides over the
 // table.
 constexpr int kTB = 512;
+constexpr int kTableSub = 1;          // 16-byte vectors per thread and source
 constexpr int kTableWgsPerCu = 2;
 
 template <class T>
-constexpr uint64_t table_tile_elems() { return (uint64_t)kTB * T::kVec; }
+constexpr uint64_t table_tile_elems() { return (uint64_t)kTB * kTableSub * T::kVec; }
 
 // The fields of a descriptor a tile needs, loaded with scalar loads.
 struct ItemHead {
@@ -569,13 +588,14 @@ __device__ __forceinline__ ItemHead load_head(const xred_item *it)
                     sload(&it->count), (int)sload(&it->nsrc)};
 }
 
-// Tile lt (of kTB vectors) of the item with header h.  CHECK: the descriptor is the
+// Tile lt (of kTB * kTableSub vectors) of the item with header h.  CHECK: the descriptor is the
 // caller's device memory, so an item with a NULL source pointer is skipped
 // (the host validates its own descriptors before staging them).
 template <class T, class Op, bool CHECK>
 __device__ __forceinline__ void table_tile(const ItemHead &h, uint64_t lt)
 {
-    constexpr uint32_t kBytes = (uint32_t)kTB * 16u;
+    constexpr int U = kTableSub;
+    constexpr uint32_t kBytes = (uint32_t)kTB * U * 16u;
     const char *const *srcs = h.srcs;
     char *dst = h.dst;
     const uint64_t count = h.count;
@@ -602,7 +622,7 @@ __device__ __forceinline__ void table_tile(const ItemHead &h, uint64_t lt)
         if (CHECK && null_src) return;
         if ((all & 15u) == 0) {
             if (toff < vbytes)
-                reduce_tile<T, Op, 0, 1, kTB>(src, nsrc, dst,
+                reduce_tile<T, Op, 0, U, kTB>(src, nsrc, dst,
                                               Tile{toff, tile_nrec(vbytes, toff, kBytes)});
         } else {
             const uint64_t e0 = lt * table_tile_elems<T>();
@@ -616,31 +636,37 @@ __device__ __forceinline__ void table_tile(const ItemHead &h, uint64_t lt)
         if (CHECK && null_src) return;
         // straight-line tile: sources beyond nsrc get a zero-length range
         const uint32_t nrec = toff < vbytes ? tile_nrec(vbytes, toff, kBytes) : 0u;
-        u32x4 in[8];
+        u32x4 in[8][U];
 #pragma unroll
         for (int q = 0; q < 8; ++q) {
             const bool on = q < nsrc;
-            in[q] = bload<kLoadStream>(make_rsrc((on ? p[q] : dst) + toff, on ? nrec : 0u),
-                                       threadIdx.x * 16u);
+            const rsrc_t r = make_rsrc((on ? p[q] : dst) + toff, on ? nrec : 0u);
+#pragma unroll
+            for (int u = 0; u < U; ++u)
+                in[q][u] = bload<kLoadStream>(r, (uint32_t)(u * kTB + threadIdx.x) * 16u);
         }
-        typename T::Acc acc[T::kVec];
-        up_vec<T>(in[0], acc);
+        const rsrc_t w = make_rsrc(dst + toff, nrec);
 #pragma unroll
-        for (int q = 1; q < 8; ++q) {
-            const bool on = q < nsrc;
-            typename T::Acc b[T::kVec];
-            up_vec<T>(in[q], b);
+        for (int u = 0; u < U; ++u) {
+            typename T::Acc acc[T::kVec];
+            up_vec<T>(in[0][u], acc);
 #pragma unroll
-            for (int e = 0; e < T::kVec; ++e) {
-                const typename T::Acc c = combine<T, Op>(acc[e], b[e]);
-                acc[e] = on ? c : acc[e];
+            for (int q = 1; q < 8; ++q) {
+                const bool on = q < nsrc;
+                typename T::Acc b[T::kVec];
+                up_vec<T>(in[q][u], b);
+#pragma unroll
+                for (int e = 0; e < T::kVec; ++e) {
+                    const typename T::Acc c = combine<T, Op>(acc[e], b[e]);
+                    acc[e] = on ? c : acc[e];
+                }
             }
-        }
-        if constexpr (__is_same(Op, OpAvg)) {
+            if constexpr (__is_same(Op, OpAvg)) {
 #pragma unroll
-            for (int e = 0; e < T::kVec; ++e) acc[e] = avg_scale<T, Op>(acc[e], nsrc);
+                for (int e = 0; e < T::kVec; ++e) acc[e] = avg_scale<T, Op>(acc[e], nsrc);
+            }
+            bstore<kStoreOut>(down_vec<T, Op>(acc), w, (uint32_t)(u * kTB + threadIdx.x) * 16u);
         }
-        bstore<kStoreOut>(down_vec<T, Op>(acc), make_rsrc(dst + toff, nrec), threadIdx.x * 16u);
     }
     // the item's last tile also takes the elements after its last full vector
     if ((lt + 1) * table_tile_elems<T>() >= count) {
