@@ -416,6 +416,7 @@ def secondary(torch, xr, L, timer, wl, flush):
 
     res["stream_mix_ceiling"] = stream_mix_ceiling(torch, xr, L, timer)
     res["small_calls"] = small_calls(torch, xr, L)
+    res["flag_handoff"] = flag_handoff(torch)
 
     # CU budget: GB/s of the P=8 bf16 reduce on FTAR-sized 8 MiB chunks
     # (4M elements per source) as the workgroup budget grows
@@ -618,6 +619,45 @@ def stream_mix_ceiling(torch, xr, L, timer):
                      "library_frac_of_ceiling": round(lib / best, 4)}
         del srcs, dsts
         torch.cuda.empty_cache()
+    return out
+
+
+def flag_handoff(torch, rounds: int = 2000, skip: int = 16):
+    """The host-to-kernel handoff of a flag in pinned host memory (the
+    host-kernel coordinated mode of Section 4.1), as a ping-pong between a
+    host thread and one polling lane (libxred_ceiling.so): the host's round
+    trip is one handoff each way.  "relayed" passes the flag through a word in
+    device memory to a second workgroup first, the hop the ring kernel's
+    poller adds.  Per round the polling lane also counts its loads of the
+    flag and times them on the device clock, which gives the latency of one
+    poll of host memory."""
+    import numpy as np
+    C = ctypes.CDLL(str(ROOT / "paper_2510_20171_amd" / "libxred_ceiling.so"))
+    C.xred_ceiling_handoff.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int,
+                                       ctypes.POINTER(ctypes.c_double),
+                                       ctypes.POINTER(ctypes.c_uint32),
+                                       ctypes.POINTER(ctypes.c_double), ctypes.c_void_p]
+    stream = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    out = {"rounds": rounds - skip}
+    for name, relay in (("direct", 0), ("relayed", 1)):
+        rtt = (ctypes.c_double * rounds)()
+        polls = (ctypes.c_uint32 * rounds)()
+        seen = (ctypes.c_double * rounds)()
+        rc = C.xred_ceiling_handoff(rounds, relay, 1000, rtt, polls, seen, stream)
+        if rc != 0:
+            raise RuntimeError(f"xred_ceiling_handoff({name}) returned {rc}")
+        r = np.array(rtt[skip:])
+        n = np.array(polls[skip:], dtype=np.float64)
+        t = np.array(seen[skip:])
+        many = n >= 2
+        out[name] = {"rtt_p10_us": round(float(np.percentile(r, 10)), 2),
+                     "rtt_p50_us": round(float(np.percentile(r, 50)), 2),
+                     "rtt_p90_us": round(float(np.percentile(r, 90)), 2),
+                     "polls_per_round_p50": float(np.median(n)),
+                     "poll_latency_us_p50": (round(float(np.median(t[many] / n[many])), 3)
+                                             if many.any() else None)}
+    out["one_way_us_est"] = round(out["direct"]["rtt_p50_us"] / 2, 2)
+    out["relay_hop_us_p50"] = round(out["relayed"]["rtt_p50_us"] - out["direct"]["rtt_p50_us"], 2)
     return out
 
 

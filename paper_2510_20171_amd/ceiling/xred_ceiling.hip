@@ -14,10 +14,15 @@
 // the memory system gives that mix of streams: the ceiling against which a
 // reduce kernel with the same mix is judged (P reads and one write for the
 // fused reduce, G reads and G writes for a simulated AllReduce in one
-// launch).
+// launch).  It also measures the host-to-kernel handoff of a flag in pinned
+// host memory (a ping-pong, below).
 #include <hip/hip_runtime.h>
 #include <stddef.h>
 #include <stdint.h>
+#include <string.h>
+
+#include <chrono>
+#include <vector>
 
 #include "../csrc/xred_kernels.hpp"
 
@@ -131,4 +136,153 @@ xred_ceiling_mix(const void *const *srcs, int nsrc, void *const *dsts, int ndst,
     default: launch_mix<0>(grid, reserve, st, s, nsrc, d, ndst, bytes); break;
     }
     return (int)hipGetLastError();
+}
+
+// ------------------------------------------------------------- handoff --
+// The host-to-kernel handoff of a flag in pinned host memory, as a ping-pong:
+// the host writes round number r to *ping; a polling lane that sees it
+// answers by writing r to *pong, which the host is spinning on.  The host's
+// round trip is one host-to-device and one device-to-host handoff.  With
+// `relay` set the polling lane (workgroup 0) passes r through a word in
+// device memory to a lane of workgroup 1, which answers: the hop the ring
+// kernel's poller adds between a flag and the workgroups that wait for it.
+// Every wait on both sides ends after `limit` device-clock ticks (device) or
+// the same time on the host clock.
+namespace {
+
+struct PingPong {
+    const uint32_t *ping;   // host pinned, written by the host
+    uint32_t *pong;         // host pinned, written by the device
+    uint32_t *relay;        // device memory (relay mode)
+    uint32_t *failed;       // host pinned: the round a device wait gave up on
+    uint32_t *polls;        // device memory: loads of the polled word per round
+    uint64_t *seen;         // device memory: ticks from round start to seeing r
+};
+
+__device__ __forceinline__ bool wait_word(const uint32_t *w, uint32_t r, bool system,
+                                          uint64_t limit, uint32_t *npolls, uint64_t *ticks)
+{
+    const uint64_t t0 = wall_clock64();
+    uint32_t n = 0;
+    for (;;) {
+        ++n;
+        const uint32_t v = system
+            ? __hip_atomic_load(w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM)
+            : __hip_atomic_load(w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        const uint64_t t = wall_clock64();
+        if (v == r) {
+            *npolls = n;
+            *ticks = t - t0;
+            return true;
+        }
+        if (t - t0 > limit) return false;
+    }
+}
+
+__global__ __launch_bounds__(64) void pingpong_kernel(PingPong q, uint32_t rounds, int relay,
+                                                      uint64_t limit)
+{
+    if (threadIdx.x != 0) return;
+    for (uint32_t r = 1; r <= rounds; ++r) {
+        uint32_t n = 0;
+        uint64_t dt = 0;
+        if (blockIdx.x == 0) {
+            if (!wait_word(q.ping, r, true, limit, &n, &dt)) {
+                __hip_atomic_store(q.failed, r, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+                return;
+            }
+            q.polls[r - 1] = n;
+            q.seen[r - 1] = dt;
+            if (relay)
+                __hip_atomic_store(q.relay, r, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            else
+                __hip_atomic_store(q.pong, r, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+        } else {
+            if (!wait_word(q.relay, r, false, limit, &n, &dt)) return;
+            __hip_atomic_store(q.pong, r, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM);
+        }
+    }
+}
+
+}  // namespace
+
+// `rounds` ping-pong rounds (see above) on `stream`; relay: 0 = the polling
+// lane answers, 1 = it relays through device memory to a second workgroup.
+// Outputs per round (arrays of `rounds`): the host's round trip in us, the
+// polling lane's loads of the flag and its device time from the start of the
+// round to seeing the flag, in us.  Round 1 includes the launch.  Returns 0,
+// a hipError_t, or -1 if a wait on either side gave up (every wait is
+// bounded by limit_ms, so the kernel has always ended when this returns).
+extern "C" __attribute__((visibility("default"))) int
+xred_ceiling_handoff(int rounds, int relay, int limit_ms, double *rtt_us, uint32_t *polls,
+                     double *seen_us, void *stream)
+{
+    if (rounds < 1 || rounds > (1 << 20) || limit_ms < 1 || !rtt_us || !polls || !seen_us)
+        return (int)hipErrorInvalidValue;
+    int dev = 0, khz = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e == hipSuccess) e = hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, dev);
+    if (e != hipSuccess) return (int)e;
+    if (khz <= 0) return (int)hipErrorInvalidValue;
+    char *host = nullptr;
+    char *devmem = nullptr;
+    const size_t dbytes = 256 + (size_t)rounds * (4 + 8);
+    e = hipHostMalloc((void **)&host, 256, hipHostMallocCoherent);
+    if (e != hipSuccess) return (int)e;
+    e = hipMalloc((void **)&devmem, dbytes);
+    if (e != hipSuccess) {
+        (void)hipHostFree(host);
+        return (int)e;
+    }
+    memset(host, 0, 256);
+    PingPong q;
+    q.ping = (const uint32_t *)host;
+    q.pong = (uint32_t *)(host + 64);
+    q.failed = (uint32_t *)(host + 128);
+    q.relay = (uint32_t *)devmem;
+    q.seen = (uint64_t *)(devmem + 256);
+    q.polls = (uint32_t *)(devmem + 256 + (size_t)rounds * 8);
+    const hipStream_t st = (hipStream_t)stream;
+    int rc = 0;
+    e = hipMemsetAsync(devmem, 0, dbytes, st);
+    if (e == hipSuccess) e = hipStreamSynchronize(st);
+    if (e == hipSuccess) {
+        const uint64_t limit = (uint64_t)khz * (uint64_t)limit_ms;   // kHz * ms = ticks
+        hipLaunchKernelGGL(pingpong_kernel, dim3(relay ? 2 : 1), dim3(64), 0, st, q,
+                           (uint32_t)rounds, relay, limit);
+        e = hipGetLastError();
+    }
+    if (e == hipSuccess) {
+        volatile uint32_t *ping = (volatile uint32_t *)host;
+        const volatile uint32_t *pong = (const volatile uint32_t *)(host + 64);
+        const auto give_up = std::chrono::milliseconds(limit_ms);
+        for (int r = 1; r <= rounds && rc == 0; ++r) {
+            const auto t0 = std::chrono::steady_clock::now();
+            __atomic_store_n(ping, (uint32_t)r, __ATOMIC_RELEASE);
+            for (uint32_t spins = 0;; ++spins) {
+                if (__atomic_load_n(pong, __ATOMIC_ACQUIRE) == (uint32_t)r) break;
+                if ((spins & 255u) == 0 && std::chrono::steady_clock::now() - t0 > give_up) {
+                    rc = -1;
+                    break;
+                }
+            }
+            rtt_us[r - 1] =
+                std::chrono::duration<double, std::micro>(std::chrono::steady_clock::now() - t0)
+                    .count();
+        }
+        e = hipStreamSynchronize(st);   // every device wait is bounded
+    }
+    if (e == hipSuccess && __atomic_load_n((uint32_t *)(host + 128), __ATOMIC_ACQUIRE) != 0)
+        rc = -1;
+    if (e == hipSuccess) {
+        std::vector<uint64_t> ticks((size_t)rounds);
+        e = hipMemcpy(ticks.data(), q.seen, (size_t)rounds * 8, hipMemcpyDeviceToHost);
+        if (e == hipSuccess)
+            e = hipMemcpy(polls, q.polls, (size_t)rounds * 4, hipMemcpyDeviceToHost);
+        for (int r = 0; r < rounds && e == hipSuccess; ++r)
+            seen_us[r] = (double)ticks[(size_t)r] * 1000.0 / (double)khz;
+    }
+    (void)hipFree(devmem);
+    (void)hipHostFree(host);
+    return e != hipSuccess ? (int)e : rc;
 }

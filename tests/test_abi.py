@@ -44,6 +44,25 @@ def test_exports_every_declared_symbol(L):
     assert exported == set(names), exported ^ set(names)
 
 
+def test_measuring_library_exports(L):
+    """bench.py's measuring kernels (stream-mix ceiling, flag handoff) are a
+    library of their own, not part of libxred's interface."""
+    from paper_2510_20171_amd import build
+    lib = build.CEILING_OUT
+    assert lib.exists()
+    out = subprocess.run(["nm", "-D", "--defined-only", str(lib)],
+                         capture_output=True, text=True, check=True).stdout
+    exported = {l.split()[-1] for l in out.splitlines() if " T " in l}
+    assert {"xred_ceiling_mix", "xred_ceiling_handoff"} <= exported, exported
+    C = ctypes.CDLL(str(lib))
+    f = C.xred_ceiling_handoff
+    f.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p,
+                  ctypes.c_void_p, ctypes.c_void_p]
+    # argument checks come before any HIP call (hipErrorInvalidValue = 1)
+    assert f(0, 0, 1000, None, None, None, None) == 1
+    assert f(4, 0, 0, None, None, None, None) == 1
+
+
 @pytest.mark.parametrize("compiler,lang", [("gcc", "c"), ("g++", "c++")])
 def test_header_compiles(tmp_path, compiler, lang):
     src = tmp_path / ("t.c" if lang == "c" else "t.cpp")
