@@ -564,7 +564,12 @@ __global__ __launch_bounds__(kB) void batched_queue_kernel(const xred_item *item
 // Other shapes on the 4096-item log-uniform batch (same box): 512 threads and
 // 8 KiB per source, two per CU, 1199 us; one or three per CU 1462 / 1472 us;
 // 16 KiB tiles one / two per CU 1321 / 1488 us; 1024 threads one per CU
-// 1314 us; 256 threads four per CU, 4 / 8 KiB tiles 1367 / 1489 us.
+// 1314 us; 256 threads four per CU, 4 / 8 KiB tiles 1367 / 1489 us.  The
+// three dependent scalar loads before a tile's loads (table entry, then the
+// descriptor, then the source pointers) also pace the workgroups: staging
+// eight pointer slots per item so that the descriptor and the pointers load
+// together made c4 slower (1241-1254 against 1204 us), like more resident
+// workgroups per CU.
 // Under a CU budget the grid is smaller and each workgroup strides over the
 // table.
 constexpr int kTB = 512;
