@@ -37,7 +37,8 @@
  *     NaN; NaN payloads of SUM/PROD/AVG results are unspecified.
  *
  * Conventions shared by every call:
- *   - All functions are thread-safe, never print and never abort.
+ *   - All functions are thread-safe and never abort; they print nothing
+ *     unless XRED_TRACE is set (below).
  *   - Buffers are device pointers owned by the caller; so is the stream
  *     (a hipStream_t passed as void*, NULL = the default stream).
  *   - Every call is stream-ordered and returns once the work is enqueued.
@@ -60,7 +61,12 @@
  *   XRED_FUSED_WAVES_PER_CU  overrides the fused kernel's resident-wave cap
  *   XRED_RR_WG_PER_CU        workgroups per CU of the round-robin batched kernel
  *   XRED_BATCH_WG_PER_CU     workgroups per CU of host-planned range batches
- * The last three are tuning overrides for measurement; leave them unset.
+ *   XRED_TRACE               anything but "0": one line on stderr per entry
+ *                            point call (its arguments), per kernel launch
+ *                            (kernel, grid, block, LDS bytes, stream, status)
+ *                            and per failed call (status and message)
+ * XRED_FUSED_WAVES_PER_CU, XRED_RR_WG_PER_CU and XRED_BATCH_WG_PER_CU are
+ * tuning overrides for measurement; leave them unset.
  */
 #ifndef XRED_H
 #define XRED_H

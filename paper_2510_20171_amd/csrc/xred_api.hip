@@ -11,6 +11,8 @@
 #include <stdlib.h>
 #include <string.h>
 
+#include <cxxabi.h>
+
 #include <algorithm>
 #include <atomic>
 #include <mutex>
@@ -18,6 +20,38 @@
 #include "xred_internal.hpp"
 
 namespace xred {
+
+bool trace_enabled()
+{
+    static const bool on = [] {
+        const char *v = getenv("XRED_TRACE");
+        return v != nullptr && *v != 0 && strcmp(v, "0") != 0;
+    }();
+    return on;
+}
+
+void trace_printf(const char *fmt, ...)
+{
+    char line[768];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(line, sizeof line, fmt, ap);
+    va_end(ap);
+    fprintf(stderr, "[xred] %s\n", line);
+}
+
+void trace_launch(const void *kernel, dim3 grid, dim3 block, size_t lds, hipStream_t stream,
+                  hipError_t status)
+{
+    const char *raw = hipKernelNameRefByPtr(kernel, stream);
+    int dm = -1;
+    char *name = raw ? abi::__cxa_demangle(raw, nullptr, nullptr, &dm) : nullptr;
+    trace_printf("launch %s grid=%u block=%u lds=%zu stream=%p -> %s",
+                 name ? name : raw ? raw : "?", grid.x, block.x, lds, (void *)stream,
+                 hipGetErrorName(status));
+    free(name);
+}
+
 namespace {
 
 constexpr int kMaxDevices = 64;
@@ -29,6 +63,7 @@ xred_status fail(xred_status s, const char *fmt, ...)
     va_start(ap, fmt);
     vsnprintf(g_err, sizeof g_err, fmt, ap);
     va_end(ap);
+    if (trace_enabled()) trace_printf("failed (status %d): %s", (int)s, g_err);
     return s;
 }
 
@@ -636,6 +671,9 @@ XRED_API xred_status xred_allreduce_local(const void *const *srcs, int nsrc, voi
                                           size_t count, xred_dtype dtype, xred_op op,
                                           void *hip_stream)
 {
+    if (trace_enabled())
+        trace_printf("xred_allreduce_local nsrc=%d count=%zu dtype=%d op=%d stream=%p", nsrc,
+                     count, (int)dtype, (int)op, hip_stream);
     if (nsrc < 1 || nsrc > XRED_MAX_SRC)
         return fail(XRED_INVALID_ARGUMENT, "nsrc = %d outside 1..%d", nsrc, XRED_MAX_SRC);
     xred_status st = check_types(dtype, op);
@@ -660,6 +698,9 @@ XRED_API xred_status xred_reduce_scatter_local(const void *const *srcs, int nsrc
                                                void *dst, size_t recvcount, xred_dtype dtype,
                                                xred_op op, void *hip_stream)
 {
+    if (trace_enabled())
+        trace_printf("xred_reduce_scatter_local nsrc=%d rank=%d recvcount=%zu dtype=%d op=%d "
+                     "stream=%p", nsrc, rank, recvcount, (int)dtype, (int)op, hip_stream);
     if (nsrc < 1 || nsrc > XRED_MAX_SRC)
         return fail(XRED_INVALID_ARGUMENT, "nsrc = %d outside 1..%d", nsrc, XRED_MAX_SRC);
     if (rank < 0 || rank >= nsrc)
@@ -690,6 +731,9 @@ XRED_API xred_status xred_reduce_copy_step(const void *in, void *acc, void *dst,
                                            xred_dtype dtype, xred_op op, unsigned flags,
                                            void *hip_stream)
 {
+    if (trace_enabled())
+        trace_printf("xred_reduce_copy_step count=%zu dtype=%d op=%d flags=%u stream=%p", count,
+                     (int)dtype, (int)op, flags, hip_stream);
     if (flags & ~(unsigned)(XRED_STEP_INIT | XRED_STEP_FINAL))
         return fail(XRED_INVALID_ARGUMENT, "unknown flag bits 0x%x", flags);
     xred_status st = check_types(dtype, op);
@@ -722,6 +766,8 @@ XRED_API xred_status xred_reduce_copy_step(const void *in, void *acc, void *dst,
 XRED_API xred_status xred_acc_cast(const void *acc, void *dst, size_t count, xred_dtype dtype,
                                    void *hip_stream)
 {
+    if (trace_enabled())
+        trace_printf("xred_acc_cast count=%zu dtype=%d stream=%p", count, (int)dtype, hip_stream);
     xred_status st = check_types(dtype, XRED_SUM);
     if (st != XRED_SUCCESS) return st;
     if (count == 0) return XRED_SUCCESS;
@@ -739,6 +785,9 @@ XRED_API xred_status xred_acc_cast(const void *acc, void *dst, size_t count, xre
 XRED_API xred_status xred_batched_reduce(const xred_item *items, int nitems, xred_dtype dtype,
                                          xred_op op, unsigned flags, void *hip_stream)
 {
+    if (trace_enabled())
+        trace_printf("xred_batched_reduce nitems=%d dtype=%d op=%d flags=%u stream=%p", nitems,
+                     (int)dtype, (int)op, flags, hip_stream);
     if (nitems < 0) return fail(XRED_INVALID_ARGUMENT, "nitems = %d", nitems);
     if (flags & ~(unsigned)XRED_ITEMS_ON_DEVICE)
         return fail(XRED_INVALID_ARGUMENT, "unknown flag bits 0x%x", flags);
@@ -761,6 +810,9 @@ XRED_API xred_status xred_batched_reduce(const xred_item *items, int nitems, xre
 XRED_API xred_status xred_batched_reduce_noalloc(const xred_item *items, int nitems,
                                                  xred_dtype dtype, xred_op op, void *hip_stream)
 {
+    if (trace_enabled())
+        trace_printf("xred_batched_reduce_noalloc nitems=%d dtype=%d op=%d stream=%p", nitems,
+                     (int)dtype, (int)op, hip_stream);
     if (nitems < 0) return fail(XRED_INVALID_ARGUMENT, "nitems = %d", nitems);
     xred_status st = check_types(dtype, op);
     if (st != XRED_SUCCESS) return st;
@@ -787,6 +839,9 @@ XRED_API xred_status xred_ring_reduce(const void *const *chunks, int nchunks, vo
                                       const uint32_t *ready, uint32_t epoch, uint64_t timeout_us,
                                       uint32_t *status, void *hip_stream)
 {
+    if (trace_enabled())
+        trace_printf("xred_ring_reduce nchunks=%d count=%zu dtype=%d op=%d flags=%s stream=%p",
+                     nchunks, count, (int)dtype, (int)op, ready ? "yes" : "no", hip_stream);
     if (nchunks < 1 || nchunks > XRED_MAX_SRC)
         return fail(XRED_INVALID_ARGUMENT, "nchunks = %d outside 1..%d", nchunks, XRED_MAX_SRC);
     xred_status st = check_types(dtype, op);
@@ -831,6 +886,9 @@ XRED_API xred_status xred_allreduce_sim(const void *const *sendbufs, void *const
                                         int nranks, size_t count, xred_dtype dtype, xred_op op,
                                         xred_schedule schedule, void *hip_stream)
 {
+    if (trace_enabled())
+        trace_printf("xred_allreduce_sim nranks=%d count=%zu dtype=%d op=%d schedule=%d "
+                     "stream=%p", nranks, count, (int)dtype, (int)op, (int)schedule, hip_stream);
     if (nranks < 1 || nranks > XRED_MAX_SRC)
         return fail(XRED_INVALID_ARGUMENT, "nranks = %d outside 1..%d", nranks, XRED_MAX_SRC);
     if (schedule < XRED_SCHEDULE_RING || schedule > XRED_SCHEDULE_RHD_ONE_LAUNCH)

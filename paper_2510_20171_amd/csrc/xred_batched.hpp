@@ -822,9 +822,8 @@ hipError_t go_grouped(const xred_item *d_items, int nitems, uint32_t ngroups, ui
 {
     size_t lds = (size_t)(lds_per_cu() / wgs_per_cu) / 512 * 512 - 512;
     if (lds < kGrpLdsBytes) lds = kGrpLdsBytes;
-    hipLaunchKernelGGL((batched_grouped_kernel<T, Op>), dim3(grid), dim3(kTB), lds, s, d_items,
-                       nitems, ngroups, m);
-    return hipGetLastError();
+    return launch_kernel(batched_grouped_kernel<T, Op>, dim3(grid), dim3(kTB), lds, s, d_items,
+                         nitems, ngroups, m);
 }
 
 // Grouped launcher for the element types Ts.
@@ -902,20 +901,17 @@ hipError_t go_rr(bool planned, const xred_item *d_items, int nitems, const uint3
     const int per_cu = planned ? rr_per_cu<T, Op, true>(steps) : rr_per_cu<T, Op, false>(steps);
     const unsigned grid = batched_rr_grid(per_cu);
     if (planned)
-        hipLaunchKernelGGL((batched_rr_kernel<T, Op, true>), dim3(grid), dim3(kB), lds, s,
-                           d_items, nitems, d_tile_start);
-    else
-        hipLaunchKernelGGL((batched_rr_kernel<T, Op, false>), dim3(grid), dim3(kB), lds, s,
-                           d_items, nitems, d_tile_start);
-    return hipGetLastError();
+        return launch_kernel(batched_rr_kernel<T, Op, true>, dim3(grid), dim3(kB), lds, s,
+                             d_items, nitems, d_tile_start);
+    return launch_kernel(batched_rr_kernel<T, Op, false>, dim3(grid), dim3(kB), lds, s, d_items,
+                         nitems, d_tile_start);
 }
 
 template <class T, class Op>
 hipError_t go(const xred_item *d_items, int nitems, const WgStart *d_wg, unsigned grid,
               hipStream_t s)
 {
-    hipLaunchKernelGGL((batched_kernel<T, Op>), dim3(grid), dim3(kB), 0, s, d_items, nitems, d_wg);
-    return hipGetLastError();
+    return launch_kernel(batched_kernel<T, Op>, dim3(grid), dim3(kB), 0, s, d_items, nitems, d_wg);
 }
 
 // Range-walking launcher for the element types Ts.

@@ -14,6 +14,16 @@
 
 namespace xred {
 
+// Launch trace: with XRED_TRACE set to anything but "0" in the environment
+// (read once per process) every entry point logs its arguments, every kernel
+// launch its kernel, grid, block, LDS bytes, stream and status, and every
+// failed call its message, one line each on stderr.  Off, a call costs one
+// predictable branch per launch.
+bool trace_enabled();
+void trace_printf(const char *fmt, ...) __attribute__((format(printf, 1, 2)));
+void trace_launch(const void *kernel, dim3 grid, dim3 block, size_t lds, hipStream_t stream,
+                  hipError_t status);
+
 // Enqueue kernel<<<grid, block, lds, stream>>>(args...) and return the launch
 // status.  hipLaunchKernel takes one pointer per argument; each argument is
 // first converted to the kernel's own parameter type.  (The <<<>>> form makes
@@ -25,7 +35,9 @@ hipError_t launch_kernel_impl(void (*kernel)(P...), dim3 grid, dim3 block, size_
 {
     std::tuple<P...> packed(std::forward<A>(args)...);
     void *ptrs[sizeof...(P) > 0 ? sizeof...(P) : 1] = {(void *)&std::get<I>(packed)...};
-    return hipLaunchKernel((const void *)kernel, grid, block, ptrs, lds, stream);
+    const hipError_t e = hipLaunchKernel((const void *)kernel, grid, block, ptrs, lds, stream);
+    if (trace_enabled()) trace_launch((const void *)kernel, grid, block, lds, stream, e);
+    return e;
 }
 
 template <class... P, class... A>

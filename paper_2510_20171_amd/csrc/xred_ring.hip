@@ -339,10 +339,10 @@ hipError_t go(const char *const *chunks, int nchunks, char *dst, size_t count,
     // of a fresh slot
     const Relay relay = relayed ? Relay{slot.words, (uint32_t)(slot.launches % 0xFFFFFFu) + 1}
                                 : Relay{nullptr, 0};
-    hipLaunchKernelGGL((ring_kernel<T, Op>), dim3((unsigned)(grid + (relayed ? 1 : 0))), dim3(kB),
-                       lds_tile_bytes<T>() * (tpw > 0 ? tpw : 1), s, ks, nchunks, dst, nvec, tail,
-                       tpw, ready, epoch, timeout, status, relay);
-    const hipError_t e = hipGetLastError();
+    const hipError_t e =
+        launch_kernel(ring_kernel<T, Op>, dim3((unsigned)(grid + (relayed ? 1 : 0))), dim3(kB),
+                      lds_tile_bytes<T>() * (tpw > 0 ? tpw : 1), s, ks, nchunks, dst, nvec, tail,
+                      tpw, ready, epoch, timeout, status, relay);
     if (relayed && e == hipSuccess) slot.commit();
     return e;
 }

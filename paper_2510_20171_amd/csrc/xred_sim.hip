@@ -135,14 +135,12 @@ hipError_t launch_sim_step(const SimStep &a, int G, bool vec, hipStream_t s)
     if (vec) {
         constexpr uint64_t kTileElems = (uint64_t)kB * kU * T::kVec;
         tiles = (maxlen / T::kVec * T::kVec + kTileElems - 1) / kTileElems + 1;   // + tail tile
-        hipLaunchKernelGGL((sim_step_vec_kernel<T, Op, COPY>), dim3(grid_for(tiles * G)),
-                           dim3(kB), 0, s, a, G, tiles);
-    } else {
-        tiles = (maxlen + kB - 1) / kB;
-        hipLaunchKernelGGL((sim_step_scalar_kernel<T, Op, COPY>), dim3(grid_for(tiles * G)),
-                           dim3(kB), 0, s, a, G, tiles);
+        return launch_kernel(sim_step_vec_kernel<T, Op, COPY>, dim3(grid_for(tiles * G)),
+                             dim3(kB), 0, s, a, G, tiles);
     }
-    return hipGetLastError();
+    tiles = (maxlen + kB - 1) / kB;
+    return launch_kernel(sim_step_scalar_kernel<T, Op, COPY>, dim3(grid_for(tiles * G)), dim3(kB),
+                         0, s, a, G, tiles);
 }
 
 // ------------------------------------------------------------ one launch --
@@ -345,18 +343,16 @@ hipError_t launch_all(const char *const *send, char *const *recv, int G, size_t 
     // 495 us capped).
     const size_t lds = rhd ? 0 : (size_t)(lds_per_cu() / (kRingWavesPerCu / (kB / 64))) / 512 * 512;
     if (rhd && vec)
-        hipLaunchKernelGGL((sim_all_kernel<T, Op, true, true>), grid, dim3(kB), lds, s, a, G, lg, M,
-                           (uint64_t)count, tiles);
-    else if (rhd)
-        hipLaunchKernelGGL((sim_all_kernel<T, Op, true, false>), grid, dim3(kB), lds, s, a, G, lg, M,
-                           (uint64_t)count, tiles);
-    else if (vec)
-        hipLaunchKernelGGL((sim_all_kernel<T, Op, false, true>), grid, dim3(kB), lds, s, a, G, lg, M,
-                           (uint64_t)count, tiles);
-    else
-        hipLaunchKernelGGL((sim_all_kernel<T, Op, false, false>), grid, dim3(kB), lds, s, a, G, lg,
-                           M, (uint64_t)count, tiles);
-    return hipGetLastError();
+        return launch_kernel(sim_all_kernel<T, Op, true, true>, grid, dim3(kB), lds, s, a, G, lg,
+                             M, (uint64_t)count, tiles);
+    if (rhd)
+        return launch_kernel(sim_all_kernel<T, Op, true, false>, grid, dim3(kB), lds, s, a, G, lg,
+                             M, (uint64_t)count, tiles);
+    if (vec)
+        return launch_kernel(sim_all_kernel<T, Op, false, true>, grid, dim3(kB), lds, s, a, G, lg,
+                             M, (uint64_t)count, tiles);
+    return launch_kernel(sim_all_kernel<T, Op, false, false>, grid, dim3(kB), lds, s, a, G, lg, M,
+                         (uint64_t)count, tiles);
 }
 
 int rank_mod(int r, int G) { return ((r % G) + G) % G; }

@@ -34,14 +34,12 @@ hipError_t go(const char *in, char *acc, char *dst, size_t count, hipStream_t s)
         const size_t tail = count % T::kVec;
         constexpr size_t kTile = (size_t)kB * kU;
         const uint64_t tiles = (nvec + kTile - 1) / kTile + (tail ? 1 : 0);
-        hipLaunchKernelGGL((step_kernel<T, Op, FLAGS, kU, kB, true>), dim3(grid_for(tiles)),
-                           dim3(kB), 0, s, in, acc, dst, nvec, tail);
-    } else {
-        hipLaunchKernelGGL((step_kernel<T, Op, FLAGS, kU, kB, false>),
-                           dim3(grid_for((count + kB - 1) / kB)), dim3(kB), 0, s, in, acc, dst,
-                           (size_t)0, count);
+        return launch_kernel(step_kernel<T, Op, FLAGS, kU, kB, true>, dim3(grid_for(tiles)),
+                             dim3(kB), 0, s, in, acc, dst, nvec, tail);
     }
-    return hipGetLastError();
+    return launch_kernel(step_kernel<T, Op, FLAGS, kU, kB, false>,
+                         dim3(grid_for((count + kB - 1) / kB)), dim3(kB), 0, s, in, acc, dst,
+                         (size_t)0, count);
 }
 
 template <class T, class Op>
@@ -64,14 +62,11 @@ hipError_t go_cast(const char *acc, char *dst, size_t count, hipStream_t s)
         const size_t tail = count % T::kVec;
         constexpr size_t kTile = (size_t)kB * kU;
         const uint64_t tiles = (nvec + kTile - 1) / kTile + (tail ? 1 : 0);
-        hipLaunchKernelGGL((acc_cast_kernel<T, kU, kB, true>), dim3(grid_for(tiles)), dim3(kB), 0,
-                           s, acc, dst, nvec, tail);
-    } else {
-        hipLaunchKernelGGL((acc_cast_kernel<T, kU, kB, false>),
-                           dim3(grid_for((count + kB - 1) / kB)), dim3(kB), 0, s, acc, dst,
-                           (size_t)0, count);
+        return launch_kernel(acc_cast_kernel<T, kU, kB, true>, dim3(grid_for(tiles)), dim3(kB),
+                             0, s, acc, dst, nvec, tail);
     }
-    return hipGetLastError();
+    return launch_kernel(acc_cast_kernel<T, kU, kB, false>, dim3(grid_for((count + kB - 1) / kB)),
+                         dim3(kB), 0, s, acc, dst, (size_t)0, count);
 }
 
 }  // namespace
