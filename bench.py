@@ -245,9 +245,10 @@ def cpu_model() -> str:
     return "unknown"
 
 
-def secondary(torch, xr, L, timer, wl, flush):
+def secondary(torch, xr, L, timer, wl, flush, res):
+    """The figures besides the headline, filled into `res` as they are taken
+    (so a failure part-way keeps the ones already measured)."""
     import numpy as np
-    res = {}
     # copy ceiling (torch's device copy kernel), 1 GiB -> 1 GiB
     a = torch.empty(1 << 29, dtype=torch.int16, device="cuda")
     b = torch.empty_like(a)
@@ -992,7 +993,12 @@ def main() -> int:
     if not args.no_secondary and args.workload == "c2":
         log("secondary workloads")
         flush = torch.empty(1 << 28, dtype=torch.float32, device="cuda")
-        result["secondary"] = secondary(torch, xr, L, timer, wl, flush)
+        result["secondary"] = {}
+        try:
+            secondary(torch, xr, L, timer, wl, flush, result["secondary"])
+        except Exception as e:   # a failed extra figure must not cost the headline line
+            result["secondary"]["error"] = f"{type(e).__name__}: {e}"
+            log(f"secondary figures stopped: {type(e).__name__}: {e}")
     print(json.dumps(result), flush=True)
     return 0
 
