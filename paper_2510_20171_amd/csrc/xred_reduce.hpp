@@ -13,13 +13,21 @@
 namespace xred {
 namespace {
 
-// Two tile shapes, both one 16-byte vector per thread:
+// Three tile shapes:
 //
 // * Launches that fit on the chip in one round (every tile resident at
-//   once) are latency-bound: they use 512-thread workgroups, uncapped, so
-//   the whole message is in flight after the fewest workgroup dispatches
-//   (8 MiB per source at P=8 bf16: 10.1 us against 10.8 us with 128-thread
-//   workgroups, same process and buffers).
+//   once) are latency-bound: they use 512-thread workgroups of one 16-byte
+//   vector per thread, uncapped, so the whole message is in flight after the
+//   fewest workgroup dispatches (8 MiB per source at P=8 bf16: 10.1 us
+//   against 10.8 us with 128-thread workgroups, same process and buffers).
+// * Up to 8 sources, launches that fit in one round with two vectors per
+//   thread (bf16: 8-16 MiB per source) use that shape too, still uncapped:
+//   one round of dispatches instead of several rounds of 128-thread
+//   workgroups (P=8 bf16, back to back / cold: 12 MiB 15.6 / 21.1 us against
+//   17.4 / 22.4; 16 MiB 21.9 / 27.2 against 25.1 / 30.2; P=4 fp32 16 MiB
+//   11.1 against 12.1 us; from 20 MiB on the 128-thread shape is as fast).
+//   Three, four, six or eight vectors per thread at 20-64 MiB gained at most
+//   a few percent and lost 6 % on P=8 fp32 at 32 MiB, so they are not used.
 // * Larger launches are bandwidth-bound: 128-thread workgroups with a
 //   bounded number of waves per CU.  HBM3E on MI355X delivers the most when
 //   a CU keeps a moderate number of loads in flight; more waves than that
@@ -41,6 +49,7 @@ constexpr int kU = 1;          // 16-byte vectors per thread per tile
 constexpr int kB = 128;        // threads per workgroup, bandwidth-bound launches
 constexpr int kBWide = 512;    // threads per workgroup, one-round launches
 constexpr int kWideWgsPerCu = 4;   // resident 512-thread workgroups per CU
+constexpr int kUWide2 = 2;         // vectors per thread of the second one-round shape (NP <= 8)
 
 // Waves per CU for a compile-time source count (0: runtime count); 0 = no cap.
 template <int NP>
@@ -85,10 +94,19 @@ hipError_t go_vec(const char *const *srcs, int nsrc, char *dst, size_t count, hi
     const uint32_t tail = (uint32_t)(count % T::kVec);
     constexpr size_t kTileWide = (size_t)kBWide * kU;
     const uint64_t tiles_wide = (nvec + kTileWide - 1) / kTileWide + (tail ? 1 : 0);
-    if (tiles_wide <= (uint64_t)device_cus() * kWideWgsPerCu)
+    const uint64_t one_round = (uint64_t)device_cus() * kWideWgsPerCu;
+    if (tiles_wide <= one_round)
         return launch_kernel(reduce_vec_kernel<T, Op, NP, MAXP, kU, kBWide>,
                              dim3(grid_for(tiles_wide)), dim3(kBWide), 0, s, ks, nsrc, dst, nvec,
                              tail);
+    if constexpr (NP >= 1 && NP <= 8) {
+        constexpr size_t kTileWide2 = (size_t)kBWide * kUWide2;
+        const uint64_t tiles_wide2 = (nvec + kTileWide2 - 1) / kTileWide2 + (tail ? 1 : 0);
+        if (tiles_wide2 <= one_round)
+            return launch_kernel(reduce_vec_kernel<T, Op, NP, MAXP, kUWide2, kBWide>,
+                                 dim3(grid_for(tiles_wide2)), dim3(kBWide), 0, s, ks, nsrc, dst,
+                                 nvec, tail);
+    }
     constexpr size_t kTile = (size_t)kB * kU;
     const uint64_t tiles = (nvec + kTile - 1) / kTile + (tail ? 1 : 0);
     return launch_kernel(reduce_vec_kernel<T, Op, NP, MAXP, kU, kB>, dim3(grid_for(tiles)),

@@ -210,21 +210,23 @@ def test_edge_matrix(xr, orc, dtype, op):
 
 @pytest.mark.parametrize("dtype,op", [("bf16", "sum"), ("f32", "max"), ("i32", "sum")])
 def test_tile_shapes_at_one_round_threshold(xr, orc, dtype, op):
-    """The fused launcher uses 512-thread tiles while every tile fits on the
-    chip in one round (4 per CU) and occupancy-capped 128-thread tiles above;
-    sizes just below and above the switch, with ragged tails, on compile-time
-    and runtime source counts."""
+    """The fused launcher uses 512-thread tiles of one vector per thread while
+    every tile fits on the chip in one round (4 per CU), then (up to 8
+    sources) 512-thread tiles of two vectors per thread while those fit in one
+    round, and occupancy-capped 128-thread tiles above; sizes at and around
+    both switches, with ragged tails, on compile-time and runtime source
+    counts."""
     cus = torch.cuda.get_device_properties(0).multi_processor_count
     vec = 16 // (2 if dtype == "bf16" else 4)
-    edge = cus * 4 * 512 * vec               # elements at the switch
+    edge = cus * 4 * 512 * vec               # elements at the first switch
     rng = np.random.default_rng(77 + DTYPES.index(dtype))
-    nmax = edge + 128 * vec * 3 + 1
+    nmax = 2 * edge + 128 * vec * 3 + 1
     # random columns (specials included) repeated with an odd period, so no
     # misplaced tile or vector lines up with an equal value
     full = [np.resize(pins.random_column_values(rng, dtype, 65536 + 13 + 2 * p), nmax)
             for p in range(32)]
     for P in (3, 8, 12, 32):
-        for n in (edge - 3, edge + 5, nmax):
+        for n in (edge - 3, edge + 5, 2 * edge, 2 * edge + 5, nmax):
             srcs = [f[:n] for f in full[:P]]
             got = _run_allreduce(xr, srcs, dtype, op)
             exp = orc.allreduce_local(srcs, dtype, op, nthreads=CORES)
