@@ -100,12 +100,13 @@ xred_status check_types(xred_dtype dtype, xred_op op)
 }
 
 // A buffer of `bytes` at p: non-NULL, aligned to `align`, no address wrap.
+// align: a power of two (an element or accumulator size)
 xred_status check_buf(const void *p, size_t bytes, size_t align, const char *name, int index)
 {
     const uintptr_t a = (uintptr_t)p;
     if (p == nullptr) return fail(XRED_INVALID_ARGUMENT, "%s[%d] is NULL", name, index);
-    if (a % align) return fail(XRED_INVALID_ARGUMENT, "%s[%d] is not %zu-byte aligned", name,
-                               index, align);
+    if (a & (align - 1)) return fail(XRED_INVALID_ARGUMENT, "%s[%d] is not %zu-byte aligned", name,
+                                     index, align);
     if (a + bytes < a) return fail(XRED_INVALID_ARGUMENT, "%s[%d] range wraps the address space",
                                    name, index);
     return XRED_SUCCESS;
@@ -120,7 +121,11 @@ bool bad_overlap(const void *a, size_t na, const void *b, size_t nb, bool exact_
     return x < y + nb && y < x + na;
 }
 
-bool mul_overflows(size_t a, size_t b) { return b != 0 && a > SIZE_MAX / b; }
+bool mul_overflows(size_t a, size_t b)
+{
+    size_t r;
+    return __builtin_mul_overflow(a, b, &r);
+}
 
 int cached_cus[kMaxDevices];
 int cached_lds[kMaxDevices];
@@ -181,6 +186,14 @@ xred_status batched_host(const xred_item *items, int nitems, xred_dtype dtype, x
     const size_t es = elem_size(dtype);
     const uint64_t te = batched_tile_elems(dtype);
     const uint64_t tt = batched_table_tile_elems(dtype);
+    // both are powers of two: tile counts by shifts, not divisions (the
+    // plan of a 4096-item batch divides per item several times)
+    if (te == 0 || (te & (te - 1)) != 0 || tt == 0 || (tt & (tt - 1)) != 0)
+        return fail(XRED_UNSUPPORTED, "batched tile sizes %llu / %llu are not powers of two",
+                    (unsigned long long)te, (unsigned long long)tt);
+    const int te_log = __builtin_ctzll(te), tt_log = __builtin_ctzll(tt);
+    auto tiles_te = [te_log](uint64_t n) { return (n >> te_log) + ((n & ((1ull << te_log) - 1)) != 0); };
+    auto tiles_tt = [tt_log](uint64_t n) { return (n >> tt_log) + ((n & ((1ull << tt_log) - 1)) != 0); };
     uint64_t total_tiles = 0, table_tiles = 0, total_ptrs = 0;
     for (int k = 0; k < nitems; ++k) {
         const xred_item &it = items[k];
@@ -201,8 +214,8 @@ xred_status batched_host(const xred_item *items, int nitems, xred_dtype dtype, x
             if (bad_overlap(it.dst, bytes, it.srcs[p], bytes, true))
                 return fail(XRED_ALIAS, "items[%d].dst partially overlaps source %u", k, p);
         }
-        total_tiles += (it.count + te - 1) / te;
-        table_tiles += (it.count + tt - 1) / tt;
+        total_tiles += tiles_te(it.count);
+        table_tiles += tiles_tt(it.count);
         total_ptrs += it.nsrc;
     }
     if (total_tiles == 0) return XRED_SUCCESS;
@@ -317,7 +330,7 @@ xred_status batched_host(const xred_item *items, int nitems, xred_dtype dtype, x
         uint16_t *h_tab = (uint16_t *)(h + items_bytes);
         uint32_t w = 0;
         for (int k = 0; k < nitems; ++k) {
-            const uint32_t nt = (uint32_t)((items[k].count + tt - 1) / tt);
+            const uint32_t nt = (uint32_t)tiles_tt(items[k].count);
             h_items[k].reserved = w;
             for (uint32_t t = 0; t < nt; ++t) h_tab[w++] = (uint16_t)k;
         }
@@ -326,7 +339,7 @@ xred_status batched_host(const xred_item *items, int nitems, xred_dtype dtype, x
         uint32_t *h_tab = (uint32_t *)(h + items_bytes);
         uint32_t w = 0;
         for (int k = 0; k < nitems; ++k) {
-            const uint32_t nt = (uint32_t)((items[k].count + tt - 1) / tt);
+            const uint32_t nt = (uint32_t)tiles_tt(items[k].count);
             h_items[k].reserved = w;
             for (uint32_t t = 0; t < nt; ++t) h_tab[w++] = (uint32_t)k;
         }
@@ -335,7 +348,7 @@ xred_status batched_host(const xred_item *items, int nitems, xred_dtype dtype, x
         uint64_t acc = 0;
         for (int k = 0; k < nitems; ++k) {
             h_pre[k] = (uint32_t)acc;
-            acc += (items[k].count + te - 1) / te;
+            acc += tiles_te(items[k].count);
         }
         h_pre[nitems] = (uint32_t)acc;
     } else {
@@ -346,7 +359,7 @@ xred_status batched_host(const xred_item *items, int nitems, xred_dtype dtype, x
             const uint64_t g0 = (uint64_t)((unsigned __int128)total_tiles * b / grid);
             const uint64_t g1 = (uint64_t)((unsigned __int128)total_tiles * (b + 1) / grid);
             for (;;) {
-                const uint64_t nt = (items[k].count + te - 1) / te;
+                const uint64_t nt = tiles_te(items[k].count);
                 if (g0 < k_first + nt) break;
                 k_first += nt;
                 ++k;
