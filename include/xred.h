@@ -55,6 +55,11 @@
  *     next synchronisation of the stream, as for any HIP kernel.
  *   - Element pointers must be aligned to the element size; 16-byte aligned
  *     buffers take the fast vector path, other alignments a slower scalar one.
+ *   - Device words the library binds to a stream (the ring's relay word, the
+ *     batch queue's counters) are looked up by the stream's handle.  Let a
+ *     stream's work finish before destroying it if a stream created later
+ *     may be handed the same handle while that work would still be running:
+ *     the two would share the words.
  *
  * Environment (read once, when first needed; results never depend on them):
  *   XRED_MAX_WORKGROUPS      initial CU budget (see xred_set_max_workgroups)
