@@ -13,7 +13,8 @@
 // Chunk s is read only after ready[s] has reached `epoch` (serial-number
 // comparison, so a producer may run ahead).  Reading host memory is what
 // costs: every wave polling pinned host flags from hundreds of workgroups at
-// once took 8-15 us per poll on MI355X, against about 2 us for one wave.  So a
+// once took 8-15 us per poll on MI355X, against 0.8-1.1 us for one lane
+// alone (a flag the host writes reaches such a lane 0.8-0.9 us later).  So a
 // flagged launch has one extra workgroup (blockIdx 0) whose first wave alone
 // polls the flags, 64 at a time (one lane per flag), and publishes the number
 // of consecutive ready chunks in a relay word in device memory; the tile
