@@ -210,7 +210,7 @@ __global__ __launch_bounds__(64) void pingpong_kernel(PingPong q, uint32_t round
 // lane answers, 1 = it relays through device memory to a second workgroup.
 // Outputs per round (arrays of `rounds`): the host's round trip in us, the
 // polling lane's loads of the flag and its device time from the start of the
-// round to seeing the flag, in us.  Round 1 includes the launch.  Returns 0,
+// round to seeing the flag, in us.  The first round includes the launch.  Returns 0,
 // a hipError_t, or -1 if a wait on either side gave up (every wait is
 // bounded by limit_ms, so the kernel has always ended when this returns).
 extern "C" __attribute__((visibility("default"))) int
