@@ -12,11 +12,12 @@ follows the definition in the C file's header: a left fold in source order
 (the per-rank reduce of the FTAR ring, Section 5, and the ReduceScatter /
 AllReduce semantics of Section 2.2).
 
-Element arrays are numpy arrays: float32 for ``f32``, uint16 bit patterns for
-``bf16`` and ``f16``, uint8 bit patterns for ``e4m3`` and ``e5m2``, int32 /
-uint32 / int64 / uint64 for the integer types.  Step-wise accumulators are
-float32 arrays for float dtypes, uint32 for 32-bit and uint64 for 64-bit
-integer dtypes.
+Element arrays are numpy arrays: float32 for ``f32``, float64 for ``f64``,
+uint16 bit patterns for ``bf16`` and ``f16``, uint8 bit patterns for ``e4m3``
+and ``e5m2``, int8 / uint8 / int32 / uint32 / int64 / uint64 for the integer
+types.  Step-wise accumulators are float32 arrays for the binary32-accumulated
+float dtypes, float64 for ``f64``, uint32 for 8- and 32-bit and uint64 for
+64-bit integer dtypes.
 """
 from __future__ import annotations
 
@@ -40,11 +41,12 @@ CFLAGS = [
 
 DTYPES = {"f32": (10, np.float32), "bf16": (11, np.uint16), "f16": (12, np.uint16),
           "i32": (13, np.int32), "u32": (14, np.uint32), "i64": (15, np.int64),
-          "u64": (16, np.uint64), "e4m3": (17, np.uint8), "e5m2": (18, np.uint8)}
+          "u64": (16, np.uint64), "e4m3": (17, np.uint8), "e5m2": (18, np.uint8),
+          "f64": (30, np.float64), "i8": (31, np.int8), "u8": (32, np.uint8)}
 OPS = {"sum": 20, "prod": 21, "max": 22, "min": 23, "avg": 24}
 ACC_NP = {"f32": np.float32, "bf16": np.float32, "f16": np.float32, "e4m3": np.float32,
           "e5m2": np.float32, "i32": np.uint32, "u32": np.uint32, "i64": np.uint64,
-          "u64": np.uint64}
+          "u64": np.uint64, "f64": np.float64, "i8": np.uint32, "u8": np.uint32}
 _INIT, _FINAL = 1, 2
 
 

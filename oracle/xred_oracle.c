@@ -16,24 +16,30 @@
  * for every element index i independently, where fold is a LEFT fold in
  * source order 0..P-1 (the paper never states an order; a fixed rank order is
  * the reading taken), up() converts an input element to the accumulator type
- * (binary32 for bf16/fp16/fp8/fp32, uint32 for int32/uint32, uint64 for
- * int64/uint64: the paper names no accumulator type), and down() converts
- * back with round-to-nearest-even.  AVG (float types) is the SUM fold
- * followed by one binary32 division by P.
+ * (binary32 for bf16/fp16/fp8/fp32, binary64 for fp64, uint32 for
+ * int8/uint8/int32/uint32 -- int8 sign-extended, uint8 zero-extended --,
+ * uint64 for int64/uint64: the paper names no accumulator type), and down()
+ * converts back with round-to-nearest-even (for the integer types: keeps the
+ * low bits).  AVG (float types) is the SUM fold followed by one division by P
+ * in the accumulator's format.
  *
- * Arithmetic is carried out in binary32 because the definition being checked
- * is binary32 accumulation; this file is compiled with -ffp-contract=off and
- * without fast-math so that every float operation is one IEEE binary32
- * operation with round-to-nearest-even, subnormals preserved.
+ * Arithmetic is carried out in binary32 (binary64 for fp64) because the
+ * definition being checked is accumulation in that format; this file is
+ * compiled with -ffp-contract=off and without fast-math so that every float
+ * operation is one IEEE operation with round-to-nearest-even, subnormals
+ * preserved.
  *
  * Readings of points the paper leaves open (each is repeated in the design
  * notes):
  *   - the accumulator starts from up(src[0][i]), never from 0, so a column of
  *     -0.0 sums to -0.0;
  *   - MAX/MIN use the total order -inf < ... < -0 < +0 < ... < +inf; a NaN
- *     among the reduced values gives the canonical quiet NaN 0x7FC00000,
- *     whatever their number (also for a single source and for the INIT step
- *     of the step-wise mode);
+ *     among the reduced values gives the canonical quiet NaN 0x7FC00000
+ *     (0x7FF8000000000000 for fp64), whatever their number (also for a single
+ *     source and for the INIT step of the step-wise mode);
+ *   - int8 / uint8 sum and product wrap modulo 2^8 (the uint32 accumulator's
+ *     low byte: wrapping modulo 2^32 first changes nothing), max / min
+ *     compare signed (int8) or unsigned (uint8);
  *   - NaN payloads of SUM/PROD/AVG are not specified ("parity unpinned" for
  *     NaN payloads: tests compare NaN-ness only);
  *   - down() of a NaN keeps the sign and gives the I/O type's quiet NaN
@@ -63,7 +69,7 @@
 
 /* The oracle's own codes; the Python loader maps dtype/op names onto them. */
 enum { XO_F32 = 10, XO_BF16 = 11, XO_F16 = 12, XO_I32 = 13, XO_U32 = 14, XO_I64 = 15,
-       XO_U64 = 16, XO_E4M3 = 17, XO_E5M2 = 18 };
+       XO_U64 = 16, XO_E4M3 = 17, XO_E5M2 = 18, XO_F64 = 30, XO_I8 = 31, XO_U8 = 32 };
 enum { XO_SUM = 20, XO_PROD = 21, XO_MAX = 22, XO_MIN = 23, XO_AVG = 24 };
 enum { XO_INIT = 1u, XO_FINAL = 2u };
 enum { XO_OK = 0, XO_BAD = -1 };
@@ -81,13 +87,16 @@ static int is_float_type(int dtype)
 
 static int is_int64_type(int dtype) { return dtype == XO_I64 || dtype == XO_U64; }
 
+static int is_int8_type(int dtype) { return dtype == XO_I8 || dtype == XO_U8; }
+
 static size_t elem_size(int dtype)
 {
     switch (dtype) {
     case XO_F32: case XO_I32: case XO_U32: return 4;
     case XO_BF16: case XO_F16: return 2;
     case XO_E4M3: case XO_E5M2: return 1;
-    case XO_I64: case XO_U64: return 8;
+    case XO_I64: case XO_U64: case XO_F64: return 8;
+    case XO_I8: case XO_U8: return 1;
     default: return 0;
     }
 }
@@ -311,18 +320,20 @@ static float op_float(int op, float a, float b)
     }
 }
 
-/* Integer ops: sum and product wrap modulo 2^32; max/min compare as signed
- * int32 for XO_I32 and as unsigned for XO_U32. */
+/* Integer ops on uint32 accumulators: sum and product wrap modulo 2^32;
+ * max/min compare as signed int32 for XO_I32 and XO_I8 (whose values are
+ * sign-extended) and as unsigned otherwise. */
 static uint32_t op_int(int op, int dtype, uint32_t a, uint32_t b)
 {
+    const int sgn = dtype == XO_I32 || dtype == XO_I8;
     switch (op) {
     case XO_SUM: return a + b;
     case XO_PROD: return a * b;
     case XO_MAX:
-        if (dtype == XO_I32) return ((int32_t)a > (int32_t)b) ? a : b;
+        if (sgn) return ((int32_t)a > (int32_t)b) ? a : b;
         return a > b ? a : b;
     default:
-        if (dtype == XO_I32) return ((int32_t)a < (int32_t)b) ? a : b;
+        if (sgn) return ((int32_t)a < (int32_t)b) ? a : b;
         return a < b ? a : b;
     }
 }
@@ -342,6 +353,64 @@ static uint64_t op_int64(int op, int dtype, uint64_t a, uint64_t b)
     }
 }
 
+/* ------------------------------------------------------------ binary64 --- */
+
+static double u2d(uint64_t u) { double d; memcpy(&d, &u, 8); return d; }
+static double canonical_nan64(void) { return u2d(0x7FF8000000000000ull); }
+
+static double max_total64(double a, double b)
+{
+    if (isnan(a) || isnan(b)) return canonical_nan64();
+    if (a > b) return a;
+    if (b > a) return b;
+    return signbit(a) ? b : a;
+}
+
+static double min_total64(double a, double b)
+{
+    if (isnan(a) || isnan(b)) return canonical_nan64();
+    if (a < b) return a;
+    if (b < a) return b;
+    return signbit(a) ? a : b;
+}
+
+static double op_f64(int op, double a, double b)
+{
+    switch (op) {
+    case XO_SUM: return a + b;
+    case XO_PROD: return a * b;
+    case XO_MAX: return max_total64(a, b);
+    default: return min_total64(a, b);
+    }
+}
+
+static double settle64(int op, double v)
+{
+    if ((op == XO_MAX || op == XO_MIN) && isnan(v)) return canonical_nan64();
+    return v;
+}
+
+static double up_f64(const void *base, uint64_t i)
+{
+    double d;
+    memcpy(&d, (const char *)base + 8 * i, 8);
+    return d;
+}
+
+static void down_f64(void *base, uint64_t i, double v) { memcpy((char *)base + 8 * i, &v, 8); }
+
+/* ------------------------------------------------------- int8 / uint8 --- */
+
+/* Widened to uint32: int8 sign-extended, uint8 zero-extended. */
+static uint32_t up_int8(const void *base, uint64_t i, int dtype)
+{
+    const uint8_t b = ((const uint8_t *)base)[i];
+    return dtype == XO_I8 ? (uint32_t)(int32_t)(int8_t)b : (uint32_t)b;
+}
+
+/* The low byte of the accumulator. */
+static void down_int8(void *base, uint64_t i, uint32_t v) { ((uint8_t *)base)[i] = (uint8_t)v; }
+
 /* MAX/MIN results: a NaN anywhere among the reduced values is reported as the
  * canonical quiet NaN, also when no binary operation was applied (P = 1). */
 static float settle(int op, float v)
@@ -355,17 +424,30 @@ static int valid_op(int op) { return op >= XO_SUM && op <= XO_AVG; }
 /* AVG is defined for float types only. */
 static int valid_pair(int dtype, int op)
 {
-    return valid_dtype(dtype) && valid_op(op) && (op != XO_AVG || is_float_type(dtype));
+    return valid_dtype(dtype) && valid_op(op) &&
+           (op != XO_AVG || is_float_type(dtype) || dtype == XO_F64);
 }
 
 /* ------------------------------------------------------ the definition --- */
 
 /* out[i] = down(fold_op(up(srcs[0][off+i]), ..., up(srcs[P-1][off+i])));
- * AVG is the SUM fold followed by one binary32 division by P. */
+ * AVG is the SUM fold followed by one division by P in the accumulator's
+ * format. */
 static void reduce_one(const void *const *srcs, int nsrc, uint64_t off, void *dst,
                        uint64_t i, int dtype, int op)
 {
-    if (is_float_type(dtype)) {
+    if (dtype == XO_F64) {
+        const int fop = op == XO_AVG ? XO_SUM : op;
+        double acc = up_f64(srcs[0], off + i);
+        for (int p = 1; p < nsrc; ++p) acc = op_f64(fop, acc, up_f64(srcs[p], off + i));
+        if (op == XO_AVG) acc = acc / (double)nsrc;
+        down_f64(dst, i, settle64(op, acc));
+    } else if (is_int8_type(dtype)) {
+        uint32_t acc = up_int8(srcs[0], off + i, dtype);
+        for (int p = 1; p < nsrc; ++p)
+            acc = op_int(op, dtype, acc, up_int8(srcs[p], off + i, dtype));
+        down_int8(dst, i, acc);
+    } else if (is_float_type(dtype)) {
         const int fop = op == XO_AVG ? XO_SUM : op;
         float acc = up_float(srcs[0], off + i, dtype);
         for (int p = 1; p < nsrc; ++p)
@@ -424,14 +506,25 @@ int xo_reduce_scatter_local(const void *const *srcs, int nsrc, int rank, void *d
  *   (no flag)     acc <- acc (+) up(in)
  *   FINAL         dst <- down(acc (+) up(in))      (acc is not written)
  *   INIT|FINAL    dst <- down(up(in))
- * acc holds binary32 for float dtypes and uint32 for integer dtypes. */
+ * acc holds binary32 for float dtypes (binary64 for fp64), uint32 for 8- and
+ * 32-bit integer dtypes and uint64 for 64-bit ones. */
 int xo_reduce_copy_step(const void *in, void *acc, void *dst, uint64_t count, int dtype,
                         int op, unsigned flags)
 {
     if (!valid_pair(dtype, op) || op == XO_AVG) return XO_BAD;
     int init = (flags & XO_INIT) != 0, fin = (flags & XO_FINAL) != 0;
     for (uint64_t i = 0; i < count; ++i) {
-        if (is_int64_type(dtype)) {
+        if (dtype == XO_F64) {
+            double x = up_f64(in, i);
+            double a = settle64(op, init ? x : op_f64(op, up_f64(acc, i), x));
+            if (fin) down_f64(dst, i, a);
+            else down_f64(acc, i, a);
+        } else if (is_int8_type(dtype)) {
+            uint32_t x = up_int8(in, i, dtype);
+            uint32_t a = init ? x : op_int(op, dtype, up_int(acc, i), x);
+            if (fin) down_int8(dst, i, a);
+            else down_int(acc, i, a);
+        } else if (is_int64_type(dtype)) {
             uint64_t x = up_int64(in, i);
             uint64_t a = init ? x : op_int64(op, dtype, up_int64(acc, i), x);
             if (fin) down_int64(dst, i, a);
@@ -457,7 +550,9 @@ int xo_acc_cast(const void *acc, void *dst, uint64_t count, int dtype)
 {
     if (!valid_dtype(dtype)) return XO_BAD;
     for (uint64_t i = 0; i < count; ++i) {
-        if (is_float_type(dtype)) down_float(dst, i, dtype, up_float(acc, i, XO_F32));
+        if (dtype == XO_F64) down_f64(dst, i, up_f64(acc, i));
+        else if (is_int8_type(dtype)) down_int8(dst, i, up_int(acc, i));
+        else if (is_float_type(dtype)) down_float(dst, i, dtype, up_float(acc, i, XO_F32));
         else if (is_int64_type(dtype)) down_int64(dst, i, up_int64(acc, i));
         else down_int(dst, i, up_int(acc, i));
     }
@@ -703,7 +798,7 @@ int xo_max_threads(void)
 #endif
 }
 
-int xo_version(void) { return 3; }
+int xo_version(void) { return 4; }
 
 /* Narrow float conversions on their own, for the pins. */
 void xo_small_to_f32_bits(const uint8_t *in, int in_size, uint32_t *out, uint64_t n, int dtype)

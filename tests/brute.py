@@ -21,6 +21,8 @@ E5M2 = dict(p=3, emin=-14, emax=15, ebits=5, bias=15, total=8, qnan=0x7E)
 E4M3 = dict(p=4, emin=-6, emax=8, ebits=4, bias=7, total=8, qnan=0x7F, fn=True)
 NARROW = {"f16": F16, "e5m2": E5M2, "e4m3": E4M3}
 CANON_NAN32 = 0x7FC00000
+F64 = dict(p=53, emin=-1022, emax=1023, ebits=11, bias=1023, total=64)
+CANON_NAN64 = 0x7FF8000000000000
 
 
 def decode(bits: int, fmt=F32):
@@ -239,6 +241,103 @@ def iop64(op: str, dtype: str, a: int, b: int) -> int:
     return max(a, b) if op == "max" else min(a, b)
 
 
+# ---- binary64: the same exact-then-round construction at p = 53 --------
+INF64 = 0x7FF0000000000000
+
+
+def _sign_bits64(s: int) -> int:
+    return s << 63
+
+
+def add64(a: int, b: int) -> int:
+    """Correctly rounded binary64 a + b (round to nearest even)."""
+    A, B = decode(a, F64), decode(b, F64)
+    if A[0] == "nan" or B[0] == "nan":
+        return CANON_NAN64
+    if A[0] == "inf" and B[0] == "inf":
+        return CANON_NAN64 if A[1] != B[1] else a
+    if A[0] == "inf":
+        return a
+    if B[0] == "inf":
+        return b
+    v = (-A[2] if A[1] else A[2]) + (-B[2] if B[1] else B[2])
+    if v == 0:
+        return _sign_bits64(1) if (A[1] and B[1]) else 0
+    return encode_rounded(1 if v < 0 else 0, abs(v), F64)
+
+
+def mul64(a: int, b: int) -> int:
+    """Correctly rounded binary64 a * b."""
+    A, B = decode(a, F64), decode(b, F64)
+    if A[0] == "nan" or B[0] == "nan":
+        return CANON_NAN64
+    s = A[1] ^ B[1]
+    if A[0] == "inf" or B[0] == "inf":
+        other = B if A[0] == "inf" else A
+        if other[0] == "fin" and other[2] == 0:
+            return CANON_NAN64
+        return _sign_bits64(s) | INF64
+    return encode_rounded(s, A[2] * B[2], F64)
+
+
+def div64(a: int, b: int) -> int:
+    """Correctly rounded binary64 a / b."""
+    A, B = decode(a, F64), decode(b, F64)
+    if A[0] == "nan" or B[0] == "nan":
+        return CANON_NAN64
+    s = A[1] ^ B[1]
+    if A[0] == "inf":
+        return CANON_NAN64 if B[0] == "inf" else _sign_bits64(s) | INF64
+    if B[0] == "inf":
+        return _sign_bits64(s)
+    if B[2] == 0:
+        return CANON_NAN64 if A[2] == 0 else _sign_bits64(s) | INF64
+    return encode_rounded(s, A[2] / B[2], F64)
+
+
+def is_nan64(b: int) -> bool:
+    return (b & INF64) == INF64 and (b & ((1 << 52) - 1)) != 0
+
+
+def _order_key64(b: int):
+    d = decode(b, F64)
+    if d[0] == "inf":
+        return (1 if d[1] == 0 else -1, 0, 0)
+    v = -d[2] if d[1] else d[2]
+    return (0, v, 0 if d[1] else 1)
+
+
+def max64(a: int, b: int) -> int:
+    if is_nan64(a) or is_nan64(b):
+        return CANON_NAN64
+    return a if _order_key64(a) >= _order_key64(b) else b
+
+
+def min64(a: int, b: int) -> int:
+    if is_nan64(a) or is_nan64(b):
+        return CANON_NAN64
+    return a if _order_key64(a) <= _order_key64(b) else b
+
+
+FOPS64 = {"sum": add64, "prod": mul64, "max": max64, "min": min64}
+
+
+def iop8(op: str, dtype: str, a: int, b: int) -> int:
+    """8-bit integer op on byte values 0..255: sum/prod modulo 2^8, max/min
+    signed for i8 and unsigned for u8 (computed on the bytes directly, not by
+    widening)."""
+    if op == "sum":
+        return (a + b) & 0xFF
+    if op == "prod":
+        return (a * b) & 0xFF
+    if dtype == "i8":
+        sa = a - 256 if a & 0x80 else a
+        sb = b - 256 if b & 0x80 else b
+        r = max(sa, sb) if op == "max" else min(sa, sb)
+        return r & 0xFF
+    return max(a, b) if op == "max" else min(a, b)
+
+
 FLOAT_DTYPES = ("f32", "bf16", "f16", "e4m3", "e5m2")
 
 
@@ -262,6 +361,21 @@ def reduce_column(vals_bits, dtype: str, op: str) -> int:
         if op in ("max", "min") and is_nan32(acc):
             acc = CANON_NAN32      # a NaN among the values, whatever their number
         return down(acc)
+    if dtype == "f64":
+        fop = FOPS64["sum" if op == "avg" else op]
+        acc = vals_bits[0]
+        for v in vals_bits[1:]:
+            acc = fop(acc, v)
+        if op == "avg":
+            acc = div64(acc, encode_rounded(0, Fraction(len(vals_bits)), F64))
+        if op in ("max", "min") and is_nan64(acc):
+            acc = CANON_NAN64
+        return acc
+    if dtype in ("i8", "u8"):
+        acc = vals_bits[0] & 0xFF
+        for v in vals_bits[1:]:
+            acc = iop8(op, dtype, acc, v & 0xFF)
+        return acc
     if dtype in ("i64", "u64"):
         m = (1 << 64) - 1
         acc = vals_bits[0] & m

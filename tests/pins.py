@@ -31,12 +31,15 @@ import brute
 
 GOLDEN = Path(__file__).resolve().parent / "golden"
 NP = {"f32": np.float32, "bf16": np.uint16, "i32": np.int32, "u32": np.uint32,
-      "f16": np.uint16, "e4m3": np.uint8, "e5m2": np.uint8, "i64": np.int64, "u64": np.uint64}
+      "f16": np.uint16, "e4m3": np.uint8, "e5m2": np.uint8, "i64": np.int64, "u64": np.uint64,
+      "f64": np.float64, "i8": np.int8, "u8": np.uint8}
 DTYPES = ("f32", "bf16", "i32", "u32")
 OPS = ("sum", "prod", "max", "min")
 # the further element types and AVG (float types only)
 MORE_DTYPES = ("f16", "e4m3", "e5m2", "i64", "u64")
-FLOATS = ("f32", "bf16", "f16", "e4m3", "e5m2")
+# the rest of the usual collective element types: binary64, 8-bit integers
+WIDE_NARROW_DTYPES = ("f64", "i8", "u8")
+FLOATS = ("f32", "bf16", "f16", "e4m3", "e5m2", "f64")
 
 
 def ops_for(dtype: str):
@@ -69,6 +72,8 @@ def _is_nan_bits(b: int, dtype: str) -> bool:
         return (b & 0x7C) == 0x7C and (b & 0x3) != 0
     if dtype == "e4m3":
         return (b & 0x7F) == 0x7F
+    if dtype == "f64":
+        return brute.is_nan64(b)
     return False
 
 
@@ -113,6 +118,28 @@ def random_column_values(rng, dtype: str, n: int) -> np.ndarray:
         mid = (rng.integers(0x20, 0x48, size=n, dtype=np.uint32).astype(np.uint8)
                | (rng.integers(0, 2, size=n, dtype=np.uint32).astype(np.uint8) << 7))
         return np.where(rng.integers(0, 2, size=n) == 0, rb, mid).astype(np.uint8)
+    if dtype == "f64":
+        pool = np.array([0x0, 0x8000000000000000, 0x7FF0000000000000, 0xFFF0000000000000,
+                         0x7FEFFFFFFFFFFFFF, 0xFFEFFFFFFFFFFFFF, 0x1, 0x8000000000000001,
+                         0x000FFFFFFFFFFFFF, 0x0010000000000000, 0x3FF0000000000000,
+                         0xBFF0000000000000, 0x3FF0000000000001, 0x3CA0000000000000,
+                         0x3CA0000000000001, 0x7FF8000000000000, 0x7FF0000000000001,
+                         0xFFF8000000000000, 0x4330000000000000], np.uint64)
+        rb = rng.integers(0, 2**64, size=n, dtype=np.uint64)
+        near = rng.standard_normal(n).view(np.uint64)
+        tiny = rng.integers(0, 1 << 53, size=n, dtype=np.uint64)
+        pick = rng.integers(0, 4, size=n)
+        out = np.where(pick == 0, pool[rng.integers(0, pool.size, n)],
+                       np.where(pick == 1, rb, np.where(pick == 2, near, tiny)))
+        return out.astype(np.uint64).view(np.float64)
+    if dtype in ("i8", "u8"):
+        sp = np.array([0, 1, 0xFF, 0x7F, 0x80, 2, 0x10], np.uint8)
+        rb = rng.integers(0, 256, size=n, dtype=np.uint32).astype(np.uint8)
+        small = rng.integers(0, 8, size=n, dtype=np.uint32).astype(np.uint8)
+        pick = rng.integers(0, 3, size=n)
+        out = np.where(pick == 0, sp[rng.integers(0, sp.size, n)],
+                       np.where(pick == 1, rb, small)).astype(np.uint8)
+        return out.view(np.int8) if dtype == "i8" else out
     if dtype in ("i64", "u64"):
         sp = np.array([0, 1, 2**64 - 1, 2**63 - 1, 2**63, 2, 2**32, 2**32 - 1], np.uint64)
         rb = rng.integers(0, 2**64, size=n, dtype=np.uint64)
@@ -592,6 +619,111 @@ def pin_more_types_closed_forms(orc, n: int = 1 << 15, seed: int = 41) -> None:
             assert np.array_equal(orc.allreduce_local(perm, dt, op), ref), f"{dt} {op} order"
 
 
+# ------------------------------------------- binary64 and 8-bit integers --
+
+def pin_wide_narrow_bruteforce(orc, seed: int = 61, ncols: int = 32,
+                               nsrc_list=(1, 2, 3, 5, 8)) -> None:
+    """fp64 (exact rational arithmetic rounded to binary64) and int8 / uint8
+    (byte arithmetic modulo 2^8, compared signed or unsigned on the bytes:
+    not the oracle's widen-then-truncate route) with every op, AVG on fp64."""
+    rng = np.random.default_rng(seed)
+    for dtype in WIDE_NARROW_DTYPES:
+        for op in ops_for(dtype):
+            for P in nsrc_list:
+                srcs = [random_column_values(rng, dtype, ncols) for _ in range(P)]
+                got = _bits(orc.allreduce_local(srcs, dtype, op))
+                sb = [_bits(s) for s in srcs]
+                for i in range(ncols):
+                    col = [int(s[i]) for s in sb]
+                    exp = brute.reduce_column(col, dtype, op)
+                    assert _same(int(got[i]), exp, dtype, op), (
+                        f"{dtype} {op} P={P} col={[hex(c) for c in col]} "
+                        f"got={int(got[i]):#x} exp={exp:#x}")
+
+
+def pin_wide_narrow_closed_forms(orc, n: int = 1 << 15, seed: int = 67) -> None:
+    """fp64 sums and products of integer-valued inputs are exact below 2^53,
+    so they equal numpy's int64 results; AVG over a power-of-two P is the exact
+    mean; fp64 max/min of finite nonzero values equal numpy's; int8 / uint8
+    sums and products equal numpy's own 8-bit wrapping arithmetic, max/min
+    numpy's; the step-wise sequence (INIT, adds, FINAL or the closing cast)
+    equals the fused fold; ReduceScatter shards concatenate to the AllReduce;
+    max/min are permutation invariant."""
+    rng = np.random.default_rng(seed)
+    ints = [rng.integers(-1000, 1001, size=n) for _ in range(8)]
+    f = [x.astype(np.float64) for x in ints]
+    tot = np.sum(np.stack(ints), axis=0)
+    assert np.array_equal(orc.allreduce_local(f, "f64", "sum"), tot.astype(np.float64))
+    small = [rng.integers(-9, 10, size=n) for _ in range(6)]
+    prod = np.prod(np.stack(small), axis=0)
+    assert np.array_equal(orc.allreduce_local([x.astype(np.float64) for x in small], "f64",
+                                              "prod"), prod.astype(np.float64))
+    for P in (2, 4, 8):
+        got = orc.allreduce_local(f[:P], "f64", "avg")
+        assert np.array_equal(got, np.sum(np.stack(ints[:P]), axis=0) / P), f"f64 avg P={P}"
+    # signed zeros in every order: the total order puts -0 below +0
+    pz, nz = np.zeros(4, np.float64), np.full(4, -0.0)
+    for srcs in ([pz, nz], [nz, pz], [pz, pz, nz], [nz, pz, pz], [pz, nz, pz]):
+        hi = _bits(orc.allreduce_local(srcs, "f64", "max"))
+        lo = _bits(orc.allreduce_local(srcs, "f64", "min"))
+        assert np.all(hi == 0) and np.all(lo == 0x8000000000000000), "f64 max/min of +-0"
+    g = [rng.standard_normal(n) + 0.5 for _ in range(7)]
+    assert np.array_equal(orc.allreduce_local(g, "f64", "max"), np.max(np.stack(g), axis=0))
+    assert np.array_equal(orc.allreduce_local(g, "f64", "min"), np.min(np.stack(g), axis=0))
+    for dt, t in (("i8", np.int8), ("u8", np.uint8)):
+        a = [random_column_values(rng, dt, n) for _ in range(9)]
+        st = np.stack(a)
+        assert np.array_equal(orc.allreduce_local(a, dt, "sum"), np.sum(st, axis=0, dtype=t))
+        assert np.array_equal(orc.allreduce_local(a, dt, "prod"), np.prod(st, axis=0, dtype=t))
+        assert np.array_equal(orc.allreduce_local(a, dt, "max"), np.max(st, axis=0))
+        assert np.array_equal(orc.allreduce_local(a, dt, "min"), np.min(st, axis=0))
+    for dt in WIDE_NARROW_DTYPES:
+        for op in OPS:
+            P, rc = 5, 41
+            srcs = [random_column_values(rng, dt, P * rc) for _ in range(P)]
+            full = _bits(orc.allreduce_local(srcs, dt, op))
+            for r in range(P):
+                sh = _bits(orc.reduce_scatter_local(srcs, r, dt, op))
+                exp = full[r * rc:(r + 1) * rc]
+                ok = [_same(int(x), int(y), dt, op) for x, y in zip(sh, exp)]
+                assert all(ok), (dt, op, r)
+            chunks = [random_column_values(rng, dt, 53) for _ in range(P)]
+            fused = _bits(orc.allreduce_local(chunks, dt, op))
+            acc = orc.reduce_copy_step(chunks[0], None, dt, op, init=True)
+            for c in chunks[1:-1]:
+                acc = orc.reduce_copy_step(c, acc, dt, op)
+            acc_copy = acc.copy()
+            fin = _bits(orc.reduce_copy_step(chunks[-1], acc, dt, op, final=True))
+            cast = _bits(orc.acc_cast(orc.reduce_copy_step(chunks[-1], acc_copy, dt, op), dt))
+            for got in (fin, cast):
+                assert all(_same(int(x), int(y), dt, op) for x, y in zip(got, fused)), (dt, op)
+            if op in ("max", "min"):
+                perm = [srcs[k] for k in rng.permutation(P)]
+                assert np.array_equal(_bits(orc.allreduce_local(perm, dt, op)), full), (dt, op)
+
+
+def pin_wide_narrow_sim(orc, seed: int = 71) -> None:
+    """The simulated ring and halving-doubling schedules on fp64 and int8 /
+    uint8 against the chain of hops computed by the brute force."""
+    rng = np.random.default_rng(seed)
+    for algo, sizes, brute_el in (("ring", (2, 3, 5), brute_ring_element),
+                                  ("rhd", (2, 4, 8), brute_rhd_element)):
+        for dtype in WIDE_NARROW_DTYPES:
+            for op in OPS:
+                for G in sizes:
+                    n = 64 * G + 70
+                    sends = [random_column_values(rng, dtype, n) for _ in range(G)]
+                    outs = [_bits(o) for o in orc.allreduce_sim(sends, dtype, op, algo)]
+                    M = sim_chunk_len(n, G)
+                    sb = [_bits(x) for x in sends]
+                    for i in sorted({0, n - 1, M - 1, M, n // 2}):
+                        col = [int(x[i]) for x in sb]
+                        exp = brute_el(col, i // M, dtype, op)
+                        for r in range(G):
+                            assert _same(int(outs[r][i]), exp, dtype, op), (
+                                f"{algo} {dtype} {op} G={G} rank {r} i={i}")
+
+
 def pin_selfcheck(orc) -> None:
     assert orc.selfcheck() == 0, "floating-point environment"
 
@@ -600,4 +732,5 @@ FAST_PINS = [pin_selfcheck, pin_golden_reduce, pin_golden_bf16, pin_bf16_vs_brut
              pin_up_bf16, pin_integer_closed_form, pin_int_mod32, pin_invariants,
              pin_composition, pin_bruteforce, pin_sim_closed_forms, pin_sim_bruteforce,
              pin_narrow_vs_torch, pin_more_types_closed_forms, pin_more_types_bruteforce,
-             pin_golden_narrow]
+             pin_golden_narrow, pin_wide_narrow_bruteforce, pin_wide_narrow_closed_forms,
+             pin_wide_narrow_sim]

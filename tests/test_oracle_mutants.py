@@ -40,8 +40,8 @@ MUTANTS = [
      "if (isnan(a)) return b;\n    if (a > b)", 1, ()),
     ("max_is_min", "if (a > b) return a;", "if (a < b) return a;", 1, ()),
     ("prod_is_sum", "case XO_PROD: return a * b;", "case XO_PROD: return a + b;", 1, ()),
-    ("int_max_unsigned", "if (dtype == XO_I32) return ((int32_t)a > (int32_t)b) ? a : b;",
-     "if (dtype == XO_I32) return (a > b) ? a : b;", 1, ()),
+    ("int_max_unsigned", "if (sgn) return ((int32_t)a > (int32_t)b) ? a : b;",
+     "if (sgn) return (a > b) ? a : b;", 1, ()),
     ("int_min_signed_for_u32", "return a < b ? a : b;",
      "return ((int32_t)a < (int32_t)b) ? a : b;", 1, ()),
     ("step_init_reads_acc", "float a = init ? x : op_float(op, up_float(acc, i, XO_F32), x);",
@@ -56,6 +56,24 @@ MUTANTS = [
      "for (int p = 1; p < nsrc; ++p)\n            acc = op_float(fop, acc, up_float(srcs[p], off + i, dtype));",
      "for (int p = nsrc - 2; p >= 0; --p)\n            acc = op_float(fop, acc, up_float(srcs[p], off + i, dtype));",
      1, ()),
+    # binary64 and 8-bit integers
+    ("i8_zero_extends", "return dtype == XO_I8 ? (uint32_t)(int32_t)(int8_t)b : (uint32_t)b;",
+     "return (uint32_t)b;", 1, ()),
+    ("int8_keeps_wrong_byte", "((uint8_t *)base)[i] = (uint8_t)v; }",
+     "((uint8_t *)base)[i] = (uint8_t)(v >> 8); }", 1, ()),
+    ("i8_max_unsigned", "const int sgn = dtype == XO_I32 || dtype == XO_I8;",
+     "const int sgn = dtype == XO_I32;", 1, ()),
+    ("f64_accumulates_in_f32", "acc = op_f64(fop, acc, up_f64(srcs[p], off + i));",
+     "acc = (double)(float)op_f64(fop, acc, up_f64(srcs[p], off + i));", 1, ()),
+    ("f64_avg_in_f32", "if (op == XO_AVG) acc = acc / (double)nsrc;",
+     "if (op == XO_AVG) acc = (double)((float)acc / (float)nsrc);", 1, ()),
+    ("f64_max_drops_nan",
+     "if (isnan(a) || isnan(b)) return canonical_nan64();\n    if (a > b)",
+     "if (isnan(a)) return b;\n    if (a > b)", 1, ()),
+    ("f64_min_ignores_zero_sign", "if (b < a) return b;\n    return signbit(a) ? a : b;\n}\n\nstatic double op_f64",
+     "if (b < a) return b;\n    return b;\n}\n\nstatic double op_f64", 1, ()),
+    ("f64_step_rounds_acc", "double a = settle64(op, init ? x : op_f64(op, up_f64(acc, i), x));",
+     "double a = settle64(op, init ? x : (double)(float)op_f64(op, up_f64(acc, i), x));", 1, ()),
     # simulated schedules
     ("ring_sendcopy_own_chunk", "const int c = mod_rank(r - 1, G);\n            memcpy(wire[r]",
      "const int c = mod_rank(r, G);\n            memcpy(wire[r]", 1, ()),
