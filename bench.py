@@ -43,11 +43,11 @@ _COMMON = [CSRC + "xred_device.hpp", CSRC + "xred_kernels.hpp", CSRC + "xred_dis
 KERNEL_SOURCES = {
     "reduce": _COMMON + [CSRC + f for f in ("xred_reduce.hpp", "xred_reduce.hip",
                                            "xred_reduce_float.hip", "xred_reduce_fp8.hip",
-                                           "xred_reduce_int.hip")],
+                                           "xred_reduce_int.hip", "xred_reduce_ext.hip")],
     "step": _COMMON + [CSRC + "xred_step.hip"],
     "batched": _COMMON + [CSRC + f for f in ("xred_batched.hpp", "xred_batched.hip",
                                             "xred_batched_float.hip", "xred_batched_fp8.hip",
-                                            "xred_batched_int.hip")],
+                                            "xred_batched_int.hip", "xred_batched_ext.hip")],
     "ring": _COMMON + [CSRC + "xred_ring.hip"],
     "sim": _COMMON + [CSRC + "xred_sim.hip"],
 }
@@ -437,10 +437,11 @@ def secondary(torch, xr, L, timer, wl, flush, res):
     del d, out
 
     # further element types and AVG at the gradient-bucket footprint: P=8
-    # sources of 128 MiB each (random bytes; fp8 bytes masked to finite values)
+    # sources of 128 MiB each (random bytes; float bytes masked to finite values)
     more = {}
     for dt, es, op in (("f16", 2, "sum"), ("e4m3", 1, "sum"), ("e5m2", 1, "sum"),
-                       ("i64", 8, "sum"), ("bf16", 2, "avg"), ("f32", 4, "avg")):
+                       ("i64", 8, "sum"), ("bf16", 2, "avg"), ("f32", 4, "avg"),
+                       ("f64", 8, "sum"), ("i8", 1, "sum"), ("u8", 1, "max")):
         n = (128 << 20) // es
         d = []
         for _ in range(8):
@@ -450,6 +451,8 @@ def secondary(torch, xr, L, timer, wl, flush, res):
             elif dt in ("f16", "bf16", "f32"):
                 x.view(torch.int16 if es == 2 else torch.int32).bitwise_and_(
                     0x3BFF if dt == "f16" else (0x3F7F if dt == "bf16" else 0x3F7FFFFF))
+            elif dt == "f64":
+                x.view(torch.int64).bitwise_and_(0x3FEFFFFFFFFFFFFF)   # finite, below 1
             d.append(x)
         out = torch.empty_like(d[0])
         arr = xr._lib.ptr_array([x.data_ptr() for x in d])

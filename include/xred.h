@@ -17,23 +17,28 @@
  *   - a LEFT fold in source order 0..P-1 (the order is fixed, so float
  *     results are deterministic and bit-reproducible);
  *   - up(): bf16, fp16, fp8 e4m3 / e5m2 -> binary32 (exact), fp32 -> binary32,
- *     int32/uint32 -> uint32, int64/uint64 -> uint64; the accumulator is
- *     binary32 for float types and uint32 / uint64 for integer types;
- *   - (+): XRED_SUM  binary32 add (round to nearest even, subnormals kept) or
- *                    addition modulo 2^32 / 2^64;
- *          XRED_PROD binary32 multiply, or the low 32 / 64 bits of the product;
+ *     fp64 -> binary64, int8 -> uint32 (sign-extended), uint8 -> uint32
+ *     (zero-extended), int32/uint32 -> uint32, int64/uint64 -> uint64; the
+ *     accumulator is binary32 for float types (binary64 for fp64) and uint32
+ *     / uint64 for integer types;
+ *   - (+): XRED_SUM  binary32 (fp64: binary64) add, round to nearest even,
+ *                    subnormals kept, or addition modulo 2^32 / 2^64;
+ *          XRED_PROD binary32 (fp64: binary64) multiply, or the low 32 / 64
+ *                    bits of the product;
  *          XRED_MAX / XRED_MIN  float: total order -inf < ... < -0 < +0 < ...
  *                    < +inf; a NaN among the reduced values gives the quiet
- *                    NaN 0x7FC00000 (also for P = 1 and the INIT step);
- *                    int32/int64 signed, uint32/uint64 unsigned;
- *          XRED_AVG  (float types only) the XRED_SUM fold, then one binary32
- *                    division by P, rounded to nearest even;
+ *                    NaN 0x7FC00000 (fp64: 0x7FF8000000000000; also for P = 1
+ *                    and the INIT step); int8/int32/int64 signed,
+ *                    uint8/uint32/uint64 unsigned;
+ *          XRED_AVG  (float types only) the XRED_SUM fold, then one division
+ *                    by P in the accumulator's format, rounded to nearest even;
  *   - the accumulator starts from up(src[0][i]) (never from zero), so a column
  *     of -0.0 sums to -0.0;
  *   - down(): binary32 -> bf16 / fp16 / e5m2 round to nearest even with
  *     subnormals and overflow to +-inf; binary32 -> e4m3 (OCP "FN": no
  *     infinity, largest finite 448) round to nearest even, saturating at
- *     +-448 on overflow and for infinities; identity otherwise.  NaN stays
+ *     +-448 on overflow and for infinities; the low byte for int8 / uint8 (so
+ *     their sums and products wrap modulo 2^8); identity otherwise.  NaN stays
  *     NaN; NaN payloads of SUM/PROD/AVG results are unspecified.
  *
  * Conventions shared by every call:
@@ -94,7 +99,10 @@ typedef enum {
     XRED_INT64 = 5,
     XRED_UINT64 = 6,
     XRED_FP8_E4M3 = 7,  /* OCP 8-bit E4M3 ("FN"), saturating */
-    XRED_FP8_E5M2 = 8   /* OCP 8-bit E5M2 */
+    XRED_FP8_E5M2 = 8,  /* OCP 8-bit E5M2 */
+    XRED_FLOAT64 = 9,   /* IEEE binary64, accumulated in binary64 */
+    XRED_INT8 = 10,
+    XRED_UINT8 = 11
 } xred_dtype;
 
 /* XRED_AVG: float types only, and only where the whole reduction happens in
@@ -164,8 +172,9 @@ XRED_API xred_status xred_reduce_scatter_local(const void *const *srcs, int nsrc
  *   INIT | FINAL             dst[i] = down(up(in[i]))              (acc unused)
  *   in       count elements of dtype
  *   acc      count accumulator elements of xred_acc_elem_size(dtype) bytes
- *            (binary32 for float dtypes, uint32 / uint64 for 32- / 64-bit
- *            integer dtypes), aligned to that size; may be NULL only for
+ *            (binary32 for float dtypes, binary64 for fp64, uint32 for 8- and
+ *            32-bit and uint64 for 64-bit integer dtypes), aligned to that
+ *            size; may be NULL only for
  *            INIT|FINAL
  *   op       not XRED_AVG (a step does not know P; use XRED_SUM and divide)
  *   dst      count elements of dtype, used only with FINAL (may be NULL otherwise)
@@ -366,8 +375,8 @@ XRED_API size_t xred_sim_chunk(size_t count, int nranks);
  */
 XRED_API unsigned xred_set_max_workgroups(unsigned max_workgroups);
 
-/* Bytes per accumulator element for dtype: 4 (binary32 or uint32), 8 (uint64
- * for int64/uint64), 0 if unknown. */
+/* Bytes per accumulator element for dtype: 4 (binary32 or uint32), 8
+ * (binary64 for fp64, uint64 for int64/uint64), 0 if unknown. */
 XRED_API size_t xred_acc_elem_size(xred_dtype dtype);
 
 /* Static, human-readable name of a status code. */

@@ -35,7 +35,8 @@ __all__ = ["allreduce_local", "reduce_scatter_local", "reduce_copy_step", "acc_c
 def _torch_dtype_name(t) -> str:
     import torch
     m = {torch.float32: "f32", torch.bfloat16: "bf16", torch.int32: "i32",
-         torch.float16: "f16", torch.int64: "i64"}
+         torch.float16: "f16", torch.int64: "i64", torch.float64: "f64", torch.int8: "i8",
+         torch.uint8: "u8"}
     for name, code in (("uint32", "u32"), ("uint64", "u64"), ("float8_e4m3fn", "e4m3"),
                        ("float8_e5m2", "e5m2")):
         if hasattr(torch, name):

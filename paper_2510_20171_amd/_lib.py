@@ -15,10 +15,10 @@ LIB_PATH = Path(__file__).resolve().parent / "libxred.so"
 
 # Values of the enums in include/xred.h.
 DTYPE = {"f32": 0, "bf16": 1, "f16": 2, "i32": 3, "u32": 4, "i64": 5, "u64": 6, "e4m3": 7,
-         "e5m2": 8}
+         "e5m2": 8, "f64": 9, "i8": 10, "u8": 11}
 ELEM_SIZE = {"f32": 4, "bf16": 2, "f16": 2, "i32": 4, "u32": 4, "i64": 8, "u64": 8, "e4m3": 1,
-             "e5m2": 1}
-ACC_SIZE = {d: 8 if d in ("i64", "u64") else 4 for d in DTYPE}
+             "e5m2": 1, "f64": 8, "i8": 1, "u8": 1}
+ACC_SIZE = {d: 8 if d in ("i64", "u64", "f64") else 4 for d in DTYPE}
 OP = {"sum": 0, "prod": 1, "max": 2, "min": 3, "avg": 4}
 STATUS = {0: "XRED_SUCCESS", 1: "XRED_INVALID_ARGUMENT", 2: "XRED_UNSUPPORTED", 3: "XRED_ALIAS",
           4: "XRED_HIP_ERROR", 5: "XRED_OUT_OF_MEMORY"}

@@ -72,7 +72,7 @@ xred_status hip_fail(hipError_t e, const char *what)
     return fail(XRED_HIP_ERROR, "%s: %s", what, hipGetErrorString(e));
 }
 
-bool known_dtype(xred_dtype d) { return d >= XRED_FLOAT32 && d <= XRED_FP8_E5M2; }
+bool known_dtype(xred_dtype d) { return d >= XRED_FLOAT32 && d <= XRED_UINT8; }
 bool known_op(xred_op o) { return o >= XRED_SUM && o <= XRED_AVG; }
 
 // Entry points whose kernels see only part of the fold (one step, a chunk at
@@ -86,7 +86,10 @@ xred_status check_no_avg(xred_op op, const char *entry)
 }
 
 // Accumulator element bytes: uint64 for 64-bit integers, else 4.
-size_t acc_size(xred_dtype d) { return d == XRED_INT64 || d == XRED_UINT64 ? 8 : 4; }
+size_t acc_size(xred_dtype d)
+{
+    return d == XRED_INT64 || d == XRED_UINT64 || d == XRED_FLOAT64 ? 8 : 4;
+}
 
 // Checks shared by every entry point on dtype and op.
 xred_status check_types(xred_dtype dtype, xred_op op)
@@ -659,7 +662,7 @@ bool supported(xred_dtype dtype, xred_op op)
 {
     const bool is_float = dtype == XRED_FLOAT32 || dtype == XRED_BFLOAT16 ||
                           dtype == XRED_FLOAT16 || dtype == XRED_FP8_E4M3 ||
-                          dtype == XRED_FP8_E5M2;
+                          dtype == XRED_FP8_E5M2 || dtype == XRED_FLOAT64;
     return known_dtype(dtype) && known_op(op) && (op != XRED_AVG || is_float);
 }
 
@@ -668,8 +671,8 @@ size_t elem_size(xred_dtype dtype)
     switch (dtype) {
     case XRED_FLOAT32: case XRED_INT32: case XRED_UINT32: return 4;
     case XRED_BFLOAT16: case XRED_FLOAT16: return 2;
-    case XRED_INT64: case XRED_UINT64: return 8;
-    case XRED_FP8_E4M3: case XRED_FP8_E5M2: return 1;
+    case XRED_INT64: case XRED_UINT64: case XRED_FLOAT64: return 8;
+    case XRED_FP8_E4M3: case XRED_FP8_E5M2: case XRED_INT8: case XRED_UINT8: return 1;
     default: return 0;
     }
 }
@@ -967,7 +970,7 @@ XRED_API const char *xred_status_string(xred_status s)
 
 XRED_API const char *xred_last_error(void) { return g_err; }
 
-XRED_API int xred_version(void) { return 20000; }
+XRED_API int xred_version(void) { return 20100; }
 
 XRED_API void xred_release(void)
 {

@@ -1,6 +1,7 @@
 // xred_batched.hip -- many independent reductions in one launch: the entry
 // points used by the C ABI, dispatching to the kernels of the element type's
-// group (xred_batched_float.hip, xred_batched_fp8.hip, xred_batched_int.hip).
+// group (xred_batched_float.hip, xred_batched_fp8.hip, xred_batched_int.hip,
+// xred_batched_ext.hip).
 #include "xred_batched.hpp"
 
 namespace xred {
@@ -24,6 +25,8 @@ hipError_t launch_batched_planned(xred_dtype dtype, xred_op op, const xred_item 
         return launch_batched_range_float(dtype, op, d_items, nitems, d_wg, grid, stream);
     case TypeGroup::kFp8:
         return launch_batched_range_fp8(dtype, op, d_items, nitems, d_wg, grid, stream);
+    case TypeGroup::kExt:
+        return launch_batched_range_ext(dtype, op, d_items, nitems, d_wg, grid, stream);
     default:
         return launch_batched_range_int(dtype, op, d_items, nitems, d_wg, grid, stream);
     }
@@ -48,6 +51,8 @@ hipError_t launch_batched_table(xred_dtype dtype, xred_op op, const xred_item *d
         return launch_batched_table_float(dtype, op, d_items, d_table, narrow, ntiles, stream);
     case TypeGroup::kFp8:
         return launch_batched_table_fp8(dtype, op, d_items, d_table, narrow, ntiles, stream);
+    case TypeGroup::kExt:
+        return launch_batched_table_ext(dtype, op, d_items, d_table, narrow, ntiles, stream);
     default:
         return launch_batched_table_int(dtype, op, d_items, d_table, narrow, ntiles, stream);
     }
@@ -68,6 +73,9 @@ hipError_t launch_batched_grouped(xred_dtype dtype, xred_op op, const xred_item 
     case TypeGroup::kFp8:
         return launch_batched_grouped_fp8(dtype, op, d_items, nitems, ngroups, m, grid,
                                           wgs_per_cu, stream);
+    case TypeGroup::kExt:
+        return launch_batched_grouped_ext(dtype, op, d_items, nitems, ngroups, m, grid,
+                                          wgs_per_cu, stream);
     default:
         return launch_batched_grouped_int(dtype, op, d_items, nitems, ngroups, m, grid,
                                           wgs_per_cu, stream);
@@ -87,6 +95,9 @@ hipError_t launch_batched_queue(xred_dtype dtype, xred_op op, const xred_item *d
     case TypeGroup::kFp8:
         return launch_batched_queue_fp8(dtype, op, d_items, nitems, next, clear, finished, grid,
                                         wgs_per_cu, stream);
+    case TypeGroup::kExt:
+        return launch_batched_queue_ext(dtype, op, d_items, nitems, next, clear, finished, grid,
+                                        wgs_per_cu, stream);
     default:
         return launch_batched_queue_int(dtype, op, d_items, nitems, next, clear, finished, grid,
                                         wgs_per_cu, stream);
@@ -101,6 +112,8 @@ hipError_t launch_batched_rr(xred_dtype dtype, xred_op op, const xred_item *d_it
         return launch_batched_rr_float(dtype, op, d_items, nitems, d_tile_start, stream);
     case TypeGroup::kFp8:
         return launch_batched_rr_fp8(dtype, op, d_items, nitems, d_tile_start, stream);
+    case TypeGroup::kExt:
+        return launch_batched_rr_ext(dtype, op, d_items, nitems, d_tile_start, stream);
     default:
         return launch_batched_rr_int(dtype, op, d_items, nitems, d_tile_start, stream);
     }

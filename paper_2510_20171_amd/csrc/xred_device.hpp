@@ -18,8 +18,12 @@
 //   (v_maximum3_f32 / v_minimum3_f32: NaN-propagating, -0 < +0), the NaN
 //   result then replaced by the quiet NaN 0x7FC00000;
 //   AVG: the SUM fold, then one correctly rounded binary32 division by P;
-//   integer SUM/PROD on uint32 / uint64 (wrap), MAX/MIN signed for int32 /
-//   int64.
+//   fp64: binary64 throughout (up and down are the identity, MAX/MIN NaN
+//   0x7FF8000000000000, AVG one binary64 division);
+//   int8 / uint8 widened to uint32 (sign- / zero-extended) and narrowed by
+//   keeping the low byte, so sums and products wrap modulo 2^8;
+//   integer SUM/PROD on uint32 / uint64 (wrap), MAX/MIN signed for int8 /
+//   int32 / int64.
 // All code here is compiled without contraction and with binary32 subnormals
 // enabled, so a float add or multiply is exactly one IEEE operation.
 #pragma once
@@ -80,6 +84,21 @@ struct TU64 {
     static constexpr bool kFloat = false, kSigned = false;
     using Acc = uint64_t;
 };
+struct TF64 {
+    static constexpr int kVec = 2, kSize = 8;
+    static constexpr bool kFloat = true, kSigned = false;
+    using Acc = double;
+};
+struct TI8 {
+    static constexpr int kVec = 16, kSize = 1;
+    static constexpr bool kFloat = false, kSigned = true;
+    using Acc = uint32_t;
+};
+struct TU8 {
+    static constexpr int kVec = 16, kSize = 1;
+    static constexpr bool kFloat = false, kSigned = false;
+    using Acc = uint32_t;
+};
 
 // Accumulator values per 16-byte vector, and 16-byte accumulator vectors
 // per 16-byte input vector (a step-wise accumulator holds kVec values of
@@ -128,7 +147,9 @@ __device__ __forceinline__ typename T::Acc combine(typename T::Acc a, typename T
 template <class T, class Op>
 __device__ __forceinline__ typename T::Acc finalize(typename T::Acc a)
 {
-    if constexpr (T::kFloat && (__is_same(Op, OpMax) || __is_same(Op, OpMin)))
+    if constexpr (__is_same(T, TF64) && (__is_same(Op, OpMax) || __is_same(Op, OpMin)))
+        return __builtin_isnan(a) ? __builtin_bit_cast(double, 0x7FF8000000000000ull) : a;
+    else if constexpr (T::kFloat && (__is_same(Op, OpMax) || __is_same(Op, OpMin)))
         return __builtin_isnan(a) ? __uint_as_float(0x7FC00000u) : a;
     else
         return a;
@@ -139,7 +160,7 @@ __device__ __forceinline__ typename T::Acc finalize(typename T::Acc a)
 template <class T, class Op>
 __device__ __forceinline__ typename T::Acc avg_scale(typename T::Acc a, int nsrc)
 {
-    if constexpr (__is_same(Op, OpAvg)) return a / (float)nsrc;
+    if constexpr (__is_same(Op, OpAvg)) return a / (typename T::Acc)nsrc;
     else return a;
 }
 
@@ -229,6 +250,18 @@ __device__ __forceinline__ void up_vec(u32x4 v, typename T::Acc (&a)[T::kVec])
             a[4 * j + 2] = hi[0];
             a[4 * j + 3] = hi[1];
         }
+    } else if constexpr (__is_same(T, TF64)) {
+        a[0] = __builtin_bit_cast(double, (uint64_t)v[0] | ((uint64_t)v[1] << 32));
+        a[1] = __builtin_bit_cast(double, (uint64_t)v[2] | ((uint64_t)v[3] << 32));
+    } else if constexpr (__is_same(T, TI8) || __is_same(T, TU8)) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+#pragma unroll
+            for (int b = 0; b < 4; ++b) {
+                const uint32_t x = (v[j] >> (8 * b)) & 0xFFu;
+                a[4 * j + b] = T::kSigned ? (uint32_t)(int32_t)(int8_t)x : x;
+            }
+        }
     } else if constexpr (T::kFloat) {
 #pragma unroll
         for (int j = 0; j < 4; ++j) a[j] = __uint_as_float(v[j]);
@@ -274,6 +307,18 @@ __device__ __forceinline__ u32x4 down_vec(const typename T::Acc (&a)[T::kVec])
         for (int j = 0; j < 4; ++j)
             r[j] = pack_fp8x4<T>(finalize<T, Op>(a[4 * j]), finalize<T, Op>(a[4 * j + 1]),
                                  finalize<T, Op>(a[4 * j + 2]), finalize<T, Op>(a[4 * j + 3]));
+    } else if constexpr (__is_same(T, TF64)) {
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+            const uint64_t b = __builtin_bit_cast(uint64_t, finalize<T, Op>(a[j]));
+            r[2 * j] = (uint32_t)b;
+            r[2 * j + 1] = (uint32_t)(b >> 32);
+        }
+    } else if constexpr (__is_same(T, TI8) || __is_same(T, TU8)) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+            r[j] = (a[4 * j] & 0xFFu) | ((a[4 * j + 1] & 0xFFu) << 8) |
+                   ((a[4 * j + 2] & 0xFFu) << 16) | ((a[4 * j + 3] & 0xFFu) << 24);
     } else if constexpr (T::kFloat) {
 #pragma unroll
         for (int j = 0; j < 4; ++j) r[j] = __float_as_uint(finalize<T, Op>(a[j]));
@@ -299,6 +344,12 @@ __device__ __forceinline__ typename T::Acc up1(const char *base, size_t i)
         return (float)((const _Float16 *)base)[i];
     else if constexpr (__is_same(T, TE4M3) || __is_same(T, TE5M2))
         return unpack_fp8x2<T, false>((uint32_t)((const uint8_t *)base)[i])[0];
+    else if constexpr (__is_same(T, TF64))
+        return ((const double *)base)[i];
+    else if constexpr (__is_same(T, TI8))
+        return (uint32_t)(int32_t)((const int8_t *)base)[i];
+    else if constexpr (__is_same(T, TU8))
+        return (uint32_t)((const uint8_t *)base)[i];
     else if constexpr (T::kFloat)
         return ((const float *)base)[i];
     else
@@ -317,6 +368,10 @@ __device__ __forceinline__ void down1(char *base, size_t i, typename T::Acc a)
         ((_Float16 *)base)[i] = (_Float16)opaque(a);
     } else if constexpr (__is_same(T, TE4M3) || __is_same(T, TE5M2)) {
         ((uint8_t *)base)[i] = (uint8_t)pack_fp8x4<T>(a, a, a, a);
+    } else if constexpr (__is_same(T, TF64)) {
+        ((double *)base)[i] = a;
+    } else if constexpr (__is_same(T, TI8) || __is_same(T, TU8)) {
+        ((uint8_t *)base)[i] = (uint8_t)a;
     } else if constexpr (T::kFloat) {
         ((float *)base)[i] = a;
     } else {
@@ -329,7 +384,10 @@ __device__ __forceinline__ void down1(char *base, size_t i, typename T::Acc a)
 template <class T>
 __device__ __forceinline__ void unpack_acc(u32x4 y, typename T::Acc *a)
 {
-    if constexpr (sizeof(typename T::Acc) == 8) {
+    if constexpr (__is_same(T, TF64)) {
+        a[0] = __builtin_bit_cast(double, (uint64_t)y[0] | ((uint64_t)y[1] << 32));
+        a[1] = __builtin_bit_cast(double, (uint64_t)y[2] | ((uint64_t)y[3] << 32));
+    } else if constexpr (sizeof(typename T::Acc) == 8) {
         a[0] = (uint64_t)y[0] | ((uint64_t)y[1] << 32);
         a[1] = (uint64_t)y[2] | ((uint64_t)y[3] << 32);
     } else if constexpr (T::kFloat) {
@@ -345,7 +403,14 @@ template <class T>
 __device__ __forceinline__ u32x4 pack_acc(const typename T::Acc *a)
 {
     u32x4 y;
-    if constexpr (sizeof(typename T::Acc) == 8) {
+    if constexpr (__is_same(T, TF64)) {
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+            const uint64_t b = __builtin_bit_cast(uint64_t, a[j]);
+            y[2 * j] = (uint32_t)b;
+            y[2 * j + 1] = (uint32_t)(b >> 32);
+        }
+    } else if constexpr (sizeof(typename T::Acc) == 8) {
         y[0] = (uint32_t)a[0];
         y[1] = (uint32_t)(a[0] >> 32);
         y[2] = (uint32_t)a[1];

@@ -21,6 +21,9 @@ hipError_t with_dtype(xred_dtype dtype, F &&f)
     case XRED_UINT64: return f(TU64{});
     case XRED_FP8_E4M3: return f(TE4M3{});
     case XRED_FP8_E5M2: return f(TE5M2{});
+    case XRED_FLOAT64: return f(TF64{});
+    case XRED_INT8: return f(TI8{});
+    case XRED_UINT8: return f(TU8{});
     }
     return hipErrorInvalidValue;
 }
@@ -35,6 +38,9 @@ template <> constexpr xred_dtype dtype_of<TI64>() { return XRED_INT64; }
 template <> constexpr xred_dtype dtype_of<TU64>() { return XRED_UINT64; }
 template <> constexpr xred_dtype dtype_of<TE4M3>() { return XRED_FP8_E4M3; }
 template <> constexpr xred_dtype dtype_of<TE5M2>() { return XRED_FP8_E5M2; }
+template <> constexpr xred_dtype dtype_of<TF64>() { return XRED_FLOAT64; }
+template <> constexpr xred_dtype dtype_of<TI8>() { return XRED_INT8; }
+template <> constexpr xred_dtype dtype_of<TU8>() { return XRED_UINT8; }
 
 // Calls f(T{}) for the one T among Ts whose dtype is `dtype` (instantiating
 // f only for Ts, so a translation unit can hold one group of types).
@@ -46,13 +52,14 @@ hipError_t with_dtype_among(xred_dtype dtype, F &&f)
     return r;
 }
 
-// The three groups the big launchers are compiled in.
-enum class TypeGroup { kFloat, kFp8, kInt };
+// The four groups the big launchers are compiled in.
+enum class TypeGroup { kFloat, kFp8, kInt, kExt };
 inline TypeGroup group_of(xred_dtype dtype)
 {
     switch (dtype) {
     case XRED_FLOAT32: case XRED_BFLOAT16: case XRED_FLOAT16: return TypeGroup::kFloat;
     case XRED_FP8_E4M3: case XRED_FP8_E5M2: return TypeGroup::kFp8;
+    case XRED_FLOAT64: case XRED_INT8: case XRED_UINT8: return TypeGroup::kExt;
     default: return TypeGroup::kInt;
     }
 }

@@ -76,6 +76,8 @@ hipError_t launch_reduce_fp8(xred_dtype dtype, xred_op op, const char *const *sr
                              char *dst, size_t count, hipStream_t stream);
 hipError_t launch_reduce_int(xred_dtype dtype, xred_op op, const char *const *srcs, int nsrc,
                              char *dst, size_t count, hipStream_t stream);
+hipError_t launch_reduce_ext(xred_dtype dtype, xred_op op, const char *const *srcs, int nsrc,
+                             char *dst, size_t count, hipStream_t stream);
 
 hipError_t launch_step(xred_dtype dtype, xred_op op, unsigned flags, const char *in, char *acc,
                        char *dst, size_t count, hipStream_t stream);
@@ -154,6 +156,7 @@ hipError_t launch_batched_grouped(xred_dtype dtype, xred_op op, const xred_item 
 XRED_BATCHED_GROUP(float)
 XRED_BATCHED_GROUP(fp8)
 XRED_BATCHED_GROUP(int)
+XRED_BATCHED_GROUP(ext)
 #undef XRED_BATCHED_GROUP
 
 // Device-resident descriptors, queued: a persistent grid takes tiles in

@@ -6,10 +6,10 @@ import numpy as np
 
 NP_BITS = {"f32": np.uint32, "bf16": np.uint16, "i32": np.uint32, "u32": np.uint32,
            "f16": np.uint16, "e4m3": np.uint8, "e5m2": np.uint8, "i64": np.uint64,
-           "u64": np.uint64}
+           "u64": np.uint64, "f64": np.uint64, "i8": np.uint8, "u8": np.uint8}
 
 
-FLOATS = ("f32", "bf16", "f16", "e4m3", "e5m2")
+FLOATS = ("f32", "bf16", "f16", "e4m3", "e5m2", "f64")
 
 
 def torch_dtype(dtype: str):
@@ -18,7 +18,8 @@ def torch_dtype(dtype: str):
     import torch
     return {"f32": torch.float32, "bf16": torch.bfloat16, "i32": torch.int32,
             "u32": torch.int32, "f16": torch.float16, "e4m3": torch.uint8,
-            "e5m2": torch.uint8, "i64": torch.int64, "u64": torch.int64}[dtype]
+            "e5m2": torch.uint8, "i64": torch.int64, "u64": torch.int64,
+            "f64": torch.float64, "i8": torch.int8, "u8": torch.uint8}[dtype]
 
 
 def to_dev(a: np.ndarray, dtype: str, device="cuda"):
@@ -31,8 +32,12 @@ def to_dev(a: np.ndarray, dtype: str, device="cuda"):
         t = torch.from_numpy(a.view(np.int16)).view(torch.float16)
     elif dtype == "f32":
         t = torch.from_numpy(a.astype(np.float32, copy=False))
-    elif dtype in ("e4m3", "e5m2"):
+    elif dtype in ("e4m3", "e5m2", "u8"):
         t = torch.from_numpy(a.view(np.uint8))
+    elif dtype == "i8":
+        t = torch.from_numpy(a.view(np.int8))
+    elif dtype == "f64":
+        t = torch.from_numpy(a.view(np.float64))
     elif dtype in ("i64", "u64"):
         t = torch.from_numpy(a.view(np.int64))
     else:
@@ -63,6 +68,8 @@ def nan_mask(b: np.ndarray, dtype: str) -> np.ndarray:
         return ((b & 0x7C) == 0x7C) & ((b & 0x3) != 0)
     if dtype == "e4m3":
         return (b & 0x7F) == 0x7F
+    if dtype == "f64":
+        return ((b & 0x7FF0000000000000) == 0x7FF0000000000000) & ((b & 0xFFFFFFFFFFFFF) != 0)
     return np.zeros(b.shape, bool)
 
 

@@ -75,11 +75,13 @@ def test_header_compiles(tmp_path, compiler, lang):
 
 
 def test_constants(L):
-    assert L.xred_version() == 20000   # 2.0.0: major*10000 + minor*100 + patch
+    assert L.xred_version() == 20100   # 2.1.0: major*10000 + minor*100 + patch
     assert L.xred_acc_elem_size(0) == 4 and L.xred_acc_elem_size(1) == 4
     assert L.xred_acc_elem_size(2) == 4 and L.xred_acc_elem_size(7) == 4
     assert L.xred_acc_elem_size(5) == 8 and L.xred_acc_elem_size(6) == 8
-    assert L.xred_acc_elem_size(99) == 0
+    assert L.xred_acc_elem_size(9) == 8                                  # fp64: binary64
+    assert L.xred_acc_elem_size(10) == 4 and L.xred_acc_elem_size(11) == 4   # int8/uint8: uint32
+    assert L.xred_acc_elem_size(12) == 0 and L.xred_acc_elem_size(99) == 0
     assert L.xred_status_string(0) == b"success"
     assert L.xred_status_string(3) == b"buffers overlap"
 
@@ -101,7 +103,10 @@ def ptrs(*xs):
     (lambda L: L.xred_allreduce_local(ptrs(A), 1, S(A + 4096), 16, 99, 0, None), 1),
     (lambda L: L.xred_allreduce_local(ptrs(A), 1, S(A + 4096), 16, 0, 9, None), 1),
     (lambda L: L.xred_allreduce_local(ptrs(A), 1, S(A + 4096), 16, 3, 4, None), 2),  # int AVG
-    (lambda L: L.xred_allreduce_local(ptrs(A), 1, S(A + 4096), 16, 9, 0, None), 1),
+    (lambda L: L.xred_allreduce_local(ptrs(A), 1, S(A + 4096), 16, 12, 0, None), 1),
+    (lambda L: L.xred_allreduce_local(ptrs(A + 4), 1, S(A + 4096), 16, 9, 0, None), 1),  # f64 align
+    (lambda L: L.xred_allreduce_local(ptrs(A), 1, S(A + 4096), 16, 10, 4, None), 2),  # int8 AVG
+    (lambda L: L.xred_allreduce_local(ptrs(A), 1, S(A + 4096), 16, 11, 4, None), 2),  # uint8 AVG
     (lambda L: L.xred_allreduce_local(ptrs(A), 1, S(A + 4096), 16, 0, 5, None), 1),
     (lambda L: L.xred_allreduce_local(ptrs(A + 4), 1, S(A + 4096), 16, 5, 0, None), 1),  # i64 align
     (lambda L: L.xred_allreduce_local(None, 1, S(A + 4096), 16, 0, 0, None), 1),
@@ -135,6 +140,9 @@ def ptrs(*xs):
     (lambda L: L.xred_ring_reduce(ptrs(A), 1, S(A + 4096), 16, 1, 4, None, 1, 0, None, None), 2),
     (lambda L: L.xred_reduce_copy_step(S(A), S(A + 4096), S(0), 16, 0, 4, 0, None), 2),  # AVG
     (lambda L: L.xred_reduce_copy_step(S(A), S(A + 4100), S(0), 16, 5, 0, 0, None), 1),  # u64 acc
+    (lambda L: L.xred_reduce_copy_step(S(A), S(A + 4100), S(0), 16, 9, 0, 0, None), 1),  # f64 acc
+    (lambda L: L.xred_reduce_copy_step(S(A), S(A + 4098), S(0), 16, 10, 0, 0, None), 1),  # i8 acc
+    (lambda L: L.xred_reduce_copy_step(S(A), S(A + 4096), S(0), 16, 9, 4, 0, None), 2),  # f64 AVG
     # xred_allreduce_sim(sends, recvs, nranks, count, dtype, op, schedule, stream)
     (lambda L: L.xred_allreduce_sim(ptrs(A), ptrs(A + 8192), 0, 16, 1, 0, 0, None), 1),
     (lambda L: L.xred_allreduce_sim(ptrs(A), ptrs(A + 8192), 65, 16, 1, 0, 0, None), 1),
@@ -222,7 +230,8 @@ def test_torch_dtypes_map_to_codes():
     torch = pytest.importorskip("torch")
     import paper_2510_20171_amd as xr
     cases = {torch.float32: "f32", torch.bfloat16: "bf16", torch.float16: "f16",
-             torch.int32: "i32", torch.int64: "i64"}
+             torch.int32: "i32", torch.int64: "i64", torch.float64: "f64", torch.int8: "i8",
+             torch.uint8: "u8"}
     for name, code in (("float8_e4m3fn", "e4m3"), ("float8_e5m2", "e5m2"), ("uint32", "u32"),
                        ("uint64", "u64")):
         if hasattr(torch, name):

@@ -34,7 +34,7 @@ pytestmark = pytest.mark.gpu
 torch = pytest.importorskip("torch")
 
 ES = {"f32": 4, "bf16": 2, "f16": 2, "e4m3": 1, "e5m2": 1, "i32": 4, "u32": 4, "i64": 8,
-      "u64": 8}
+      "u64": 8, "f64": 8, "i8": 1, "u8": 1}
 
 
 @pytest.fixture(scope="module")
@@ -223,7 +223,8 @@ def test_device_batch_queue_item_limit(xr, orc, K):
     gu.assert_parity(out, orc.allreduce_local(srcs_np, "i32", "sum"), "i32", "sum", f"K={K}")
 
 
-RAND_DTYPES = ("f32", "bf16", "f16", "e4m3", "e5m2", "i32", "u32", "i64", "u64")
+RAND_DTYPES = ("f32", "bf16", "f16", "e4m3", "e5m2", "i32", "u32", "i64", "u64", "f64",
+               "i8", "u8")
 
 
 @pytest.mark.parametrize("seed", range(4))

@@ -1,12 +1,12 @@
 """GPU parity of the further element types (fp16, OCP fp8 e4m3 / e5m2, int64,
-uint64) and of AVG, against the CPU oracle, bit for bit (NaN payloads of float
-sum/prod/avg compare by NaN-ness only).
+uint64, fp64, int8, uint8) and of AVG, against the CPU oracle, bit for bit
+(NaN payloads of float sum/prod/avg compare by NaN-ness only).
 
 Covered for every new dtype x op: the fused reduce over source counts 1..33
 and sizes from one element to several tiles with ragged tails; a size past
 the one-round tile-shape switch; element-aligned buffers (scalar path);
-reduce-scatter; every step-wise flag with the closing cast (binary32 or
-uint64 accumulator); batched items; all steps in one launch (ring); the
+reduce-scatter; every step-wise flag with the closing cast (binary32,
+binary64, uint32 or uint64 accumulator); batched items; all steps in one launch (ring); the
 simulated ring and halving-doubling schedules.  AVG runs on every float type
 through the fused, reduce-scatter and batched paths.
 """
@@ -22,7 +22,7 @@ import workloads as wl
 pytestmark = pytest.mark.gpu
 torch = pytest.importorskip("torch")
 
-NEW = ("f16", "e4m3", "e5m2", "i64", "u64")
+NEW = ("f16", "e4m3", "e5m2", "i64", "u64", "f64", "i8", "u8")
 CORES = min(16, len(os.sched_getaffinity(0)))
 
 
@@ -67,11 +67,12 @@ def test_fused_matrix(xr, orc, dtype):
 
 
 @pytest.mark.parametrize("dtype,op", [("e4m3", "sum"), ("f16", "avg"), ("i64", "max"),
-                                      ("e5m2", "prod")])
+                                      ("e5m2", "prod"), ("f64", "avg"), ("f64", "min"),
+                                      ("i8", "sum"), ("u8", "max")])
 def test_past_one_round(xr, orc, dtype, op):
     """Sizes beyond the one-round launch (occupancy-capped tiles), ragged."""
     cus = torch.cuda.get_device_properties(0).multi_processor_count
-    vec = {"f16": 8, "e4m3": 16, "e5m2": 16, "i64": 2}[dtype]
+    vec = {"f16": 8, "e4m3": 16, "e5m2": 16, "i64": 2, "f64": 2, "i8": 16, "u8": 16}[dtype]
     n = cus * 4 * 512 * vec * 2 + 77
     rng = np.random.default_rng(7)
     base = [pins.random_column_values(rng, dtype, 65536 + 13 + 2 * p) for p in range(8)]
@@ -114,8 +115,9 @@ def test_reduce_scatter(xr, orc, dtype):
 @pytest.mark.parametrize("dtype", NEW)
 def test_stepwise(xr, orc, dtype):
     rng = np.random.default_rng(13)
-    acc_t = torch.int64 if dtype in ("i64", "u64") else torch.float32
-    acc_bits = "u64" if dtype in ("i64", "u64") else "f32"
+    acc_t, acc_bits = {"i64": (torch.int64, "u64"), "u64": (torch.int64, "u64"),
+                       "f64": (torch.float64, "f64"), "i8": (torch.int32, "u32"),
+                       "u8": (torch.int32, "u32")}.get(dtype, (torch.float32, "f32"))
     for op in ("sum", "max", "prod"):
         for n in (4096 * 3 + 7, 999):
             chunks = [pins.random_column_values(rng, dtype, n) for _ in range(5)]

@@ -18,9 +18,10 @@ import pins
 pytestmark = pytest.mark.gpu
 torch = pytest.importorskip("torch")
 
-DTYPES = ("f32", "bf16", "f16", "e4m3", "e5m2", "i32", "u32", "i64", "u64")
+DTYPES = ("f32", "bf16", "f16", "e4m3", "e5m2", "i32", "u32", "i64", "u64", "f64", "i8",
+          "u8")
 ES = {"f32": 4, "bf16": 2, "f16": 2, "e4m3": 1, "e5m2": 1, "i32": 4, "u32": 4, "i64": 8,
-      "u64": 8}
+      "u64": 8, "f64": 8, "i8": 1, "u8": 1}
 CASES = 40
 
 
