@@ -516,9 +516,10 @@ def secondary(torch, xr, L, timer, wl, flush, res):
     res["large_p8_bf16"] = big
 
     # co-scheduling: P=8 bf16 x 8 MiB reduces on one stream while bf16 8192^3
-    # matrix products run on another (both default priority), per CU budget;
-    # the reduce loop alone lasts about as long as the products
-    sg, sr = torch.cuda.Stream(), torch.cuda.Stream()
+    # matrix products run on another (both default priority), on two ordinary
+    # streams (per workgroup budget) and on the two streams of a CU partition
+    # (the reduce on 16 or 32 CUs, the products on the others); the reduce loop
+    # alone lasts about as long as the products
     n = 4 << 20
     d = [torch.randn(n, device="cuda").to(torch.bfloat16) for _ in range(8)]
     out = torch.empty_like(d[0])
@@ -528,7 +529,7 @@ def secondary(torch, xr, L, timer, wl, flush, res):
     gc = torch.empty_like(ga)
     reps_g = 20
 
-    def run(g, reps_r):
+    def run(sg, sr, g, reps_r):
         """(products' span, reduces' span, span of both) in ms."""
         ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
         torch.cuda.synchronize()
@@ -548,31 +549,50 @@ def secondary(torch, xr, L, timer, wl, flush, res):
         both = max(ends) - min(0.0, ev[0].elapsed_time(ev[2]))
         return ev[0].elapsed_time(ev[1]), ev[2].elapsed_time(ev[3]), both
 
-    run(True, 10)
-    g_alone, _, _ = run(True, 0)
-    co = {"gemm_alone_ms": round(g_alone / reps_g, 3),
-          "gemm_TFLOPs": round(2 * 8192 ** 3 * reps_g / g_alone / 1e9, 0)}
+    def pair(sg, sr):
+        """The two loops alone and together on streams sg (products) and sr."""
+        run(sg, sr, True, 10)
+        g_alone, _, _ = run(sg, sr, True, 0)
+        _, r1, _ = run(sg, sr, False, 100)
+        reps = max(10, int(g_alone / (r1 / 100)))
+        _, r_alone, _ = run(sg, sr, False, reps)
+        g_with, r_with, both = run(sg, sr, True, reps)
+        # the two streams overlapped only if both finished well before
+        # the sum of their times alone
+        overlapped = both < 0.9 * (g_alone + r_alone)
+        e = {"gemm_ms_alone": round(g_alone / reps_g, 3),
+             "reduce_us_alone": round(r_alone / reps * 1e3, 1),
+             "reduce_GBs_alone": round(9 * n * 2 * reps / r_alone / 1e6, 1),
+             "reduce_us_with_gemm": round(r_with / reps * 1e3, 1),
+             "span_both_ms": round(both, 3), "sum_alone_ms": round(g_alone + r_alone, 3),
+             "overlapped": overlapped}
+        if overlapped:
+            e["gemm_slowdown_pct"] = round(100 * (g_with / g_alone - 1), 1)
+        return e, reps
+
+    sg, sr = torch.cuda.Stream(), torch.cuda.Stream()
+    run(sg, sr, True, 10)
+    g_full, _, _ = run(sg, sr, True, 0)
+    co = {"gemm_alone_ms": round(g_full / reps_g, 3),
+          "gemm_TFLOPs": round(2 * 8192 ** 3 * reps_g / g_full / 1e9, 0)}
     prev = xr.set_max_workgroups(0)
     try:
-        for budget in (16, 64, 0):
+        for budget in (16, 0):
             xr.set_max_workgroups(budget)
-            _, r1, _ = run(False, 100)
-            reps = max(10, int(g_alone / (r1 / 100)))
-            _, r_alone, _ = run(False, reps)
-            g_with, r_with, both = run(True, reps)
-            # the two streams overlapped only if both finished well before
-            # the sum of their times alone
-            overlapped = both < 0.9 * (g_alone + r_alone)
-            entry = {"reduce_us_alone": round(r_alone / reps * 1e3, 1),
-                     "reduce_us_with_gemm": round(r_with / reps * 1e3, 1),
-                     "span_both_ms": round(both, 3),
-                     "sum_alone_ms": round(g_alone + r_alone, 3),
-                     "overlapped": overlapped}
-            if overlapped:
-                entry["gemm_slowdown_pct"] = round(100 * (g_with / g_alone - 1), 1)
-            co[f"budget_{budget or 'none'}"] = entry
+            co[f"streams_budget_{budget or 'none'}"], _ = pair(sg, sr)
     finally:
         xr.set_max_workgroups(prev)
+    # the same work on the whole chip, one loop after the other
+    _, r_full, _ = run(sg, sr, False, 200)
+    for ncu in (16, 32):
+        a, b = xr.stream_create_partition(ncu)
+        try:
+            e, reps = pair(torch.cuda.ExternalStream(b), torch.cuda.ExternalStream(a))
+        finally:
+            xr.stream_destroy(a)
+            xr.stream_destroy(b)
+        e["serial_on_all_cus_ms"] = round(g_full + r_full / 200 * reps, 3)
+        co[f"partition_{ncu}_cus"] = e
     res["coschedule_gemm_bf16"] = co
     del d, out, ga, gb, gc
     return res

@@ -368,12 +368,45 @@ XRED_API size_t xred_sim_chunk(size_t count, int nranks);
  * behind the network (Section 5).  Results do not depend on it.  Process-wide;
  * returns the previous value.  xred_ring_reduce applies it too, but never goes
  * below the workgroups its on-chip accumulators need (one per 4 tiles).
- * The budget bounds the workgroups a launch may have in flight; whether a
- * reduce on one stream runs concurrently with a kernel on another is up to
- * the runtime's hardware queues (on the measured box a reduce and a bf16
- * matrix product on two streams did not overlap, capped or not).
+ * The budget bounds the workgroups a launch may have in flight; it does not
+ * make a reduce run beside a kernel that fills the chip: on MI355X a bf16
+ * matrix product's workgroups take whole CUs, and a reduce on another stream
+ * waits for free CUs and then runs alone (measured: the two streams take the
+ * sum of their times, capped or not).  xred_stream_create_partition gives the
+ * reduce CUs of its own.
  */
 XRED_API unsigned xred_set_max_workgroups(unsigned max_workgroups);
+
+/*
+ * Co-scheduling by a CU partition (the paper keeps its collective kernels to
+ * a few thread blocks so compute keeps the rest of the GPU, Section 5).
+ * Creates, on the current device, a HIP stream whose kernels run only on
+ * `ncu` compute units, ncu / X of them on each of the device's X XCDs, and,
+ * if `rest` is not NULL, a second stream whose kernels run only on all the
+ * other CUs.  Kernels on the two streams then run at the same time, each on
+ * its own CUs: a reduce launched on *stream beside a matrix product on *rest
+ * (measured on MI355X: P=8 x 8 MiB bf16 reduces on 16 CUs at ~1 TB/s,
+ * concurrently with the product).  A kernel sized for the whole chip runs
+ * slower on a partition than the CU count alone suggests (torch's bf16
+ * matrix products lost ~40 % on any partial CU set), so the partition pays
+ * off only where the compute side tolerates it.
+ *   ncu     a positive multiple of X below the CU count (256 CUs, X = 8 on
+ *           MI355X: 8, 16, ..., 248)
+ *   stream  receives the new stream (a hipStream_t); NULL on failure
+ *   rest    NULL, or receives the second stream; NULL on failure
+ * Each stream is a hardware queue of its own; the runtime has few per process
+ * and refuses more with XRED_HIP_ERROR (nothing is created then).  The
+ * streams are ordinary HIP streams to every libxred entry point and to other
+ * libraries; destroy them with xred_stream_destroy or hipStreamDestroy.
+ * Errors: XRED_INVALID_ARGUMENT (stream NULL, ncu out of range),
+ * XRED_UNSUPPORTED (CU count not a multiple of the XCD count),
+ * XRED_HIP_ERROR.
+ */
+XRED_API xred_status xred_stream_create_partition(int ncu, void **stream, void **rest);
+
+/* Waits for the work enqueued on `stream` (not NULL), then destroys it.
+ * Errors: XRED_INVALID_ARGUMENT, XRED_HIP_ERROR. */
+XRED_API xred_status xred_stream_destroy(void *stream);
 
 /* Bytes per accumulator element for dtype: 4 (binary32 or uint32), 8
  * (binary64 for fp64, uint64 for int64/uint64), 0 if unknown. */

@@ -28,7 +28,7 @@ from ._lib import (ACC_SIZE, ALIAS, DTYPE, ELEM_SIZE, EXPORTS, HIP_ERROR, INVALI
 __all__ = ["allreduce_local", "reduce_scatter_local", "reduce_copy_step", "acc_cast",
            "batched_reduce_noalloc",
            "batched_reduce", "ring_reduce", "ring_max_count", "allreduce_sim", "sim_chunk",
-           "set_max_workgroups", "pack_items", "acc_elem_size", "version", "release",
+           "set_max_workgroups", "stream_create_partition", "stream_destroy", "pack_items", "acc_elem_size", "version", "release",
            "XredError", "load", "EXPORTS"]
 
 
@@ -249,6 +249,20 @@ def ring_max_count(dtype: str) -> int:
 def set_max_workgroups(n: int) -> int:
     """CU budget for later launches (0 = none); returns the previous value."""
     return int(load().xred_set_max_workgroups(n))
+
+
+def stream_create_partition(ncu: int, rest: bool = True):
+    """Streams on a CU partition of the current device (xred_stream_create_partition):
+    (handle on ncu CUs, handle on the other CUs or None), as integers."""
+    a, b = ctypes.c_void_p(), ctypes.c_void_p()
+    check(load().xred_stream_create_partition(ncu, ctypes.byref(a),
+                                              ctypes.byref(b) if rest else None))
+    return a.value, (b.value if rest else None)
+
+
+def stream_destroy(handle: int) -> None:
+    """xred_stream_destroy: waits for the stream's work, then destroys it."""
+    check(load().xred_stream_destroy(handle))
 
 
 def acc_elem_size(dtype: str) -> int:

@@ -42,7 +42,9 @@ class XredItem(ctypes.Structure):
 EXPORTS = ("xred_allreduce_local", "xred_reduce_scatter_local", "xred_reduce_copy_step",
            "xred_acc_cast", "xred_batched_reduce", "xred_batched_reduce_noalloc",
            "xred_ring_reduce", "xred_ring_max_count",
-           "xred_allreduce_sim", "xred_sim_chunk", "xred_set_max_workgroups", "xred_acc_elem_size", "xred_status_string",
+           "xred_allreduce_sim", "xred_sim_chunk", "xred_set_max_workgroups",
+           "xred_stream_create_partition", "xred_stream_destroy", "xred_acc_elem_size",
+           "xred_status_string",
            "xred_last_error", "xred_version", "xred_release")
 
 _lib = None
@@ -88,8 +90,11 @@ def load(path: Path = LIB_PATH) -> ctypes.CDLL:
     L.xred_ring_max_count.restype = sz
     for f in ("xred_allreduce_local", "xred_reduce_scatter_local", "xred_reduce_copy_step",
               "xred_acc_cast", "xred_batched_reduce", "xred_batched_reduce_noalloc",
-              "xred_ring_reduce", "xred_allreduce_sim"):
+              "xred_ring_reduce", "xred_allreduce_sim", "xred_stream_create_partition",
+              "xred_stream_destroy"):
         getattr(L, f).restype = ctypes.c_int
+    L.xred_stream_create_partition.argtypes = [i32, ctypes.POINTER(vp), ctypes.POINTER(vp)]
+    L.xred_stream_destroy.argtypes = [vp]
     L.xred_set_max_workgroups.argtypes = [ctypes.c_uint]
     L.xred_set_max_workgroups.restype = ctypes.c_uint
     L.xred_acc_elem_size.argtypes = [i32]

@@ -286,3 +286,40 @@ xred_ceiling_handoff(int rounds, int relay, int limit_ms, double *rtt_us, uint32
     (void)hipHostFree(host);
     return e != hipSuccess ? (int)e : rc;
 }
+
+// ------------------------------------------------------------ placement --
+// Where the workgroups of a launch on `stream` ran: one word per workgroup,
+// xcd << 16 | se << 8 | sh << 4 | cu, from the hardware's XCC_ID register
+// and the shader-engine, shader-array and CU fields of its HW_ID register (a
+// CU's address within its XCD).  Every workgroup of 1024 threads (at most
+// two fit on a CU) sleeps about 10 us before it records, so later
+// workgroups find the CUs they could use busy and spread over all of them.
+namespace {
+
+constexpr int kPlaceThreads = 1024;
+
+__global__ __launch_bounds__(kPlaceThreads) void placement_kernel(uint32_t *out, unsigned n)
+{
+#pragma unroll
+    for (int i = 0; i < 3; ++i) __builtin_amdgcn_s_sleep(127);
+    if (threadIdx.x != 0 || blockIdx.x >= n) return;
+    // s_getreg operand: register id | first bit << 6 | (bits - 1) << 11
+    const uint32_t hw = __builtin_amdgcn_s_getreg(4 | (0 << 6) | (31 << 11));    // HW_ID
+    const uint32_t xcc = __builtin_amdgcn_s_getreg(20 | (0 << 6) | (31 << 11));  // XCC_ID
+    const uint32_t cu = (hw >> 8) & 0xF, sh = (hw >> 12) & 1, se = (hw >> 13) & 7;
+    out[blockIdx.x] = (xcc & 0xF) << 16 | se << 8 | sh << 4 | cu;
+}
+
+}  // namespace
+
+// Runs `grid` workgroups of the placement kernel on `stream` and writes each
+// one's XCD and CU to out[0..grid) (device memory).  Stream-ordered; returns
+// the hipError_t of the launch.
+extern "C" __attribute__((visibility("default"))) int
+xred_ceiling_placement(uint32_t *out, unsigned grid, void *stream)
+{
+    if (out == nullptr || grid == 0) return (int)hipErrorInvalidValue;
+    hipLaunchKernelGGL(placement_kernel, dim3(grid), dim3(kPlaceThreads), 0,
+                       (hipStream_t)stream, out, grid);
+    return (int)hipGetLastError();
+}

@@ -950,6 +950,69 @@ XRED_API unsigned xred_set_max_workgroups(unsigned max_workgroups)
     return g_max_workgroups.exchange(max_workgroups);
 }
 
+}  // extern "C"
+
+namespace {
+__global__ void empty_kernel() {}
+}  // namespace
+
+extern "C" {
+
+XRED_API xred_status xred_stream_create_partition(int ncu, void **stream, void **rest)
+{
+    if (trace_enabled())
+        trace_printf("xred_stream_create_partition ncu=%d rest=%s", ncu, rest ? "yes" : "no");
+    if (stream == nullptr) return fail(XRED_INVALID_ARGUMENT, "stream is NULL");
+    *stream = nullptr;
+    if (rest != nullptr) *rest = nullptr;
+    if (ncu < 1) return fail(XRED_INVALID_ARGUMENT, "ncu = %d", ncu);
+    int dev = 0, cus = 0, xcds = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e == hipSuccess) e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev);
+    if (e == hipSuccess) e = hipDeviceGetAttribute(&xcds, hipDeviceAttributeNumberOfXccs, dev);
+    if (e != hipSuccess) return hip_fail(e, "device query");
+    if (xcds < 1) xcds = 1;
+    // bit b of a queue's CU mask is CU b / xcds of XCD b % xcds, so the
+    // first ncu bits give every XCD ncu / xcds CUs (and the rest the others)
+    constexpr int kMaxMaskWords = 32;
+    if (cus % xcds != 0 || cus > 32 * kMaxMaskWords)
+        return fail(XRED_UNSUPPORTED, "%d CUs over %d XCDs", cus, xcds);
+    if (ncu % xcds != 0 || ncu >= cus)
+        return fail(XRED_INVALID_ARGUMENT, "ncu = %d: a multiple of the %d XCDs below %d needed",
+                    ncu, xcds, cus);
+    uint32_t mine[kMaxMaskWords] = {}, other[kMaxMaskWords] = {};
+    const uint32_t nwords = (uint32_t)(cus + 31) / 32;
+    for (int b = 0; b < cus; ++b) (b < ncu ? mine : other)[b / 32] |= 1u << (b % 32);
+    hipStream_t made[2] = {nullptr, nullptr};
+    const int want = rest != nullptr ? 2 : 1;
+    for (int i = 0; i < want && e == hipSuccess; ++i) {
+        e = hipExtStreamCreateWithCUMask(&made[i], nwords, i == 0 ? mine : other);
+        // the runtime may set a queue up at its first use: an empty kernel
+        // and a wait here turn a queue it cannot give into an error of this call
+        if (e == hipSuccess) e = launch_kernel(empty_kernel, dim3(1), dim3(64), 0, made[i]);
+        if (e == hipSuccess) e = hipStreamSynchronize(made[i]);
+    }
+    if (e != hipSuccess) {
+        for (hipStream_t s : made)
+            if (s != nullptr) (void)hipStreamDestroy(s);
+        return hip_fail(e, "CU-masked stream");
+    }
+    *stream = made[0];
+    if (rest != nullptr) *rest = made[1];
+    return XRED_SUCCESS;
+}
+
+XRED_API xred_status xred_stream_destroy(void *stream)
+{
+    if (trace_enabled()) trace_printf("xred_stream_destroy stream=%p", stream);
+    if (stream == nullptr) return fail(XRED_INVALID_ARGUMENT, "stream is NULL");
+    // its work ends first, so a stream created later under the same handle
+    // finds the handle's device words as this one left them
+    hipError_t e = hipStreamSynchronize((hipStream_t)stream);
+    if (e == hipSuccess) e = hipStreamDestroy((hipStream_t)stream);
+    return e == hipSuccess ? XRED_SUCCESS : hip_fail(e, "hipStreamDestroy");
+}
+
 XRED_API size_t xred_acc_elem_size(xred_dtype dtype)
 {
     return known_dtype(dtype) ? acc_size(dtype) : 0;

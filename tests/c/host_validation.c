@@ -171,6 +171,15 @@ int main(void)
     if (xred_version() <= 0) ++failures;
     if (xred_acc_elem_size(XRED_INT64) != 8 || xred_acc_elem_size((xred_dtype)99) != 0) ++failures;
     if (xred_sim_chunk(1000, 8) == 0 || xred_sim_chunk(1000, 0) != 0) ++failures;
+    /* CU partition: slot checks first, then the device query fails */
+    void *ps = (void *)1, *pr = (void *)1;
+    EXPECT(xred_stream_create_partition(16, NULL, &pr), XRED_INVALID_ARGUMENT);
+    EXPECT(xred_stream_create_partition(0, &ps, &pr), XRED_INVALID_ARGUMENT);
+    if (ps != NULL || pr != NULL) ++failures;
+    ps = (void *)1;
+    EXPECT(xred_stream_create_partition(16, &ps, NULL), NODEV);
+    if (ps != NULL) ++failures;
+    EXPECT(xred_stream_destroy(NULL), XRED_INVALID_ARGUMENT);
     const unsigned prev = xred_set_max_workgroups(7);
     if (xred_set_max_workgroups(prev) != 7) ++failures;
     xred_release();

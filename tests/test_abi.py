@@ -53,7 +53,8 @@ def test_measuring_library_exports(L):
     out = subprocess.run(["nm", "-D", "--defined-only", str(lib)],
                          capture_output=True, text=True, check=True).stdout
     exported = {l.split()[-1] for l in out.splitlines() if " T " in l}
-    assert {"xred_ceiling_mix", "xred_ceiling_handoff"} <= exported, exported
+    assert {"xred_ceiling_mix", "xred_ceiling_handoff", "xred_ceiling_placement"} <= exported, \
+        exported
     C = ctypes.CDLL(str(lib))
     f = C.xred_ceiling_handoff
     f.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p,
@@ -61,6 +62,10 @@ def test_measuring_library_exports(L):
     # argument checks come before any HIP call (hipErrorInvalidValue = 1)
     assert f(0, 0, 1000, None, None, None, None) == 1
     assert f(4, 0, 0, None, None, None, None) == 1
+    g = C.xred_ceiling_placement
+    g.argtypes = [ctypes.c_void_p, ctypes.c_uint, ctypes.c_void_p]
+    assert g(None, 16, None) == 1
+    assert g(ctypes.c_void_p(4096), 0, None) == 1
 
 
 @pytest.mark.parametrize("compiler,lang", [("gcc", "c"), ("g++", "c++")])
@@ -206,6 +211,20 @@ def test_zero_counts_succeed_without_launch(L):
     assert L.xred_batched_reduce(it, 2, 1, 0, 0, None) == 0
     assert L.xred_allreduce_sim(ptrs(A, A + 4096), ptrs(A + 8192, A + 12288), 2, 0, 1, 0, 0,
                                 None) == 0
+
+
+def test_partition_argument_checks(L):
+    """The CU partition's argument checks that need no device: a NULL stream
+    slot or a CU count below one is rejected, and nothing is written to the
+    slots but NULL."""
+    a, b = ctypes.c_void_p(1234), ctypes.c_void_p(5678)
+    assert L.xred_stream_create_partition(16, None, ctypes.byref(b)) == 1
+    assert L.xred_stream_create_partition(0, ctypes.byref(a), ctypes.byref(b)) == 1
+    assert a.value is None and b.value is None
+    a = ctypes.c_void_p(1234)
+    assert L.xred_stream_create_partition(-8, ctypes.byref(a), None) == 1
+    assert a.value is None
+    assert L.xred_stream_destroy(None) == 1
 
 
 def test_sim_chunk_rule(L):
