@@ -32,9 +32,32 @@
 namespace xred {
 namespace {
 
-constexpr int kB = 256;    // threads per workgroup
+constexpr int kB = 256;    // threads per workgroup of the per-step kernels
 constexpr int kU = 1;      // 16-byte vectors per thread per tile
-constexpr int kRingWavesPerCu = 12;   // resident waves per CU of the one-launch ring
+// Workgroup shape of the one-launch kernel, per schedule and size: threads,
+// and resident waves per CU (0: no cap).  Measured with 8 ranks x 64M bf16
+// on three buffer layouts (separate allocations, allocations among freed
+// holes, slices of one allocation), in microseconds against the
+// traffic-only kernel with the same 8 reads and 8 writes at its best cap
+// (340 / 352-355 / 344-345):
+//   ring  512 threads, 8 waves (one workgroup per CU): 342-343 / 348-352 /
+//         344-345; 256 threads, 12 waves: 357 / 369-375 / 383-384; 128
+//         threads, 8 waves: 340-342 / 352-359 / 343-344; 512 threads, 16 or
+//         24 waves: 383-395; 1024 threads, 16 waves: 386-410
+//   RHD   (more partials live in registers) 64 threads, 16 waves: 347 / 345
+//         / 351; 64 threads uncapped: 353-356; 128 threads uncapped:
+//         363-367; 128 threads, 8 / 12 / 16 waves: 489 / 421-427 / 356-381;
+//         256 threads uncapped: 380-383 / 393-394 / 410-413
+// Below 8 MiB per rank the launch is a few rounds long and the smaller
+// workgroups lose (8 ranks of 1M bf16: RHD 10.2 against 6.9 us, ring 6.7
+// against 6.5; at 4M: ring 21.3 against 24.6, RHD 25.5 against 26.9), so
+// such calls keep 256 threads, 12 waves (ring) and uncapped (RHD).
+struct SimShape {
+    int threads, waves;
+};
+constexpr SimShape kRingShape{512, 8}, kRhdShape{64, 16};
+constexpr SimShape kRingSmallShape{256, 12}, kRhdSmallShape{256, 0};
+constexpr uint64_t kSimLargeBytes = 8u << 20;   // bytes per rank from which the large shapes run
 
 // One step: rank q's message, own contribution and output, already offset to
 // the chunk (or group of blocks) the rank works on, and its length.
@@ -289,11 +312,11 @@ __device__ __forceinline__ void fold_chunk(const SimAll &a, int G, int lg, int c
 // buffers (items dealt chunk by chunk in turn spread them over G places in
 // each: 8 ranks x 64M bf16, ring, 12 waves per CU, 355 against 374 us).
 // VEC: 16-byte aligned buffers; otherwise one element per thread.
-template <class T, class Op, bool RHD, bool VEC>
-__global__ __launch_bounds__(kB) void sim_all_kernel(SimAll a, int G, int lg, uint64_t M,
+template <class T, class Op, bool RHD, bool VEC, int BT>
+__global__ __launch_bounds__(BT) void sim_all_kernel(SimAll a, int G, int lg, uint64_t M,
                                                      uint64_t count, uint64_t tiles)
 {
-    constexpr uint32_t kTileBytes = (uint32_t)kB * 16u;
+    constexpr uint32_t kTileBytes = (uint32_t)BT * 16u;
     const uint64_t work = tiles * (uint64_t)G;
     for (uint64_t w = blockIdx.x; w < work; w += gridDim.x) {
         const int c = (int)(w / tiles);
@@ -315,10 +338,28 @@ __global__ __launch_bounds__(kB) void sim_all_kernel(SimAll a, int G, int lg, ui
                                        Lane<T, false>{lo + nvec * T::kVec + threadIdx.x});
             }
         } else {
-            const uint64_t e = t * kB + threadIdx.x;
+            const uint64_t e = t * BT + threadIdx.x;
             if (e < len) fold_chunk<T, Op, RHD>(a, G, lg, c, Lane<T, false>{lo + e});
         }
     }
+}
+
+// One launch of sim_all_kernel with BT threads per workgroup, at most
+// `waves` resident waves per CU (0: no cap) through an LDS reservation no
+// thread touches.
+template <class T, class Op, bool RHD, int BT>
+hipError_t launch_all_shape(const SimAll &a, int G, int lg, uint64_t M, size_t count, bool vec,
+                            int waves, hipStream_t s)
+{
+    const uint64_t tiles = vec ? (M * T::kSize + BT * 16u - 1) / (BT * 16u) + 1 : (M + BT - 1) / BT;
+    const dim3 grid(grid_for(tiles * (uint64_t)G));
+    const int wgs = waves / (BT / 64) > 0 ? waves / (BT / 64) : 1;
+    const size_t lds = waves > 0 ? (size_t)(lds_per_cu() / wgs) / 512 * 512 : 0;
+    if (vec)
+        return launch_kernel(sim_all_kernel<T, Op, RHD, true, BT>, grid, dim3(BT), lds, s, a, G,
+                             lg, M, (uint64_t)count, tiles);
+    return launch_kernel(sim_all_kernel<T, Op, RHD, false, BT>, grid, dim3(BT), lds, s, a, G, lg,
+                         M, (uint64_t)count, tiles);
 }
 
 template <class T, class Op>
@@ -333,26 +374,18 @@ hipError_t launch_all(const char *const *send, char *const *recv, int G, size_t 
     int lg = 0;
     while ((1 << lg) < G) ++lg;
     const uint64_t M = sim_chunk(count, G);
-    const uint64_t tiles = vec ? (M * T::kSize + kB * 16u - 1) / (kB * 16u) + 1 : (M + kB - 1) / kB;
-    const dim3 grid(grid_for(tiles * (uint64_t)G));
-    // The ring's G reads and G writes per element stream fastest with about
-    // 12 resident waves per CU, set by an LDS reservation no thread touches
-    // (8 ranks x 64M bf16: 355 us against 391 us uncapped; the traffic-only
-    // kernel with the same streams peaks at 8-12 waves); halving-doubling
-    // keeps more partials in registers and runs best uncapped (383 against
-    // 495 us capped).
-    const size_t lds = rhd ? 0 : (size_t)(lds_per_cu() / (kRingWavesPerCu / (kB / 64))) / 512 * 512;
-    if (rhd && vec)
-        return launch_kernel(sim_all_kernel<T, Op, true, true>, grid, dim3(kB), lds, s, a, G, lg,
-                             M, (uint64_t)count, tiles);
+    const bool large = (uint64_t)count * T::kSize >= kSimLargeBytes;
+    if (rhd && large)
+        return launch_all_shape<T, Op, true, kRhdShape.threads>(a, G, lg, M, count, vec,
+                                                                kRhdShape.waves, s);
     if (rhd)
-        return launch_kernel(sim_all_kernel<T, Op, true, false>, grid, dim3(kB), lds, s, a, G, lg,
-                             M, (uint64_t)count, tiles);
-    if (vec)
-        return launch_kernel(sim_all_kernel<T, Op, false, true>, grid, dim3(kB), lds, s, a, G, lg,
-                             M, (uint64_t)count, tiles);
-    return launch_kernel(sim_all_kernel<T, Op, false, false>, grid, dim3(kB), lds, s, a, G, lg, M,
-                         (uint64_t)count, tiles);
+        return launch_all_shape<T, Op, true, kRhdSmallShape.threads>(a, G, lg, M, count, vec,
+                                                                     kRhdSmallShape.waves, s);
+    if (large)
+        return launch_all_shape<T, Op, false, kRingShape.threads>(a, G, lg, M, count, vec,
+                                                                  kRingShape.waves, s);
+    return launch_all_shape<T, Op, false, kRingSmallShape.threads>(a, G, lg, M, count, vec,
+                                                                   kRingSmallShape.waves, s);
 }
 
 int rank_mod(int r, int G) { return ((r % G) + G) % G; }

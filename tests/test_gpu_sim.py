@@ -150,3 +150,41 @@ def test_most_ranks(xr, orc, G):
                 for variant in (schedule, schedule + "1"):
                     outs = _run(xr, sends, dtype, op, variant)
                     _check(outs, exp, dtype, op, f"{variant} {dtype} {op} G={G} n={n}")
+
+
+@pytest.mark.parametrize("dtype,op,G,n", [
+    ("bf16", "sum", 8, (8 << 20) // 2 - 1),        # one element below 8 MiB per rank
+    ("bf16", "max", 3, (8 << 20) // 2 + 37),       # past it: the large workgroup shapes
+    ("f32", "prod", 5, (8 << 20) // 4 + 5),
+    ("u8", "sum", 16, (8 << 20) + 3),
+    ("i8", "min", 4, (8 << 20) + 64 * 4 + 1),
+    ("f64", "sum", 8, (8 << 20) // 8 + 9),
+])
+def test_one_launch_shapes_by_size(xr, orc, dtype, op, G, n):
+    """The one-launch schedules pick their workgroup shape by bytes per rank
+    (8 MiB): both sides of the switch, ragged chunks, 1- to 8-byte elements,
+    and halving-doubling where G is a power of two."""
+    rng = np.random.default_rng(90 + G)
+    sends = [pins.random_column_values(rng, dtype, n) for _ in range(G)]
+    for schedule in ("ring", "rhd") if G & (G - 1) == 0 else ("ring",):
+        exp = orc.allreduce_sim(sends, dtype, op, schedule, nthreads=CORES)
+        outs = _run(xr, sends, dtype, op, schedule + "1")
+        _check(outs, exp, dtype, op, f"{schedule}1 {dtype} {op} G={G} n={n}")
+        del outs
+        torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("schedule", ["ring1", "rhd1"])
+def test_one_launch_large_element_aligned(xr, orc, schedule):
+    """Past 8 MiB per rank with buffers one element off 16-byte alignment:
+    the scalar path of the large shapes."""
+    rng = np.random.default_rng(95)
+    G, n = 4, (8 << 20) // 2 + 3
+    sends_np = [pins.random_column_values(rng, "bf16", n) for _ in range(G)]
+    big = [gu.to_dev(np.concatenate([np.zeros(1, s.dtype), s]), "bf16") for s in sends_np]
+    rbig = [torch.empty_like(b) for b in big]
+    recvs = [b[1:] for b in rbig]
+    xr.allreduce_sim([b[1:] for b in big], recvs, "sum", schedule=schedule, dtype="bf16")
+    torch.cuda.synchronize()
+    _check(recvs, orc.allreduce_sim(sends_np, "bf16", "sum", _oracle_schedule(schedule),
+                                    nthreads=CORES), "bf16", "sum", f"element-aligned {schedule}")
