@@ -388,7 +388,7 @@ XRED_API unsigned xred_set_max_workgroups(unsigned max_workgroups);
  * (measured on MI355X: P=8 x 8 MiB bf16 reduces on 16 CUs at ~1 TB/s,
  * concurrently with the product).  A kernel sized for the whole chip runs
  * slower on a partition than the CU count alone suggests (torch's bf16
- * matrix products lost ~40 % on any partial CU set), so the partition pays
+ * matrix products lost 27-37 % on any partial CU set), so the partition pays
  * off only where the compute side tolerates it.
  *   ncu     a positive multiple of X below the CU count (256 CUs, X = 8 on
  *           MI355X: 8, 16, ..., 248)
