@@ -9,6 +9,8 @@ patterns with the special values of each type (pins.random_column_values).
 Results must match the oracle bit for bit (NaN payloads of float
 sum/prod/avg by NaN-ness only).  The case is printed before it runs.
 """
+import os
+
 import numpy as np
 import pytest
 
@@ -23,6 +25,7 @@ DTYPES = ("f32", "bf16", "f16", "e4m3", "e5m2", "i32", "u32", "i64", "u64", "f64
 ES = {"f32": 4, "bf16": 2, "f16": 2, "e4m3": 1, "e5m2": 1, "i32": 4, "u32": 4, "i64": 8,
       "u64": 8, "f64": 8, "i8": 1, "u8": 1}
 CASES = 40
+CORES = min(16, len(os.sched_getaffinity(0)))
 
 
 @pytest.fixture(scope="module")
@@ -204,3 +207,37 @@ def test_random_sim(xr, orc, seed):
         torch.cuda.synchronize()
         for r in range(G):
             gu.assert_parity(recvs[r], exp[r], dtype, op, f"case {case} rank {r}")
+
+
+@pytest.mark.parametrize("seed", range(2))
+def test_random_sim_one_launch_large(xr, orc, seed):
+    """The one-launch schedules around and past 8 MiB per rank, where their
+    workgroup shapes change: random type, op, rank count, alignment and
+    in-place output, lengths within a few vectors of the switch or up to
+    1.5 times past it."""
+    rng = np.random.default_rng(9400 + seed)
+    for case in range(6):
+        dtype = DTYPES[rng.integers(0, len(DTYPES))]
+        op = _op(rng, dtype, avg_ok=False)
+        schedule = ("ring1", "rhd1")[rng.integers(0, 2)]
+        G = int(rng.integers(2, 9)) if schedule == "ring1" else 1 << int(rng.integers(1, 4))
+        edge = (8 << 20) // ES[dtype]
+        vec = 16 // ES[dtype]
+        if rng.random() < 0.5:
+            n = edge + vec * int(rng.integers(-2, 3)) + int(rng.integers(-1, 2))
+        else:
+            n = edge + int(rng.integers(0, edge // 2))
+        off = int(rng.integers(0, 2))
+        in_place = rng.random() < 0.3
+        _say(case, f"allreduce_sim {schedule} {dtype} {op} G={G} n={n} offset={off} "
+                   f"in_place={in_place}")
+        sends_np = [pins.random_column_values(rng, dtype, n) for _ in range(G)]
+        exp = orc.allreduce_sim(sends_np, dtype, op, schedule.rstrip("1"), nthreads=CORES)
+        sends = _dev(sends_np, dtype, off)
+        recvs = sends if in_place else [_empty(n, dtype, off) for _ in range(G)]
+        xr.allreduce_sim(sends, recvs, op, schedule=schedule, dtype=dtype)
+        torch.cuda.synchronize()
+        for r in range(G):
+            gu.assert_parity(recvs[r], exp[r], dtype, op, f"case {case} rank {r}")
+        del sends, recvs
+        torch.cuda.empty_cache()
