@@ -52,10 +52,15 @@ constexpr int kWideWgsPerCu = 4;   // resident 512-thread workgroups per CU
 constexpr int kUWide2 = 2;         // vectors per thread of the second one-round shape (NP <= 8)
 
 // Waves per CU for a compile-time source count (0: runtime count); 0 = no cap.
+// Five and six sources stream best with more waves than seven or eight (bf16
+// at 128 MiB per source on two boxes, 12 / 16 / 20 waves: P=5 6.39-6.61 /
+// 6.85-7.10 / 6.92-7.08 TB/s, P=6 6.69-6.82 / 6.91-6.98 / 6.90-6.91); two to
+// four sources are within noise of uncapped at 16-28 waves.
 template <int NP>
 constexpr int waves_per_cu()
 {
-    return NP == 0 ? 16 : NP <= 4 ? 0 : NP <= 8 ? 12 : NP <= 16 ? 10 : NP <= 32 ? 6 : 4;
+    return NP == 0 ? 16 : NP <= 4 ? 0 : NP == 5 ? 20 : NP == 6 ? 16 : NP <= 8 ? 12
+         : NP <= 16 ? 10 : NP <= 32 ? 6 : 4;
 }
 
 // The cap of a bandwidth-bound launch with `bytes` per source.
@@ -64,7 +69,7 @@ int waves_for(size_t bytes)
 {
     if (NP >= 5 && NP <= 8) {
         if (bytes > ((size_t)384 << 20)) return 24;
-        if (bytes > ((size_t)192 << 20)) return 16;
+        if (bytes > ((size_t)192 << 20)) return waves_per_cu<NP>() > 16 ? waves_per_cu<NP>() : 16;
         if (bytes <= ((size_t)24 << 20)) return 24;
     }
     return waves_per_cu<NP>();
