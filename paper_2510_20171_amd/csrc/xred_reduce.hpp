@@ -51,7 +51,8 @@ constexpr int kBWide = 512;    // threads per workgroup, one-round launches
 constexpr int kWideWgsPerCu = 4;   // resident 512-thread workgroups per CU
 constexpr int kUWide2 = 2;         // vectors per thread of the second one-round shape (NP <= 8)
 
-// Waves per CU for a compile-time source count (0: runtime count); 0 = no cap.
+// Waves per CU for a compile-time source count (NP = 0, a runtime count: see
+// waves_for); 0 = no cap.
 // Five and six sources stream best with more waves than seven or eight (bf16
 // at 128 MiB per source on two boxes, 12 / 16 / 20 waves: P=5 6.39-6.61 /
 // 6.85-7.10 / 6.92-7.08 TB/s, P=6 6.69-6.82 / 6.91-6.98 / 6.90-6.91); two to
@@ -59,14 +60,19 @@ constexpr int kUWide2 = 2;         // vectors per thread of the second one-round
 template <int NP>
 constexpr int waves_per_cu()
 {
-    return NP == 0 ? 16 : NP <= 4 ? 0 : NP == 5 ? 20 : NP == 6 ? 16 : NP <= 8 ? 12
+    return NP == 0 ? 12 : NP <= 4 ? 0 : NP == 5 ? 20 : NP == 6 ? 16 : NP <= 8 ? 12
          : NP <= 16 ? 10 : NP <= 32 ? 6 : 4;
 }
 
-// The cap of a bandwidth-bound launch with `bytes` per source.
+// The cap of a bandwidth-bound launch with `bytes` per source.  A runtime
+// source count takes fewer waves the more sources each thread reads (bf16 at
+// 32 MiB per source, 8 / 10 / 12 / 16 waves: 9 sources 6.23-6.26 / 6.22-6.26 /
+// 6.37-6.44 / 6.28-6.30 TB/s, 24 sources 6.28-6.29 / 6.29 / 6.26-6.30 /
+// 6.06, 48 sources 6.52-6.54 / 6.54 / 6.38-6.40 / 6.10-6.12).
 template <int NP>
-int waves_for(size_t bytes)
+int waves_for(size_t bytes, int nsrc)
 {
+    if (NP == 0) return nsrc <= 12 ? 12 : nsrc <= 48 ? 10 : 6;
     if (NP >= 5 && NP <= 8) {
         if (bytes > ((size_t)384 << 20)) return 24;
         if (bytes > ((size_t)192 << 20)) return waves_per_cu<NP>() > 16 ? waves_per_cu<NP>() : 16;
@@ -115,7 +121,7 @@ hipError_t go_vec(const char *const *srcs, int nsrc, char *dst, size_t count, hi
     constexpr size_t kTile = (size_t)kB * kU;
     const uint64_t tiles = (nvec + kTile - 1) / kTile + (tail ? 1 : 0);
     return launch_kernel(reduce_vec_kernel<T, Op, NP, MAXP, kU, kB>, dim3(grid_for(tiles)),
-                         dim3(kB), lds_for_waves(waves_for<NP>(count * T::kSize)), s, ks, nsrc,
+                         dim3(kB), lds_for_waves(waves_for<NP>(count * T::kSize, nsrc)), s, ks, nsrc,
                          dst, nvec, tail);
 }
 
