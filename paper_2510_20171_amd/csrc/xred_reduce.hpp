@@ -69,10 +69,17 @@ constexpr int waves_per_cu()
 // 32 MiB per source, 8 / 10 / 12 / 16 waves: 9 sources 6.23-6.26 / 6.22-6.26 /
 // 6.37-6.44 / 6.28-6.30 TB/s, 24 sources 6.28-6.29 / 6.29 / 6.26-6.30 /
 // 6.06, 48 sources 6.52-6.54 / 6.54 / 6.38-6.40 / 6.10-6.12).
-template <int NP>
+// Eight-bit integers (sixteen 32-bit accumulators per vector) want 16 waves
+// for 5-8 sources (P=8 at 128 MiB per source, 12 / 16 waves: uint8 max 6.64-6.66
+// / 6.84 TB/s, int8 sum 6.80-6.86 / 6.90-6.91; the other types are best at 12).
+template <class T, int NP>
 int waves_for(size_t bytes, int nsrc)
 {
     if (NP == 0) return nsrc <= 12 ? 12 : nsrc <= 48 ? 10 : 6;
+    constexpr bool kByteInt = !T::kFloat && T::kSize == 1;
+    if (kByteInt && NP >= 5 && NP <= 8 && bytes > ((size_t)24 << 20) &&
+        bytes <= ((size_t)192 << 20))
+        return waves_per_cu<NP>() > 16 ? waves_per_cu<NP>() : 16;
     if (NP >= 5 && NP <= 8) {
         if (bytes > ((size_t)384 << 20)) return 24;
         if (bytes > ((size_t)192 << 20)) return waves_per_cu<NP>() > 16 ? waves_per_cu<NP>() : 16;
@@ -121,7 +128,7 @@ hipError_t go_vec(const char *const *srcs, int nsrc, char *dst, size_t count, hi
     constexpr size_t kTile = (size_t)kB * kU;
     const uint64_t tiles = (nvec + kTile - 1) / kTile + (tail ? 1 : 0);
     return launch_kernel(reduce_vec_kernel<T, Op, NP, MAXP, kU, kB>, dim3(grid_for(tiles)),
-                         dim3(kB), lds_for_waves(waves_for<NP>(count * T::kSize, nsrc)), s, ks, nsrc,
+                         dim3(kB), lds_for_waves(waves_for<T, NP>(count * T::kSize, nsrc)), s, ks, nsrc,
                          dst, nvec, tail);
 }
 
