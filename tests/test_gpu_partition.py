@@ -8,7 +8,8 @@
   (and, on the smallest partition, the ring in one launch, whose grid is
   sized for the whole chip and so runs in rounds there) on the partition's
   stream, a host-descriptor batch on the rest's, all enqueued before any is
-  waited for.
+  waited for; on 8 CUs also the ring gated by host flags and a batch with
+  device descriptors, whose grids are sized for the whole chip.
 - CU counts that are not a multiple of the XCD count, or not below the CU
   count, are rejected and create nothing.
 """
@@ -20,6 +21,7 @@ import pytest
 
 import gpu_util as gu
 import pins
+from test_gpu_ring import PinnedWords
 
 pytestmark = pytest.mark.gpu
 torch = pytest.importorskip("torch")
@@ -84,9 +86,35 @@ def test_partition_places_and_reduces(env, orc, ncu):
         xr.allreduce_local(srcs, out, stream=a)
         xr.batched_reduce(list(zip(bsrc, bout)), "sum", dtype="f32", stream=b)
         if ncu == 8:
+            # a grid sized for the whole chip on 8 CUs: the ring with and
+            # without host flags (the poller is workgroup 0, dispatched first;
+            # tile workgroups wait only for it), and a device-descriptor batch
+            # (the queue kernel: most of its workgroups start once the first
+            # ones have taken every tile)
             chunks = [gu.to_dev(s, "bf16") for s in srcs_np[:4]]
             rout = torch.empty(n, dtype=torch.bfloat16, device="cuda")
             xr.ring_reduce(chunks, rout, stream=a)
+            flags = PinnedWords(4)
+            for i in range(4):
+                flags.set(i, 1)
+            fout = torch.empty(n, dtype=torch.bfloat16, device="cuda")
+            L = xr.load()
+            xr._lib.check(L.xred_ring_reduce(
+                xr._lib.ptr_array([c.data_ptr() for c in chunks]), 4,
+                ctypes.c_void_p(fout.data_ptr()), n, xr.DTYPE["bf16"], xr.OP["sum"], flags.dev, 1,
+                2_000_000, None, ctypes.c_void_p(a)))
+            dsizes = [int(x) for x in rng.integers(1, 30000, size=300)]
+            dsrc_np = [[pins.random_column_values(rng, "bf16", m) for _ in range(5)] for m in dsizes]
+            dsrc = [[gu.to_dev(x, "bf16") for x in row] for row in dsrc_np]
+            dout = [torch.empty(m, dtype=torch.bfloat16, device="cuda") for m in dsizes]
+            ptrs = [torch.tensor([x.data_ptr() for x in row], dtype=torch.int64, device="cuda")
+                    for row in dsrc]
+            rows = np.zeros(len(dsizes), xr.ITEM_DTYPE)
+            for k, (pa, o) in enumerate(zip(ptrs, dout)):
+                rows[k] = (pa.data_ptr(), o.data_ptr(), o.numel(), 5, 0)
+            ditems = torch.from_numpy(rows.view(np.uint8).copy()).to("cuda")
+            torch.cuda.synchronize()
+            xr.batched_reduce(ditems, "sum", dtype="bf16", stream=a)
         for s in (a, b):
             torch.cuda.ExternalStream(s).synchronize()
         gu.assert_parity(out, orc.allreduce_local(srcs_np, "bf16", "sum"), "bf16", "sum",
@@ -95,8 +123,13 @@ def test_partition_places_and_reduces(env, orc, ncu):
             gu.assert_parity(o, orc.allreduce_local(row, "f32", "sum"), "f32", "sum",
                              f"batch item {k} on the other {cus - ncu} CUs")
         if ncu == 8:
-            gu.assert_parity(rout, orc.allreduce_local(srcs_np[:4], "bf16", "sum"), "bf16",
-                             "sum", "one-launch ring on 8 CUs")
+            ring_exp = orc.allreduce_local(srcs_np[:4], "bf16", "sum")
+            gu.assert_parity(rout, ring_exp, "bf16", "sum", "one-launch ring on 8 CUs")
+            gu.assert_parity(fout, ring_exp, "bf16", "sum", "flagged ring on 8 CUs")
+            flags.free()
+            for k, (row, o) in enumerate(zip(dsrc_np, dout)):
+                gu.assert_parity(o, orc.allreduce_local(row, "bf16", "sum"), "bf16", "sum",
+                                 f"device-descriptor item {k} on 8 CUs")
     finally:
         xr.stream_destroy(a)
         xr.stream_destroy(b)
