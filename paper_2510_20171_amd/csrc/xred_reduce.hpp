@@ -6,6 +6,8 @@
 
 #include <stdlib.h>
 
+#include <algorithm>
+
 #include "xred_dispatch.hpp"
 #include "xred_internal.hpp"
 #include "xred_kernels.hpp"
@@ -110,26 +112,31 @@ hipError_t go_vec(const char *const *srcs, int nsrc, char *dst, size_t count, hi
     for (int p = nsrc; p < MAXP; ++p) ks.p[p] = nullptr;
     const size_t nvec = count / T::kVec;
     const uint32_t tail = (uint32_t)(count % T::kVec);
+    // a short first tile up to the first source's next 128-byte line
+    const size_t mis = (uintptr_t)srcs[0] & 127u;
+    const uint32_t head = (uint32_t)(mis == 0 ? 0 : std::min<size_t>(128 - mis, nvec * 16));
+    const size_t hv = head / 16, first = head != 0 ? 1 : 0;
     constexpr size_t kTileWide = (size_t)kBWide * kU;
-    const uint64_t tiles_wide = (nvec + kTileWide - 1) / kTileWide + (tail ? 1 : 0);
+    const uint64_t tiles_wide = first + (nvec - hv + kTileWide - 1) / kTileWide + (tail ? 1 : 0);
     const uint64_t one_round = (uint64_t)device_cus() * kWideWgsPerCu;
     if (tiles_wide <= one_round)
         return launch_kernel(reduce_vec_kernel<T, Op, NP, MAXP, kU, kBWide>,
                              dim3(grid_for(tiles_wide)), dim3(kBWide), 0, s, ks, nsrc, dst, nvec,
-                             tail);
+                             tail, head);
     if constexpr (NP >= 1 && NP <= 8) {
         constexpr size_t kTileWide2 = (size_t)kBWide * kUWide2;
-        const uint64_t tiles_wide2 = (nvec + kTileWide2 - 1) / kTileWide2 + (tail ? 1 : 0);
+        const uint64_t tiles_wide2 =
+            first + (nvec - hv + kTileWide2 - 1) / kTileWide2 + (tail ? 1 : 0);
         if (tiles_wide2 <= one_round)
             return launch_kernel(reduce_vec_kernel<T, Op, NP, MAXP, kUWide2, kBWide>,
                                  dim3(grid_for(tiles_wide2)), dim3(kBWide), 0, s, ks, nsrc, dst,
-                                 nvec, tail);
+                                 nvec, tail, head);
     }
     constexpr size_t kTile = (size_t)kB * kU;
-    const uint64_t tiles = (nvec + kTile - 1) / kTile + (tail ? 1 : 0);
+    const uint64_t tiles = first + (nvec - hv + kTile - 1) / kTile + (tail ? 1 : 0);
     return launch_kernel(reduce_vec_kernel<T, Op, NP, MAXP, kU, kB>, dim3(grid_for(tiles)),
                          dim3(kB), lds_for_waves(waves_for<T, NP>(count * T::kSize, nsrc)), s, ks, nsrc,
-                         dst, nvec, tail);
+                         dst, nvec, tail, head);
 }
 
 template <class T, class Op>
