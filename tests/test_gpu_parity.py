@@ -267,6 +267,53 @@ def test_misaligned_and_guard_bands(xr, orc, dtype):
             assert np.all(raw[(G + shift + n) * es:] == canary)
 
 
+@pytest.mark.parametrize("dtype", ["bf16", "f32", "u8", "f64"])
+def test_line_misaligned_buffers(xr, orc, dtype):
+    """16-byte-aligned buffers that start inside a 128-byte line take the
+    vector path with a short first tile up to the first source's next line:
+    every byte offset of 16..112, lengths shorter than that first tile, equal
+    to it, one vector past it, around one tile of each launch shape past it
+    and past one round of workgroups (ragged tails included); the sources
+    sharing one offset or not, the output at another; canaries around the
+    output stay untouched."""
+    rng = np.random.default_rng(13)
+    es = {"bf16": 2, "f32": 4, "u8": 1, "f64": 8}[dtype]
+    vec = 16 // es
+    G = 256           # guard bytes on each side of the output
+    cases = []
+    for off in range(16, 128, 16):
+        head = (128 - off) // es
+        for n in (1, vec - 1, head - vec, head, head + 1, head + vec, head + 128 * vec - 3,
+                  head + 128 * vec + 5, head + 512 * vec + 1, head + 1024 * vec + 7,
+                  head + 300000 * vec // 8 + 3):
+            if n >= 1:
+                cases.append((off, n, (1, 3, 8, 17)[len(cases) % 4]))
+    # past one round of workgroups: the multi-round 128-thread tiles
+    cases += [(48, (128 - 48) // es + 1100000 * vec + 5, 3),
+              (80, (128 - 80) // es + 600000 * vec + 9, 17)]
+    for k, (off, n, P) in enumerate(cases):
+        same = k % 3 != 2
+        srcs = [pins.random_column_values(rng, dtype, n) for _ in range(P)]
+        views = []
+        for p, a in enumerate(srcs):
+            o = off if same or p == 0 else (off + 16 * p) % 128
+            big = torch.zeros(o + n * es + 128, dtype=torch.uint8, device="cuda")
+            assert big.data_ptr() % 128 == 0
+            v = big[o:o + n * es].view(gu.torch_dtype(dtype))
+            v.copy_(gu.to_dev(a, dtype))
+            views.append((big, v))
+        dofs = (off + 48) % 128
+        store = torch.full((G + dofs + n * es + G,), 0x5A, dtype=torch.uint8, device="cuda")
+        out = store[G + dofs:G + dofs + n * es].view(gu.torch_dtype(dtype))
+        xr.allreduce_local([v for _, v in views], out, "sum", dtype=dtype)
+        torch.cuda.synchronize()
+        what = f"line-misaligned {dtype} P={P} offset={off} n={n} same={same}"
+        gu.assert_parity(out, orc.allreduce_local(srcs, dtype, "sum"), dtype, "sum", what)
+        raw = store.cpu().numpy()
+        assert np.all(raw[:G + dofs] == 0x5A), what
+        assert np.all(raw[G + dofs + n * es:] == 0x5A), what
+
+
 @pytest.mark.parametrize("dtype", DTYPES)
 def test_in_place(xr, orc, dtype):
     rng = np.random.default_rng(8)
