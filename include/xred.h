@@ -216,7 +216,10 @@ XRED_API xred_status xred_acc_cast(const void *acc, void *dst, size_t count, xre
  *            of staged data or more are copied on a stream the library owns
  *            (one per device, default priority), which the caller's stream
  *            then waits for through an event, so the copy overlaps earlier
- *            work on the caller's stream.  Not capturable: on a
+ *            work on the caller's stream.  When a slot is free again is
+ *            tracked on a second stream the library owns, never by an event
+ *            left on the caller's stream, so the caller may destroy its
+ *            stream as soon as the call returns.  Not capturable: on a
  *            stream under graph capture the call returns XRED_UNSUPPORTED
  *            (a replay would copy whatever a later call left in the slot).
  *   XRED_ITEMS_ON_DEVICE: `items` and every items[k].srcs are DEVICE memory,

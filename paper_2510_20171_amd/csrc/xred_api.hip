@@ -163,6 +163,13 @@ struct Pool {
     Slot slot[kSlots];
     unsigned next = 0;
     hipStream_t copy = nullptr;    // side stream for the copies of large batches
+    // Stream on which each slot's `done` event is recorded, after waiting for
+    // the caller's stream to pass the launch that read the slot.  No event the
+    // library keeps is ever recorded on a caller's stream: the caller may
+    // destroy its stream at any time, and an event last recorded on a
+    // destroyed stream cannot be waited for afterwards (the runtime answered
+    // such a wait with a capture error).
+    hipStream_t track = nullptr;
 };
 // Staged batches at least this large are copied on the pool's side stream, so
 // the copy overlaps the kernel already running on the caller's stream; smaller
@@ -309,6 +316,11 @@ xred_status batched_host(const xred_item *items, int nitems, xred_dtype dtype, x
         pool.copy = nullptr;
         return hip_fail(e, "hipStreamCreate(copy stream)");
     }
+    if (!pool.track &&
+        (e = hipStreamCreateWithFlags(&pool.track, hipStreamNonBlocking)) != hipSuccess) {
+        pool.track = nullptr;
+        return hip_fail(e, "hipStreamCreate(tracking stream)");
+    }
 
     char *h = (char *)s.host;
     char *d = (char *)(direct ? s.host_dev : s.dev);
@@ -397,11 +409,18 @@ xred_status batched_host(const xred_item *items, int nitems, xred_dtype dtype, x
         le = launch_batched_planned(dtype, op, (const xred_item *)d, nitems,
                                     (const WgStart *)(d + items_bytes), grid, stream);
     // The copy is enqueued whatever the launch did: the slot stays busy until
-    // the stream has passed it.
+    // the stream has passed it.  `done` marks that point on the caller's
+    // stream only long enough for the tracking stream to wait for it, and is
+    // then recorded again on the tracking stream (the pending wait keeps the
+    // first record), so when the call returns it belongs to the library's
+    // stream and completes once the caller's stream has passed the launch.
     e = hipEventRecord(s.done, stream);
+    if (e == hipSuccess) e = hipStreamWaitEvent(pool.track, s.done, 0);
+    if (e == hipSuccess) e = hipEventRecord(s.done, pool.track);
     if (e != hipSuccess) {
         (void)hipStreamSynchronize(stream);
-        return hip_fail(e, "hipEventRecord(staging slot)");
+        (void)hipStreamSynchronize(pool.track);
+        return hip_fail(e, "staging slot tracking");
     }
     s.pending = true;
     if (le != hipSuccess) return hip_fail(le, "batched launch");
@@ -1045,7 +1064,7 @@ XRED_API void xred_release(void)
         std::lock_guard<std::mutex> lock(pool.mu);
         bool any = false;
         for (Slot &s : pool.slot) any |= s.host != nullptr || s.done != nullptr;
-        any |= pool.copy != nullptr;
+        any |= pool.copy != nullptr || pool.track != nullptr;
         if (!any) continue;
         (void)hipSetDevice(d);
         for (Slot &s : pool.slot) {
@@ -1055,7 +1074,8 @@ XRED_API void xred_release(void)
             s.done = s.copied = nullptr;
         }
         if (pool.copy) (void)hipStreamDestroy(pool.copy);
-        pool.copy = nullptr;
+        if (pool.track) (void)hipStreamDestroy(pool.track);
+        pool.copy = pool.track = nullptr;
     }
     if (have_dev) (void)hipSetDevice(cur);
 }

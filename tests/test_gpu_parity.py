@@ -585,6 +585,60 @@ def _staged_bytes(sizes, nsrc, tile_elems):
     return 32 * len(sizes) + (width * tiles + 7) // 8 * 8 + 8 * nsrc * len(sizes)
 
 
+def test_batched_host_caller_stream_destroyed(xr, orc):
+    """Host batches on streams the caller destroys as soon as each call has
+    finished (more such streams than the library has staging slots; batches
+    read in place, copied on the caller's stream and copied on the library's
+    side stream), then host batches on the current stream: every call
+    succeeds and every item matches the oracle.  The library keeps no event
+    on a caller's stream (waiting later for an event last recorded on a
+    destroyed stream fails in the runtime)."""
+    hip = ctypes.CDLL("libamdhip64.so")
+    hip.hipStreamCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+    hip.hipStreamDestroy.argtypes = [ctypes.c_void_p]
+    hip.hipStreamSynchronize.argtypes = [ctypes.c_void_p]
+    rng = np.random.default_rng(77)
+    for r in range(12):
+        K, nsrc = ((20, 3), (2000, 3), (3000, 8))[r % 3]
+        sizes = rng.integers(1, 300, size=K)
+        srcs_np = [[pins.random_column_values(rng, "f32", int(n)) for _ in range(nsrc)]
+                   for n in sizes]
+        total = int(sizes.sum())
+        flat = [gu.to_dev(np.concatenate([row[p] for row in srcs_np]), "f32")
+                for p in range(nsrc)]
+        out = torch.zeros(total, dtype=torch.float32, device="cuda")
+        items, pos = [], 0
+        for n in sizes.tolist():
+            items.append(([f[pos:pos + n] for f in flat], out[pos:pos + n]))
+            pos += n
+        torch.cuda.synchronize()
+        if r < 9 and r % 2 == 0:
+            h = ctypes.c_void_p()
+            assert hip.hipStreamCreate(ctypes.byref(h)) == 0
+            xr.batched_reduce(items, "sum", dtype="f32", stream=h.value)
+            assert hip.hipStreamSynchronize(h) == 0
+            assert hip.hipStreamDestroy(h) == 0
+        elif r < 9:
+            # a CU-masked stream (a hardware queue of its own), destroyed
+            # through the library, with other runtime objects made and freed
+            # after it
+            a, b = xr.stream_create_partition(8)
+            xr.batched_reduce(items, "sum", dtype="f32", stream=b)
+            xr.stream_destroy(a)
+            xr.stream_destroy(b)
+            junk = [torch.empty(1 << 16).pin_memory() for _ in range(4)]
+            side = torch.cuda.Stream()
+            with torch.cuda.stream(side):
+                torch.ones(16, device="cuda").add_(1)
+            side.synchronize()
+            del junk
+        else:
+            xr.batched_reduce(items, "sum", dtype="f32")
+            torch.cuda.synchronize()
+        exp = np.concatenate([orc.allreduce_local(row, "f32", "sum") for row in srcs_np])
+        gu.assert_parity(out, exp, "f32", "sum", f"round {r} (K={K}, nsrc={nsrc})")
+
+
 @pytest.mark.parametrize("K,nruns,maxn,nsrc", [(3000, 12, 300, 8), (40, 12, 300, 3)])
 def test_batched_host_batches_back_to_back(xr, orc, K, nruns, maxn, nsrc):
     """Host batches enqueued back to back on two alternating caller streams
