@@ -585,7 +585,11 @@ def secondary(torch, xr, L, timer, wl, flush, res):
     # the same work on the whole chip, one loop after the other
     _, r_full, _ = run(sg, sr, False, 200)
     for ncu in (16, 32):
-        a, b = xr.stream_create_partition(ncu)
+        try:
+            a, b = xr.stream_create_partition(ncu)
+        except xr.XredError as err:   # the runtime may refuse more hardware queues
+            co[f"partition_{ncu}_cus"] = {"error": str(err)}
+            continue
         try:
             e, reps = pair(torch.cuda.ExternalStream(b), torch.cuda.ExternalStream(a))
         finally:
