@@ -205,30 +205,37 @@ __device__ __forceinline__ void reduce_elem(const Src &src, int nsrc, char *dst,
 }
 
 // ------------------------------------------------------ fused P-source --
-// dst[i] = fold_p src_p[i] for nvec*kVec + tail elements, all pointers 16 B
-// aligned.  Tiles of B*U vectors (the last one ragged, cut by the buffer
-// range check); the tail (< kVec elements) is done by one workgroup, scalar.
-// `head` (a multiple of 16 below 128, at most nvec*16) is the byte length of
-// a first, short tile that ends where the first source reaches a 128-byte
-// line: the other tiles then start on line boundaries, so no line is split
-// between two tiles (whose workgroups, on different XCDs, would each fetch
-// it).
+// dst[i] = fold_p src_p[i] for lead + nvec*kVec + tail elements, every
+// pointer at the same offset within 16 bytes: the first `lead` elements
+// (fewer than a vector) bring them all to a 16-byte boundary and, like the
+// last `tail` ones, are done by one workgroup, scalar; the nvec vectors
+// between go in tiles of B*U vectors (the last one ragged, cut by the buffer
+// range check).  `head` (a multiple of 16 below 128, at most nvec*16) is the
+// byte length of a first, short tile that ends where the first source
+// reaches a 128-byte line: the other tiles then start on line boundaries, so
+// no line is split between two tiles (whose workgroups, on different XCDs,
+// would each fetch it).
 template <class T, class Op, int NP, int MAXP, int U, int B>
 __global__ __launch_bounds__(B) void reduce_vec_kernel(KernargSrc<MAXP> src, int nsrc, char *dst,
-                                                       size_t nvec, uint32_t tail, uint32_t head)
+                                                       size_t nvec, uint32_t tail, uint32_t head,
+                                                       uint32_t lead)
 {
     constexpr uint32_t kTileBytes = (uint32_t)B * U * 16u;
     const size_t vbytes = nvec * 16;
+    const size_t lb = (size_t)lead * T::kSize;   // bytes before the first vector
     const uint32_t first = head != 0 ? 1u : 0u;
     const size_t ntiles = first + (vbytes - head + kTileBytes - 1) / kTileBytes;
     for (size_t t = blockIdx.x; t < ntiles; t += gridDim.x) {
         const bool h = t < first;
         const size_t off = h ? 0 : head + (t - first) * kTileBytes;
         reduce_tile<T, Op, NP, U, B>(src, nsrc, dst,
-                                     Tile{off, h ? head : tile_nrec(vbytes, off, kTileBytes)});
+                                     Tile{lb + off, h ? head : tile_nrec(vbytes, off, kTileBytes)});
     }
-    if (tail != 0 && blockIdx.x == ntiles % gridDim.x && threadIdx.x < tail)
-        reduce_elem<T, Op>(src, nsrc, dst, nvec * T::kVec + threadIdx.x);
+    if ((tail | lead) != 0 && blockIdx.x == ntiles % gridDim.x) {
+        if (threadIdx.x < tail)
+            reduce_elem<T, Op>(src, nsrc, dst, lead + nvec * T::kVec + threadIdx.x);
+        if (threadIdx.x < lead) reduce_elem<T, Op>(src, nsrc, dst, threadIdx.x);
+    }
 }
 
 // Any alignment: one element per thread per step.

@@ -105,46 +105,52 @@ size_t lds_for_waves(int waves)
 }
 
 template <class T, class Op, int NP, int MAXP>
-hipError_t go_vec(const char *const *srcs, int nsrc, char *dst, size_t count, hipStream_t s)
+hipError_t go_vec(const char *const *srcs, int nsrc, char *dst, size_t count, uint32_t lead,
+                  hipStream_t s)
 {
     KernargSrc<MAXP> ks;
     for (int p = 0; p < nsrc; ++p) ks.p[p] = srcs[p];
     for (int p = nsrc; p < MAXP; ++p) ks.p[p] = nullptr;
-    const size_t nvec = count / T::kVec;
-    const uint32_t tail = (uint32_t)(count % T::kVec);
+    const size_t nvec = (count - lead) / T::kVec;
+    const uint32_t tail = (uint32_t)((count - lead) % T::kVec);
     // a short first tile up to the first source's next 128-byte line
-    const size_t mis = (uintptr_t)srcs[0] & 127u;
+    const size_t mis = ((uintptr_t)srcs[0] + (size_t)lead * T::kSize) & 127u;
     const uint32_t head = (uint32_t)(mis == 0 ? 0 : std::min<size_t>(128 - mis, nvec * 16));
     const size_t hv = head / 16, first = head != 0 ? 1 : 0;
     constexpr size_t kTileWide = (size_t)kBWide * kU;
-    const uint64_t tiles_wide = first + (nvec - hv + kTileWide - 1) / kTileWide + (tail ? 1 : 0);
+    const uint64_t tiles_wide = first + (nvec - hv + kTileWide - 1) / kTileWide + ((tail | lead) ? 1 : 0);
     const uint64_t one_round = (uint64_t)device_cus() * kWideWgsPerCu;
     if (tiles_wide <= one_round)
         return launch_kernel(reduce_vec_kernel<T, Op, NP, MAXP, kU, kBWide>,
                              dim3(grid_for(tiles_wide)), dim3(kBWide), 0, s, ks, nsrc, dst, nvec,
-                             tail, head);
+                             tail, head, lead);
     if constexpr (NP >= 1 && NP <= 8) {
         constexpr size_t kTileWide2 = (size_t)kBWide * kUWide2;
         const uint64_t tiles_wide2 =
-            first + (nvec - hv + kTileWide2 - 1) / kTileWide2 + (tail ? 1 : 0);
+            first + (nvec - hv + kTileWide2 - 1) / kTileWide2 + ((tail | lead) ? 1 : 0);
         if (tiles_wide2 <= one_round)
             return launch_kernel(reduce_vec_kernel<T, Op, NP, MAXP, kUWide2, kBWide>,
                                  dim3(grid_for(tiles_wide2)), dim3(kBWide), 0, s, ks, nsrc, dst,
-                                 nvec, tail, head);
+                                 nvec, tail, head, lead);
     }
     constexpr size_t kTile = (size_t)kB * kU;
-    const uint64_t tiles = first + (nvec - hv + kTile - 1) / kTile + (tail ? 1 : 0);
+    const uint64_t tiles = first + (nvec - hv + kTile - 1) / kTile + ((tail | lead) ? 1 : 0);
     return launch_kernel(reduce_vec_kernel<T, Op, NP, MAXP, kU, kB>, dim3(grid_for(tiles)),
                          dim3(kB), lds_for_waves(waves_for<T, NP>(count * T::kSize, nsrc)), s, ks, nsrc,
-                         dst, nvec, tail, head);
+                         dst, nvec, tail, head, lead);
 }
 
 template <class T, class Op>
 hipError_t go(const char *const *srcs, int nsrc, char *dst, size_t count, hipStream_t s)
 {
-    uintptr_t bits = (uintptr_t)dst;
-    for (int p = 0; p < nsrc; ++p) bits |= (uintptr_t)srcs[p];
-    if (bits & 15u) {
+    // Pointers all at one offset m within 16 bytes (views at one element
+    // offset, a reduce-scatter shard) take the vector path after `lead`
+    // elements that bring them to a 16-byte boundary; others are scalar.
+    const uintptr_t m = (uintptr_t)dst & 15u;
+    bool common = true;
+    for (int p = 0; p < nsrc; ++p) common = common && ((uintptr_t)srcs[p] & 15u) == m;
+    const uint32_t lead = m == 0 ? 0u : (uint32_t)((16 - m) / T::kSize);
+    if (!common || lead >= count) {
         KernargSrc<XRED_MAX_SRC> ks;
         for (int p = 0; p < nsrc; ++p) ks.p[p] = srcs[p];
         for (int p = nsrc; p < XRED_MAX_SRC; ++p) ks.p[p] = nullptr;
@@ -154,26 +160,26 @@ hipError_t go(const char *const *srcs, int nsrc, char *dst, size_t count, hipStr
     }
     constexpr bool kWide = is_core_type<T>() && !__is_same(Op, OpAvg);
     switch (nsrc) {
-    case 1: return go_vec<T, Op, 1, 8>(srcs, nsrc, dst, count, s);
-    case 2: return go_vec<T, Op, 2, 8>(srcs, nsrc, dst, count, s);
-    case 3: return go_vec<T, Op, 3, 8>(srcs, nsrc, dst, count, s);
-    case 4: return go_vec<T, Op, 4, 8>(srcs, nsrc, dst, count, s);
-    case 5: return go_vec<T, Op, 5, 8>(srcs, nsrc, dst, count, s);
-    case 6: return go_vec<T, Op, 6, 8>(srcs, nsrc, dst, count, s);
-    case 7: return go_vec<T, Op, 7, 8>(srcs, nsrc, dst, count, s);
-    case 8: return go_vec<T, Op, 8, 8>(srcs, nsrc, dst, count, s);
+    case 1: return go_vec<T, Op, 1, 8>(srcs, nsrc, dst, count, lead, s);
+    case 2: return go_vec<T, Op, 2, 8>(srcs, nsrc, dst, count, lead, s);
+    case 3: return go_vec<T, Op, 3, 8>(srcs, nsrc, dst, count, lead, s);
+    case 4: return go_vec<T, Op, 4, 8>(srcs, nsrc, dst, count, lead, s);
+    case 5: return go_vec<T, Op, 5, 8>(srcs, nsrc, dst, count, lead, s);
+    case 6: return go_vec<T, Op, 6, 8>(srcs, nsrc, dst, count, lead, s);
+    case 7: return go_vec<T, Op, 7, 8>(srcs, nsrc, dst, count, lead, s);
+    case 8: return go_vec<T, Op, 8, 8>(srcs, nsrc, dst, count, lead, s);
     case 16:
-        if constexpr (kWide) return go_vec<T, Op, 16, 16>(srcs, nsrc, dst, count, s);
+        if constexpr (kWide) return go_vec<T, Op, 16, 16>(srcs, nsrc, dst, count, lead, s);
         break;
     case 32:
-        if constexpr (kWide) return go_vec<T, Op, 32, 32>(srcs, nsrc, dst, count, s);
+        if constexpr (kWide) return go_vec<T, Op, 32, 32>(srcs, nsrc, dst, count, lead, s);
         break;
     case 64:
-        if constexpr (kWide) return go_vec<T, Op, 64, 64>(srcs, nsrc, dst, count, s);
+        if constexpr (kWide) return go_vec<T, Op, 64, 64>(srcs, nsrc, dst, count, lead, s);
         break;
     default: break;
     }
-    return go_vec<T, Op, 0, XRED_MAX_SRC>(srcs, nsrc, dst, count, s);
+    return go_vec<T, Op, 0, XRED_MAX_SRC>(srcs, nsrc, dst, count, lead, s);
 }
 
 

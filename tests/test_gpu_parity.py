@@ -268,6 +268,48 @@ def test_misaligned_and_guard_bands(xr, orc, dtype):
 
 
 @pytest.mark.parametrize("dtype", ["bf16", "f32", "u8", "f64"])
+def test_element_offsets_within_16_bytes(xr, orc, dtype):
+    """Buffers that are element- but not 16-byte aligned: when every pointer
+    sits at the same offset within 16 bytes, the first elements up to the
+    next boundary are folded one by one and the rest takes the vector path
+    (lengths at, below and just past that lead, and long ones); sources at
+    different offsets, or the output at another one, take the scalar path.
+    Canaries around the output stay untouched."""
+    rng = np.random.default_rng(17)
+    es = {"bf16": 2, "f32": 4, "u8": 1, "f64": 8}[dtype]
+    G = 64
+    cases = []
+    for m in range(es, 16, es):                 # every element offset within 16 B
+        lead = (16 - m) // es
+        for n in (1, lead - 1, lead, lead + 1, lead + 16 // es + 3, 70001, 600011):
+            if n >= 1:
+                cases.append(("common", m, n))
+    cases += [("sources differ", es, 70001), ("output differs", es, 70001),
+              ("sources differ", es, 5), ("output differs", 16 - es, 600011)]
+    for k, (kind, m, n) in enumerate(cases):
+        P = (2, 3, 8, 17)[k % 4]
+        srcs = [pins.random_column_values(rng, dtype, n) for _ in range(P)]
+        keep, views = [], []
+        for p, a in enumerate(srcs):
+            o = m if kind != "sources differ" or p % 2 == 0 else (m + es) % 16
+            big = torch.zeros(o + n * es + 16, dtype=torch.uint8, device="cuda")
+            v = big[o:o + n * es].view(gu.torch_dtype(dtype))
+            v.copy_(gu.to_dev(a, dtype))
+            keep.append(big)
+            views.append(v)
+        do = m if kind != "output differs" else (m + es) % 16
+        store = torch.full((G + do + n * es + G,), 0x5A, dtype=torch.uint8, device="cuda")
+        out = store[G + do:G + do + n * es].view(gu.torch_dtype(dtype))
+        xr.allreduce_local(views, out, "sum", dtype=dtype)
+        torch.cuda.synchronize()
+        what = f"{kind} {dtype} P={P} offset={m} n={n}"
+        gu.assert_parity(out, orc.allreduce_local(srcs, dtype, "sum"), dtype, "sum", what)
+        raw = store.cpu().numpy()
+        assert np.all(raw[:G + do] == 0x5A), what
+        assert np.all(raw[G + do + n * es:] == 0x5A), what
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32", "u8", "f64"])
 def test_line_misaligned_buffers(xr, orc, dtype):
     """16-byte-aligned buffers that start inside a 128-byte line take the
     vector path with a short first tile up to the first source's next line:
