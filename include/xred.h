@@ -59,11 +59,12 @@
  *   - Device faults (e.g. a pointer to freed memory) surface at the caller's
  *     next synchronisation of the stream, as for any HIP kernel.
  *   - Element pointers must be aligned to the element size; 16-byte aligned
- *     buffers take the fast vector path.  xred_allreduce_local and
- *     xred_reduce_scatter_local also take it when every pointer of the call
- *     sits at the same offset within 16 bytes (views at one element offset):
- *     the elements before the next 16-byte boundary are folded one by one.
- *     Other alignments take a slower scalar path with the same results.
+ *     buffers take the fast vector path.  xred_allreduce_local,
+ *     xred_reduce_scatter_local and every item of xred_batched_reduce also
+ *     take it when all pointers of the call (of the item) sit at the same
+ *     offset within 16 bytes (views at one element offset): the elements
+ *     before the next 16-byte boundary are folded one by one.  Other
+ *     alignments take a slower scalar path with the same results.
  *   - Device words the library binds to a stream (the ring's relay word, the
  *     batch queue's counters) are looked up by the stream's handle.  Let a
  *     stream's work finish before destroying it if a stream created later

@@ -119,6 +119,22 @@ __device__ __forceinline__ uint64_t block_exclusive_scan(uint64_t v, uint64_t *s
     return before + incl - v;
 }
 
+// An item's buffers take the vector path when every pointer sits at the same
+// offset m within 16 bytes (diff: the bits in which some source's address
+// differs from dst's) and m is a whole number of elements: the first
+// (16 - m) / size elements, fewer than a vector, are folded one by one and
+// the rest is 16-byte aligned.  Returns that element count (at most count),
+// or kNoVector.
+constexpr uint64_t kNoVector = ~0ull;
+template <class T>
+__device__ __forceinline__ uint64_t item_lead(uintptr_t diff, uintptr_t dst, uint64_t count)
+{
+    const uintptr_t m = dst & 15u;
+    if ((diff & 15u) != 0 || m % T::kSize != 0) return kNoVector;
+    const uint64_t lead = m == 0 ? 0 : (16 - m) / T::kSize;
+    return lead < count ? lead : count;
+}
+
 // Tile lt (of SUB sub-tiles of kB*kU vectors) of one item.
 template <class T, class Op, int SUB = kSub>
 __device__ void batched_tile(const xred_item &it, uint64_t lt)
@@ -127,24 +143,26 @@ __device__ void batched_tile(const xred_item &it, uint64_t lt)
     constexpr uint64_t kTileElems = (uint64_t)kB * kU * SUB * T::kVec;
     const char *const *sp = (const char *const *)it.srcs;
     const int nsrc = (int)it.nsrc;
-    uintptr_t bits = (uintptr_t)it.dst;
+    uintptr_t diff = 0;   // bits in which some source's address differs from dst's
     bool null_src = false;
     for (int p = 0; p < nsrc; ++p) {
         const uintptr_t q = (uintptr_t)sload(sp + p);
-        bits |= q;
+        diff |= q ^ (uintptr_t)it.dst;
         null_src |= q == 0;
     }
     if (null_src) return;
     char *dst = (char *)it.dst;
     const GlobalSrc src{sp};
     const uint64_t count = it.count;
-    if ((bits & 15u) == 0) {
-        const size_t nvec = count / T::kVec;
+    const uint64_t lead = item_lead<T>(diff, (uintptr_t)dst, count);
+    if (lead != kNoVector) {
+        const size_t lb = (size_t)lead * T::kSize;   // bytes before the first vector
+        const size_t nvec = (count - lead) / T::kVec;
         const size_t vbytes = nvec * 16;
         for (int h = 0; h < SUB; ++h) {
             const size_t off = lt * kTileBytes + (size_t)h * kSubBytes;
             if (off >= vbytes) break;
-            const Tile tl{off, tile_nrec(vbytes, off, kSubBytes)};
+            const Tile tl{lb + off, tile_nrec(vbytes, off, kSubBytes)};
             switch (nsrc) {
             case 1: reduce_tile<T, Op, 1, kU, kB>(src, nsrc, dst, tl); break;
             case 2: reduce_tile<T, Op, 2, kU, kB>(src, nsrc, dst, tl); break;
@@ -160,10 +178,13 @@ __device__ void batched_tile(const xred_item &it, uint64_t lt)
             default: reduce_tile<T, Op, 0, kU, kB>(src, nsrc, dst, tl); break;
             }
         }
-        // the item's last tile also takes the elements after its last full vector
+        // the item's first tile also takes the elements before its first
+        // vector, its last tile those after its last full vector
+        if (lt == 0 && threadIdx.x < lead) reduce_elem<T, Op>(src, nsrc, dst, threadIdx.x);
         if ((lt + 1) * kTileElems >= count) {
-            const uint32_t tail = (uint32_t)(count % T::kVec);
-            if (threadIdx.x < tail) reduce_elem<T, Op>(src, nsrc, dst, nvec * T::kVec + threadIdx.x);
+            const uint32_t tail = (uint32_t)((count - lead) % T::kVec);
+            if (threadIdx.x < tail)
+                reduce_elem<T, Op>(src, nsrc, dst, lead + nvec * T::kVec + threadIdx.x);
         }
     } else {
         const uint64_t e0 = lt * kTileElems;
@@ -218,9 +239,11 @@ struct TileDesc {
     uint64_t lt;              // tile within the item
     uint32_t k;               // item
     int nsrc;
-    bool fast;                // nsrc <= 8, no NULL source, all pointers 16-byte aligned
+    uint32_t lead;            // elements before the first vector (item_lead; 0 unless fast)
+    bool fast;                // nsrc <= 8, no NULL source, every pointer at one offset in 16 B
 };
 
+template <class T>
 __device__ __forceinline__ void fetch_desc(TileDesc &d, const xred_item *items, uint32_t k,
                                            uint64_t lt)
 {
@@ -231,15 +254,17 @@ __device__ __forceinline__ void fetch_desc(TileDesc &d, const xred_item *items, 
     d.dst = (char *)sload(&it->dst);
     d.count = sload(&it->count);
     d.nsrc = (int)sload(&it->nsrc);
-    uintptr_t bits = (uintptr_t)d.dst;
+    uintptr_t diff = 0;
     bool null_src = false;
 #pragma unroll
     for (int q = 0; q < 8; ++q) {
         d.p[q] = q < d.nsrc ? sload(d.srcs + q) : nullptr;
-        bits |= (uintptr_t)d.p[q];
+        diff |= q < d.nsrc ? (uintptr_t)d.p[q] ^ (uintptr_t)d.dst : 0;
         null_src |= q < d.nsrc && d.p[q] == nullptr;
     }
-    d.fast = d.nsrc <= 8 && !null_src && (bits & 15u) == 0;
+    const uint64_t lead = item_lead<T>(diff, (uintptr_t)d.dst, d.count);
+    d.fast = d.nsrc <= 8 && !null_src && lead != kNoVector;
+    d.lead = d.fast ? (uint32_t)lead : 0u;
 }
 
 template <class T, class Op, bool PLANNED>
@@ -282,31 +307,32 @@ __global__ __launch_bounds__(kB) void batched_rr_kernel(const xred_item *items, 
         }
         __syncthreads();
         TileDesc cur, nxt;
-        fetch_desc(cur, items, __builtin_amdgcn_readfirstlane(s_list[0].x),
+        fetch_desc<T>(cur, items, __builtin_amdgcn_readfirstlane(s_list[0].x),
                    __builtin_amdgcn_readfirstlane(s_list[0].y));
         for (int j = 0; j < n; ++j) {
             // Issue the current tile's loads.  Straight-line code: sources
             // beyond nsrc, and tiles not on the fast path, get a zero-length
             // buffer range, so their loads return 0 without touching memory
             // and their store is dropped.
-            const size_t nvec = cur.count / T::kVec;
+            const size_t lb = (size_t)cur.lead * T::kSize;
+            const size_t nvec = (cur.count - cur.lead) / T::kVec;
             const size_t vbytes = nvec * 16, toff = cur.lt * kTileBytes;
             const uint32_t nrec = cur.fast && toff < vbytes ? tile_nrec(vbytes, toff, kTileBytes) : 0u;
             u32x4 in[8][kSub];
 #pragma unroll
             for (int q = 0; q < 8; ++q) {
                 const bool on = q < cur.nsrc;
-                const rsrc_t r = make_rsrc((on ? cur.p[q] : cur.dst) + toff, on ? nrec : 0u);
+                const rsrc_t r = make_rsrc((on ? cur.p[q] : cur.dst) + lb + toff, on ? nrec : 0u);
 #pragma unroll
                 for (int h = 0; h < kSub; ++h)
                     in[q][h] = bload<kLoadStream>(r, (uint32_t)(h * kB + threadIdx.x) * 16u);
             }
             // fetch the next tile's descriptor while those loads are in flight
             if (j + 1 < n)
-                fetch_desc(nxt, items, __builtin_amdgcn_readfirstlane(s_list[j + 1].x),
+                fetch_desc<T>(nxt, items, __builtin_amdgcn_readfirstlane(s_list[j + 1].x),
                            __builtin_amdgcn_readfirstlane(s_list[j + 1].y));
             // fold (unused sources skipped by a uniform select) and store
-            const rsrc_t w = make_rsrc(cur.dst + toff, nrec);
+            const rsrc_t w = make_rsrc(cur.dst + lb + toff, nrec);
 #pragma unroll
             for (int h = 0; h < kSub; ++h) {
                 typename T::Acc acc[T::kVec];
@@ -329,11 +355,13 @@ __global__ __launch_bounds__(kB) void batched_rr_kernel(const xred_item *items, 
                 bstore<kStoreOut>(down_vec<T, Op>(acc), w, (uint32_t)(h * kB + threadIdx.x) * 16u);
             }
             if (cur.fast) {
+                if (cur.lt == 0 && threadIdx.x < cur.lead)
+                    reduce_elem<T, Op>(GlobalSrc{cur.srcs}, cur.nsrc, cur.dst, threadIdx.x);
                 if ((cur.lt + 1) * tile_elems<T>() >= cur.count) {
-                    const uint32_t tail = (uint32_t)(cur.count % T::kVec);
+                    const uint32_t tail = (uint32_t)((cur.count - cur.lead) % T::kVec);
                     if (threadIdx.x < tail)
                         reduce_elem<T, Op>(GlobalSrc{cur.srcs}, cur.nsrc, cur.dst,
-                                           nvec * T::kVec + threadIdx.x);
+                                           cur.lead + nvec * T::kVec + threadIdx.x);
                 }
             } else {
                 batched_tile<T, Op>(load_item(items, cur.k), cur.lt);
@@ -476,21 +504,22 @@ __global__ __launch_bounds__(kB) void batched_queue_kernel(const xred_item *item
     TileDesc cur{};
     if (g < total) {
         const int k = find_item(s_pre, nitems, (uint32_t)g);
-        fetch_desc(cur, items, (uint32_t)k, uniform64(g - s_pre[k]));
+        fetch_desc<T>(cur, items, (uint32_t)k, uniform64(g - s_pre[k]));
     }
     for (int b = 0; g < total; ++b) {
         uint64_t c = 0;
         if (threadIdx.x == 0) c = claim();   // answered while this tile streams
         // straight-line tile: sources beyond nsrc, and tiles off the fast
         // path, get a zero-length buffer range
-        const size_t nvec = cur.count / T::kVec;
+        const size_t lb = (size_t)cur.lead * T::kSize;
+        const size_t nvec = (cur.count - cur.lead) / T::kVec;
         const size_t vbytes = nvec * 16, toff = cur.lt * kTileBytes;
         const uint32_t nrec = cur.fast && toff < vbytes ? tile_nrec(vbytes, toff, kTileBytes) : 0u;
         u32x4 in[8][SUB];
 #pragma unroll
         for (int p = 0; p < 8; ++p) {
             const bool on = p < cur.nsrc;
-            const rsrc_t r = make_rsrc((on ? cur.p[p] : cur.dst) + toff, on ? nrec : 0u);
+            const rsrc_t r = make_rsrc((on ? cur.p[p] : cur.dst) + lb + toff, on ? nrec : 0u);
 #pragma unroll
             for (int h = 0; h < SUB; ++h)
                 in[p][h] = bload<kLoadStream>(r, (uint32_t)(h * kB + threadIdx.x) * 16u);
@@ -504,9 +533,9 @@ __global__ __launch_bounds__(kB) void batched_queue_kernel(const xred_item *item
         TileDesc nxt{};
         if (gn < total) {
             const int k = find_item(s_pre, nitems, (uint32_t)gn);
-            fetch_desc(nxt, items, (uint32_t)k, uniform64(gn - s_pre[k]));
+            fetch_desc<T>(nxt, items, (uint32_t)k, uniform64(gn - s_pre[k]));
         }
-        const rsrc_t w = make_rsrc(cur.dst + toff, nrec);
+        const rsrc_t w = make_rsrc(cur.dst + lb + toff, nrec);
 #pragma unroll
         for (int h = 0; h < SUB; ++h) {
             typename T::Acc acc[T::kVec];
@@ -529,11 +558,13 @@ __global__ __launch_bounds__(kB) void batched_queue_kernel(const xred_item *item
             bstore<kStoreOut>(down_vec<T, Op>(acc), w, (uint32_t)(h * kB + threadIdx.x) * 16u);
         }
         if (cur.fast) {
+            if (cur.lt == 0 && threadIdx.x < cur.lead)
+                reduce_elem<T, Op>(GlobalSrc{cur.srcs}, cur.nsrc, cur.dst, threadIdx.x);
             if ((cur.lt + 1) * kTileElems >= cur.count) {
-                const uint32_t tail = (uint32_t)(cur.count % T::kVec);
+                const uint32_t tail = (uint32_t)((cur.count - cur.lead) % T::kVec);
                 if (threadIdx.x < tail)
                     reduce_elem<T, Op>(GlobalSrc{cur.srcs}, cur.nsrc, cur.dst,
-                                       nvec * T::kVec + threadIdx.x);
+                                       cur.lead + nvec * T::kVec + threadIdx.x);
             }
         } else {
             batched_tile<T, Op, SUB>(load_item(items, cur.k), cur.lt);
@@ -608,29 +639,33 @@ __device__ __forceinline__ void table_tile(const ItemHead &h, uint64_t lt)
     const uint64_t count = h.count;
     const int nsrc = h.nsrc;
     const GlobalSrc src{srcs};
-    const size_t nvec = count / T::kVec, vbytes = nvec * 16, toff = lt * kBytes;
+    const size_t toff = lt * kBytes;
     const char *p[8];
-    uintptr_t bits = (uintptr_t)dst;
+    uintptr_t diff = 0;   // bits in which some source's address differs from dst's
     bool null_src = false;
 #pragma unroll
     for (int q = 0; q < 8; ++q) {
         p[q] = q < nsrc ? sload(srcs + q) : nullptr;
-        bits |= (uintptr_t)p[q];
+        diff |= q < nsrc ? (uintptr_t)p[q] ^ (uintptr_t)dst : 0;
         null_src |= q < nsrc && p[q] == nullptr;
     }
-    if (nsrc > 8 || (bits & 15u) != 0) {
+    uint64_t lead = item_lead<T>(diff, (uintptr_t)dst, count);
+    if (nsrc > 8 || lead == kNoVector) {
         // the general tile: any source count, element-aligned buffers
-        uintptr_t all = (uintptr_t)dst;
+        uintptr_t all = 0;
         for (int q = 0; q < nsrc; ++q) {
             const uintptr_t x = (uintptr_t)sload(srcs + q);
-            all |= x;
+            all |= x ^ (uintptr_t)dst;
             null_src |= x == 0;
         }
         if (CHECK && null_src) return;
-        if ((all & 15u) == 0) {
+        lead = item_lead<T>(all, (uintptr_t)dst, count);
+        if (lead != kNoVector) {
+            const size_t nvec = (count - lead) / T::kVec, vbytes = nvec * 16;
             if (toff < vbytes)
-                reduce_tile<T, Op, 0, U, kTB>(src, nsrc, dst,
-                                              Tile{toff, tile_nrec(vbytes, toff, kBytes)});
+                reduce_tile<T, Op, 0, U, kTB>(
+                    src, nsrc, dst,
+                    Tile{(size_t)lead * T::kSize + toff, tile_nrec(vbytes, toff, kBytes)});
         } else {
             const uint64_t e0 = lt * table_tile_elems<T>();
             const uint64_t e1 =
@@ -642,17 +677,19 @@ __device__ __forceinline__ void table_tile(const ItemHead &h, uint64_t lt)
     } else {
         if (CHECK && null_src) return;
         // straight-line tile: sources beyond nsrc get a zero-length range
+        const size_t lb = (size_t)lead * T::kSize;
+        const size_t vbytes = (count - lead) / T::kVec * 16;
         const uint32_t nrec = toff < vbytes ? tile_nrec(vbytes, toff, kBytes) : 0u;
         u32x4 in[8][U];
 #pragma unroll
         for (int q = 0; q < 8; ++q) {
             const bool on = q < nsrc;
-            const rsrc_t r = make_rsrc((on ? p[q] : dst) + toff, on ? nrec : 0u);
+            const rsrc_t r = make_rsrc((on ? p[q] : dst) + lb + toff, on ? nrec : 0u);
 #pragma unroll
             for (int u = 0; u < U; ++u)
                 in[q][u] = bload<kLoadStream>(r, (uint32_t)(u * kTB + threadIdx.x) * 16u);
         }
-        const rsrc_t w = make_rsrc(dst + toff, nrec);
+        const rsrc_t w = make_rsrc(dst + lb + toff, nrec);
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             typename T::Acc acc[T::kVec];
@@ -675,10 +712,14 @@ __device__ __forceinline__ void table_tile(const ItemHead &h, uint64_t lt)
             bstore<kStoreOut>(down_vec<T, Op>(acc), w, (uint32_t)(u * kTB + threadIdx.x) * 16u);
         }
     }
-    // the item's last tile also takes the elements after its last full vector
+    // the item's first tile also takes the elements before its first vector,
+    // its last tile those after its last full vector
+    if (lt == 0 && threadIdx.x < lead) reduce_elem<T, Op>(src, nsrc, dst, threadIdx.x);
     if ((lt + 1) * table_tile_elems<T>() >= count) {
-        const uint32_t tail = (uint32_t)(count % T::kVec);
-        if (threadIdx.x < tail) reduce_elem<T, Op>(src, nsrc, dst, nvec * T::kVec + threadIdx.x);
+        const uint64_t nvec = (count - lead) / T::kVec;
+        const uint32_t tail = (uint32_t)((count - lead) % T::kVec);
+        if (threadIdx.x < tail)
+            reduce_elem<T, Op>(src, nsrc, dst, lead + nvec * T::kVec + threadIdx.x);
     }
 }
 

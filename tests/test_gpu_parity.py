@@ -627,6 +627,87 @@ def _staged_bytes(sizes, nsrc, tile_elems):
     return 32 * len(sizes) + (width * tiles + 7) // 8 * 8 + 8 * nsrc * len(sizes)
 
 
+@pytest.mark.parametrize("dtype", ["bf16", "f32", "u8", "f64"])
+@pytest.mark.parametrize("on_device", [False, True])
+def test_batched_element_offsets(xr, orc, dtype, on_device):
+    """Batch items whose buffers are element- but not 16-byte aligned: items
+    whose pointers all sit at one offset within 16 bytes fold the elements
+    before the next boundary one by one and take the vector path for the
+    rest (every offset; lengths below, at and past that lead, several tiles;
+    up to 8 sources and the general tile's 9-17); items whose sources sit at
+    different offsets, or whose output does, take the scalar path.  Host
+    and device descriptors (past 64 items: the queue kernel); canaries
+    between the outputs stay untouched."""
+    rng = np.random.default_rng(19 + on_device)
+    es = {"bf16": 2, "f32": 4, "u8": 1, "f64": 8}[dtype]
+    items_np, specs = [], []
+    for m in range(es, 16, es):
+        lead = (16 - m) // es
+        for n in (1, lead - 1, lead, lead + 1, lead + 16 // es + 3, 9000, 40001):
+            if n >= 1:
+                specs.append(("common", m, n))
+    specs += [("sources differ", es, 9000), ("output differs", es, 40001),
+              ("sources differ", 16 - es, 3), ("output differs", es, 17)]
+    if on_device:   # past 64 items: the queue kernel, not the one-run kernel
+        specs = (specs * (70 // len(specs) + 1))[:max(70, len(specs))]
+    keep, items, rows, outs, G = [], [], [], [], 64
+    for k, (kind, m, n) in enumerate(specs):
+        P = (1, 3, 8, 9, 17)[k % 5]
+        srcs = [pins.random_column_values(rng, dtype, n) for _ in range(P)]
+        items_np.append(srcs)
+        views = []
+        for p, a in enumerate(srcs):
+            o = m if kind != "sources differ" or p % 2 == 0 else (m + es) % 16
+            big = torch.zeros(o + n * es + 16, dtype=torch.uint8, device="cuda")
+            v = big[o:o + n * es].view(gu.torch_dtype(dtype))
+            v.copy_(gu.to_dev(a, dtype))
+            keep.append(big)
+            views.append(v)
+        do = m if kind != "output differs" else (m + es) % 16
+        store = torch.full((G + do + n * es + G,), 0x5A, dtype=torch.uint8, device="cuda")
+        out = store[G + do:G + do + n * es].view(gu.torch_dtype(dtype))
+        outs.append((store, out, do, n, kind, m, P))
+        items.append((views, out))
+        if on_device:
+            pa = torch.tensor([v.data_ptr() for v in views], dtype=torch.int64, device="cuda")
+            keep.append(pa)
+            rows.append((pa.data_ptr(), out.data_ptr(), n, P, 0))
+    torch.cuda.synchronize()
+    if on_device:
+        arr = np.zeros(len(rows), xr.ITEM_DTYPE)
+        for k, r in enumerate(rows):
+            arr[k] = r
+        desc = torch.from_numpy(arr.view(np.uint8).copy()).to("cuda")
+        xr.batched_reduce(desc, "sum", dtype=dtype)
+    else:
+        xr.batched_reduce(items, "sum", dtype=dtype)
+    torch.cuda.synchronize()
+    exps = [orc.allreduce_local(srcs, dtype, "sum") for srcs in items_np]
+
+    def check(how):
+        for exp, (store, out, do, n, kind, m, P) in zip(exps, outs):
+            what = f"{kind} {dtype} P={P} offset={m} n={n} {how}"
+            gu.assert_parity(out, exp, dtype, "sum", what)
+            raw = store.cpu().numpy()
+            assert np.all(raw[:G + do] == 0x5A), what
+            assert np.all(raw[G + do + n * es:] == 0x5A), what
+
+    check("device descriptors" if on_device else "host descriptors")
+    if on_device:
+        # under graph capture the batch runs as runs of items dealt tile by
+        # tile (not the queue kernel); replayed twice over zeroed outputs
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            xr.batched_reduce(desc, "sum", dtype=dtype)
+        for r in range(2):
+            for _, out, *_ in outs:
+                out.view(torch.uint8).zero_()
+            torch.cuda.synchronize()
+            g.replay()
+            torch.cuda.synchronize()
+            check(f"graph replay {r}")
+
+
 def test_batched_host_caller_stream_destroyed(xr, orc):
     """Host batches on streams the caller destroys as soon as each call has
     finished (more such streams than the library has staging slots; batches
