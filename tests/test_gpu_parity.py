@@ -273,8 +273,9 @@ def test_element_offsets_within_16_bytes(xr, orc, dtype):
     sits at the same offset within 16 bytes, the first elements up to the
     next boundary are folded one by one and the rest takes the vector path
     (lengths at, below and just past that lead, and long ones); sources at
-    different offsets, or the output at another one, take the scalar path.
-    Canaries around the output stay untouched."""
+    different offsets take the scalar path, the output at another offset
+    the vector loads with split stores.  Canaries around the output stay
+    untouched."""
     rng = np.random.default_rng(17)
     es = {"bf16": 2, "f32": 4, "u8": 1, "f64": 8}[dtype]
     G = 64
@@ -307,6 +308,72 @@ def test_element_offsets_within_16_bytes(xr, orc, dtype):
         raw = store.cpu().numpy()
         assert np.all(raw[:G + do] == 0x5A), what
         assert np.all(raw[G + do + n * es:] == 0x5A), what
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32", "u8", "f64", "e5m2", "i64"])
+def test_output_at_another_offset(xr, orc, dtype):
+    """Sources at one offset within 16 bytes and the output at another (the
+    shard of every rank but some of a reduce-scatter with an odd shard
+    length): the sources are read in vectors after the lead and each result
+    vector is stored in aligned pieces of 1, 2, 4 or 8 bytes.  Every pair of
+    element offsets; lengths just past the lead, past one vector, across a
+    few tiles with a ragged tail, and long; 1 to 17 sources (every first and
+    last group size of the runtime-count fold); sum, and max / avg / prod on
+    some.  Canaries around the output stay untouched."""
+    rng = np.random.default_rng(19)
+    es = xr.ELEM_SIZE[dtype]
+    G = 64
+    offs = list(range(0, 16, es))
+    cases = []
+    for ms in offs:
+        for md in offs:
+            if md == ms:
+                continue
+            lead = (16 - ms) % 16 // es
+            for n in (lead + 1, lead + 16 // es + 3, 128 * 3 * 16 // es + 7):
+                cases.append((ms, md, n))
+    big = [(ms, md, 600011) for ms, md in ((offs[1], 0), (0, offs[-1]), (offs[-1], offs[1]))
+           if ms != md]
+    ops = ["sum", "max", "avg" if dtype in gu.FLOATS else "min", "prod"]
+    for k, (ms, md, n) in enumerate(cases + big):
+        P = (1, 3, 8, 9, 17, 5, 16, 2)[k % 8]
+        op = ops[k % 4] if n < 600011 else "sum"
+        srcs = [pins.random_column_values(rng, dtype, n) for _ in range(P)]
+        keep, views = [], []
+        for a in srcs:
+            b = torch.zeros(ms + n * es + 16, dtype=torch.uint8, device="cuda")
+            v = b[ms:ms + n * es].view(gu.torch_dtype(dtype))
+            v.copy_(gu.to_dev(a, dtype))
+            keep.append(b)
+            views.append(v)
+        store = torch.full((G + md + n * es + G,), 0x5A, dtype=torch.uint8, device="cuda")
+        out = store[G + md:G + md + n * es].view(gu.torch_dtype(dtype))
+        xr.allreduce_local(views, out, op, dtype=dtype)
+        torch.cuda.synchronize()
+        what = f"{dtype} {op} P={P} sources at {ms} output at {md} n={n}"
+        gu.assert_parity(out, orc.allreduce_local(srcs, dtype, op), dtype, op, what)
+        raw = store.cpu().numpy()
+        assert np.all(raw[:G + md] == 0x5A), what
+        assert np.all(raw[G + md + n * es:] == 0x5A), what
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "u8", "f32"])
+def test_reduce_scatter_odd_shards(xr, orc, dtype):
+    """A reduce-scatter with an odd shard length: every rank's shard (rank 0
+    aligned, the others at other offsets within 16 bytes) against the
+    oracle, P = 8 and 16, one shard of a few tiles and one of 4 MiB."""
+    rng = np.random.default_rng(23)
+    for P, rc in ((8, 12345), (16, 3001), (8, (1 << 21) + 1)):
+        if rc > 1 << 20 and dtype != "bf16":
+            continue
+        srcs = [pins.random_column_values(rng, dtype, P * rc) for _ in range(P)]
+        d = [gu.to_dev(s, dtype) for s in srcs]
+        for r in range(P):
+            out = torch.empty(rc, dtype=d[0].dtype, device="cuda")
+            xr.reduce_scatter_local(d, r, out, "sum", dtype=dtype)
+            torch.cuda.synchronize()
+            gu.assert_parity(out, orc.reduce_scatter_local(srcs, r, dtype, "sum"), dtype, "sum",
+                             f"rs P={P} recvcount={rc} rank {r}")
 
 
 @pytest.mark.parametrize("dtype", ["bf16", "f32", "u8", "f64"])
