@@ -64,11 +64,11 @@
  *     take it when all pointers of the call (of the item) sit at the same
  *     offset within 16 bytes (views at one element offset): the elements
  *     before the next 16-byte boundary are folded one by one.
- *     xred_allreduce_local and xred_reduce_scatter_local read in vectors too
- *     when only the sources share an offset and dst sits at another (a
- *     reduce-scatter shard of odd length): results are realigned through
- *     LDS and stored as aligned 16-byte vectors.  Other alignments take a
- *     slower scalar path with the same results.
+ *     The same calls and items read in vectors too when only the sources
+ *     share an offset and dst sits at another (a reduce-scatter shard of odd
+ *     length): results are realigned across lanes and stored as aligned
+ *     16-byte vectors.  Sources at different offsets take a slower scalar
+ *     path with the same results.
  *   - Device words the library binds to a stream (the ring's relay word, the
  *     batch queue's counters) are looked up by the stream's handle.  Let a
  *     stream's work finish before destroying it if a stream created later

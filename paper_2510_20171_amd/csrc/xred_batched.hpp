@@ -135,6 +135,21 @@ __device__ __forceinline__ uint64_t item_lead(uintptr_t diff, uintptr_t dst, uin
     return lead < count ? lead : count;
 }
 
+// When item_lead finds no vector path but every source sits at one offset m
+// within 16 bytes (sdiff: the bits in which some source's address differs
+// from the first one's, s0) and m is a whole number of elements, the sources
+// still read in vectors after the first (16 - m) / size elements and the
+// output is realigned (split_tile).  Returns that element count, or kNoVector
+// (sources at different offsets, or an item no longer than the lead).
+template <class T>
+__device__ __forceinline__ uint64_t sources_lead(uintptr_t sdiff, uintptr_t s0, uint64_t count)
+{
+    const uintptr_t m = s0 & 15u;
+    if ((sdiff & 15u) != 0 || m % T::kSize != 0) return kNoVector;
+    const uint64_t lead = m == 0 ? 0 : (16 - m) / T::kSize;
+    return lead < count ? lead : kNoVector;
+}
+
 // Tile lt (of SUB sub-tiles of kB*kU vectors) of one item.
 template <class T, class Op, int SUB = kSub>
 __device__ void batched_tile(const xred_item &it, uint64_t lt)
@@ -144,17 +159,27 @@ __device__ void batched_tile(const xred_item &it, uint64_t lt)
     const char *const *sp = (const char *const *)it.srcs;
     const int nsrc = (int)it.nsrc;
     uintptr_t diff = 0;   // bits in which some source's address differs from dst's
+    uintptr_t sdiff = 0;  // ... from the first source's
+    const uintptr_t s0 = (uintptr_t)sload(sp);
     bool null_src = false;
     for (int p = 0; p < nsrc; ++p) {
         const uintptr_t q = (uintptr_t)sload(sp + p);
         diff |= q ^ (uintptr_t)it.dst;
+        sdiff |= q ^ s0;
         null_src |= q == 0;
     }
     if (null_src) return;
     char *dst = (char *)it.dst;
     const GlobalSrc src{sp};
     const uint64_t count = it.count;
-    const uint64_t lead = item_lead<T>(diff, (uintptr_t)dst, count);
+    uint64_t lead = item_lead<T>(diff, (uintptr_t)dst, count);
+    // the output at another offset than the sources: realigned stores (c > 0)
+    uint32_t c = 0;
+    if (lead == kNoVector) {
+        lead = sources_lead<T>(sdiff, s0, count);
+        if (lead != kNoVector) c = (uint32_t)(((uintptr_t)dst + lead * T::kSize) & 15u);
+        if (c == 0) lead = kNoVector;
+    }
     if (lead != kNoVector) {
         const size_t lb = (size_t)lead * T::kSize;   // bytes before the first vector
         const size_t nvec = (count - lead) / T::kVec;
@@ -163,6 +188,10 @@ __device__ void batched_tile(const xred_item &it, uint64_t lt)
             const size_t off = lt * kTileBytes + (size_t)h * kSubBytes;
             if (off >= vbytes) break;
             const Tile tl{lb + off, tile_nrec(vbytes, off, kSubBytes)};
+            if (c != 0) {
+                split_tile<T, Op, kB>(src, nsrc, dst, tl, c);
+                continue;
+            }
             switch (nsrc) {
             case 1: reduce_tile<T, Op, 1, kU, kB>(src, nsrc, dst, tl); break;
             case 2: reduce_tile<T, Op, 2, kU, kB>(src, nsrc, dst, tl); break;
@@ -652,20 +681,29 @@ __device__ __forceinline__ void table_tile(const ItemHead &h, uint64_t lt)
     uint64_t lead = item_lead<T>(diff, (uintptr_t)dst, count);
     if (nsrc > 8 || lead == kNoVector) {
         // the general tile: any source count, element-aligned buffers
-        uintptr_t all = 0;
+        uintptr_t all = 0, sdiff = 0;
+        const uintptr_t s0 = (uintptr_t)p[0];
         for (int q = 0; q < nsrc; ++q) {
             const uintptr_t x = (uintptr_t)sload(srcs + q);
             all |= x ^ (uintptr_t)dst;
+            sdiff |= x ^ s0;
             null_src |= x == 0;
         }
         if (CHECK && null_src) return;
         lead = item_lead<T>(all, (uintptr_t)dst, count);
+        uint32_t c = 0;   // > 0: the output at another offset than the sources
+        if (lead == kNoVector) {
+            lead = sources_lead<T>(sdiff, s0, count);
+            if (lead != kNoVector) c = (uint32_t)(((uintptr_t)dst + lead * T::kSize) & 15u);
+            if (c == 0) lead = kNoVector;
+        }
         if (lead != kNoVector) {
             const size_t nvec = (count - lead) / T::kVec, vbytes = nvec * 16;
-            if (toff < vbytes)
-                reduce_tile<T, Op, 0, U, kTB>(
-                    src, nsrc, dst,
-                    Tile{(size_t)lead * T::kSize + toff, tile_nrec(vbytes, toff, kBytes)});
+            const Tile tl{(size_t)lead * T::kSize + toff, tile_nrec(vbytes, toff, kBytes)};
+            if (toff < vbytes) {
+                if (c != 0) split_tile<T, Op, kTB>(src, nsrc, dst, tl, c);
+                else reduce_tile<T, Op, 0, U, kTB>(src, nsrc, dst, tl);
+            }
         } else {
             const uint64_t e0 = lt * table_tile_elems<T>();
             const uint64_t e1 =

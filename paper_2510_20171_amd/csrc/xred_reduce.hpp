@@ -15,8 +15,6 @@
 namespace xred {
 namespace {
 
-typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
-
 // Three tile shapes:
 //
 // * Launches that fit on the chip in one round (every tile resident at
@@ -107,141 +105,31 @@ size_t lds_for_waves(int waves)
 }
 
 // ------------------------------------------------- split destination --
-// Sources at one offset m within 16 bytes, the destination at another: after
-// `lead` elements every source is on a 16-byte boundary and is read in
-// vectors exactly as in reduce_vec_kernel, but dst + lead elements sits c
-// bytes (0 < c < 16, a multiple of the element size) past a 16-byte
-// boundary.  Each tile's results go through LDS: lane q writes its 16-byte
-// result, and after a barrier builds the 16 output bytes that start c bytes
-// before its own (the last c bytes of lane q-1's result and the first 16-c
-// of its own, joined with byte funnel shifts) and stores them as one aligned
-// vector.  Only the two chunks cut by the tile's ends (16-c bytes at its
-// start, c at its end, shared with the neighbouring tiles) are stored in
-// aligned pieces of the largest power of two dividing c.  A reduce-scatter
-// shard of odd length leaves every rank's shard but some in this case (P=8
-// bf16, 16 MiB per source: 51 us element by element, 32 us storing every
-// result in 2-byte pieces).  One 128-thread shape, any source count (the
-// first group takes up to 8 sources, all loads of a group in flight).
-template <class T, class Op, int B, class Src>
-__device__ __forceinline__ void fold_any(typename T::Acc (&acc)[1][T::kVec], const Src &src,
-                                         int nsrc, Tile tl)
-{
-    const int g0 = nsrc < 8 ? nsrc : 8;
-    switch (g0) {
-    case 1: fold_group<T, Op, 1, 1, B, true>(acc, src, 0, tl); break;
-    case 2: fold_group<T, Op, 2, 1, B, true>(acc, src, 0, tl); break;
-    case 3: fold_group<T, Op, 3, 1, B, true>(acc, src, 0, tl); break;
-    case 4: fold_group<T, Op, 4, 1, B, true>(acc, src, 0, tl); break;
-    case 5: fold_group<T, Op, 5, 1, B, true>(acc, src, 0, tl); break;
-    case 6: fold_group<T, Op, 6, 1, B, true>(acc, src, 0, tl); break;
-    case 7: fold_group<T, Op, 7, 1, B, true>(acc, src, 0, tl); break;
-    default: fold_group<T, Op, 8, 1, B, true>(acc, src, 0, tl); break;
-    }
-    int p = g0;
-    for (; p + 8 <= nsrc; p += 8) fold_group<T, Op, 8, 1, B, false>(acc, src, p, tl);
-    switch (nsrc - p) {
-    case 1: fold_group<T, Op, 1, 1, B, false>(acc, src, p, tl); break;
-    case 2: fold_group<T, Op, 2, 1, B, false>(acc, src, p, tl); break;
-    case 3: fold_group<T, Op, 3, 1, B, false>(acc, src, p, tl); break;
-    case 4: fold_group<T, Op, 4, 1, B, false>(acc, src, p, tl); break;
-    case 5: fold_group<T, Op, 5, 1, B, false>(acc, src, p, tl); break;
-    case 6: fold_group<T, Op, 6, 1, B, false>(acc, src, p, tl); break;
-    case 7: fold_group<T, Op, 7, 1, B, false>(acc, src, p, tl); break;
-    default: break;
-    }
-}
-
-// Bytes [s, s+16) of the 32 bytes lo:hi (lo at the lower address), 0 < s < 16.
-__device__ __forceinline__ u32x4 bytes_from(u32x4 lo, u32x4 hi, uint32_t s)
-{
-    const uint32_t w[8] = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
-    const uint32_t b = s & 3u;
-    u32x4 o;
-    switch (s >> 2) {
-    case 0:
-        for (int i = 0; i < 4; ++i) o[i] = __builtin_amdgcn_alignbyte(w[i + 1], w[i], b);
-        break;
-    case 1:
-        for (int i = 0; i < 4; ++i) o[i] = __builtin_amdgcn_alignbyte(w[i + 2], w[i + 1], b);
-        break;
-    case 2:
-        for (int i = 0; i < 4; ++i) o[i] = __builtin_amdgcn_alignbyte(w[i + 3], w[i + 2], b);
-        break;
-    default:
-        for (int i = 0; i < 4; ++i) o[i] = __builtin_amdgcn_alignbyte(w[i + 4], w[i + 3], b);
-        break;
-    }
-    return o;
-}
-
-// `piece` bytes (1, 2, 4 or 8) copied from LDS at `from` to byte `off` of r;
-// both addresses are multiples of piece.
-__device__ __forceinline__ void store_piece(const char *from, rsrc_t r, uint32_t off,
-                                            uint32_t piece)
-{
-    switch (piece) {
-    case 8:
-        __builtin_amdgcn_raw_buffer_store_b64(*(const u32x2 *)from, r, off, 0, kStoreOut);
-        break;
-    case 4:
-        __builtin_amdgcn_raw_buffer_store_b32(*(const uint32_t *)from, r, off, 0, kStoreOut);
-        break;
-    case 2:
-        __builtin_amdgcn_raw_buffer_store_b16(*(const unsigned short *)from, r, off, 0,
-                                              kStoreOut);
-        break;
-    default:
-        __builtin_amdgcn_raw_buffer_store_b8(*(const unsigned char *)from, r, off, 0, kStoreOut);
-        break;
-    }
-}
-
-// reduce_vec_kernel's tiles (U = 1) with shifted stores; tail and lead as
-// there.  Dynamic LDS: at least 2*B*16 bytes (two tile buffers, so one
-// barrier per tile suffices).
+// Sources at one offset m within 16 bytes, the destination at another (a
+// reduce-scatter shard of odd length leaves every rank's shard but some in
+// this case): after `lead` elements every source is on a 16-byte boundary
+// and is read in vectors as in reduce_vec_kernel, and each tile's results are
+// realigned to dst's 16-byte grid and stored in aligned vectors (split_tile).
+// P=8 bf16, 16 MiB per source: 51 us element by element, 32 us storing every
+// result in 2-byte pieces, 24 us realigned (23.3 us with every buffer
+// aligned).  One 128-thread shape, any source count.
+// reduce_vec_kernel's tiles (U = 1) through split_tile; tail and lead as
+// there.
 template <class T, class Op, int B>
 __global__ __launch_bounds__(B) void reduce_split_kernel(KernargSrc<XRED_MAX_SRC> src, int nsrc,
                                                          char *dst, size_t nvec, uint32_t tail,
                                                          uint32_t head, uint32_t lead, uint32_t c)
 {
-    static_assert(B >= 64 + 16, "the tile-end pieces are stored by lanes 64..79");
-    extern __shared__ __attribute__((aligned(16))) char split_lds[];
     constexpr uint32_t kTileBytes = (uint32_t)B * 16u;
     const size_t vbytes = nvec * 16;
     const size_t lb = (size_t)lead * T::kSize;
     const uint32_t first = head != 0 ? 1u : 0u;
     const size_t ntiles = first + (vbytes - head + kTileBytes - 1) / kTileBytes;
-    const uint32_t piece = c & (~c + 1u);
-    const uint32_t q = threadIdx.x;
-    uint32_t parity = 0;
-    for (size_t t = blockIdx.x; t < ntiles; t += gridDim.x, parity ^= 1u) {
+    for (size_t t = blockIdx.x; t < ntiles; t += gridDim.x) {
         const bool h = t < first;
         const size_t off = h ? 0 : head + (t - first) * kTileBytes;
-        const Tile tl{lb + off, h ? head : tile_nrec(vbytes, off, kTileBytes)};
-        typename T::Acc acc[1][T::kVec];
-        fold_any<T, Op, B>(acc, src, nsrc, tl);
-        if constexpr (__is_same(Op, OpAvg)) {
-#pragma unroll
-            for (int j = 0; j < T::kVec; ++j) acc[0][j] = avg_scale<T, Op>(acc[0][j], nsrc);
-        }
-        const u32x4 mine = down_vec<T, Op>(acc[0]);
-        char *buf = split_lds + parity * kTileBytes;
-        *(u32x4 *)(buf + 16 * q) = mine;
-        __syncthreads();
-        // whole chunks: lane q (1 <= q < nrec/16) stores output bytes
-        // [16q - c, 16q + 16 - c) of the tile, from base dst + tl.off - c
-        if (q >= 1) {
-            const u32x4 prev = *(const u32x4 *)(buf + 16 * (q - 1));
-            bstore<kStoreOut>(bytes_from(prev, mine, 16u - c),
-                              make_rsrc(dst + tl.off - c, tl.nrec), 16u * q);
-        }
-        // the cut chunks: bytes [0, 16 - c) by lanes 0.., [nrec - c, nrec) by lanes 64..
-        const rsrc_t w = make_rsrc(dst + tl.off, tl.nrec);
-        if (q < (16u - c) / piece) store_piece(buf + q * piece, w, q * piece, piece);
-        if (q >= 64 && q - 64 < c / piece) {
-            const uint32_t o = tl.nrec - c + (q - 64) * piece;
-            store_piece(buf + o, w, o, piece);
-        }
+        split_tile<T, Op, B>(src, nsrc, dst,
+                             Tile{lb + off, h ? head : tile_nrec(vbytes, off, kTileBytes)}, c);
     }
     if ((tail | lead) != 0 && blockIdx.x == ntiles % gridDim.x) {
         if (threadIdx.x < tail)
@@ -284,10 +172,9 @@ hipError_t go_split(const char *const *srcs, int nsrc, char *dst, size_t count, 
     const size_t hv = head / 16, first = head != 0 ? 1 : 0;
     const uint32_t c = (uint32_t)(((uintptr_t)dst + (size_t)lead * T::kSize) & 15u);
     const uint64_t tiles = first + (nvec - hv + kB - 1) / kB + ((tail | lead) ? 1 : 0);
-    const size_t lds = std::max<size_t>(lds_for_waves(waves_split<T>(count * T::kSize, nsrc)),
-                                        2 * kB * 16);
-    return launch_kernel(reduce_split_kernel<T, Op, kB>, dim3(grid_for(tiles)), dim3(kB), lds, s,
-                         ks, nsrc, dst, nvec, tail, head, lead, c);
+    return launch_kernel(reduce_split_kernel<T, Op, kB>, dim3(grid_for(tiles)), dim3(kB),
+                         lds_for_waves(waves_split<T>(count * T::kSize, nsrc)), s, ks, nsrc, dst,
+                         nvec, tail, head, lead, c);
 }
 
 template <class T, class Op, int NP, int MAXP>

@@ -695,30 +695,43 @@ def _staged_bytes(sizes, nsrc, tile_elems):
 
 
 @pytest.mark.parametrize("dtype", ["bf16", "f32", "u8", "f64"])
-@pytest.mark.parametrize("on_device", [False, True])
-def test_batched_element_offsets(xr, orc, dtype, on_device):
+@pytest.mark.parametrize("mode", ["host", "device", "device_small"])
+def test_batched_element_offsets(xr, orc, dtype, mode):
     """Batch items whose buffers are element- but not 16-byte aligned: items
     whose pointers all sit at one offset within 16 bytes fold the elements
     before the next boundary one by one and take the vector path for the
     rest (every offset; lengths below, at and past that lead, several tiles;
-    up to 8 sources and the general tile's 9-17); items whose sources sit at
-    different offsets, or whose output does, take the scalar path.  Host
-    and device descriptors (past 64 items: the queue kernel); canaries
-    between the outputs stay untouched."""
-    rng = np.random.default_rng(19 + on_device)
+    up to 8 sources and the general tile's 9-17); items whose sources share
+    an offset and whose output sits at another read in vectors and store
+    realigned (every pair of offsets, lengths from just past the lead to
+    several tiles); items whose sources sit at different offsets take the
+    scalar path.  Host descriptors (the tile-table kernel), device
+    descriptors past 64 items (the queue kernel; under graph capture runs
+    dealt tile by tile) and a device batch of at most 64 items (one run:
+    the round-robin kernel); canaries between the outputs stay untouched."""
+    on_device = mode != "host"
+    rng = np.random.default_rng(19 + on_device + (mode == "device_small"))
     es = {"bf16": 2, "f32": 4, "u8": 1, "f64": 8}[dtype]
     items_np, specs = [], []
     for m in range(es, 16, es):
         lead = (16 - m) // es
         for n in (1, lead - 1, lead, lead + 1, lead + 16 // es + 3, 9000, 40001):
             if n >= 1:
-                specs.append(("common", m, n))
-    specs += [("sources differ", es, 9000), ("output differs", es, 40001),
-              ("sources differ", 16 - es, 3), ("output differs", es, 17)]
-    if on_device:   # past 64 items: the queue kernel, not the one-run kernel
+                specs.append(("common", m, n, m))
+    specs += [("sources differ", es, 9000, es), ("sources differ", 16 - es, 3, 16 - es)]
+    split = []
+    for m in range(0, 16, es):
+        lead = (16 - m) % 16 // es
+        for j, do in enumerate(d for d in range(0, 16, es) if d != m):
+            split.append(("output differs", m, (lead + 1, lead + 16 // es + 3, 9000, 40001)[j % 4], do))
+    if mode == "device_small":
+        specs = split[::max(1, len(split) // 60)][:60]
+    else:
+        specs += split
+    if mode == "device":   # past 64 items: the queue kernel, not the one-run kernel
         specs = (specs * (70 // len(specs) + 1))[:max(70, len(specs))]
     keep, items, rows, outs, G = [], [], [], [], 64
-    for k, (kind, m, n) in enumerate(specs):
+    for k, (kind, m, n, do) in enumerate(specs):
         P = (1, 3, 8, 9, 17)[k % 5]
         srcs = [pins.random_column_values(rng, dtype, n) for _ in range(P)]
         items_np.append(srcs)
@@ -730,7 +743,6 @@ def test_batched_element_offsets(xr, orc, dtype, on_device):
             v.copy_(gu.to_dev(a, dtype))
             keep.append(big)
             views.append(v)
-        do = m if kind != "output differs" else (m + es) % 16
         store = torch.full((G + do + n * es + G,), 0x5A, dtype=torch.uint8, device="cuda")
         out = store[G + do:G + do + n * es].view(gu.torch_dtype(dtype))
         outs.append((store, out, do, n, kind, m, P))
@@ -753,13 +765,13 @@ def test_batched_element_offsets(xr, orc, dtype, on_device):
 
     def check(how):
         for exp, (store, out, do, n, kind, m, P) in zip(exps, outs):
-            what = f"{kind} {dtype} P={P} offset={m} n={n} {how}"
+            what = f"{kind} {dtype} P={P} offset={m} output offset={do} n={n} {how}"
             gu.assert_parity(out, exp, dtype, "sum", what)
             raw = store.cpu().numpy()
             assert np.all(raw[:G + do] == 0x5A), what
             assert np.all(raw[G + do + n * es:] == 0x5A), what
 
-    check("device descriptors" if on_device else "host descriptors")
+    check(f"{mode} descriptors")
     if on_device:
         # under graph capture the batch runs as runs of items dealt tile by
         # tile (not the queue kernel); replayed twice over zeroed outputs
