@@ -502,6 +502,26 @@ def secondary(torch, xr, L, timer, wl, flush, res):
         del d, out
     res["latency_p8_bf16"] = lat
 
+    # reduce-scatter over the same share (P=8 bf16, 8 ranks, shards of 2^23
+    # and 2^23 + 1 elements): with the odd length rank 1's shard starts 2
+    # bytes past a 16-byte boundary in every send buffer while its output is
+    # aligned (the realigned stores); rank 0's is aligned either way
+    rs = {}
+    stream = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    for rc in (1 << 23, (1 << 23) + 1):
+        sends = [torch.empty(8 * rc, dtype=torch.bfloat16, device="cuda").uniform_(-1, 1)
+                 for _ in range(8)]
+        out = torch.empty(rc, dtype=torch.bfloat16, device="cuda")
+        arr = xr._lib.ptr_array([t.data_ptr() for t in sends])
+        for rank in (0, 1):
+            ms = timer.loop_ms(lambda: L.xred_reduce_scatter_local(
+                arr, 8, rank, ctypes.c_void_p(out.data_ptr()), rc, 1, 0, stream), 200)
+            rs[f"recvcount_{rc}_rank{rank}"] = {"us_per_call": round(ms * 1e3, 2),
+                                                "GBs": round(9 * rc * 2 / ms / 1e6, 1)}
+        del sends, out, arr
+        torch.cuda.empty_cache()
+    res["reduce_scatter_p8_bf16_share"] = rs
+
     # messages larger than the bucket: 8 bf16 sources of 256 and 512 MiB (the
     # launches whose occupancy cap grows with the bytes per source)
     big = {}
