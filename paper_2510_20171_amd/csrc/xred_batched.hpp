@@ -189,7 +189,7 @@ __device__ void batched_tile(const xred_item &it, uint64_t lt)
             if (off >= vbytes) break;
             const Tile tl{lb + off, tile_nrec(vbytes, off, kSubBytes)};
             if (c != 0) {
-                split_tile<T, Op, kB>(src, nsrc, dst, tl, c);
+                split_tile<T, Op, 1, kB>(src, nsrc, dst, tl, c);
                 continue;
             }
             switch (nsrc) {
@@ -701,7 +701,7 @@ __device__ __forceinline__ void table_tile(const ItemHead &h, uint64_t lt)
             const size_t nvec = (count - lead) / T::kVec, vbytes = nvec * 16;
             const Tile tl{(size_t)lead * T::kSize + toff, tile_nrec(vbytes, toff, kBytes)};
             if (toff < vbytes) {
-                if (c != 0) split_tile<T, Op, kTB>(src, nsrc, dst, tl, c);
+                if (c != 0) split_tile<T, Op, 1, kTB>(src, nsrc, dst, tl, c);
                 else reduce_tile<T, Op, 0, U, kTB>(src, nsrc, dst, tl);
             }
         } else {

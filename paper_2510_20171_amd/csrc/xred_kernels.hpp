@@ -206,34 +206,34 @@ __device__ __forceinline__ void reduce_elem(const Src &src, int nsrc, char *dst,
 
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
-// Any number of sources at one 16-byte-aligned tile, U = 1: the first group
-// takes up to 8 sources, then groups of 8 and a remainder, all loads of a
-// group in flight; fold order 0..nsrc-1.
-template <class T, class Op, int B, class Src>
-__device__ __forceinline__ void fold_any(typename T::Acc (&acc)[1][T::kVec], const Src &src,
+// Any number of sources at one 16-byte-aligned tile: the first group takes
+// up to 8 sources, then groups of 8 and a remainder, all loads of a group in
+// flight; fold order 0..nsrc-1.
+template <class T, class Op, int U, int B, class Src>
+__device__ __forceinline__ void fold_any(typename T::Acc (&acc)[U][T::kVec], const Src &src,
                                          int nsrc, Tile tl)
 {
     const int g0 = nsrc < 8 ? nsrc : 8;
     switch (g0) {
-    case 1: fold_group<T, Op, 1, 1, B, true>(acc, src, 0, tl); break;
-    case 2: fold_group<T, Op, 2, 1, B, true>(acc, src, 0, tl); break;
-    case 3: fold_group<T, Op, 3, 1, B, true>(acc, src, 0, tl); break;
-    case 4: fold_group<T, Op, 4, 1, B, true>(acc, src, 0, tl); break;
-    case 5: fold_group<T, Op, 5, 1, B, true>(acc, src, 0, tl); break;
-    case 6: fold_group<T, Op, 6, 1, B, true>(acc, src, 0, tl); break;
-    case 7: fold_group<T, Op, 7, 1, B, true>(acc, src, 0, tl); break;
-    default: fold_group<T, Op, 8, 1, B, true>(acc, src, 0, tl); break;
+    case 1: fold_group<T, Op, 1, U, B, true>(acc, src, 0, tl); break;
+    case 2: fold_group<T, Op, 2, U, B, true>(acc, src, 0, tl); break;
+    case 3: fold_group<T, Op, 3, U, B, true>(acc, src, 0, tl); break;
+    case 4: fold_group<T, Op, 4, U, B, true>(acc, src, 0, tl); break;
+    case 5: fold_group<T, Op, 5, U, B, true>(acc, src, 0, tl); break;
+    case 6: fold_group<T, Op, 6, U, B, true>(acc, src, 0, tl); break;
+    case 7: fold_group<T, Op, 7, U, B, true>(acc, src, 0, tl); break;
+    default: fold_group<T, Op, 8, U, B, true>(acc, src, 0, tl); break;
     }
     int p = g0;
-    for (; p + 8 <= nsrc; p += 8) fold_group<T, Op, 8, 1, B, false>(acc, src, p, tl);
+    for (; p + 8 <= nsrc; p += 8) fold_group<T, Op, 8, U, B, false>(acc, src, p, tl);
     switch (nsrc - p) {
-    case 1: fold_group<T, Op, 1, 1, B, false>(acc, src, p, tl); break;
-    case 2: fold_group<T, Op, 2, 1, B, false>(acc, src, p, tl); break;
-    case 3: fold_group<T, Op, 3, 1, B, false>(acc, src, p, tl); break;
-    case 4: fold_group<T, Op, 4, 1, B, false>(acc, src, p, tl); break;
-    case 5: fold_group<T, Op, 5, 1, B, false>(acc, src, p, tl); break;
-    case 6: fold_group<T, Op, 6, 1, B, false>(acc, src, p, tl); break;
-    case 7: fold_group<T, Op, 7, 1, B, false>(acc, src, p, tl); break;
+    case 1: fold_group<T, Op, 1, U, B, false>(acc, src, p, tl); break;
+    case 2: fold_group<T, Op, 2, U, B, false>(acc, src, p, tl); break;
+    case 3: fold_group<T, Op, 3, U, B, false>(acc, src, p, tl); break;
+    case 4: fold_group<T, Op, 4, U, B, false>(acc, src, p, tl); break;
+    case 5: fold_group<T, Op, 5, U, B, false>(acc, src, p, tl); break;
+    case 6: fold_group<T, Op, 6, U, B, false>(acc, src, p, tl); break;
+    case 7: fold_group<T, Op, 7, U, B, false>(acc, src, p, tl); break;
     default: break;
     }
 }
@@ -261,37 +261,26 @@ __device__ __forceinline__ u32x4 bytes_from(u32x4 lo, u32x4 hi, uint32_t s)
     return o;
 }
 
-// A tile whose sources sit on 16-byte boundaries (tl.off past each source
-// pointer) and whose output dst + tl.off sits c bytes past one (0 < c < 16, a
-// multiple of the element size).  Lane q folds vector q as reduce_tile does
-// with U = 1.  Output bytes [16q - c, 16q + 16 - c) of the tile are lane
-// q-1's last c result bytes and lane q's first 16 - c, so every lane but the
-// first of its wavefront takes its neighbour's result (a lane shuffle) and
-// stores one aligned 16-byte vector.  The two chunks cut by a wavefront's
-// ends (16 - c bytes at its first lane, c at its last lane with a vector)
-// go out in aligned pieces of the largest power of two dividing c, 16 bytes
-// in all, from up to 16 lanes in one store instruction.  Every lane of the
-// workgroup must be active.
-template <class T, class Op, int B, class Src>
-__device__ __forceinline__ void split_tile(const Src &src, int nsrc, char *dst, Tile tl,
-                                           uint32_t c)
+// The 16-byte results of B lanes, lane q's for output bytes [16q, 16q + 16)
+// of `base`, where base sits c bytes past a 16-byte boundary (0 < c < 16, a
+// multiple of the element size) and `nrec` of the B*16 bytes exist.  Output
+// bytes [16q - c, 16q + 16 - c) are lane q-1's last c result bytes and lane
+// q's first 16 - c, so every lane but the first of its wavefront takes its
+// neighbour's result (a lane shuffle) and stores one aligned 16-byte vector.
+// The two chunks cut by a wavefront's ends (16 - c bytes at its first lane,
+// c at its last lane with a vector) go out in aligned pieces of the largest
+// power of two dividing c, 16 bytes in all, from up to 16 lanes in one store
+// instruction.  Every lane of the workgroup must be active.
+__device__ __forceinline__ void split_store(u32x4 mine, char *base, uint32_t nrec, uint32_t c)
 {
-    typename T::Acc acc[1][T::kVec];
-    fold_any<T, Op, B>(acc, src, nsrc, tl);
-    if constexpr (__is_same(Op, OpAvg)) {
-#pragma unroll
-        for (int j = 0; j < T::kVec; ++j) acc[0][j] = avg_scale<T, Op>(acc[0][j], nsrc);
-    }
-    const u32x4 mine = down_vec<T, Op>(acc[0]);
     const uint32_t q = threadIdx.x, l = q & 63u;
     u32x4 prev;
 #pragma unroll
     for (int i = 0; i < 4; ++i) prev[i] = __shfl_up(mine[i], 1u, 64);
     if (l != 0)
-        bstore<kStoreOut>(bytes_from(prev, mine, 16u - c), make_rsrc(dst + tl.off - c, tl.nrec),
-                          16u * q);
+        bstore<kStoreOut>(bytes_from(prev, mine, 16u - c), make_rsrc(base - c, nrec), 16u * q);
     const uint32_t w0 = (uint32_t)__builtin_amdgcn_readfirstlane((int)(q >> 6)) * 64u;
-    const uint32_t nl = tl.nrec / 16u;   // lanes of the tile with a vector
+    const uint32_t nl = nrec / 16u;   // lanes with a vector
     if (w0 >= nl) return;
     const uint32_t last = nl - 1u - w0 < 63u ? nl - 1u - w0 : 63u;
     u32x4 r0, rl;
@@ -305,11 +294,11 @@ __device__ __forceinline__ void split_tile(const Src &src, int nsrc, char *dst, 
     if (l >= 16u / piece) return;
     const bool head = l < hp;
     const uint32_t o = head ? l * piece : 16u - c + (l - hp) * piece;   // byte of the vector
-    const uint32_t at = 16u * (w0 + (head ? 0u : last)) + o;             // byte of the tile
+    const uint32_t at = 16u * (w0 + (head ? 0u : last)) + o;             // byte of `base`
     const u32x4 v = head ? r0 : rl;
     const uint32_t d = o >> 2;
     const uint32_t x = d == 0 ? v[0] : d == 1 ? v[1] : d == 2 ? v[2] : v[3];
-    const rsrc_t w = make_rsrc(dst + tl.off, tl.nrec);
+    const rsrc_t w = make_rsrc(base, nrec);
     switch (piece) {
     case 8: {
         const u32x2 x2 = {x, d == 0 ? v[1] : v[3]};
@@ -325,6 +314,30 @@ __device__ __forceinline__ void split_tile(const Src &src, int nsrc, char *dst, 
         __builtin_amdgcn_raw_buffer_store_b8((unsigned char)(x >> (8u * (o & 3u))), w, at, 0,
                                              kStoreOut);
         break;
+    }
+}
+
+// A tile whose sources sit on 16-byte boundaries (tl.off past each source
+// pointer) and whose output dst + tl.off sits c bytes past one: U vectors
+// per thread folded as reduce_tile does, then each block of B vectors
+// stored realigned (split_store).
+template <class T, class Op, int U, int B, class Src>
+__device__ __forceinline__ void split_tile(const Src &src, int nsrc, char *dst, Tile tl,
+                                           uint32_t c)
+{
+    typename T::Acc acc[U][T::kVec];
+    fold_any<T, Op, U, B>(acc, src, nsrc, tl);
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+        if constexpr (__is_same(Op, OpAvg)) {
+#pragma unroll
+            for (int j = 0; j < T::kVec; ++j) acc[u][j] = avg_scale<T, Op>(acc[u][j], nsrc);
+        }
+        const uint32_t start = (uint32_t)u * B * 16u;
+        if (start >= tl.nrec) break;
+        const uint32_t left = tl.nrec - start;
+        split_store(down_vec<T, Op>(acc[u]), dst + tl.off + start,
+                    left < (uint32_t)B * 16u ? left : (uint32_t)B * 16u, c);
     }
 }
 

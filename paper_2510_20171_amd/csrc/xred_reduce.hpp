@@ -112,15 +112,18 @@ size_t lds_for_waves(int waves)
 // realigned to dst's 16-byte grid and stored in aligned vectors (split_tile).
 // P=8 bf16, 16 MiB per source: 51 us element by element, 32 us storing every
 // result in 2-byte pieces, 24 us realigned (23.3 us with every buffer
-// aligned).  One 128-thread shape, any source count.
+// aligned).  Any source count; the vector path's three shapes: launches
+// that fit on the chip in one round take 512-thread workgroups of one vector
+// per thread, or (up to 8 sources) two, the others 128-thread workgroups
+// under the vector path's occupancy cap.
 // reduce_vec_kernel's tiles (U = 1) through split_tile; tail and lead as
 // there.
-template <class T, class Op, int B>
+template <class T, class Op, int U, int B>
 __global__ __launch_bounds__(B) void reduce_split_kernel(KernargSrc<XRED_MAX_SRC> src, int nsrc,
                                                          char *dst, size_t nvec, uint32_t tail,
                                                          uint32_t head, uint32_t lead, uint32_t c)
 {
-    constexpr uint32_t kTileBytes = (uint32_t)B * 16u;
+    constexpr uint32_t kTileBytes = (uint32_t)B * U * 16u;
     const size_t vbytes = nvec * 16;
     const size_t lb = (size_t)lead * T::kSize;
     const uint32_t first = head != 0 ? 1u : 0u;
@@ -128,7 +131,7 @@ __global__ __launch_bounds__(B) void reduce_split_kernel(KernargSrc<XRED_MAX_SRC
     for (size_t t = blockIdx.x; t < ntiles; t += gridDim.x) {
         const bool h = t < first;
         const size_t off = h ? 0 : head + (t - first) * kTileBytes;
-        split_tile<T, Op, B>(src, nsrc, dst,
+        split_tile<T, Op, U, B>(src, nsrc, dst,
                              Tile{lb + off, h ? head : tile_nrec(vbytes, off, kTileBytes)}, c);
     }
     if ((tail | lead) != 0 && blockIdx.x == ntiles % gridDim.x) {
@@ -171,8 +174,20 @@ hipError_t go_split(const char *const *srcs, int nsrc, char *dst, size_t count, 
     const uint32_t head = (uint32_t)(mis == 0 ? 0 : std::min<size_t>(128 - mis, nvec * 16));
     const size_t hv = head / 16, first = head != 0 ? 1 : 0;
     const uint32_t c = (uint32_t)(((uintptr_t)dst + (size_t)lead * T::kSize) & 15u);
-    const uint64_t tiles = first + (nvec - hv + kB - 1) / kB + ((tail | lead) ? 1 : 0);
-    return launch_kernel(reduce_split_kernel<T, Op, kB>, dim3(grid_for(tiles)), dim3(kB),
+    const uint64_t extra = (tail | lead) ? 1 : 0;
+    const uint64_t one_round = (uint64_t)device_cus() * kWideWgsPerCu;
+    const uint64_t tiles_wide = first + (nvec - hv + kBWide - 1) / kBWide + extra;
+    if (tiles_wide <= one_round)
+        return launch_kernel(reduce_split_kernel<T, Op, 1, kBWide>, dim3(grid_for(tiles_wide)),
+                             dim3(kBWide), 0, s, ks, nsrc, dst, nvec, tail, head, lead, c);
+    constexpr size_t kTileWide2 = (size_t)kBWide * kUWide2;
+    const uint64_t tiles_wide2 = first + (nvec - hv + kTileWide2 - 1) / kTileWide2 + extra;
+    if (nsrc <= 8 && tiles_wide2 <= one_round)
+        return launch_kernel(reduce_split_kernel<T, Op, kUWide2, kBWide>,
+                             dim3(grid_for(tiles_wide2)), dim3(kBWide), 0, s, ks, nsrc, dst, nvec,
+                             tail, head, lead, c);
+    const uint64_t tiles = first + (nvec - hv + kB - 1) / kB + extra;
+    return launch_kernel(reduce_split_kernel<T, Op, 1, kB>, dim3(grid_for(tiles)), dim3(kB),
                          lds_for_waves(waves_split<T>(count * T::kSize, nsrc)), s, ks, nsrc, dst,
                          nvec, tail, head, lead, c);
 }

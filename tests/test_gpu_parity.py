@@ -317,9 +317,10 @@ def test_output_at_another_offset(xr, orc, dtype):
     length): the sources are read in vectors after the lead and each result
     vector is stored in aligned pieces of 1, 2, 4 or 8 bytes.  Every pair of
     element offsets; lengths just past the lead, past one vector, across a
-    few tiles with a ragged tail, and long; 1 to 17 sources (every first and
-    last group size of the runtime-count fold); sum, and max / avg / prod on
-    some.  Canaries around the output stay untouched."""
+    few tiles with a ragged tail, long, and past one round of wide
+    workgroups; 1 to 17 sources (every first and last group size of the
+    runtime-count fold); sum, and max / avg / prod on some.  Canaries around
+    the output stay untouched."""
     rng = np.random.default_rng(19)
     es = xr.ELEM_SIZE[dtype]
     G = 64
@@ -334,10 +335,15 @@ def test_output_at_another_offset(xr, orc, dtype):
                 cases.append((ms, md, n))
     big = [(ms, md, 600011) for ms, md in ((offs[1], 0), (0, offs[-1]), (offs[-1], offs[1]))
            if ms != md]
+    # past one round of 512-thread workgroups: two vectors per thread (P=2),
+    # and 128-thread workgroups (P=9)
+    wide = [(offs[1], 0, (9 << 20) // es + 5), (offs[-1], 0, (9 << 20) // es + 3)]
     ops = ["sum", "max", "avg" if dtype in gu.FLOATS else "min", "prod"]
-    for k, (ms, md, n) in enumerate(cases + big):
+    for k, (ms, md, n) in enumerate(cases + big + wide):
         P = (1, 3, 8, 9, 17, 5, 16, 2)[k % 8]
         op = ops[k % 4] if n < 600011 else "sum"
+        if k >= len(cases) + len(big):
+            P = (2, 9)[k - len(cases) - len(big)]
         srcs = [pins.random_column_values(rng, dtype, n) for _ in range(P)]
         keep, views = [], []
         for a in srcs:
