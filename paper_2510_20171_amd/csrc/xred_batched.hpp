@@ -268,8 +268,9 @@ struct TileDesc {
     uint64_t lt;              // tile within the item
     uint32_t k;               // item
     int nsrc;
-    uint32_t lead;            // elements before the first vector (item_lead; 0 unless fast)
-    bool fast;                // nsrc <= 8, no NULL source, every pointer at one offset in 16 B
+    uint32_t lead;            // elements before the first vector (0 unless fast)
+    uint32_t c;               // > 0: the output sits c bytes off the sources' vector grid
+    bool fast;                // nsrc <= 8, no NULL source, the sources at one offset in 16 B
 };
 
 template <class T>
@@ -283,17 +284,45 @@ __device__ __forceinline__ void fetch_desc(TileDesc &d, const xred_item *items, 
     d.dst = (char *)sload(&it->dst);
     d.count = sload(&it->count);
     d.nsrc = (int)sload(&it->nsrc);
-    uintptr_t diff = 0;
+    uintptr_t diff = 0, sdiff = 0;
     bool null_src = false;
 #pragma unroll
     for (int q = 0; q < 8; ++q) {
         d.p[q] = q < d.nsrc ? sload(d.srcs + q) : nullptr;
         diff |= q < d.nsrc ? (uintptr_t)d.p[q] ^ (uintptr_t)d.dst : 0;
+        sdiff |= q < d.nsrc ? (uintptr_t)d.p[q] ^ (uintptr_t)d.p[0] : 0;
         null_src |= q < d.nsrc && d.p[q] == nullptr;
     }
-    const uint64_t lead = item_lead<T>(diff, (uintptr_t)d.dst, d.count);
+    uint64_t lead = item_lead<T>(diff, (uintptr_t)d.dst, d.count);
+    d.c = 0;
+    if (lead == kNoVector) {
+        // the sources at one offset, the output at another: realigned stores
+        const uint64_t sl = sources_lead<T>(sdiff, (uintptr_t)d.p[0], d.count);
+        const uint32_t c =
+            sl != kNoVector ? (uint32_t)(((uintptr_t)d.dst + sl * T::kSize) & 15u) : 0u;
+        if (c != 0) {
+            lead = sl;
+            d.c = c;
+        }
+    }
     d.fast = d.nsrc <= 8 && !null_src && lead != kNoVector;
     d.lead = d.fast ? (uint32_t)lead : 0u;
+}
+
+// Sub-tile h of a straight-line tile whose vectors start at byte `off` of
+// d's output (nrec bytes of the tile exist): one aligned vector per thread,
+// or realigned stores when the output sits d.c bytes off the sources' grid.
+__device__ __forceinline__ void tile_store(u32x4 v, rsrc_t w, const TileDesc &d, size_t off,
+                                           uint32_t nrec, int h)
+{
+    if (d.c == 0) {
+        bstore<kStoreOut>(v, w, (uint32_t)(h * kB + threadIdx.x) * 16u);
+        return;
+    }
+    const uint32_t start = (uint32_t)h * kSubBytes;
+    if (start >= nrec) return;
+    const uint32_t left = nrec - start;
+    split_store(v, d.dst + off + start, left < kSubBytes ? left : kSubBytes, d.c);
 }
 
 template <class T, class Op, bool PLANNED>
@@ -381,7 +410,7 @@ __global__ __launch_bounds__(kB) void batched_rr_kernel(const xred_item *items, 
 #pragma unroll
                     for (int e = 0; e < T::kVec; ++e) acc[e] = avg_scale<T, Op>(acc[e], cur.nsrc);
                 }
-                bstore<kStoreOut>(down_vec<T, Op>(acc), w, (uint32_t)(h * kB + threadIdx.x) * 16u);
+                tile_store(down_vec<T, Op>(acc), w, cur, lb + toff, nrec, h);
             }
             if (cur.fast) {
                 if (cur.lt == 0 && threadIdx.x < cur.lead)
@@ -584,7 +613,7 @@ __global__ __launch_bounds__(kB) void batched_queue_kernel(const xred_item *item
 #pragma unroll
                 for (int e = 0; e < T::kVec; ++e) acc[e] = avg_scale<T, Op>(acc[e], cur.nsrc);
             }
-            bstore<kStoreOut>(down_vec<T, Op>(acc), w, (uint32_t)(h * kB + threadIdx.x) * 16u);
+            tile_store(down_vec<T, Op>(acc), w, cur, lb + toff, nrec, h);
         }
         if (cur.fast) {
             if (cur.lt == 0 && threadIdx.x < cur.lead)
