@@ -285,7 +285,11 @@ XRED_API xred_status xred_batched_reduce_noalloc(const xred_item *items, int nit
  * chunks, with the accumulator kept on chip (LDS) between steps, so only
  * the chunks are read and only dst is written.
  *   chunks     host array of nchunks (1..XRED_MAX_SRC) device pointers to count
- *              elements each; all buffers 16-byte aligned (else XRED_UNSUPPORTED)
+ *              elements each, all at one offset within 16 bytes (else
+ *              XRED_UNSUPPORTED); the elements before their next 16-byte
+ *              boundary are folded one by one with the tail.  dst may sit at
+ *              any element offset (at another one than the chunks, results
+ *              are realigned across lanes before the 16-byte stores).
  *   count      at most xred_ring_max_count(dtype) (else XRED_UNSUPPORTED)
  *   ready      NULL: every chunk is ready at launch.  Otherwise nchunks
  *              uint32 words the GPU can read coherently (hipHostMalloc'd or
@@ -304,8 +308,8 @@ XRED_API xred_status xred_batched_reduce_noalloc(const xred_item *items, int nit
  *              to *status (if status is not NULL) and stops; dst is then
  *              unspecified.  The caller zeroes *status before the call if it
  *              wants to check it.
- * Errors: as xred_allreduce_local; XRED_UNSUPPORTED for misaligned buffers or
- * counts beyond the capacity.
+ * Errors: as xred_allreduce_local; XRED_UNSUPPORTED for chunks at different
+ * offsets within 16 bytes or counts beyond the capacity.
  */
 XRED_API xred_status xred_ring_reduce(const void *const *chunks, int nchunks, void *dst,
                                       size_t count, xred_dtype dtype, xred_op op,

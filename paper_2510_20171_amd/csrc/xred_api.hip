@@ -888,15 +888,16 @@ XRED_API xred_status xred_ring_reduce(const void *const *chunks, int nchunks, vo
     if (mul_overflows(count, es)) return fail(XRED_INVALID_ARGUMENT, "count * size overflows");
     const size_t bytes = count * es;
     if ((st = check_buf(dst, bytes, es, "dst", 0)) != XRED_SUCCESS) return st;
-    uintptr_t bits = (uintptr_t)dst;
+    uintptr_t diff = 0;   // bits in which some chunk's address differs from the first's
     for (int p = 0; p < nchunks; ++p) {
         if ((st = check_buf(chunks[p], bytes, es, "chunks", p)) != XRED_SUCCESS) return st;
         if (bad_overlap(dst, bytes, chunks[p], bytes, true))
             return fail(XRED_ALIAS, "dst partially overlaps chunks[%d]", p);
-        bits |= (uintptr_t)chunks[p];
+        diff |= (uintptr_t)chunks[p] ^ (uintptr_t)chunks[0];
     }
-    if (bits & 15u)
-        return fail(XRED_UNSUPPORTED, "xred_ring_reduce needs 16-byte aligned buffers");
+    if (diff & 15u)
+        return fail(XRED_UNSUPPORTED,
+                    "xred_ring_reduce needs every chunk at one offset within 16 bytes");
     if (ready != nullptr && ((uintptr_t)ready & 3u))
         return fail(XRED_INVALID_ARGUMENT, "ready is not 4-byte aligned");
     if (status != nullptr && ((uintptr_t)status & 3u))

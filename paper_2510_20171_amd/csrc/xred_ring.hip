@@ -173,11 +173,12 @@ __device__ int poll_own(const uint32_t *ready, uint32_t epoch, int next, int nch
 
 // Chunks [next, upto) of tile j (byte offset off, nrec bytes exist), in groups
 // of kGroup loaded before folding; the accumulator comes from the first chunk
-// or LDS and goes to dst (last round) or LDS.
-template <class T, class Op, int POL>
+// or LDS and goes to dst (last round) or LDS.  SPLIT: dst + off sits c bytes
+// past a 16-byte boundary (0 < c < 16) and the results are stored realigned.
+template <class T, class Op, int POL, bool SPLIT>
 __device__ __forceinline__ void fold_round(const KernargSrc<XRED_MAX_SRC> &chunks, int nchunks,
                                            char *dst, u32x4 *s_acc, int j, size_t off,
-                                           uint32_t nrec, int next, int upto)
+                                           uint32_t nrec, int next, int upto, uint32_t c)
 {
     constexpr int H = acc_vecs<T>();
     constexpr int PV = acc_per_vec<T>();
@@ -209,17 +210,26 @@ __device__ __forceinline__ void fold_round(const KernargSrc<XRED_MAX_SRC> &chunk
         }
     }
     if (upto == nchunks) {
-        bstore<kStoreOut>(down_vec<T, Op>(a), make_rsrc(dst + off, nrec),
-                          (uint32_t)threadIdx.x * 16u);
+        if constexpr (SPLIT)
+            split_store(down_vec<T, Op>(a), dst + off, nrec, c);
+        else
+            bstore<kStoreOut>(down_vec<T, Op>(a), make_rsrc(dst + off, nrec),
+                              (uint32_t)threadIdx.x * 16u);
     } else {
 #pragma unroll
         for (int h = 0; h < H; ++h) *acc_slot<T>(s_acc, j, h) = pack_acc<T>(&a[PV * h]);
     }
 }
 
-template <class T, class Op>
+// Chunks at one offset within 16 bytes: the first `lead` elements (fewer
+// than a vector) bring them to a 16-byte boundary and are folded one by one
+// with the `tail` after the last full vector; SPLIT: dst sits c bytes off
+// that grid (a separate instantiation, so the aligned kernel carries none of
+// the realignment).
+template <class T, class Op, bool SPLIT>
 __global__ __launch_bounds__(kB) void ring_kernel(KernargSrc<XRED_MAX_SRC> chunks, int nchunks,
                                                   char *dst, size_t nvec, uint32_t tail,
+                                                  uint32_t lead, uint32_t c,
                                                   int tiles_per_wg, const uint32_t *ready,
                                                   uint32_t epoch, uint64_t timeout,
                                                   uint32_t *status, Relay relay)
@@ -237,6 +247,7 @@ __global__ __launch_bounds__(kB) void ring_kernel(KernargSrc<XRED_MAX_SRC> chunk
     const size_t wg = blockIdx.x - (relayed ? 1u : 0u);
     const size_t nwg = gridDim.x - (relayed ? 1u : 0u);
     const size_t vbytes = nvec * 16;
+    const size_t lb = (size_t)lead * T::kSize;
     const size_t ntiles = (nvec + kB - 1) / kB;
     int next = 0;
     while (next < nchunks) {
@@ -256,29 +267,33 @@ __global__ __launch_bounds__(kB) void ring_kernel(KernargSrc<XRED_MAX_SRC> chunk
         for (int j = 0; j < tiles_per_wg; ++j) {
             const size_t t = wg + (size_t)j * nwg;
             if (t >= ntiles) break;
-            const size_t off = t * kTileBytes;
-            const uint32_t nrec = tile_nrec(vbytes, off, kTileBytes);
+            const size_t toff = t * kTileBytes;
+            const uint32_t nrec = tile_nrec(vbytes, toff, kTileBytes);
             if (flagged)
-                fold_round<T, Op, kLoadCoherent>(chunks, nchunks, dst, s_acc, j, off, nrec, next,
-                                                 upto);
+                fold_round<T, Op, kLoadCoherent, SPLIT>(chunks, nchunks, dst, s_acc, j,
+                                                        lb + toff, nrec, next, upto, c);
             else
-                fold_round<T, Op, kLoadStream>(chunks, nchunks, dst, s_acc, j, off, nrec, next,
-                                               upto);
+                fold_round<T, Op, kLoadStream, SPLIT>(chunks, nchunks, dst, s_acc, j, lb + toff,
+                                                      nrec, next, upto, c);
         }
         next = upto;
         __syncthreads();   // s_upto is rewritten by the next round
     }
-    // Elements after the last full vector: one workgroup, once every chunk was
-    // seen ready (its plain loads need the acquire the vector loads avoid).
-    if (next == nchunks && tail != 0 && wg == ntiles % nwg && threadIdx.x < tail) {
+    // Elements before the first and after the last full vector: one
+    // workgroup, once every chunk was seen ready (its plain loads need the
+    // acquire the vector loads avoid).
+    if (next == nchunks && (tail | lead) != 0 && wg == ntiles % nwg &&
+        (threadIdx.x < tail || threadIdx.x < lead)) {
         if (flagged) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "");
-        reduce_elem<T, Op>(chunks, nchunks, dst, nvec * T::kVec + threadIdx.x);
+        if (threadIdx.x < tail)
+            reduce_elem<T, Op>(chunks, nchunks, dst, lead + nvec * T::kVec + threadIdx.x);
+        if (threadIdx.x < lead) reduce_elem<T, Op>(chunks, nchunks, dst, threadIdx.x);
     }
 }
 
-// Resident workgroups per CU of ring_kernel<T, Op> with the LDS of
-// kMaxTilesPerWg tiles (cached per device: the host path stays free of
-// runtime queries after the first launch).
+// Resident workgroups per CU of both ring_kernel<T, Op, *> variants with
+// the LDS of kMaxTilesPerWg tiles (cached per device: the host path stays
+// free of runtime queries after the first launch).
 template <class T, class Op>
 int ring_per_cu()
 {
@@ -287,11 +302,14 @@ int ring_per_cu()
     if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) dev = 0;
     int v = __atomic_load_n(&cache[dev], __ATOMIC_RELAXED);
     if (v <= 0) {
-        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&v, (const void *)ring_kernel<T, Op>, kB,
-                                                         lds_tile_bytes<T>() * kMaxTilesPerWg) !=
-                hipSuccess ||
-            v <= 0)
+        const size_t lds = lds_tile_bytes<T>() * kMaxTilesPerWg;
+        int w = 0;
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(
+                &v, (const void *)ring_kernel<T, Op, false>, kB, lds) != hipSuccess ||
+            hipOccupancyMaxActiveBlocksPerMultiprocessor(
+                &w, (const void *)ring_kernel<T, Op, true>, kB, lds) != hipSuccess)
             v = 1;
+        v = std::max(1, std::min(v, w));
         __atomic_store_n(&cache[dev], v, __ATOMIC_RELAXED);
     }
     return v;
@@ -315,8 +333,12 @@ hipError_t go(const char *const *chunks, int nchunks, char *dst, size_t count,
 {
     KernargSrc<XRED_MAX_SRC> ks;
     for (int p = 0; p < XRED_MAX_SRC; ++p) ks.p[p] = p < nchunks ? chunks[p] : nullptr;
-    const size_t nvec = count / T::kVec;
-    const uint32_t tail = (uint32_t)(count % T::kVec);
+    // the chunks share one offset m within 16 bytes (checked by the caller)
+    const uintptr_t m = (uintptr_t)chunks[0] & 15u;
+    const uint32_t lead = (uint32_t)std::min<size_t>(m == 0 ? 0 : (16 - m) / T::kSize, count);
+    const size_t nvec = (count - lead) / T::kVec;
+    const uint32_t tail = (uint32_t)((count - lead) % T::kVec);
+    const uint32_t c = (uint32_t)(((uintptr_t)dst + (size_t)lead * T::kSize) & 15u);
     const size_t ntiles = (nvec + kB - 1) / kB;
     // The relay word of the stream (tickets follow the order of the launches:
     // the slot stays locked until the launch is committed).
@@ -340,10 +362,13 @@ hipError_t go(const char *const *chunks, int nchunks, char *dst, size_t count,
     // of a fresh slot
     const Relay relay = relayed ? Relay{slot.words, (uint32_t)(slot.launches % 0xFFFFFFu) + 1}
                                 : Relay{nullptr, 0};
+    const dim3 g((unsigned)(grid + (relayed ? 1 : 0)));
+    const size_t lds = lds_tile_bytes<T>() * (tpw > 0 ? tpw : 1);
     const hipError_t e =
-        launch_kernel(ring_kernel<T, Op>, dim3((unsigned)(grid + (relayed ? 1 : 0))), dim3(kB),
-                      lds_tile_bytes<T>() * (tpw > 0 ? tpw : 1), s, ks, nchunks, dst, nvec, tail,
-                      tpw, ready, epoch, timeout, status, relay);
+        c == 0 ? launch_kernel(ring_kernel<T, Op, false>, g, dim3(kB), lds, s, ks, nchunks, dst,
+                               nvec, tail, lead, c, tpw, ready, epoch, timeout, status, relay)
+               : launch_kernel(ring_kernel<T, Op, true>, g, dim3(kB), lds, s, ks, nchunks, dst,
+                               nvec, tail, lead, c, tpw, ready, epoch, timeout, status, relay);
     if (relayed && e == hipSuccess) slot.commit();
     return e;
 }

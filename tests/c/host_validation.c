@@ -134,8 +134,10 @@ int main(void)
     const void **c16 = ptrs(16, 200);
     EXPECT(xred_ring_reduce(c16, 0, fake(0), 1024, XRED_BFLOAT16, XRED_SUM, NULL, 0, 0, NULL, NULL),
            XRED_INVALID_ARGUMENT);
-    EXPECT(xred_ring_reduce(c16, 16, (char *)fake(0) + 2, 1024, XRED_BFLOAT16, XRED_SUM, NULL, 0, 0,
-                            NULL, NULL), XRED_UNSUPPORTED);
+    const void **c16b = ptrs(16, 200);
+    c16b[5] = (const char *)c16b[5] + 2;   /* one chunk at another offset within 16 bytes */
+    EXPECT(xred_ring_reduce(c16b, 16, fake(0), 1024, XRED_BFLOAT16, XRED_SUM, NULL, 0, 0, NULL,
+                            NULL), XRED_UNSUPPORTED);
     EXPECT(xred_ring_reduce(c16, 16, fake(0), 1024, XRED_BFLOAT16, XRED_SUM,
                             (const uint32_t *)((char *)fake(7) + 2), 0, 0, NULL, NULL),
            XRED_INVALID_ARGUMENT);

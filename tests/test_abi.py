@@ -139,7 +139,8 @@ def ptrs(*xs):
     (lambda L: L.xred_batched_reduce(None, 1, 1, 0, 4, None), 1),
     (lambda L: L.xred_ring_reduce(ptrs(A), 0, S(A + 4096), 16, 1, 0, None, 1, 0, None, None), 1),
     (lambda L: L.xred_ring_reduce(ptrs(A), 65, S(A + 4096), 16, 1, 0, None, 1, 0, None, None), 1),
-    (lambda L: L.xred_ring_reduce(ptrs(A + 2), 1, S(A + 4096), 16, 1, 0, None, 1, 0, None, None), 2),
+    (lambda L: L.xred_ring_reduce(ptrs(A + 2, A + 4096), 2, S(A + 8192), 16, 1, 0, None, 1, 0, None,
+                                  None), 2),
     (lambda L: L.xred_ring_reduce(ptrs(A), 1, S(A + 8), 16, 1, 0, None, 1, 0, None, None), 3),
     (lambda L: L.xred_ring_reduce(ptrs(A), 1, S(A + 4096), 16, 1, 0, S(A + 1), 1, 0, None, None), 1),
     (lambda L: L.xred_ring_reduce(ptrs(A), 1, S(A + 4096), 16, 1, 4, None, 1, 0, None, None), 2),

@@ -97,6 +97,67 @@ def test_ring_parity_no_flags(xr, orc, dtype, op):
                              f"ring {dtype} {op} chunks={nchunks} n={n}")
 
 
+@pytest.mark.parametrize("dtype", ["bf16", "f32", "u8"])
+def test_ring_element_offsets(xr, orc, dtype):
+    """Chunks that are element- but not 16-byte aligned, all at one offset m
+    within 16 bytes: the elements before the next boundary are folded one by
+    one with the tail, the rest in vectors; dst at the same offset, aligned,
+    or at a third one (realigned stores).  Every offset; lengths within the
+    lead, just past it, across several tiles with a ragged tail; without
+    flags and with every flag set before the launch.  Canaries around dst
+    stay untouched; chunks at different offsets are refused."""
+    rng = np.random.default_rng(41)
+    es = {"bf16": 2, "f32": 4, "u8": 1}[dtype]
+    G = 64
+    L = xr.load()
+    cases = []
+    for m in range(0, 16, es):
+        lead = (16 - m) % 16 // es
+        for k, do in enumerate(sorted({m, 0, (m + 3 * es) % 16})):
+            n = (max(lead, 1), lead + 1, 3 * 512 * 16 // es + 5)[k % 3]
+            cases.append((m, do, n))
+    cases.append((es, 0, 70001))
+    for k, (m, do, n) in enumerate(cases):
+        P = (1, 3, 8, 16)[k % 4]
+        flagged = k % 2 == 1
+        chunks = [pins.random_column_values(rng, dtype, n) for _ in range(P)]
+        keep, arr = [], []
+        for a in chunks:
+            b = torch.zeros(m + n * es + 16, dtype=torch.uint8, device="cuda")
+            v = b[m:m + n * es].view(gu.torch_dtype(dtype))
+            v.copy_(gu.to_dev(a, dtype))
+            keep.append(b)
+            arr.append(v.data_ptr())
+        store = torch.full((G + do + n * es + G,), 0x5A, dtype=torch.uint8, device="cuda")
+        out = store[G + do:G + do + n * es]
+        flags = PinnedWords(P) if flagged else None
+        if flagged:
+            for i in range(P):
+                flags.set(i, 1)
+        torch.cuda.synchronize()
+        xr._lib.check(L.xred_ring_reduce(
+            xr._lib.ptr_array(arr), P, ctypes.c_void_p(out.data_ptr()), n, xr.DTYPE[dtype],
+            xr.OP["sum"], flags.dev if flagged else None, 1, 2_000_000, None,
+            ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)))
+        torch.cuda.synchronize()
+        if flagged:
+            flags.free()
+        what = f"ring {dtype} P={P} chunks at {m} dst at {do} n={n} flags={flagged}"
+        gu.assert_parity(out.view(gu.torch_dtype(dtype)), orc.allreduce_local(chunks, dtype, "sum"),
+                         dtype, "sum", what)
+        raw = store.cpu().numpy()
+        assert np.all(raw[:G + do] == 0x5A), what
+        assert np.all(raw[G + do + n * es:] == 0x5A), what
+    # one chunk at another offset: refused, nothing launched
+    a = torch.zeros(4096, dtype=torch.uint8, device="cuda")
+    out = torch.zeros(1024, dtype=torch.uint8, device="cuda")
+    st = L.xred_ring_reduce(xr._lib.ptr_array([a.data_ptr(), a.data_ptr() + 2048 + es]), 2,
+                            ctypes.c_void_p(out.data_ptr()), 64 // es, xr.DTYPE[dtype],
+                            xr.OP["sum"], None, 1, 0, None,
+                            ctypes.c_void_p(torch.cuda.current_stream().cuda_stream))
+    assert st == xr.UNSUPPORTED, st
+
+
 def test_ring_c3_full_and_multi_tile(xr, orc):
     """The step-wise workload (16 x 2^20 bf16) in one launch, and a chunk large
     enough that each workgroup holds several accumulator tiles."""
