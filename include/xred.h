@@ -68,7 +68,10 @@
  *     share an offset and dst sits at another (a reduce-scatter shard of odd
  *     length): results are realigned across lanes and stored as aligned
  *     16-byte vectors.  Sources at different offsets take a slower scalar
- *     path with the same results.
+ *     path with the same results.  xred_ring_reduce refuses chunks at
+ *     different offsets (see there); xred_reduce_copy_step, xred_acc_cast and
+ *     xred_allreduce_sim take the vector path only when every buffer they
+ *     touch is 16-byte aligned, else the scalar one.
  *   - Device words the library binds to a stream (the ring's relay word, the
  *     batch queue's counters) are looked up by the stream's handle.  Let a
  *     stream's work finish before destroying it if a stream created later
