@@ -209,12 +209,10 @@ __device__ void batched_tile(const xred_item &it, uint64_t lt)
         }
         // the item's first tile also takes the elements before its first
         // vector, its last tile those after its last full vector
-        if (lt == 0 && threadIdx.x < lead) reduce_elem<T, Op>(src, nsrc, dst, threadIdx.x);
-        if ((lt + 1) * kTileElems >= count) {
-            const uint32_t tail = (uint32_t)((count - lead) % T::kVec);
-            if (threadIdx.x < tail)
-                reduce_elem<T, Op>(src, nsrc, dst, lead + nvec * T::kVec + threadIdx.x);
-        }
+        reduce_ends<T, Op>(src, nsrc, dst, lt == 0 ? (uint32_t)lead : 0u,
+                           (lt + 1) * kTileElems >= count ? (uint32_t)((count - lead) % T::kVec)
+                                                          : 0u,
+                           lead + nvec * T::kVec);
     } else {
         const uint64_t e0 = lt * kTileElems;
         const uint64_t e1 = count < e0 + kTileElems ? count : e0 + kTileElems;
@@ -413,14 +411,12 @@ __global__ __launch_bounds__(kB) void batched_rr_kernel(const xred_item *items, 
                 tile_store(down_vec<T, Op>(acc), w, cur, lb + toff, nrec, h);
             }
             if (cur.fast) {
-                if (cur.lt == 0 && threadIdx.x < cur.lead)
-                    reduce_elem<T, Op>(GlobalSrc{cur.srcs}, cur.nsrc, cur.dst, threadIdx.x);
-                if ((cur.lt + 1) * tile_elems<T>() >= cur.count) {
-                    const uint32_t tail = (uint32_t)((cur.count - cur.lead) % T::kVec);
-                    if (threadIdx.x < tail)
-                        reduce_elem<T, Op>(GlobalSrc{cur.srcs}, cur.nsrc, cur.dst,
-                                           cur.lead + nvec * T::kVec + threadIdx.x);
-                }
+                reduce_ends<T, Op>(GlobalSrc{cur.srcs}, cur.nsrc, cur.dst,
+                                   cur.lt == 0 ? cur.lead : 0u,
+                                   (cur.lt + 1) * tile_elems<T>() >= cur.count
+                                       ? (uint32_t)((cur.count - cur.lead) % T::kVec)
+                                       : 0u,
+                                   cur.lead + nvec * T::kVec);
             } else {
                 batched_tile<T, Op>(load_item(items, cur.k), cur.lt);
             }
@@ -616,14 +612,12 @@ __global__ __launch_bounds__(kB) void batched_queue_kernel(const xred_item *item
             tile_store(down_vec<T, Op>(acc), w, cur, lb + toff, nrec, h);
         }
         if (cur.fast) {
-            if (cur.lt == 0 && threadIdx.x < cur.lead)
-                reduce_elem<T, Op>(GlobalSrc{cur.srcs}, cur.nsrc, cur.dst, threadIdx.x);
-            if ((cur.lt + 1) * kTileElems >= cur.count) {
-                const uint32_t tail = (uint32_t)((cur.count - cur.lead) % T::kVec);
-                if (threadIdx.x < tail)
-                    reduce_elem<T, Op>(GlobalSrc{cur.srcs}, cur.nsrc, cur.dst,
-                                       cur.lead + nvec * T::kVec + threadIdx.x);
-            }
+            reduce_ends<T, Op>(GlobalSrc{cur.srcs}, cur.nsrc, cur.dst,
+                               cur.lt == 0 ? cur.lead : 0u,
+                               (cur.lt + 1) * kTileElems >= cur.count
+                                   ? (uint32_t)((cur.count - cur.lead) % T::kVec)
+                                   : 0u,
+                               cur.lead + nvec * T::kVec);
         } else {
             batched_tile<T, Op, SUB>(load_item(items, cur.k), cur.lt);
         }
@@ -781,13 +775,11 @@ __device__ __forceinline__ void table_tile(const ItemHead &h, uint64_t lt)
     }
     // the item's first tile also takes the elements before its first vector,
     // its last tile those after its last full vector
-    if (lt == 0 && threadIdx.x < lead) reduce_elem<T, Op>(src, nsrc, dst, threadIdx.x);
-    if ((lt + 1) * table_tile_elems<T>() >= count) {
-        const uint64_t nvec = (count - lead) / T::kVec;
-        const uint32_t tail = (uint32_t)((count - lead) % T::kVec);
-        if (threadIdx.x < tail)
-            reduce_elem<T, Op>(src, nsrc, dst, lead + nvec * T::kVec + threadIdx.x);
-    }
+    reduce_ends<T, Op>(src, nsrc, dst, lt == 0 ? (uint32_t)lead : 0u,
+                       (lt + 1) * table_tile_elems<T>() >= count
+                           ? (uint32_t)((count - lead) % T::kVec)
+                           : 0u,
+                       lead + (count - lead) / T::kVec * T::kVec);
 }
 
 // NARROW: the table holds 16-bit item indices (batches of at most 65536

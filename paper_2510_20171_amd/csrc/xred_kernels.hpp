@@ -194,14 +194,34 @@ __device__ __forceinline__ void reduce_tile(const Src &src, int nsrc, char *dst,
         bstore<kStoreOut>(down_vec<T, Op>(acc[u]), w, (uint32_t)(u * B + threadIdx.x) * 16u);
 }
 
-// Element i (scalar path): used for tails shorter than a vector and for
-// buffers that are not all 16-byte aligned.
+// Element i (scalar path): used for leads and tails shorter than a vector
+// and for buffers at different offsets within 16 bytes.  The loads of up to
+// 8 sources are issued before they are folded, in source order.
 template <class T, class Op, class Src>
 __device__ __forceinline__ void reduce_elem(const Src &src, int nsrc, char *dst, size_t i)
 {
-    typename T::Acc a = up1<T>(src(0), i);
-    for (int p = 1; p < nsrc; ++p) a = combine<T, Op>(a, up1<T>(src(p), i));
+    typename T::Acc a{};
+    for (int p = 0; p < nsrc; p += 8) {
+        typename T::Acc x[8];
+#pragma unroll
+        for (int q = 0; q < 8; ++q)
+            if (p + q < nsrc) x[q] = up1<T>(src(p + q), i);
+#pragma unroll
+        for (int q = 0; q < 8; ++q)
+            if (p + q < nsrc) a = p + q == 0 ? x[q] : combine<T, Op>(a, x[q]);
+    }
     down1<T, Op>(dst, i, avg_scale<T, Op>(a, nsrc));
+}
+
+// The elements of one reduction outside its vectors: the first nl (its lead,
+// or 0) and the nt from element tail_at on (its tail, or 0), one per thread
+// of the first wavefront, so both are folded by one chain of loads.
+template <class T, class Op, class Src>
+__device__ __forceinline__ void reduce_ends(const Src &src, int nsrc, char *dst, uint32_t nl,
+                                            uint32_t nt, size_t tail_at)
+{
+    const uint32_t t = threadIdx.x;
+    if (t < nl + nt) reduce_elem<T, Op>(src, nsrc, dst, t < nl ? (size_t)t : tail_at + (t - nl));
 }
 
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
@@ -368,11 +388,8 @@ __global__ __launch_bounds__(B) void reduce_vec_kernel(KernargSrc<MAXP> src, int
         reduce_tile<T, Op, NP, U, B>(src, nsrc, dst,
                                      Tile{lb + off, h ? head : tile_nrec(vbytes, off, kTileBytes)});
     }
-    if ((tail | lead) != 0 && blockIdx.x == ntiles % gridDim.x) {
-        if (threadIdx.x < tail)
-            reduce_elem<T, Op>(src, nsrc, dst, lead + nvec * T::kVec + threadIdx.x);
-        if (threadIdx.x < lead) reduce_elem<T, Op>(src, nsrc, dst, threadIdx.x);
-    }
+    if ((tail | lead) != 0 && blockIdx.x == ntiles % gridDim.x)
+        reduce_ends<T, Op>(src, nsrc, dst, lead, tail, lead + nvec * T::kVec);
 }
 
 // Any alignment: one element per thread per step.

@@ -134,11 +134,8 @@ __global__ __launch_bounds__(B) void reduce_split_kernel(KernargSrc<XRED_MAX_SRC
         split_tile<T, Op, U, B>(src, nsrc, dst,
                              Tile{lb + off, h ? head : tile_nrec(vbytes, off, kTileBytes)}, c);
     }
-    if ((tail | lead) != 0 && blockIdx.x == ntiles % gridDim.x) {
-        if (threadIdx.x < tail)
-            reduce_elem<T, Op>(src, nsrc, dst, lead + nvec * T::kVec + threadIdx.x);
-        if (threadIdx.x < lead) reduce_elem<T, Op>(src, nsrc, dst, threadIdx.x);
-    }
+    if ((tail | lead) != 0 && blockIdx.x == ntiles % gridDim.x)
+        reduce_ends<T, Op>(src, nsrc, dst, lead, tail, lead + nvec * T::kVec);
 }
 
 // waves_for with the compile-time counts the vector path would pick.

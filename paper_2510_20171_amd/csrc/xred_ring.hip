@@ -283,11 +283,9 @@ __global__ __launch_bounds__(kB) void ring_kernel(KernargSrc<XRED_MAX_SRC> chunk
     // workgroup, once every chunk was seen ready (its plain loads need the
     // acquire the vector loads avoid).
     if (next == nchunks && (tail | lead) != 0 && wg == ntiles % nwg &&
-        (threadIdx.x < tail || threadIdx.x < lead)) {
+        threadIdx.x < tail + lead) {
         if (flagged) __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "");
-        if (threadIdx.x < tail)
-            reduce_elem<T, Op>(chunks, nchunks, dst, lead + nvec * T::kVec + threadIdx.x);
-        if (threadIdx.x < lead) reduce_elem<T, Op>(chunks, nchunks, dst, threadIdx.x);
+        reduce_ends<T, Op>(chunks, nchunks, dst, lead, tail, lead + nvec * T::kVec);
     }
 }
 
