@@ -1053,7 +1053,7 @@ XRED_API const char *xred_status_string(xred_status s)
 
 XRED_API const char *xred_last_error(void) { return g_err; }
 
-XRED_API int xred_version(void) { return 20300; }
+XRED_API int xred_version(void) { return 20301; }
 
 XRED_API void xred_release(void)
 {

@@ -80,7 +80,7 @@ def test_header_compiles(tmp_path, compiler, lang):
 
 
 def test_constants(L):
-    assert L.xred_version() == 20300   # 2.3.0: major*10000 + minor*100 + patch
+    assert L.xred_version() == 20301   # 2.3.1: major*10000 + minor*100 + patch
     assert L.xred_acc_elem_size(0) == 4 and L.xred_acc_elem_size(1) == 4
     assert L.xred_acc_elem_size(2) == 4 and L.xred_acc_elem_size(7) == 4
     assert L.xred_acc_elem_size(5) == 8 and L.xred_acc_elem_size(6) == 8

@@ -363,6 +363,50 @@ def test_output_at_another_offset(xr, orc, dtype):
         assert np.all(raw[G + md + n * es:] == 0x5A), what
 
 
+@pytest.mark.parametrize("dtype", ["bf16", "f32", "u8", "f64", "e4m3", "i32"])
+def test_sources_at_different_offsets(xr, orc, dtype):
+    """Sources at different offsets within 16 bytes (each at the very start
+    of its own allocation, so nothing before it may be read): every source's
+    vectors are realigned to the output's grid, the lead and the tail are
+    folded element by element.  Offsets drawn per source and for the output;
+    lengths below, at and just past the shortest vector launch, a few tiles
+    with a ragged tail, and long; 2 to 17 sources; sum, max, avg / min and
+    prod.  Canaries around the output stay untouched."""
+    rng = np.random.default_rng(29)
+    es = xr.ELEM_SIZE[dtype]
+    G = 64
+    ops = ["sum", "max", "avg" if dtype in gu.FLOATS else "min", "prod"]
+    cases = []
+    for k in range(48):
+        offs = [int(rng.integers(0, 16 // es)) * es for _ in range(17)]
+        offs[1] = (offs[0] + es) % 16            # at least two offsets differ
+        do = int(rng.integers(0, 16 // es)) * es
+        lead = (((16 - do) % 16) + 16) // es
+        n = (lead + 32 // es - 1, lead + 32 // es, lead + 32 // es + 1, lead + 48 // es + 3,
+             3 * 128 * 16 // es + 7, 600011)[k % 6]
+        cases.append((offs, do, n, (2, 3, 8, 9, 17, 8)[k % 6]))
+    for k, (offs, do, n, P) in enumerate(cases):
+        op = ops[k % 4] if n < 600011 else "sum"
+        srcs = [pins.random_column_values(rng, dtype, n) for _ in range(P)]
+        keep, views = [], []
+        for p, a in enumerate(srcs):
+            o = offs[p]
+            b = torch.zeros(o + n * es, dtype=torch.uint8, device="cuda")
+            v = b[o:o + n * es].view(gu.torch_dtype(dtype))
+            v.copy_(gu.to_dev(a, dtype))
+            keep.append(b)
+            views.append(v)
+        store = torch.full((G + do + n * es + G,), 0x5A, dtype=torch.uint8, device="cuda")
+        out = store[G + do:G + do + n * es].view(gu.torch_dtype(dtype))
+        xr.allreduce_local(views, out, op, dtype=dtype)
+        torch.cuda.synchronize()
+        what = f"{dtype} {op} P={P} sources at {offs[:P]} output at {do} n={n}"
+        gu.assert_parity(out, orc.allreduce_local(srcs, dtype, op), dtype, op, what)
+        raw = store.cpu().numpy()
+        assert np.all(raw[:G + do] == 0x5A), what
+        assert np.all(raw[G + do + n * es:] == 0x5A), what
+
+
 @pytest.mark.parametrize("dtype", ["bf16", "u8", "f32"])
 def test_reduce_scatter_odd_shards(xr, orc, dtype):
     """A reduce-scatter with an odd shard length: every rank's shard (rank 0
