@@ -67,11 +67,10 @@
  *     The same calls and items read in vectors too when only the sources
  *     share an offset and dst sits at another (a reduce-scatter shard of odd
  *     length): results are realigned across lanes and stored as aligned
- *     16-byte vectors.  xred_allreduce_local and xred_reduce_scatter_local
- *     read in vectors even when their sources sit at different offsets:
- *     each source's vectors are realigned to dst's grid across lanes (calls
- *     shorter than a few vectors, and batch items whose sources sit at
- *     different offsets, take a slower scalar path with the same results).
+ *     16-byte vectors.  They read in vectors even when their sources sit at
+ *     different offsets: each source's vectors are realigned to dst's grid
+ *     across lanes (calls and items shorter than a few vectors take a slower
+ *     scalar path with the same results).
  *     xred_ring_reduce refuses chunks at different offsets (see there);
  *     xred_reduce_copy_step, xred_acc_cast and
  *     xred_allreduce_sim take the vector path only when every buffer they

@@ -213,6 +213,20 @@ __device__ void batched_tile(const xred_item &it, uint64_t lt)
                            (lt + 1) * kTileElems >= count ? (uint32_t)((count - lead) % T::kVec)
                                                           : 0u,
                            lead + nvec * T::kVec);
+    } else if (const uint32_t sl = shift_lead<T>((uintptr_t)dst, count * T::kSize)) {
+        // sources at different offsets: vectors realigned to dst's grid
+        const size_t lb = (size_t)sl * T::kSize;
+        const size_t nvec = (count * T::kSize - lb - 16) / 16, vbytes = nvec * 16;
+        for (int h = 0; h < SUB; ++h) {
+            const size_t off = lt * kTileBytes + (size_t)h * kSubBytes;
+            if (off >= vbytes) break;
+            shift_tile<T, Op, kB>(src, nsrc, dst, lb, off, tile_nrec(vbytes, off, kSubBytes));
+        }
+        reduce_ends<T, Op>(src, nsrc, dst, lt == 0 ? sl : 0u,
+                           (lt + 1) * kTileElems >= count
+                               ? (uint32_t)(count - sl - nvec * T::kVec)
+                               : 0u,
+                           sl + nvec * T::kVec);
     } else {
         const uint64_t e0 = lt * kTileElems;
         const uint64_t e1 = count < e0 + kTileElems ? count : e0 + kTileElems;
@@ -727,6 +741,18 @@ __device__ __forceinline__ void table_tile(const ItemHead &h, uint64_t lt)
                 if (c != 0) split_tile<T, Op, 1, kTB>(src, nsrc, dst, tl, c);
                 else reduce_tile<T, Op, 0, U, kTB>(src, nsrc, dst, tl);
             }
+        } else if (const uint32_t sl = shift_lead<T>((uintptr_t)dst, count * T::kSize)) {
+            // sources at different offsets: vectors realigned to dst's grid
+            const size_t lb = (size_t)sl * T::kSize;
+            const size_t nvec = (count * T::kSize - lb - 16) / 16, vbytes = nvec * 16;
+            if (toff < vbytes)
+                shift_tile<T, Op, kTB>(src, nsrc, dst, lb, toff, tile_nrec(vbytes, toff, kBytes));
+            reduce_ends<T, Op>(src, nsrc, dst, lt == 0 ? sl : 0u,
+                               (lt + 1) * table_tile_elems<T>() >= count
+                                   ? (uint32_t)(count - sl - nvec * T::kVec)
+                                   : 0u,
+                               sl + nvec * T::kVec);
+            return;
         } else {
             const uint64_t e0 = lt * table_tile_elems<T>();
             const uint64_t e1 =

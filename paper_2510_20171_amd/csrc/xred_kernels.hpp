@@ -337,6 +337,74 @@ __device__ __forceinline__ void split_store(u32x4 mine, char *base, uint32_t nre
     }
 }
 
+// One tile of B output vectors when the sources sit at different offsets
+// within 16 bytes: the output grid is dst's, output vector q of the tile
+// starts at byte lb + off + 16q of dst, which is 16-byte aligned, and of
+// every source, where source p's bytes sit s_p into its aligned vectors
+// A_p[q], A_p[q+1] (A_p counted from src_p + lb - s_p, which must not lie
+// before src_p, and A_p one past the tile must lie inside the source).
+// Lane q loads A_p[q] and takes A_p[q+1] from the next lane (a lane
+// shuffle; the wavefront's last lane loads it), joining the two with byte
+// funnel shifts; sources on the grid skip both.  The loads of up to 8
+// sources are in flight before they are folded in source order.  nrec bytes
+// of the tile exist.  Every lane of the workgroup must be active.
+template <class T, class Op, int B, class Src>
+__device__ __forceinline__ void shift_tile(const Src &src, int nsrc, char *dst, size_t lb,
+                                           size_t off, uint32_t nrec)
+{
+    const uint32_t q = threadIdx.x;
+    typename T::Acc acc[T::kVec];
+    for (int p0 = 0; p0 < nsrc; p0 += 8) {
+        u32x4 lo[8], hi[8];
+        uint32_t sh[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            if (p0 + j < nsrc) {
+                const char *a = src(p0 + j) + lb;
+                sh[j] = (uint32_t)((uintptr_t)a & 15u);
+                // vectors q and q+1 of the tile; the range covers one vector
+                // past the tile, which exists in every source
+                const rsrc_t r = make_rsrc(a - sh[j] + off, nrec + 16u);
+                lo[j] = bload<kLoadStream>(r, 16u * q);
+                if (sh[j] != 0 && (q & 63u) == 63u) hi[j] = bload<kLoadStream>(r, 16u * q + 16u);
+            }
+        }
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            if (p0 + j < nsrc) {
+                u32x4 v = lo[j];
+                if (sh[j] != 0) {
+                    u32x4 nx;
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) nx[i] = __shfl_down(lo[j][i], 1u, 64);
+                    if ((q & 63u) == 63u) nx = hi[j];
+                    v = bytes_from(lo[j], nx, sh[j]);
+                }
+                if (p0 + j == 0) up_vec<T>(v, acc);
+                else fold_vec<T, Op>(acc, v);
+            }
+        }
+    }
+    if constexpr (__is_same(Op, OpAvg)) {
+#pragma unroll
+        for (int e = 0; e < T::kVec; ++e) acc[e] = avg_scale<T, Op>(acc[e], nsrc);
+    }
+    bstore<kStoreOut>(down_vec<T, Op>(acc), make_rsrc(dst + lb + off, nrec), 16u * q);
+}
+
+// The lead shift_tile needs for a reduction of `bytes` bytes into dst: dst's
+// next 16-byte boundary and one vector more, in elements; 0 when the
+// reduction is too short for one vector with a vector after it, or dst is
+// not element-aligned (a device descriptor's), which is then folded element
+// by element.
+template <class T>
+__host__ __device__ __forceinline__ uint32_t shift_lead(uintptr_t dst, size_t bytes)
+{
+    if (dst % T::kSize != 0) return 0u;
+    const uint32_t lb = (uint32_t)(((16u - (dst & 15u)) & 15u) + 16u);
+    return bytes >= (size_t)lb + 32 ? lb / (uint32_t)T::kSize : 0u;
+}
+
 // A tile whose sources sit on 16-byte boundaries (tl.off past each source
 // pointer) and whose output dst + tl.off sits c bytes past one: U vectors
 // per thread folded as reduce_tile does, then each block of B vectors

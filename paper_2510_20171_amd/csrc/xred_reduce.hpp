@@ -140,17 +140,11 @@ __global__ __launch_bounds__(B) void reduce_split_kernel(KernargSrc<XRED_MAX_SRC
 
 // --------------------------------------------------- shifted sources --
 // Sources at different offsets within 16 bytes: the output grid is dst's.
-// Output vector k holds elements lead + kVec*k .. of every stream, where
-// lead reaches dst's next 16-byte boundary and one vector more; source p
-// holds them s_p bytes into its aligned vectors A_p[k], A_p[k+1] (A_p[0] =
-// src_p + lead*size - s_p, never before src_p since lead*size >= 16).  Lane
-// q loads A_p[q] of its tile and takes A_p[q+1] from the next lane (a lane
-// shuffle; the wavefront's last lane loads it), joining the two with byte
-// funnel shifts (bytes_from); the loads of up to 8 sources are in flight
-// before they are folded in source order.  nvec stops short of every source's end by a
-// vector, so A_p[nvec] still lies inside each source; the lead and the
-// tail are folded element by element.  (P=8 x 64M bf16 with the sources at
-// alternating offsets: 574 us element by element.)
+// The first `lead` elements reach dst's next 16-byte boundary and one vector
+// more, so every source's aligned base lies inside it, and nvec stops a
+// vector short of every source's end; the tiles between are shift_tile's,
+// the lead and the tail are folded element by element.  (P=8 x 64M bf16
+// with the sources at alternating offsets: 574 us element by element.)
 template <class T, class Op, int B>
 __global__ __launch_bounds__(B) void reduce_shift_kernel(KernargSrc<XRED_MAX_SRC> src, int nsrc,
                                                          char *dst, size_t nvec, uint32_t tail,
@@ -160,49 +154,9 @@ __global__ __launch_bounds__(B) void reduce_shift_kernel(KernargSrc<XRED_MAX_SRC
     const size_t vbytes = nvec * 16;
     const size_t lb = (size_t)lead * T::kSize;
     const size_t ntiles = (vbytes + kTileBytes - 1) / kTileBytes;
-    const uint32_t q = threadIdx.x;
     for (size_t t = blockIdx.x; t < ntiles; t += gridDim.x) {
         const size_t off = t * kTileBytes;
-        const uint32_t nrec = tile_nrec(vbytes, off, kTileBytes);
-        typename T::Acc acc[T::kVec];
-        for (int p0 = 0; p0 < nsrc; p0 += 8) {
-            u32x4 lo[8], hi[8];
-            uint32_t sh[8];
-#pragma unroll
-            for (int j = 0; j < 8; ++j) {
-                if (p0 + j < nsrc) {
-                    const char *a = src(p0 + j) + lb;
-                    sh[j] = (uint32_t)((uintptr_t)a & 15u);
-                    // vectors q and q+1 of the tile; the range covers one
-                    // vector past the tile, which exists in every source
-                    const rsrc_t r = make_rsrc(a - sh[j] + off, nrec + 16u);
-                    lo[j] = bload<kLoadStream>(r, 16u * q);
-                    if (sh[j] != 0 && (q & 63u) == 63u)
-                        hi[j] = bload<kLoadStream>(r, 16u * q + 16u);
-                }
-            }
-#pragma unroll
-            for (int j = 0; j < 8; ++j) {
-                if (p0 + j < nsrc) {
-                    u32x4 v = lo[j];
-                    if (sh[j] != 0) {
-                        // vector q+1 from the next lane; the wavefront's last lane loaded it
-                        u32x4 nx;
-#pragma unroll
-                        for (int i = 0; i < 4; ++i) nx[i] = __shfl_down(lo[j][i], 1u, 64);
-                        if ((q & 63u) == 63u) nx = hi[j];
-                        v = bytes_from(lo[j], nx, sh[j]);
-                    }
-                    if (p0 + j == 0) up_vec<T>(v, acc);
-                    else fold_vec<T, Op>(acc, v);
-                }
-            }
-        }
-        if constexpr (__is_same(Op, OpAvg)) {
-#pragma unroll
-            for (int e = 0; e < T::kVec; ++e) acc[e] = avg_scale<T, Op>(acc[e], nsrc);
-        }
-        bstore<kStoreOut>(down_vec<T, Op>(acc), make_rsrc(dst + lb + off, nrec), 16u * q);
+        shift_tile<T, Op, B>(src, nsrc, dst, lb, off, tile_nrec(vbytes, off, kTileBytes));
     }
     if (blockIdx.x == ntiles % gridDim.x)
         reduce_ends<T, Op>(src, nsrc, dst, lead, tail, lead + nvec * T::kVec);
@@ -314,10 +268,10 @@ hipError_t go(const char *const *srcs, int nsrc, char *dst, size_t count, hipStr
     if (!common) {
         // dst's next 16-byte boundary and one vector more, then vectors up to
         // a vector short of the end (see reduce_shift_kernel)
-        const uint32_t slead =
-            (uint32_t)((((16 - ((uintptr_t)dst & 15u)) & 15u) + 16u) / T::kSize);
-        const size_t bytes = count * T::kSize, slb = (size_t)slead * T::kSize;
-        if (bytes >= slb + 32) {
+        const size_t bytes = count * T::kSize;
+        const uint32_t slead = shift_lead<T>((uintptr_t)dst, bytes);
+        const size_t slb = (size_t)slead * T::kSize;
+        if (slead != 0) {
             KernargSrc<XRED_MAX_SRC> ks;
             for (int p = 0; p < nsrc; ++p) ks.p[p] = srcs[p];
             for (int p = nsrc; p < XRED_MAX_SRC; ++p) ks.p[p] = nullptr;

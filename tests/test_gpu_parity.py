@@ -754,8 +754,9 @@ def test_batched_element_offsets(xr, orc, dtype, mode):
     up to 8 sources and the general tile's 9-17); items whose sources share
     an offset and whose output sits at another read in vectors and store
     realigned (every pair of offsets, lengths from just past the lead to
-    several tiles); items whose sources sit at different offsets take the
-    scalar path.  Host descriptors (the tile-table kernel), device
+    several tiles); items whose sources sit at different offsets read
+    vectors realigned to the output's grid, or go element by element when
+    too short.  Host descriptors (the tile-table kernel), device
     descriptors past 64 items (the queue kernel; under graph capture runs
     dealt tile by tile) and a device batch of at most 64 items (one run:
     the round-robin kernel); canaries between the outputs stay untouched."""
@@ -774,10 +775,14 @@ def test_batched_element_offsets(xr, orc, dtype, mode):
         lead = (16 - m) % 16 // es
         for j, do in enumerate(d for d in range(0, 16, es) if d != m):
             split.append(("output differs", m, (lead + 1, lead + 16 // es + 3, 9000, 40001)[j % 4], do))
+    # sources at two offsets, lengths on both sides of the shortest realigned
+    # launch (the lead is 16 to 31 bytes, then two vectors) and long
+    differ = [("sources differ", m, n, (m + 3 * es) % 16)
+              for m in sorted({0, es, 16 - es}) for n in (48 // es + 2, 64 // es + 5, 40001)]
     if mode == "device_small":
-        specs = split[::max(1, len(split) // 60)][:60]
+        specs = split[::max(1, len(split) // 50)][:50] + differ[:10]
     else:
-        specs += split
+        specs += split + differ
     if mode == "device":   # past 64 items: the queue kernel, not the one-run kernel
         specs = (specs * (70 // len(specs) + 1))[:max(70, len(specs))]
     keep, items, rows, outs, G = [], [], [], [], 64
